@@ -1,0 +1,216 @@
+"""ctypes front end of the plain CPU oracle (``oracle.c``).
+
+TEST INFRASTRUCTURE ONLY: imported by the tests, by the package smoke check
+and by the benchmark's CPU-baseline leg, never by the product path.  It
+imports nothing from the GPU package and the GPU package imports nothing
+from here.
+
+Every function takes and returns numpy arrays; tables are float32
+``[num_keys, dim]`` row-major and are updated in place by the ``step_*`` and
+``push`` calls, exactly like the store they check.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+CFLAGS = ["-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared"]
+
+
+def build(force: bool = True) -> str:
+    """Compile ``oracle.c`` with gcc (no fast-math, no contraction)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", *CFLAGS, "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build(force=True)
+        L = C.CDLL(_LIB)
+        p, i64, i32, f32, f64 = C.c_void_p, C.c_int64, C.c_int32, C.c_float, C.c_double
+        sig = {
+            "orc_pull": (i64, [p, i64, i32, p, i64, p]),
+            "orc_dedup": (i64, [i64, p, i64, p, p, p, p]),
+            "orc_adagrad_row": (None, [p, p, p, i32, f32, f32]),
+            "orc_push": (i64, [p, p, i64, i32, f32, f32, p, i64, p]),
+            "orc_complex_score": (f64, [p, p, p, i32]),
+            "orc_grad_mf": (f64, [p, i64, i32, p, p, p, i64, i64, f32, p, p, p]),
+            "orc_grad_kge": (f64, [p, i64, i32, p, p, p, p, i64, i32, i32, i64, p, p, p]),
+            "orc_grad_sgns": (f64, [p, i64, i32, p, p, p, i64, i32, i32, i64, p, p, p]),
+            "orc_grad_ctr": (f64, [p, i64, i32, p, p, i64, i32, p, p, p]),
+            "orc_step_mf": (f64, [p, p, i64, i32, f32, f32, p, p, p, i64, i64, f32, p]),
+            "orc_step_kge": (f64, [p, p, i64, i32, f32, f32, p, p, p, p, i64, i32, i32, i64, p]),
+            "orc_step_sgns": (f64, [p, p, i64, i32, f32, f32, p, p, p, i64, i32, i32, i64, p]),
+            "orc_step_ctr": (f64, [p, p, i64, i32, f32, f32, p, p, i64, i32, p]),
+        }
+        for name, (res, args) in sig.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _p(a: np.ndarray):
+    return a.ctypes.data_as(C.c_void_p)
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def _table(W):
+    assert W.dtype == np.float32 and W.flags.c_contiguous and W.ndim == 2
+    return W
+
+
+# ---------------------------------------------------------------------------
+def pull(W, keys):
+    W = _table(W)
+    keys = _c(keys, np.int64)
+    out = np.empty((keys.size, W.shape[1]), np.float32)
+    bad = lib().orc_pull(_p(W), W.shape[0], W.shape[1], _p(keys), keys.size, _p(out))
+    return out, int(bad)
+
+
+def dedup(num_keys, keys):
+    keys = _c(keys, np.int64)
+    n = keys.size
+    uniq = np.empty(max(n, 1), np.int64)
+    perm = np.empty(max(n, 1), np.int32)
+    offs = np.empty(n + 1, np.int32)
+    nu = np.zeros(1, np.int32)
+    bad = lib().orc_dedup(num_keys, _p(keys), n, _p(uniq), _p(perm), _p(offs), _p(nu))
+    u = int(nu[0])
+    return uniq[:u].copy(), perm[:n].copy(), offs[: u + 1].copy(), int(bad)
+
+
+def adagrad_row(w, acc, g, lr, eps):
+    w, acc, g = _c(w, np.float32), _c(acc, np.float32), _c(g, np.float32)
+    lib().orc_adagrad_row(_p(w), _p(acc), _p(g), w.size, lr, eps)
+    return w, acc
+
+
+def push(W, G, keys, grads, lr, eps):
+    W, G = _table(W), _table(G)
+    keys = _c(keys, np.int64)
+    grads = _c(grads, np.float32).reshape(keys.size, W.shape[1])
+    return int(lib().orc_push(_p(W), _p(G), W.shape[0], W.shape[1], lr, eps, _p(keys), keys.size,
+                              _p(grads)))
+
+
+def complex_score(s, r, o):
+    s, r, o = _c(s, np.float32), _c(r, np.float32), _c(o, np.float32)
+    return float(lib().orc_complex_score(_p(s), _p(r), _p(o), s.size // 2))
+
+
+def grad_mf(W, row, col, val, col_off, lam):
+    W = _table(W)
+    row, col, val = _c(row, np.int32), _c(col, np.int32), _c(val, np.float32)
+    B = row.size
+    keys = np.empty(2 * B, np.int64)
+    grads = np.empty((2 * B, W.shape[1]), np.float32)
+    bad = C.c_int64(0)
+    loss = lib().orc_grad_mf(_p(W), W.shape[0], W.shape[1], _p(row), _p(col), _p(val), B,
+                             col_off, lam, _p(keys), _p(grads), C.byref(bad))
+    return keys, grads, float(loss), int(bad.value)
+
+
+def grad_kge(W, head, rel, tail, neg, n_head_neg, rel_off):
+    W = _table(W)
+    head, rel, tail = _c(head, np.int32), _c(rel, np.int32), _c(tail, np.int32)
+    neg = _c(neg, np.int32)
+    B = head.size
+    n_neg = neg.size // max(B, 1) if B else 0
+    per = 3 + n_neg
+    keys = np.empty(B * per, np.int64)
+    grads = np.empty((B * per, W.shape[1]), np.float32)
+    bad = C.c_int64(0)
+    loss = lib().orc_grad_kge(_p(W), W.shape[0], W.shape[1], _p(head), _p(rel), _p(tail), _p(neg),
+                              B, n_neg, n_head_neg, rel_off, _p(keys), _p(grads), C.byref(bad))
+    return keys, grads, float(loss), int(bad.value)
+
+
+def grad_sgns(W, centre, ctx, neg, window, out_off):
+    W = _table(W)
+    centre, ctx, neg = _c(centre, np.int32), _c(ctx, np.int32), _c(neg, np.int32)
+    B = centre.size
+    slots = 2 * window
+    n_neg = neg.size // max(B * slots, 1) if B else 0
+    per = 1 + slots * (1 + n_neg)
+    keys = np.empty(B * per, np.int64)
+    grads = np.empty((B * per, W.shape[1]), np.float32)
+    bad = C.c_int64(0)
+    loss = lib().orc_grad_sgns(_p(W), W.shape[0], W.shape[1], _p(centre), _p(ctx), _p(neg), B,
+                               window, n_neg, out_off, _p(keys), _p(grads), C.byref(bad))
+    return keys, grads, float(loss), int(bad.value)
+
+
+def grad_ctr(W, keys, label):
+    W = _table(W)
+    keys, label = _c(keys, np.int64), _c(label, np.float32)
+    B = label.size
+    F = keys.size // max(B, 1) if B else 0
+    okeys = np.empty(B * F, np.int64)
+    grads = np.empty((B * F, W.shape[1]), np.float32)
+    bad = C.c_int64(0)
+    loss = lib().orc_grad_ctr(_p(W), W.shape[0], W.shape[1], _p(keys), _p(label), B, F,
+                              _p(okeys), _p(grads), C.byref(bad))
+    return okeys, grads, float(loss), int(bad.value)
+
+
+def step_mf(W, G, row, col, val, col_off, lam, lr, eps):
+    W, G = _table(W), _table(G)
+    row, col, val = _c(row, np.int32), _c(col, np.int32), _c(val, np.float32)
+    bad = C.c_int64(0)
+    loss = lib().orc_step_mf(_p(W), _p(G), W.shape[0], W.shape[1], lr, eps, _p(row), _p(col),
+                             _p(val), row.size, col_off, lam, C.byref(bad))
+    return float(loss), int(bad.value)
+
+
+def step_kge(W, G, head, rel, tail, neg, n_head_neg, rel_off, lr, eps):
+    W, G = _table(W), _table(G)
+    head, rel, tail = _c(head, np.int32), _c(rel, np.int32), _c(tail, np.int32)
+    neg = _c(neg, np.int32)
+    B = head.size
+    n_neg = neg.size // max(B, 1) if B else 0
+    bad = C.c_int64(0)
+    loss = lib().orc_step_kge(_p(W), _p(G), W.shape[0], W.shape[1], lr, eps, _p(head), _p(rel),
+                              _p(tail), _p(neg), B, n_neg, n_head_neg, rel_off, C.byref(bad))
+    return float(loss), int(bad.value)
+
+
+def step_sgns(W, G, centre, ctx, neg, window, out_off, lr, eps):
+    W, G = _table(W), _table(G)
+    centre, ctx, neg = _c(centre, np.int32), _c(ctx, np.int32), _c(neg, np.int32)
+    B = centre.size
+    n_neg = neg.size // max(B * 2 * window, 1) if B else 0
+    bad = C.c_int64(0)
+    loss = lib().orc_step_sgns(_p(W), _p(G), W.shape[0], W.shape[1], lr, eps, _p(centre), _p(ctx),
+                               _p(neg), B, window, n_neg, out_off, C.byref(bad))
+    return float(loss), int(bad.value)
+
+
+def step_ctr(W, G, keys, label, lr, eps):
+    W, G = _table(W), _table(G)
+    keys, label = _c(keys, np.int64), _c(label, np.float32)
+    B = label.size
+    F = keys.size // max(B, 1) if B else 0
+    bad = C.c_int64(0)
+    loss = lib().orc_step_ctr(_p(W), _p(G), W.shape[0], W.shape[1], lr, eps, _p(keys), _p(label),
+                              B, F, C.byref(bad))
+    return float(loss), int(bad.value)
