@@ -1,0 +1,186 @@
+/*
+ * adapm.h -- C ABI of a single-GPU (MI355X, gfx950) sparse parameter store.
+ *
+ * The store is the node-local parameter store that a parameter manager
+ * provides to its workers: global read and write access to model parameters
+ * by key (Section 1), served locally from memory shared with the workers
+ * (Section 4, Figure 3), with the updates of all workers to one parameter
+ * merged into the store (Appendix B.1.2).  Every task in the paper trains
+ * with SGD and AdaGrad (Appendix C); the store applies AdaGrad on write.
+ *
+ * Semantics of one step (deterministic, synchronous minibatch):
+ *   pull all rows the batch needs from the pre-step table, compute
+ *   per-occurrence gradients from those values, sum the gradients of each
+ *   distinct key, apply one AdaGrad update per distinct key:
+ *     G <- G + g*g ;  W <- W - lr * ( g / (sqrt(G) + eps) )    (fp32, per element)
+ *   Sums of more than one term are accumulated in fp64 and rounded once.
+ *
+ * Conventions shared by all calls
+ *   - Plain C types only.  "device" pointers are HIP device memory (e.g. a
+ *     torch.cuda tensor's data_ptr()); "host" pointers are ordinary memory.
+ *   - Tables are fp32, row-major, dense: row k of a table with `dim` columns
+ *     starts at element k*dim.  The caller owns the value table W and the
+ *     AdaGrad accumulator table G (both num_keys*dim floats, device); the
+ *     store borrows them for its lifetime and never frees them.
+ *   - `stream` is a hipStream_t (NULL = the legacy default stream).  Every
+ *     call is enqueued asynchronously on that stream; nothing synchronizes
+ *     unless stated.  A store must be used from one stream at a time.
+ *   - Argument errors are detected on the host before anything is enqueued
+ *     and returned immediately (nothing is launched).  Errors that only the
+ *     device can see (a key outside [0, num_keys)) set a sticky flag in the
+ *     store that ps_get_error() reports; the offending pulled row is zero,
+ *     and the offending occurrence (or the whole training unit it belongs
+ *     to, for the step calls) contributes nothing.
+ *   - n = 0 (or B = 0) is a valid no-op that returns PS_OK.
+ *   - Output buffers must not alias the tables or each other.
+ *   - Workspace: calls that need scratch memory take (ws, ws_bytes) from
+ *     the caller, sized by ps_workspace_bytes(); the library allocates no
+ *     device memory except a small status block in ps_create().
+ */
+#ifndef ADAPM_H
+#define ADAPM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ps_store ps_store;   /* opaque host handle */
+typedef int32_t ps_status;
+
+#define PS_OK               0
+#define PS_ERR_INVALID     (-1)   /* bad argument (null pointer, negative size, bad dim ...) */
+#define PS_ERR_KEY_RANGE   (-2)   /* a key outside [0, num_keys) was seen on the device */
+#define PS_ERR_WORKSPACE   (-3)   /* ws_bytes smaller than ps_workspace_bytes() */
+#define PS_ERR_DEVICE      (-4)   /* a HIP runtime call failed */
+#define PS_ERR_UNSUPPORTED (-5)   /* a size beyond what the kernels handle */
+
+/* operation codes for ps_workspace_bytes() */
+#define PS_OP_PULL      0
+#define PS_OP_PUSH      1
+#define PS_OP_DEDUP     2
+#define PS_OP_STEP_MF   3
+#define PS_OP_STEP_KGE  4
+#define PS_OP_STEP_SGNS 5
+#define PS_OP_STEP_CTR  6
+
+/* Limits: num_keys in [1, 2^31-1]; dim in [1, 2048]; key occurrences per
+ * call n < 2^31 - 2^20. */
+
+/* Create a store over caller-owned device tables W (values) and G
+ * (AdaGrad accumulators), each num_keys*dim floats, with AdaGrad learning
+ * rate lr > 0 and eps >= 0.  Allocates one small device status block and
+ * clears it on `stream`.  *out receives the handle (NULL on error). */
+ps_status ps_create(ps_store** out, int64_t num_keys, int32_t dim, float* values, float* accum,
+                    float lr, float eps, void* stream);
+
+/* Free the handle and its status block (not the tables).  NULL is a no-op.
+ * Synchronizes the device before freeing. */
+ps_status ps_destroy(ps_store* s);
+
+/* Workspace bytes a call needs.  `units` is the batch size of the call
+ * (keys for PULL/PUSH/DEDUP; entries, triples, centres or samples for the
+ * steps) and `per_unit` the key occurrences each unit creates: 1 for
+ * PULL/PUSH/DEDUP, 2 for MF, 3+n_neg for KGE, 1+2*window*(1+n_neg) for
+ * SGNS, F for CTR.  Returns 0 for an invalid combination. */
+size_t ps_workspace_bytes(int64_t num_keys, int32_t dim, int32_t op, int64_t units, int64_t per_unit);
+
+/* Read access (Section 1: global read access to parameters by key).
+ * out[i*dim + c] = W[keys[i]*dim + c] for i < n, a bit copy.
+ * keys: device int64[n]; out: device float[n*dim].  No workspace. */
+ps_status ps_pull(ps_store* s, const int64_t* keys, int64_t n, float* out, void* stream);
+
+/* Write access with merging (Appendix B.1.2: updates to a parameter are
+ * merged into its store; Appendix C: AdaGrad).  grads[i*dim..] is the
+ * gradient row of occurrence i with key keys[i]; all occurrences of one key
+ * are summed (fp64, then rounded to fp32) and one AdaGrad update is applied
+ * per distinct key.  keys: device int64[n]; grads: device float[n*dim]. */
+ps_status ps_push(ps_store* s, const int64_t* keys, int64_t n, const float* grads,
+                  void* ws, size_t ws_bytes, void* stream);
+
+/* The merge order used by ps_push, exposed for bit-exact checking: a stable
+ * sort of the occurrences by key.  Keys outside [0, num_keys) sort after all
+ * valid keys in their original order and belong to no segment.
+ *   uniq      device int64[n]  : distinct valid keys ascending (first U used)
+ *   perm      device int32[n]  : occurrence index at each sorted position
+ *   offsets   device int32[n+1]: offsets[u] = first sorted position of uniq[u],
+ *                                offsets[U] = number of valid occurrences
+ *   num_unique device int32[1] : U
+ *   err       device int32[1] or NULL: set to 1 if an invalid key was seen
+ *                                (never cleared by this call)            */
+ps_status ps_dedup(int64_t num_keys, const int64_t* keys, int64_t n, int64_t* uniq, int32_t* perm,
+                   int32_t* offsets, int32_t* num_unique, int32_t* err,
+                   void* ws, size_t ws_bytes, void* stream);
+
+/* One matrix-factorization step (Appendix C, "Matrix factorization").
+ * Entry b = (row[b], col[b], val[b]) uses keys u = row[b] and
+ * m = col_key_offset + col[b]; with e = val - <W_u, W_m>:
+ *   loss = e^2/2 + lambda/2 (|W_u|^2 + |W_m|^2)
+ *   grad_u = lambda W_u - e W_m ,  grad_m = lambda W_m - e W_u
+ * row, col: device int32[B]; val: device float[B]; loss: device double[1]
+ * receives the summed loss of the step (may be NULL). */
+ps_status ps_step_mf(ps_store* s, const int32_t* row, const int32_t* col, const float* val,
+                     int64_t B, int64_t col_key_offset, float lambda, double* loss,
+                     void* ws, size_t ws_bytes, void* stream);
+
+/* One ComplEx knowledge-graph-embedding step with negative sampling
+ * (Appendix C, "Knowledge graph embeddings").  Rows hold [Re | Im] of a
+ * complex vector of dim/2 components (dim must be even).  Triple t uses
+ * keys head[t], rel_key_offset + rel[t], tail[t]; neg[t*n_neg + j] replaces
+ * the head for j < n_head_neg and the tail otherwise.  Score
+ * phi = Re(sum_k s_k r_k conj(o_k)); loss softplus(-y phi), y = +1 for the
+ * true triple and -1 for each corrupted one.
+ * head, rel, tail: device int32[B]; neg: device int32[B*n_neg]. */
+ps_status ps_step_kge(ps_store* s, const int32_t* head, const int32_t* rel, const int32_t* tail,
+                      const int32_t* neg, int64_t B, int32_t n_neg, int32_t n_head_neg,
+                      int64_t rel_key_offset, double* loss, void* ws, size_t ws_bytes,
+                      void* stream);
+
+/* One skip-gram negative-sampling step (Appendix C, "Word vectors").
+ * Centre b has input key centre[b]; slot q < 2*window holds a context word
+ * ctx[b*2w + q] (-1 = no word, the slot is skipped) and n_neg negatives
+ * neg[(b*2w + q)*n_neg + k]; output keys are out_key_offset + word.  With
+ * x = <u, v_centre>: loss softplus(-x) for the context, softplus(x) for a
+ * negative; grad u = a v, grad v = sum a u with a = -sigmoid(-x) resp.
+ * sigmoid(x). */
+ps_status ps_step_sgns(ps_store* s, const int32_t* centre, const int32_t* ctx, const int32_t* neg,
+                       int64_t B, int32_t window, int32_t n_neg, int64_t out_key_offset,
+                       double* loss, void* ws, size_t ws_bytes, void* stream);
+
+/* One CTR embedding step (Appendix C, "Click-through-rate prediction",
+ * embedding part).  Sample b has F keys keys[b*F + f] and a label in {0,1}:
+ *   S = sum_f e_f,  z = sum_{f<g} <e_f, e_g>,  loss = softplus(z) - y z
+ *   grad e_f = (sigmoid(z) - y)(S - e_f)
+ * keys: device int64[B*F]; label: device float[B]. */
+ps_status ps_step_ctr(ps_store* s, const int64_t* keys, const float* label, int64_t B, int32_t F,
+                      double* loss, void* ws, size_t ws_bytes, void* stream);
+
+/* Synchronize `stream`, then return and clear the store's sticky device
+ * error (PS_OK or PS_ERR_KEY_RANGE). */
+ps_status ps_get_error(ps_store* s, void* stream);
+
+/* Static description of a status code. */
+const char* ps_status_string(ps_status st);
+
+/* Message of the last error raised on the calling thread ("" if none). */
+const char* ps_last_error_message(void);
+
+/* Kernel timing (instrumentation).  While enabled, the store brackets each
+ * launch of the listed kernels with HIP events on the launch stream.
+ * ps_read_timing() synchronizes those events and returns the summed
+ * duration (ms) and launch count of one kernel since the last reset, then
+ * resets it.  kernel_id: 0 = segmented reduce + AdaGrad, 1 = task gradient,
+ * 2 = radix scatter, 3 = pull. */
+#define PS_KERNEL_SEGREDUCE 0
+#define PS_KERNEL_TASKGRAD  1
+#define PS_KERNEL_SCATTER   2
+#define PS_KERNEL_PULL      3
+ps_status ps_set_timing(ps_store* s, int32_t enable);
+ps_status ps_read_timing(ps_store* s, int32_t kernel_id, double* total_ms, int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ADAPM_H */

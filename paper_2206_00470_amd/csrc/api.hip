@@ -1,0 +1,609 @@
+// C ABI of the gfx950 parameter store: argument checks, workspace layout and
+// the launch sequence of each call.  See include/adapm.h for the contract.
+#include "adapm.h"
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "common.hpp"
+#include "push.hpp"
+#include "sort.hpp"
+#include "tasks.hpp"
+
+using namespace adapm;
+
+// ======================================================================== errors
+namespace {
+
+thread_local std::string g_last_error;
+
+ps_status fail(ps_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+#define HIP_TRY(expr)                                                                        \
+  do {                                                                                       \
+    hipError_t e_ = (expr);                                                                  \
+    if (e_ != hipSuccess) return fail(PS_ERR_DEVICE, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+#define LAUNCHED(name) HIP_TRY(hipGetLastError())
+
+constexpr int64_t MAX_OCC = (int64_t(1) << 31) - (int64_t(1) << 20);
+constexpr int NUM_TIMED = 4;
+constexpr size_t MAX_TIMED_LAUNCHES = 1 << 14;
+
+}  // namespace
+
+// ======================================================================== store
+struct ps_store {
+  int64_t num_keys;
+  int32_t dim;
+  float* W;
+  float* G;
+  float lr;
+  float eps;
+  int32_t* status;   // device: [0] sticky key-range flag
+  bool timing = false;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> events[NUM_TIMED];
+  size_t used[NUM_TIMED] = {0, 0, 0, 0};
+};
+
+namespace {
+
+// Brackets one launch with HIP events on its stream while timing is enabled.
+struct Timed {
+  ps_store* s;
+  int id;
+  hipStream_t st;
+  hipEvent_t end = nullptr;
+  Timed(ps_store* s_, int id_, hipStream_t st_) : s(s_), id(id_), st(st_) {
+    if (!s || !s->timing || s->used[id] >= MAX_TIMED_LAUNCHES) return;
+    auto& v = s->events[id];
+    if (s->used[id] == v.size()) {
+      hipEvent_t a, b;
+      if (hipEventCreate(&a) != hipSuccess) return;
+      if (hipEventCreate(&b) != hipSuccess) {
+        (void)hipEventDestroy(a);
+        return;
+      }
+      v.emplace_back(a, b);
+    }
+    auto& pr = v[s->used[id]];
+    if (hipEventRecord(pr.first, st) != hipSuccess) return;
+    end = pr.second;
+  }
+  ~Timed() {
+    if (end && hipEventRecord(end, st) == hipSuccess) s->used[id] += 1;
+  }
+};
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// ------------------------------------------------------------------ row shapes
+bool row_shape(int dim, bool vec_ok, RowShape* s) {
+  if (dim <= 0) return false;
+  if (vec_ok && dim % 4 == 0) {
+    const int nvec = dim / 4;
+    s->VW = 4;
+    if (nvec <= 4) { s->L = 4; s->NV = 1; }
+    else if (nvec <= 8) { s->L = 8; s->NV = 1; }
+    else if (nvec <= 16) { s->L = 16; s->NV = 1; }
+    else if (nvec <= 32) { s->L = 32; s->NV = 1; }
+    else if (nvec <= 64) { s->L = 64; s->NV = 1; }
+    else if (nvec <= 128) { s->L = 64; s->NV = 2; }
+    else if (nvec <= 256) { s->L = 64; s->NV = 4; }
+    else if (nvec <= 512) { s->L = 64; s->NV = 8; }
+    else return false;
+    return true;
+  }
+  s->VW = 1;
+  s->L = 64;
+  if (dim <= 64) s->NV = 1;
+  else if (dim <= 128) s->NV = 2;
+  else if (dim <= 256) s->NV = 4;
+  else if (dim <= 512) s->NV = 8;
+  else return false;
+  return true;
+}
+
+template <class F>
+ps_status with_shape(const RowShape& s, F&& f) {
+#define ADAPM_SHAPE(L_, NV_, VW_) \
+  if (s.L == L_ && s.NV == NV_ && s.VW == VW_) return f.template operator()<L_, NV_, VW_>();
+  ADAPM_SHAPE(4, 1, 4)
+  ADAPM_SHAPE(8, 1, 4)
+  ADAPM_SHAPE(16, 1, 4)
+  ADAPM_SHAPE(32, 1, 4)
+  ADAPM_SHAPE(64, 1, 4)
+  ADAPM_SHAPE(64, 2, 4)
+  ADAPM_SHAPE(64, 4, 4)
+  ADAPM_SHAPE(64, 8, 4)
+  ADAPM_SHAPE(64, 1, 1)
+  ADAPM_SHAPE(64, 2, 1)
+  ADAPM_SHAPE(64, 4, 1)
+  ADAPM_SHAPE(64, 8, 1)
+#undef ADAPM_SHAPE
+  return fail(PS_ERR_UNSUPPORTED, "no kernel for row shape L=%d NV=%d VW=%d", s.L, s.NV, s.VW);
+}
+
+// ------------------------------------------------------------------ workspace
+struct Carver {
+  char* base;
+  size_t off = 0;
+  explicit Carver(void* b) : base(static_cast<char*>(b)) {}
+  template <class T>
+  T* take(size_t count) {
+    off = (off + 255) & ~size_t(255);
+    T* p = reinterpret_cast<T*>(base ? base + off : nullptr);
+    off += count * sizeof(T);
+    return p;
+  }
+};
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+RadixPlan radix_plan(int64_t num_keys) {
+  // the sentinel num_keys must be representable
+  int bits = 0;
+  while (bits < 32 && (uint64_t(1) << bits) <= uint64_t(num_keys)) ++bits;
+  RadixPlan p{};
+  p.passes = (bits + 7) / 8;
+  if (p.passes < 1) p.passes = 1;
+  const int per = (bits + p.passes - 1) / p.passes;
+  for (int i = 0; i < p.passes; ++i) {
+    p.shift[i] = i * per;
+    int b = bits - i * per;
+    p.bits[i] = b < per ? (b < 1 ? 1 : b) : per;
+  }
+  return p;
+}
+
+// Buffers of the sort + segment pipeline, carved from the workspace.
+struct SortBufs {
+  SegHeader* hdr;
+  uint32_t* ghist;        // [MAX_PASSES][MAX_BINS]
+  uint32_t* counts;       // [MAX_BINS][tiles]
+  uint32_t* k[2];
+  uint32_t* v[2];
+  uint32_t* rank;         // [n] (steps that scatter gradients to sorted order)
+  uint32_t* tstat;        // [3][tiles]
+  int32_t* seg_off;       // [n+1]
+  int32_t* chunk_start;   // [n+1]
+  int32_t* chunk_seg;     // [n]
+  int32_t* split_list;    // [n/CHUNK + 2]
+  double* partial;        // [2*(n/CHUNK+1)][dim]
+  int64_t tiles;
+};
+
+void carve_sort(Carver& c, int64_t n, int dim, bool want_rank, bool want_segments, SortBufs* b) {
+  b->tiles = ceil_div(n, TILE);
+  b->hdr = c.take<SegHeader>(16);   // header and histogram are cleared together
+  b->ghist = c.take<uint32_t>(MAX_PASSES * MAX_BINS);
+  b->counts = c.take<uint32_t>(size_t(MAX_BINS) * b->tiles);
+  b->k[0] = c.take<uint32_t>(n);
+  b->k[1] = c.take<uint32_t>(n);
+  b->v[0] = c.take<uint32_t>(n);
+  b->v[1] = c.take<uint32_t>(n);
+  b->rank = want_rank ? c.take<uint32_t>(n) : nullptr;
+  b->tstat = c.take<uint32_t>(3 * b->tiles);
+  b->seg_off = want_segments ? c.take<int32_t>(n + 1) : nullptr;
+  b->chunk_start = c.take<int32_t>(n + 1);
+  b->chunk_seg = c.take<int32_t>(n);
+  b->split_list = c.take<int32_t>(n / CHUNK + 2);
+  b->partial = c.take<double>(size_t(2) * (n / CHUNK + 1) * dim);
+}
+
+struct Plan {
+  SortBufs sb;
+  float* grads = nullptr;      // per-occurrence gradient rows (MF, CTR)
+  double* loss_part = nullptr;
+  size_t bytes = 0;
+};
+
+constexpr int64_t LOSS_GRID = 2048;
+
+bool plan_op(void* ws, int64_t num_keys, int dim, int op, int64_t units, int64_t per_unit, Plan* p) {
+  (void)num_keys;
+  const int64_t n = units * per_unit;
+  Carver c(ws);
+  switch (op) {
+    case PS_OP_PUSH:
+      carve_sort(c, n, dim, false, true, &p->sb);
+      break;
+    case PS_OP_DEDUP:
+      carve_sort(c, n, dim, false, false, &p->sb);
+      break;
+    case PS_OP_STEP_MF:
+    case PS_OP_STEP_CTR:
+      carve_sort(c, n, dim, true, true, &p->sb);
+      p->grads = c.take<float>(size_t(n) * dim);
+      p->loss_part = c.take<double>(LOSS_GRID);
+      break;
+    default:
+      return false;
+  }
+  p->bytes = c.off + 256;
+  return true;
+}
+
+// ------------------------------------------------------------------ pipeline pieces
+void clear_header(const SortBufs& b, hipStream_t st) {
+  const int64_t words = (reinterpret_cast<char*>(b.ghist + MAX_PASSES * MAX_BINS) -
+                         reinterpret_cast<char*>(b.hdr)) / 4;
+  hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(BLOCK), 0, st, reinterpret_cast<uint32_t*>(b.hdr), words);
+}
+
+// Stable radix sort of the keys produced by `ks`.  Returns the sorted keys;
+// the permutation ends in `perm_out` if given, else in a workspace buffer
+// (*perm).  With want_rank, b.rank receives the inverse permutation.
+template <class KS>
+ps_status run_sort(ps_store* s, KS ks, int64_t n, int64_t num_keys, SortBufs& b, int32_t* err,
+                   uint32_t* perm_out, bool want_rank, hipStream_t st, uint32_t** keys_sorted,
+                   uint32_t** perm) {
+  const RadixPlan plan = radix_plan(num_keys);
+  const int tiles = (int)b.tiles;
+  clear_header(b, st);
+  LAUNCHED(k_zero_words);
+  hipLaunchKernelGGL(k_keyprep<KS>, dim3(tiles), dim3(BLOCK), 0, st, ks, n, (uint32_t)num_keys, plan, b.k[0],
+                     b.counts, tiles, b.ghist, err);
+  LAUNCHED(k_keyprep);
+  int src = 0;
+  for (int p = 0; p < plan.passes; ++p) {
+    const int bins = 1 << plan.bits[p];
+    const bool last = p == plan.passes - 1;
+    if (p > 0) {
+      hipLaunchKernelGGL(k_radix_count, dim3(tiles), dim3(BLOCK), 0, st, b.k[src], n, plan.shift[p],
+                         plan.bits[p], b.counts, tiles);
+      LAUNCHED(k_radix_count);
+    }
+    hipLaunchKernelGGL(k_radix_scan, dim3(bins), dim3(BLOCK), 0, st, b.counts, tiles, b.ghist + p * MAX_BINS);
+    LAUNCHED(k_radix_scan);
+    uint32_t* vout = (last && perm_out) ? perm_out : b.v[1 - src];
+    uint32_t* rank = (last && want_rank) ? b.rank : nullptr;
+    Timed t(s, PS_KERNEL_SCATTER, st);
+    if (p == 0 && rank)
+      hipLaunchKernelGGL((k_radix_scatter<true, true>), dim3(tiles), dim3(BLOCK), 0, st, b.k[src], nullptr, n,
+                         plan.shift[p], plan.bits[p], b.counts, tiles, b.k[1 - src], vout, rank);
+    else if (p == 0)
+      hipLaunchKernelGGL((k_radix_scatter<true, false>), dim3(tiles), dim3(BLOCK), 0, st, b.k[src], nullptr, n,
+                         plan.shift[p], plan.bits[p], b.counts, tiles, b.k[1 - src], vout, nullptr);
+    else if (rank)
+      hipLaunchKernelGGL((k_radix_scatter<false, true>), dim3(tiles), dim3(BLOCK), 0, st, b.k[src], b.v[src], n,
+                         plan.shift[p], plan.bits[p], b.counts, tiles, b.k[1 - src], vout, rank);
+    else
+      hipLaunchKernelGGL((k_radix_scatter<false, false>), dim3(tiles), dim3(BLOCK), 0, st, b.k[src], b.v[src],
+                         n, plan.shift[p], plan.bits[p], b.counts, tiles, b.k[1 - src], vout, nullptr);
+    LAUNCHED(k_radix_scatter);
+    src = 1 - src;
+    if (last) *perm = vout;
+  }
+  *keys_sorted = b.k[src];
+  return PS_OK;
+}
+
+ps_status run_segments(const SortBufs& b, const uint32_t* ks, int64_t n, int64_t num_keys, int32_t* seg_off,
+                       int64_t* uniq64, hipStream_t st) {
+  const int tiles = (int)b.tiles;
+  hipLaunchKernelGGL(k_seg_count, dim3(tiles), dim3(BLOCK), 0, st, ks, n, (uint32_t)num_keys, b.tstat, tiles);
+  LAUNCHED(k_seg_count);
+  hipLaunchKernelGGL(k_seg_scan, dim3(1), dim3(BLOCK), 0, st, b.tstat, tiles, b.hdr, seg_off, b.chunk_start);
+  LAUNCHED(k_seg_scan);
+  hipLaunchKernelGGL(k_seg_write, dim3(tiles), dim3(BLOCK), 0, st, ks, n, (uint32_t)num_keys, b.tstat, tiles,
+                     seg_off, uniq64, b.chunk_start, b.chunk_seg);
+  LAUNCHED(k_seg_write);
+  return PS_OK;
+}
+
+int64_t reduce_grid(int64_t n, int L) {
+  const int64_t gpb = BLOCK / L;
+  int64_t g = ceil_div(n + n / CHUNK + 1, gpb);
+  if (g > 8192) g = 8192;
+  g = ceil_div(g, NUM_XCD) * NUM_XCD;
+  return g;
+}
+
+// Segmented fp64 reduce of the occurrences' gradients + AdaGrad, for keys in
+// [key_lo, key_hi), then the finalize pass for segments longer than a chunk.
+template <class Src>
+ps_status run_reduce(ps_store* s, const SortBufs& b, const uint32_t* ks, Src src, int64_t n, uint32_t key_lo,
+                     uint32_t key_hi, hipStream_t st) {
+  RowShape shape;
+  if (!row_shape(s->dim, true, &shape)) return fail(PS_ERR_UNSUPPORTED, "dim %d not supported", s->dim);
+  SegView sv{ks, b.seg_off, b.chunk_start, b.chunk_seg, b.hdr};
+  return with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
+    const int64_t grid = reduce_grid(n, L);
+    {
+      Timed t(s, PS_KERNEL_SEGREDUCE, st);
+      hipLaunchKernelGGL((k_segreduce<L, NV, VW, Src>), dim3(grid), dim3(BLOCK), 0, st, sv, src, s->W, s->G,
+                         s->dim, s->lr, s->eps, b.partial, b.split_list, b.hdr, key_lo, key_hi);
+    }
+    LAUNCHED(k_segreduce);
+    int64_t fgrid = n / CHUNK + 1;
+    if (fgrid > 1024) fgrid = 1024;
+    const size_t lds = size_t(BLOCK / L) * s->dim * sizeof(double);
+    hipLaunchKernelGGL((k_seg_finalize<L, NV, VW>), dim3(fgrid), dim3(BLOCK), lds, st, sv, s->W, s->G, s->dim,
+                       s->lr, s->eps, b.partial, b.split_list);
+    LAUNCHED(k_seg_finalize);
+    return PS_OK;
+  });
+}
+
+ps_status check_ws(const Plan& p, void* ws, size_t ws_bytes) {
+  if (!ws) return fail(PS_ERR_INVALID, "workspace pointer is NULL");
+  if (ws_bytes < p.bytes) return fail(PS_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, p.bytes);
+  return PS_OK;
+}
+
+ps_status check_store(const ps_store* s) {
+  if (!s) return fail(PS_ERR_INVALID, "store is NULL");
+  return PS_OK;
+}
+
+ps_status check_n(int64_t n, int64_t per_unit) {
+  if (n < 0) return fail(PS_ERR_INVALID, "negative size %lld", (long long)n);
+  if (per_unit > 0 && n > MAX_OCC / per_unit)
+    return fail(PS_ERR_UNSUPPORTED, "%lld units x %lld occurrences exceed the 32-bit occurrence index",
+                (long long)n, (long long)per_unit);
+  return PS_OK;
+}
+
+hipStream_t as_stream(void* p) { return static_cast<hipStream_t>(p); }
+
+}  // namespace
+
+// ======================================================================== C ABI
+extern "C" {
+
+const char* ps_status_string(ps_status st) {
+  switch (st) {
+    case PS_OK: return "ok";
+    case PS_ERR_INVALID: return "invalid argument";
+    case PS_ERR_KEY_RANGE: return "key outside [0, num_keys)";
+    case PS_ERR_WORKSPACE: return "workspace too small";
+    case PS_ERR_DEVICE: return "HIP runtime error";
+    case PS_ERR_UNSUPPORTED: return "unsupported size";
+    default: return "unknown status";
+  }
+}
+
+const char* ps_last_error_message(void) { return g_last_error.c_str(); }
+
+ps_status ps_create(ps_store** out, int64_t num_keys, int32_t dim, float* values, float* accum, float lr,
+                    float eps, void* stream) {
+  if (!out) return fail(PS_ERR_INVALID, "out is NULL");
+  *out = nullptr;
+  if (num_keys < 1 || num_keys > INT32_MAX) return fail(PS_ERR_INVALID, "num_keys %lld outside [1, 2^31-1]", (long long)num_keys);
+  RowShape shape;
+  if (dim < 1 || !row_shape(dim, true, &shape))
+    return fail(PS_ERR_UNSUPPORTED, "dim %d unsupported (<= 2048 if a multiple of 4, else <= 512)", dim);
+  if (!values || !accum) return fail(PS_ERR_INVALID, "table pointer is NULL");
+  if (values == accum) return fail(PS_ERR_INVALID, "values and accumulators alias");
+  if (dim % 4 == 0 && (!aligned16(values) || !aligned16(accum)))
+    return fail(PS_ERR_INVALID, "tables must be 16-byte aligned");
+  if (!(lr > 0.0f) || !(eps >= 0.0f)) return fail(PS_ERR_INVALID, "need lr > 0 and eps >= 0");
+  ps_store* s = new ps_store();
+  s->num_keys = num_keys;
+  s->dim = dim;
+  s->W = values;
+  s->G = accum;
+  s->lr = lr;
+  s->eps = eps;
+  hipError_t e = hipMalloc(&s->status, 256);
+  if (e != hipSuccess) {
+    delete s;
+    return fail(PS_ERR_DEVICE, "hipMalloc(status): %s", hipGetErrorString(e));
+  }
+  hipStream_t st = as_stream(stream);
+  hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(BLOCK), 0, st, reinterpret_cast<uint32_t*>(s->status), int64_t(64));
+  e = hipGetLastError();
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) {
+    (void)hipFree(s->status);
+    delete s;
+    return fail(PS_ERR_DEVICE, "status clear: %s", hipGetErrorString(e));
+  }
+  *out = s;
+  return PS_OK;
+}
+
+ps_status ps_destroy(ps_store* s) {
+  if (!s) return PS_OK;
+  hipError_t e = hipDeviceSynchronize();
+  for (auto& v : s->events)
+    for (auto& pr : v) {
+      (void)hipEventDestroy(pr.first);
+      (void)hipEventDestroy(pr.second);
+    }
+  hipError_t f = hipFree(s->status);
+  delete s;
+  if (e != hipSuccess) return fail(PS_ERR_DEVICE, "hipDeviceSynchronize: %s", hipGetErrorString(e));
+  if (f != hipSuccess) return fail(PS_ERR_DEVICE, "hipFree: %s", hipGetErrorString(f));
+  return PS_OK;
+}
+
+size_t ps_workspace_bytes(int64_t num_keys, int32_t dim, int32_t op, int64_t units, int64_t per_unit) {
+  if (num_keys < 1 || dim < 1 || units < 0 || per_unit < 1) return 0;
+  if (op == PS_OP_PULL) return 0;
+  if (units > MAX_OCC / per_unit) return 0;
+  Plan p;
+  if (!plan_op(nullptr, num_keys, dim, op, units, per_unit, &p)) return 0;
+  return p.bytes;
+}
+
+ps_status ps_pull(ps_store* s, const int64_t* keys, int64_t n, float* out, void* stream) {
+  if (ps_status st = check_store(s)) return st;
+  if (ps_status st = check_n(n, 1)) return st;
+  if (n == 0) return PS_OK;
+  if (!keys || !out) return fail(PS_ERR_INVALID, "keys or out is NULL");
+  RowShape shape;
+  row_shape(s->dim, aligned16(out), &shape);
+  hipStream_t st = as_stream(stream);
+  return with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
+    int64_t grid = ceil_div(n, BLOCK / L);
+    if (grid > 65536) grid = 65536;
+    Timed t(s, PS_KERNEL_PULL, st);
+    hipLaunchKernelGGL((k_pull<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->num_keys, s->dim, keys, n,
+                       out, s->status);
+    LAUNCHED(k_pull);
+    return PS_OK;
+  });
+}
+
+ps_status ps_push(ps_store* s, const int64_t* keys, int64_t n, const float* grads, void* ws, size_t ws_bytes,
+                  void* stream) {
+  if (ps_status st = check_store(s)) return st;
+  if (ps_status st = check_n(n, 1)) return st;
+  if (n == 0) return PS_OK;
+  if (!keys || !grads) return fail(PS_ERR_INVALID, "keys or grads is NULL");
+  if (s->dim % 4 == 0 && !aligned16(grads)) return fail(PS_ERR_INVALID, "grads must be 16-byte aligned");
+  Plan p;
+  plan_op(ws, s->num_keys, s->dim, PS_OP_PUSH, n, 1, &p);
+  if (ps_status st = check_ws(p, ws, ws_bytes)) return st;
+  hipStream_t st = as_stream(stream);
+  uint32_t *ks, *perm;
+  if (ps_status r = run_sort(s, KeysInt64{keys}, n, s->num_keys, p.sb, s->status, nullptr, false, st, &ks, &perm))
+    return r;
+  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st)) return r;
+  return run_reduce(s, p.sb, ks, SrcIndirect{grads, perm, s->dim}, n, 0u, (uint32_t)s->num_keys, st);
+}
+
+ps_status ps_dedup(int64_t num_keys, const int64_t* keys, int64_t n, int64_t* uniq, int32_t* perm,
+                   int32_t* offsets, int32_t* num_unique, int32_t* err, void* ws, size_t ws_bytes, void* stream) {
+  if (num_keys < 1 || num_keys > INT32_MAX) return fail(PS_ERR_INVALID, "num_keys %lld outside [1, 2^31-1]", (long long)num_keys);
+  if (ps_status st = check_n(n, 1)) return st;
+  if (!offsets || !num_unique) return fail(PS_ERR_INVALID, "offsets or num_unique is NULL");
+  hipStream_t st = as_stream(stream);
+  if (n == 0) {
+    hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(BLOCK), 0, st, reinterpret_cast<uint32_t*>(offsets), int64_t(1));
+    LAUNCHED(k_zero_words);
+    hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(BLOCK), 0, st, reinterpret_cast<uint32_t*>(num_unique), int64_t(1));
+    LAUNCHED(k_zero_words);
+    return PS_OK;
+  }
+  if (!keys || !uniq || !perm) return fail(PS_ERR_INVALID, "keys, uniq or perm is NULL");
+  Plan p;
+  plan_op(ws, num_keys, 1, PS_OP_DEDUP, n, 1, &p);
+  if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
+  uint32_t *ks, *pm;
+  if (ps_status r = run_sort(nullptr, KeysInt64{keys}, n, num_keys, p.sb, err, reinterpret_cast<uint32_t*>(perm),
+                             false, st, &ks, &pm))
+    return r;
+  if (ps_status r = run_segments(p.sb, ks, n, num_keys, offsets, uniq, st)) return r;
+  HIP_TRY(hipMemcpyAsync(num_unique, &p.sb.hdr->num_unique, sizeof(int32_t), hipMemcpyDeviceToDevice, st));
+  return PS_OK;
+}
+
+ps_status ps_step_mf(ps_store* s, const int32_t* row, const int32_t* col, const float* val, int64_t B,
+                     int64_t col_key_offset, float lambda, double* loss, void* ws, size_t ws_bytes, void* stream) {
+  if (ps_status st = check_store(s)) return st;
+  if (ps_status st = check_n(B, 2)) return st;
+  hipStream_t st = as_stream(stream);
+  if (B == 0) {
+    if (loss) {
+      hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(BLOCK), 0, st, reinterpret_cast<uint32_t*>(loss), int64_t(2));
+      LAUNCHED(k_zero_words);
+    }
+    return PS_OK;
+  }
+  if (!row || !col || !val) return fail(PS_ERR_INVALID, "row, col or val is NULL");
+  if (col_key_offset < 0) return fail(PS_ERR_INVALID, "negative col_key_offset");
+  const int64_t n = 2 * B;
+  Plan p;
+  plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_MF, B, 2, &p);
+  if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
+  uint32_t *ks, *perm;
+  KeysMF kmf{row, col, col_key_offset, s->num_keys};
+  if (ps_status r = run_sort(s, kmf, n, s->num_keys, p.sb, s->status, nullptr, true, st, &ks, &perm)) return r;
+  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st)) return r;
+  RowShape shape;
+  row_shape(s->dim, true, &shape);
+  ps_status r = with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
+    int64_t grid = ceil_div(B, BLOCK / L);
+    if (grid > LOSS_GRID) grid = LOSS_GRID;
+    {
+      Timed t(s, PS_KERNEL_TASKGRAD, st);
+      hipLaunchKernelGGL((k_mf_grad<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->num_keys, s->dim, row,
+                         col, val, B, col_key_offset, lambda, p.sb.rank, p.grads, p.loss_part);
+    }
+    LAUNCHED(k_mf_grad);
+    if (loss) {
+      hipLaunchKernelGGL(k_sum_loss, dim3(1), dim3(BLOCK), 0, st, p.loss_part, grid, loss);
+      LAUNCHED(k_sum_loss);
+    }
+    return PS_OK;
+  });
+  if (r) return r;
+  return run_reduce(s, p.sb, ks, SrcSorted{p.grads, s->dim}, n, 0u, (uint32_t)s->num_keys, st);
+}
+
+ps_status ps_step_kge(ps_store* s, const int32_t* head, const int32_t* rel, const int32_t* tail, const int32_t* neg,
+                      int64_t B, int32_t n_neg, int32_t n_head_neg, int64_t rel_key_offset, double* loss, void* ws,
+                      size_t ws_bytes, void* stream) {
+  (void)s; (void)head; (void)rel; (void)tail; (void)neg; (void)B; (void)n_neg; (void)n_head_neg;
+  (void)rel_key_offset; (void)loss; (void)ws; (void)ws_bytes; (void)stream;
+  return fail(PS_ERR_UNSUPPORTED, "ps_step_kge not built yet");
+}
+
+ps_status ps_step_sgns(ps_store* s, const int32_t* centre, const int32_t* ctx, const int32_t* neg, int64_t B,
+                       int32_t window, int32_t n_neg, int64_t out_key_offset, double* loss, void* ws,
+                       size_t ws_bytes, void* stream) {
+  (void)s; (void)centre; (void)ctx; (void)neg; (void)B; (void)window; (void)n_neg; (void)out_key_offset;
+  (void)loss; (void)ws; (void)ws_bytes; (void)stream;
+  return fail(PS_ERR_UNSUPPORTED, "ps_step_sgns not built yet");
+}
+
+ps_status ps_step_ctr(ps_store* s, const int64_t* keys, const float* label, int64_t B, int32_t F, double* loss,
+                      void* ws, size_t ws_bytes, void* stream) {
+  (void)s; (void)keys; (void)label; (void)B; (void)F; (void)loss; (void)ws; (void)ws_bytes; (void)stream;
+  return fail(PS_ERR_UNSUPPORTED, "ps_step_ctr not built yet");
+}
+
+ps_status ps_get_error(ps_store* s, void* stream) {
+  if (ps_status st = check_store(s)) return st;
+  HIP_TRY(hipStreamSynchronize(as_stream(stream)));
+  int32_t flag = 0;
+  HIP_TRY(hipMemcpy(&flag, s->status, sizeof flag, hipMemcpyDeviceToHost));
+  if (flag) {
+    HIP_TRY(hipMemset(s->status, 0, sizeof flag));
+    HIP_TRY(hipDeviceSynchronize());
+    return fail(PS_ERR_KEY_RANGE, "a key outside [0, %lld) was seen", (long long)s->num_keys);
+  }
+  return PS_OK;
+}
+
+ps_status ps_set_timing(ps_store* s, int32_t enable) {
+  if (ps_status st = check_store(s)) return st;
+  s->timing = enable != 0;
+  return PS_OK;
+}
+
+ps_status ps_read_timing(ps_store* s, int32_t kernel_id, double* total_ms, int64_t* launches) {
+  if (ps_status st = check_store(s)) return st;
+  if (kernel_id < 0 || kernel_id >= NUM_TIMED || !total_ms || !launches)
+    return fail(PS_ERR_INVALID, "bad kernel id or output pointer");
+  double tot = 0.0;
+  auto& v = s->events[kernel_id];
+  for (size_t i = 0; i < s->used[kernel_id]; ++i) {
+    HIP_TRY(hipEventSynchronize(v[i].second));
+    float ms = 0.0f;
+    HIP_TRY(hipEventElapsedTime(&ms, v[i].first, v[i].second));
+    tot += ms;
+  }
+  *total_ms = tot;
+  *launches = (int64_t)s->used[kernel_id];
+  s->used[kernel_id] = 0;
+  return PS_OK;
+}
+
+}  // extern "C"

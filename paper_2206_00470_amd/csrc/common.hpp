@@ -1,0 +1,148 @@
+// Shared device helpers and constants of the gfx950 parameter-store kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace adapm {
+
+constexpr int WAVE = 64;                 // CDNA wavefront width
+constexpr int BLOCK = 256;               // threads per workgroup for every kernel here
+constexpr int WAVES_PER_BLOCK = BLOCK / WAVE;
+constexpr int SORT_ITEMS = 16;           // keys per thread in the radix tiles
+constexpr int TILE = BLOCK * SORT_ITEMS; // keys per radix tile (4096)
+constexpr int MAX_PASSES = 4;            // 32-bit keys, at most 8 bits per pass
+constexpr int MAX_BINS = 256;
+constexpr int CHUNK = 128;               // longest run of occurrences one group reduces alone
+constexpr int NUM_XCD = 8;               // MI355X: 8 accelerator dies, each with its own L2
+constexpr int64_t ABSENT = INT64_MIN;    // a key source's "no occurrence here" marker
+
+// Device-side counters written by the segment kernels and read by the
+// reduce kernels, so that no host round trip is needed to size grids.
+struct SegHeader {
+  uint32_t num_unique;   // U: distinct valid keys
+  uint32_t num_chunks;   // reduce work items
+  uint32_t num_valid;    // occurrences with a valid key (a prefix of the sorted order)
+  uint32_t num_split;    // segments longer than one chunk, listed for the finalize pass
+};
+
+// ------------------------------------------------------------------ lanes
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+__device__ __forceinline__ uint64_t lanemask_lt() {
+  const int l = lane_id();
+  return l == 0 ? 0ull : (~0ull >> (64 - l));
+}
+
+// Butterfly sum over aligned groups of L lanes (L a power of two <= 64).
+// Every lane of the group ends with the same value: a+b and b+a round alike.
+template <int L>
+__device__ __forceinline__ double group_sum(double v) {
+#pragma unroll
+  for (int o = L / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, L);
+  return v;
+}
+
+// ------------------------------------------------------------------ block scan
+// Exclusive scan of one uint32 per thread over a 256-thread block; returns the
+// thread's exclusive prefix and writes the block total to *total.
+// `smem` needs WAVES_PER_BLOCK + 1 words.
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t x, uint32_t* smem, uint32_t* total) {
+  const int lane = lane_id();
+  const int w = threadIdx.x / WAVE;
+  uint32_t inc = x;
+#pragma unroll
+  for (int o = 1; o < WAVE; o <<= 1) {
+    uint32_t y = __shfl_up(inc, o, WAVE);
+    if (lane >= o) inc += y;
+  }
+  if (lane == WAVE - 1) smem[w] = inc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t run = 0;
+    for (int i = 0; i < WAVES_PER_BLOCK; ++i) {
+      uint32_t t = smem[i];
+      smem[i] = run;
+      run += t;
+    }
+    smem[WAVES_PER_BLOCK] = run;
+  }
+  __syncthreads();
+  uint32_t res = smem[w] + inc - x;
+  *total = smem[WAVES_PER_BLOCK];
+  __syncthreads();
+  return res;
+}
+
+// Sum of one double per thread over the block (fixed order: waves, then
+// wave totals in wave order), result valid in thread 0.
+__device__ __forceinline__ double block_sum_double(double v, double* smem) {
+  v = group_sum<WAVE>(v);
+  const int w = threadIdx.x / WAVE;
+  if (lane_id() == 0) smem[w] = v;
+  __syncthreads();
+  double r = 0.0;
+  if (threadIdx.x == 0) {
+    for (int i = 0; i < WAVES_PER_BLOCK; ++i) r += smem[i];
+  }
+  __syncthreads();
+  return r;
+}
+
+// ------------------------------------------------------------------ AdaGrad
+// One element, fp32, in the fixed order G' = G + g*g; W' = W - lr*(g/(sqrt(G')+eps)).
+// Built with -ffp-contract=off and correctly rounded sqrt/div, so each
+// operation rounds once exactly as written.
+__device__ __forceinline__ void adagrad_elem(float& w, float& acc, float g, float lr, float eps) {
+  float t = g * g;
+  float a = acc + t;
+  float s = __builtin_sqrtf(a);
+  float den = s + eps;
+  float q = g / den;
+  float step = lr * q;
+  acc = a;
+  w = w - step;
+}
+
+// ------------------------------------------------------------------ row fragments
+// A group of L lanes covers one row of `dim` floats: lane `gl` owns the
+// VW-wide vectors at columns (gl + v*L)*VW for v < NV.
+template <int VW> struct vec_t;
+template <> struct vec_t<1> { using type = float; };
+template <> struct vec_t<2> { using type = float2; };
+template <> struct vec_t<4> { using type = float4; };
+
+template <int VW>
+__device__ __forceinline__ void load_frag(const float* p, float* out) {
+  if constexpr (VW == 4) {
+    float4 x = *reinterpret_cast<const float4*>(p);
+    out[0] = x.x; out[1] = x.y; out[2] = x.z; out[3] = x.w;
+  } else if constexpr (VW == 2) {
+    float2 x = *reinterpret_cast<const float2*>(p);
+    out[0] = x.x; out[1] = x.y;
+  } else {
+    out[0] = *p;
+  }
+}
+
+template <int VW>
+__device__ __forceinline__ void store_frag(float* p, const float* in) {
+  if constexpr (VW == 4) {
+    *reinterpret_cast<float4*>(p) = make_float4(in[0], in[1], in[2], in[3]);
+  } else if constexpr (VW == 2) {
+    *reinterpret_cast<float2*>(p) = make_float2(in[0], in[1]);
+  } else {
+    *p = in[0];
+  }
+}
+
+// Non-temporal fragment store for streams that are read back only once.
+template <int VW>
+__device__ __forceinline__ void store_frag_nt(float* p, const float* in) {
+#pragma unroll
+  for (int e = 0; e < VW; ++e) __builtin_nontemporal_store(in[e], p + e);
+}
+
+}  // namespace adapm

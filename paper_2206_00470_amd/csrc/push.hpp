@@ -1,0 +1,248 @@
+// Read access (pull) and merged write access (segmented reduce + AdaGrad).
+//
+// Work is mapped to "groups" of L lanes, one group per row: L is the power of
+// two that covers dim/VW vectors (VW = 4 floats when dim % 4 == 0), so a
+// 400-byte MF row is one 16-byte load per lane of a 32-lane half-wave and a
+// wavefront serves two rows at once.
+#pragma once
+
+#include "common.hpp"
+
+namespace adapm {
+
+struct RowShape {
+  int L;    // lanes per row group
+  int NV;   // vectors per lane
+  int VW;   // floats per vector
+};
+
+// ------------------------------------------------------------------ pull
+template <int L, int NV, int VW>
+__global__ __launch_bounds__(BLOCK) void k_pull(const float* __restrict__ W, int64_t num_keys, int dim,
+                                                const int64_t* __restrict__ keys, int64_t n,
+                                                float* __restrict__ out, int32_t* __restrict__ err) {
+  constexpr int GPB = BLOCK / L;
+  const int gl = threadIdx.x % L;
+  int bad = 0;
+  for (int64_t i = (int64_t)blockIdx.x * GPB + threadIdx.x / L; i < n; i += (int64_t)gridDim.x * GPB) {
+    const int64_t key = keys[i];
+    const bool ok = key >= 0 && key < num_keys;
+    bad |= !ok;
+    const float* src = W + (ok ? key : 0) * (int64_t)dim;
+    float* dst = out + i * (int64_t)dim;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int c = (gl + v * L) * VW;
+      if (c < dim) {
+        float x[VW];
+        if (ok) load_frag<VW>(src + c, x);
+        else
+#pragma unroll
+          for (int e = 0; e < VW; ++e) x[e] = 0.0f;
+        store_frag<VW>(dst + c, x);
+      }
+    }
+  }
+  if (__syncthreads_or(bad) && threadIdx.x == 0) atomicOr(err, 1);
+}
+
+// ------------------------------------------------------------------ gradient sources
+// A source yields the fp32 gradient fragment of the occurrence at sorted
+// position j (the fragment of lane gl of its row group).
+
+// Gradient rows in occurrence order, read through the sort permutation.
+struct SrcIndirect {
+  const float* grads;
+  const uint32_t* perm;
+  int dim;
+  template <int L, int NV, int VW>
+  __device__ __forceinline__ void load(int64_t j, int gl, float* x) const {
+    const float* row = grads + (int64_t)perm[j] * dim;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int c = (gl + v * L) * VW;
+      if (c < dim) load_frag<VW>(row + c, x + v * VW);
+    }
+  }
+};
+
+// Gradient rows already stored at their sorted positions.
+struct SrcSorted {
+  const float* grads;
+  int dim;
+  template <int L, int NV, int VW>
+  __device__ __forceinline__ void load(int64_t j, int gl, float* x) const {
+    const float* row = grads + j * dim;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int c = (gl + v * L) * VW;
+      if (c < dim) load_frag<VW>(row + c, x + v * VW);
+    }
+  }
+};
+
+// ------------------------------------------------------------------ reduce
+struct SegView {
+  const uint32_t* keys;        // sorted u32 keys
+  const int32_t* seg_off;      // [U+1]
+  const int32_t* chunk_start;  // [nchunks+1]
+  const int32_t* chunk_seg;    // [nchunks]
+  const SegHeader* hdr;
+};
+
+// Map a workgroup index to a group-slot so that consecutive work items stay
+// on one accelerator die (workgroups are dealt round-robin over the 8 dies,
+// each with its own L2): die x gets the x-th contiguous slice of the slots.
+__device__ __forceinline__ int64_t xcd_slot(int64_t block, int64_t nblocks) {
+  if (nblocks % NUM_XCD != 0) return block;
+  const int64_t per = nblocks / NUM_XCD;
+  return (block % NUM_XCD) * per + block / NUM_XCD;
+}
+
+// Chunk c covers sorted positions [chunk_start[c], chunk_start[c+1]) of one
+// segment.  The group sums its gradient rows in position order in fp64.  If
+// the chunk is the whole segment it rounds the sum to fp32 and applies
+// AdaGrad to the key's row; otherwise it stores the fp64 partial in the slot
+// of its CHUNK-aligned block (2 slots per block: the chunk starting at the
+// block start, and the one starting inside it) for k_seg_finalize; the
+// first chunk of such a segment also appends the segment to split_list.
+template <int L, int NV, int VW, class Src>
+__global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, float* __restrict__ W,
+                                                     float* __restrict__ G, int dim, float lr, float eps,
+                                                     double* __restrict__ partial,
+                                                     int32_t* __restrict__ split_list, SegHeader* split_hdr,
+                                                     uint32_t key_lo, uint32_t key_hi) {
+  constexpr int GPB = BLOCK / L;
+  constexpr int NE = NV * VW;
+  constexpr int UNROLL = NE <= 4 ? 8 : 4;
+  const int gl = threadIdx.x % L;
+  const int64_t nchunks = sv.hdr->num_chunks;
+  const int64_t stride = (int64_t)gridDim.x * GPB;
+  for (int64_t c = xcd_slot(blockIdx.x, gridDim.x) * GPB + threadIdx.x / L; c < nchunks; c += stride) {
+    const int64_t j0 = sv.chunk_start[c];
+    const int64_t j1 = sv.chunk_start[c + 1];
+    const uint32_t key = sv.keys[j0];
+    if (key < key_lo || key >= key_hi) continue;
+    const int32_t u = sv.chunk_seg[c];
+    const int64_t s0 = sv.seg_off[u];
+    const int64_t s1 = sv.seg_off[u + 1];
+    const bool whole = (j0 == s0) && (j1 == s1);
+    float* wrow = W + (int64_t)key * dim;
+    float* grow = G + (int64_t)key * dim;
+    float wv[NE], gv[NE];
+    if (whole) {   // issue the table reads early, they do not depend on the sum
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int col = (gl + v * L) * VW;
+        if (col < dim) {
+          load_frag<VW>(wrow + col, wv + v * VW);
+          load_frag<VW>(grow + col, gv + v * VW);
+        }
+      }
+    }
+    double acc[NE];
+#pragma unroll
+    for (int e = 0; e < NE; ++e) acc[e] = 0.0;
+    int64_t j = j0;
+    for (; j + UNROLL <= j1; j += UNROLL) {
+      float x[UNROLL][NE];
+#pragma unroll
+      for (int q = 0; q < UNROLL; ++q) src.template load<L, NV, VW>(j + q, gl, x[q]);
+#pragma unroll
+      for (int q = 0; q < UNROLL; ++q)
+#pragma unroll
+        for (int e = 0; e < NE; ++e) acc[e] += (double)x[q][e];
+    }
+    for (; j < j1; ++j) {
+      float x[NE];
+      src.template load<L, NV, VW>(j, gl, x);
+#pragma unroll
+      for (int e = 0; e < NE; ++e) acc[e] += (double)x[e];
+    }
+    if (whole) {
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int col = (gl + v * L) * VW;
+        if (col < dim) {
+#pragma unroll
+          for (int e = 0; e < VW; ++e)
+            adagrad_elem(wv[v * VW + e], gv[v * VW + e], (float)acc[v * VW + e], lr, eps);
+          store_frag<VW>(wrow + col, wv + v * VW);
+          store_frag<VW>(grow + col, gv + v * VW);
+        }
+      }
+    } else {
+      if (j0 == s0 && gl == 0) split_list[atomicAdd(&split_hdr->num_split, 1u)] = u;
+      const int64_t slot = 2 * (j0 / CHUNK) + ((j0 % CHUNK) != 0);
+      double* p = partial + slot * dim;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int col = (gl + v * L) * VW;
+        if (col < dim)
+#pragma unroll
+          for (int e = 0; e < VW; ++e) p[col + e] = acc[v * VW + e];
+      }
+    }
+  }
+}
+
+// Segments longer than one chunk: one workgroup per split segment (listed by
+// k_segreduce).  Its BLOCK/L row groups each add every (BLOCK/L)-th chunk
+// partial in order, the group results are added in group order, rounded once
+// and applied with AdaGrad.  The order is fixed, so the result is
+// deterministic.
+template <int L, int NV, int VW>
+__global__ __launch_bounds__(BLOCK) void k_seg_finalize(SegView sv, float* __restrict__ W, float* __restrict__ G,
+                                                        int dim, float lr, float eps,
+                                                        const double* __restrict__ partial,
+                                                        const int32_t* __restrict__ split_list) {
+  constexpr int GPB = BLOCK / L;
+  constexpr int NE = NV * VW;
+  extern __shared__ double lds[];   // [GPB][dim]
+  const int gl = threadIdx.x % L;
+  const int g = threadIdx.x / L;
+  const int64_t nsplit = sv.hdr->num_split;
+  for (int64_t e = blockIdx.x; e < nsplit; e += gridDim.x) {
+    const int32_t u = split_list[e];
+    const int64_t s0 = sv.seg_off[u];
+    const int64_t s1 = sv.seg_off[u + 1];
+    const uint32_t key = sv.keys[s0];
+    const int64_t b0 = s0 / CHUNK;
+    const int64_t m = (s1 - 1) / CHUNK - b0 + 1;   // number of chunk partials
+    double acc[NE];
+#pragma unroll
+    for (int q = 0; q < NE; ++q) acc[q] = 0.0;
+    for (int64_t k = g; k < m; k += GPB) {
+      const int64_t slot = k == 0 ? 2 * b0 + ((s0 % CHUNK) != 0) : 2 * (b0 + k);
+      const double* p = partial + slot * dim;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int col = (gl + v * L) * VW;
+        if (col < dim)
+#pragma unroll
+          for (int q = 0; q < VW; ++q) acc[v * VW + q] += p[col + q];
+      }
+    }
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int col = (gl + v * L) * VW;
+      if (col < dim)
+#pragma unroll
+        for (int q = 0; q < VW; ++q) lds[g * dim + col + q] = acc[v * VW + q];
+    }
+    __syncthreads();
+    float* wrow = W + (int64_t)key * dim;
+    float* grow = G + (int64_t)key * dim;
+    for (int col = threadIdx.x; col < dim; col += BLOCK) {
+      double s = 0.0;
+      for (int gg = 0; gg < GPB; ++gg) s += lds[gg * dim + col];
+      float w = wrow[col], a = grow[col];
+      adagrad_elem(w, a, (float)s, lr, eps);
+      wrow[col] = w;
+      grow[col] = a;
+    }
+    __syncthreads();
+  }
+}
+
+}  // namespace adapm

@@ -1,0 +1,175 @@
+"""Python front end of the parameter store: torch tensors in, C ABI calls out.
+
+Only argument marshalling happens here (pointers, sizes, the current HIP
+stream, a cached workspace tensor); every step of the computation runs in
+the HIP kernels of ``libadapm_hip.so``.
+"""
+from __future__ import annotations
+
+import ctypes as C
+
+import torch
+
+from . import _lib
+from ._lib import check, lib
+
+
+def _ptr(t):
+    return C.c_void_p(t.data_ptr()) if t is not None else C.c_void_p(0)
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return C.c_void_p(s.cuda_stream)
+
+
+def _dev(t: torch.Tensor, dtype, name: str):
+    if not (t.is_cuda and t.dtype == dtype and t.is_contiguous()):
+        raise TypeError(f"{name} must be a contiguous {dtype} CUDA tensor")
+    return t
+
+
+class Workspace:
+    """A device byte buffer that grows to the largest request seen."""
+
+    def __init__(self, device):
+        self.device = device
+        self.buf = None
+
+    def get(self, nbytes: int):
+        if nbytes == 0:
+            return C.c_void_p(0), 0
+        if self.buf is None or self.buf.numel() < nbytes:
+            self.buf = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        return C.c_void_p(self.buf.data_ptr()), self.buf.numel()
+
+
+class Store:
+    """A parameter store over caller-owned tables W (values) and G (AdaGrad
+    accumulators), float32 [num_keys, dim] CUDA tensors."""
+
+    def __init__(self, W: torch.Tensor, G: torch.Tensor, lr: float = 0.1, eps: float = 1e-10, stream=None):
+        _dev(W, torch.float32, "W")
+        _dev(G, torch.float32, "G")
+        if W.shape != G.shape or W.dim() != 2:
+            raise ValueError("W and G must be [num_keys, dim] tensors of one shape")
+        self.W, self.G = W, G
+        self.num_keys, self.dim = W.shape
+        self.lr, self.eps = lr, eps
+        self.ws = Workspace(W.device)
+        h = C.c_void_p()
+        check(lib().ps_create(C.byref(h), self.num_keys, self.dim, _ptr(W), _ptr(G), lr, eps, _stream(stream)))
+        self._h = h
+
+    def close(self):
+        if getattr(self, "_h", None):
+            check(lib().ps_destroy(self._h))
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # ---------------------------------------------------------------- sizing
+    def workspace_bytes(self, op: int, units: int, per_unit: int = 1) -> int:
+        return int(lib().ps_workspace_bytes(self.num_keys, self.dim, op, units, per_unit))
+
+    def _ws(self, op, units, per_unit):
+        return self.ws.get(self.workspace_bytes(op, units, per_unit))
+
+    # ---------------------------------------------------------------- read / write
+    def pull(self, keys: torch.Tensor, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        _dev(keys, torch.int64, "keys")
+        n = keys.numel()
+        if out is None:
+            out = torch.empty((n, self.dim), dtype=torch.float32, device=self.W.device)
+        _dev(out, torch.float32, "out")
+        check(lib().ps_pull(self._h, _ptr(keys), n, _ptr(out), _stream(stream)))
+        return out
+
+    def push(self, keys: torch.Tensor, grads: torch.Tensor, stream=None):
+        _dev(keys, torch.int64, "keys")
+        _dev(grads, torch.float32, "grads")
+        n = keys.numel()
+        if grads.numel() != n * self.dim:
+            raise ValueError("grads must hold n*dim floats")
+        ws, wsb = self._ws(_lib.PS_OP_PUSH, n, 1)
+        check(lib().ps_push(self._h, _ptr(keys), n, _ptr(grads), ws, wsb, _stream(stream)))
+
+    # ---------------------------------------------------------------- task steps
+    def _loss(self, loss):
+        if loss is None:
+            loss = torch.empty(1, dtype=torch.float64, device=self.W.device)
+        return _dev(loss, torch.float64, "loss")
+
+    def step_mf(self, row, col, val, col_key_offset: int, lam: float, loss=None, stream=None):
+        _dev(row, torch.int32, "row"), _dev(col, torch.int32, "col"), _dev(val, torch.float32, "val")
+        B = row.numel()
+        loss = self._loss(loss)
+        ws, wsb = self._ws(_lib.PS_OP_STEP_MF, B, 2)
+        check(lib().ps_step_mf(self._h, _ptr(row), _ptr(col), _ptr(val), B, col_key_offset, lam, _ptr(loss),
+                               ws, wsb, _stream(stream)))
+        return loss
+
+    def step_kge(self, head, rel, tail, neg, n_head_neg: int, rel_key_offset: int, loss=None, stream=None):
+        for t, nm in ((head, "head"), (rel, "rel"), (tail, "tail"), (neg, "neg")):
+            _dev(t, torch.int32, nm)
+        B = head.numel()
+        n_neg = neg.numel() // B if B else 0
+        loss = self._loss(loss)
+        ws, wsb = self._ws(_lib.PS_OP_STEP_KGE, B, 3 + n_neg)
+        check(lib().ps_step_kge(self._h, _ptr(head), _ptr(rel), _ptr(tail), _ptr(neg), B, n_neg, n_head_neg,
+                                rel_key_offset, _ptr(loss), ws, wsb, _stream(stream)))
+        return loss
+
+    def step_sgns(self, centre, ctx, neg, window: int, out_key_offset: int, loss=None, stream=None):
+        for t, nm in ((centre, "centre"), (ctx, "ctx"), (neg, "neg")):
+            _dev(t, torch.int32, nm)
+        B = centre.numel()
+        n_neg = neg.numel() // (B * 2 * window) if B else 0
+        loss = self._loss(loss)
+        ws, wsb = self._ws(_lib.PS_OP_STEP_SGNS, B, 1 + 2 * window * (1 + n_neg))
+        check(lib().ps_step_sgns(self._h, _ptr(centre), _ptr(ctx), _ptr(neg), B, window, n_neg, out_key_offset,
+                                 _ptr(loss), ws, wsb, _stream(stream)))
+        return loss
+
+    def step_ctr(self, keys, label, loss=None, stream=None):
+        _dev(keys, torch.int64, "keys"), _dev(label, torch.float32, "label")
+        B = label.numel()
+        F = keys.numel() // B if B else 0
+        loss = self._loss(loss)
+        ws, wsb = self._ws(_lib.PS_OP_STEP_CTR, B, max(F, 1))
+        check(lib().ps_step_ctr(self._h, _ptr(keys), _ptr(label), B, F, _ptr(loss), ws, wsb, _stream(stream)))
+        return loss
+
+    # ---------------------------------------------------------------- status and timing
+    def error(self, stream=None) -> int:
+        """Synchronize, then return and clear the sticky device status."""
+        return int(lib().ps_get_error(self._h, _stream(stream)))
+
+    def set_timing(self, on: bool):
+        check(lib().ps_set_timing(self._h, 1 if on else 0))
+
+    def read_timing(self, kernel_id: int):
+        ms, n = C.c_double(0.0), C.c_int64(0)
+        check(lib().ps_read_timing(self._h, kernel_id, C.byref(ms), C.byref(n)))
+        return ms.value, n.value
+
+
+def dedup(num_keys: int, keys: torch.Tensor, err: torch.Tensor | None = None, stream=None):
+    """Stable duplicate-key merge order of `keys`: (uniq, perm, offsets, U)."""
+    _dev(keys, torch.int64, "keys")
+    n = keys.numel()
+    dev = keys.device
+    uniq = torch.empty(max(n, 1), dtype=torch.int64, device=dev)
+    perm = torch.empty(max(n, 1), dtype=torch.int32, device=dev)
+    offs = torch.empty(n + 1, dtype=torch.int32, device=dev)
+    nu = torch.empty(1, dtype=torch.int32, device=dev)
+    nbytes = int(lib().ps_workspace_bytes(num_keys, 1, _lib.PS_OP_DEDUP, n, 1)) if n else 0
+    ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    check(lib().ps_dedup(num_keys, _ptr(keys), n, _ptr(uniq), _ptr(perm), _ptr(offs), _ptr(nu), _ptr(err),
+                         _ptr(ws), nbytes, _stream(stream)))
+    U = int(nu.item())
+    return uniq[:U], perm[:n], offs[:U + 1], U

@@ -1,0 +1,102 @@
+"""The C ABI without a GPU: the library loads, exports every declared entry
+point, and rejects bad arguments on the host before touching the device."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2206_00470_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "adapm.h")
+
+
+def declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ps_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared()
+    for n in ("ps_create", "ps_destroy", "ps_pull", "ps_push", "ps_dedup", "ps_step_mf", "ps_step_kge",
+              "ps_step_sgns", "ps_step_ctr", "ps_get_error", "ps_workspace_bytes"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    L = _lib.lib()
+    for n in declared():
+        assert hasattr(L, n), n
+
+
+def test_binding_covers_every_declared_symbol():
+    assert sorted(_lib.SIGNATURES) == declared()
+
+
+def test_status_strings():
+    L = _lib.lib()
+    for st in (0, -1, -2, -3, -4, -5):
+        assert L.ps_status_string(st)
+    assert L.ps_status_string(-99) == b"unknown status"
+
+
+def test_create_rejects_bad_arguments_on_host():
+    L = _lib.lib()
+    h = C.c_void_p(1)
+    fake = C.c_void_p(0x1000)
+    other = C.c_void_p(0x2000)
+    assert L.ps_create(None, 10, 4, fake, other, 0.1, 0.0, None) == _lib.PS_ERR_INVALID
+    assert L.ps_create(C.byref(h), 0, 4, fake, other, 0.1, 0.0, None) == _lib.PS_ERR_INVALID
+    assert h.value is None
+    assert L.ps_create(C.byref(h), 10, 0, fake, other, 0.1, 0.0, None) == _lib.PS_ERR_UNSUPPORTED
+    assert L.ps_create(C.byref(h), 10, 4096, fake, other, 0.1, 0.0, None) == _lib.PS_ERR_UNSUPPORTED
+    assert L.ps_create(C.byref(h), 10, 513, fake, other, 0.1, 0.0, None) == _lib.PS_ERR_UNSUPPORTED
+    assert L.ps_create(C.byref(h), 10, 4, None, other, 0.1, 0.0, None) == _lib.PS_ERR_INVALID
+    assert L.ps_create(C.byref(h), 10, 4, fake, fake, 0.1, 0.0, None) == _lib.PS_ERR_INVALID
+    assert L.ps_create(C.byref(h), 10, 4, C.c_void_p(0x1004), other, 0.1, 0.0, None) == _lib.PS_ERR_INVALID
+    assert L.ps_create(C.byref(h), 10, 4, fake, other, 0.0, 0.0, None) == _lib.PS_ERR_INVALID
+    assert L.ps_create(C.byref(h), 10, 4, fake, other, 0.1, -1.0, None) == _lib.PS_ERR_INVALID
+    assert b"lr" in L.ps_last_error_message()
+
+
+def test_calls_on_null_store_are_rejected():
+    L = _lib.lib()
+    p = C.c_void_p(0x1000)
+    assert L.ps_pull(None, p, 1, p, None) == _lib.PS_ERR_INVALID
+    assert L.ps_push(None, p, 1, p, p, 1 << 20, None) == _lib.PS_ERR_INVALID
+    assert L.ps_step_mf(None, p, p, p, 1, 0, 0.01, None, p, 1 << 20, None) == _lib.PS_ERR_INVALID
+    assert L.ps_get_error(None, None) == _lib.PS_ERR_INVALID
+    assert L.ps_destroy(None) == _lib.PS_OK
+    ms, n = C.c_double(), C.c_int64()
+    assert L.ps_read_timing(None, 0, C.byref(ms), C.byref(n)) == _lib.PS_ERR_INVALID
+
+
+def test_dedup_rejects_bad_arguments_on_host():
+    L = _lib.lib()
+    p = C.c_void_p(0x1000)
+    assert L.ps_dedup(0, p, 4, p, p, p, p, None, p, 1 << 20, None) == _lib.PS_ERR_INVALID
+    assert L.ps_dedup(10, p, -1, p, p, p, p, None, p, 1 << 20, None) == _lib.PS_ERR_INVALID
+    assert L.ps_dedup(10, p, 1 << 31, p, p, p, p, None, p, 1 << 40, None) == _lib.PS_ERR_UNSUPPORTED
+    assert L.ps_dedup(10, p, 4, p, p, None, p, None, p, 1 << 20, None) == _lib.PS_ERR_INVALID
+    need = L.ps_workspace_bytes(10, 1, _lib.PS_OP_DEDUP, 4, 1)
+    assert L.ps_dedup(10, p, 4, p, p, p, p, None, p, need - 1, None) == _lib.PS_ERR_WORKSPACE
+    assert L.ps_dedup(10, p, 4, p, p, p, p, None, None, need, None) == _lib.PS_ERR_INVALID
+
+
+@pytest.mark.parametrize("op,per", [(_lib.PS_OP_PUSH, 1), (_lib.PS_OP_DEDUP, 1), (_lib.PS_OP_STEP_MF, 2),
+                                    (_lib.PS_OP_STEP_KGE, 103), (_lib.PS_OP_STEP_SGNS, 261),
+                                    (_lib.PS_OP_STEP_CTR, 26)])
+def test_workspace_sizes(op, per):
+    L = _lib.lib()
+    small = L.ps_workspace_bytes(1000, 100, op, 10, per)
+    big = L.ps_workspace_bytes(1000, 100, op, 10_000, per)
+    assert 0 < small < big
+    assert L.ps_workspace_bytes(1000, 100, op, (1 << 31) // per, per) == 0   # beyond 32-bit occurrence index
+    assert L.ps_workspace_bytes(0, 100, op, 10, per) == 0
+    assert L.ps_workspace_bytes(1000, 100, op, 10, 0) == 0
+
+
+def test_pull_needs_no_workspace():
+    assert _lib.lib().ps_workspace_bytes(1000, 100, _lib.PS_OP_PULL, 10, 1) == 0

@@ -1,0 +1,208 @@
+"""GPU parity of the store's core calls against the CPU oracle:
+pull (bit-exact), dedup (bit-exact), push (tolerance; untouched rows bit-exact)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2206_00470_amd import Store, dedup
+from paper_2206_00470_amd.workloads import Zipf, normal_table, random_push
+from tests.helpers import assert_bitwise, assert_close_tables, say
+
+pytestmark = pytest.mark.gpu
+
+LR, EPS = 0.1, 1e-10
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def make_store(K, d, seed, g_fill=False):
+    W = normal_table(K, d, 0.1, seed, 1)
+    rng = np.random.default_rng(seed)
+    G = (rng.uniform(0, 1, (K, d)).astype(np.float32) if g_fill else np.zeros((K, d), np.float32))
+    return W, G
+
+
+# ------------------------------------------------------------------ pull
+@pytest.mark.parametrize("K,d,n", [(1, 4, 1), (5000, 16, 4097), (5000, 100, 100_003), (3000, 3, 777),
+                                   (3000, 300, 5000), (1 << 16, 64, 70_000), (2000, 256, 3000), (700, 2048, 999)])
+def test_pull_bitexact(K, d, n):
+    say(f"pull K={K} d={d} n={n}")
+    W, G = make_store(K, d, 7)
+    rng = np.random.default_rng(n)
+    keys = rng.integers(0, K, n)
+    Wt, Gt = dev(W), dev(G)
+    s = Store(Wt, Gt, LR, EPS)
+    out = s.pull(dev(keys))
+    assert s.error() == 0
+    ref, bad = oracle.pull(W, keys)
+    assert_bitwise(out.cpu().numpy(), ref, "pull")
+
+
+def test_pull_invalid_keys_zero_rows_and_flag():
+    K, d = 1000, 100
+    W, G = make_store(K, d, 8)
+    keys = np.array([0, -1, 999, 1000, 5, 1 << 40, 3], np.int64)
+    s = Store(dev(W), dev(G), LR, EPS)
+    out = s.pull(dev(keys))
+    assert s.error() == -2
+    assert s.error() == 0          # sticky flag is cleared by reading it
+    ref, bad = oracle.pull(W, keys)
+    assert bad == 3
+    assert_bitwise(out.cpu().numpy(), ref, "pull with invalid keys")
+
+
+def test_pull_empty_is_noop():
+    W, G = make_store(10, 8, 9)
+    s = Store(dev(W), dev(G), LR, EPS)
+    out = s.pull(torch.empty(0, dtype=torch.int64, device="cuda"))
+    assert out.shape == (0, 8) and s.error() == 0
+
+
+# ------------------------------------------------------------------ dedup
+DEDUP_CASES = [
+    (1, 1, None), (1, 50, None), (5, 1, None), (37, 1000, None), (1500, 2048, 1.1),
+    (1500, 4095, 1.1), (1500, 4096, 1.1), (1500, 4097, 1.1), (11_000_000, 300_000, 1.1),
+    ((1 << 25), 212_992, 1.05), (100_000, 1 << 20, None), (2_000_000, 5_000_000, 1.0),
+    ((1 << 31) - 1, 10_000, None), (256, 70_000, None),
+]
+
+
+@pytest.mark.parametrize("num_keys,n,zipf", DEDUP_CASES)
+def test_dedup_bitexact(num_keys, n, zipf):
+    say(f"dedup num_keys={num_keys} n={n} zipf={zipf}")
+    if zipf is None:
+        keys = np.random.default_rng(n).integers(0, num_keys, n)
+    else:
+        keys = Zipf(min(num_keys, 2_000_000), zipf, 3, 4).sample(np.random.default_rng(n), n).astype(np.int64)
+    uniq, perm, offs, U = dedup(num_keys, dev(keys))
+    ru, rp, ro, bad = oracle.dedup(num_keys, keys)
+    assert U == ru.size
+    assert_bitwise(uniq.cpu().numpy(), ru, "uniq")
+    assert_bitwise(perm.cpu().numpy(), rp, "perm")
+    assert_bitwise(offs.cpu().numpy(), ro, "offsets")
+
+
+def test_dedup_invalid_keys_sort_last_and_flag():
+    num_keys = 1000
+    rng = np.random.default_rng(11)
+    keys = rng.integers(-50, num_keys + 50, 9000)
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    uniq, perm, offs, U = dedup(num_keys, dev(keys), err=err)
+    ru, rp, ro, bad = oracle.dedup(num_keys, keys)
+    assert bad > 0 and int(err.item()) == 1
+    assert_bitwise(uniq.cpu().numpy(), ru, "uniq")
+    assert_bitwise(perm.cpu().numpy(), rp, "perm")
+    assert_bitwise(offs.cpu().numpy(), ro, "offsets")
+
+
+def test_dedup_empty():
+    uniq, perm, offs, U = dedup(10, torch.empty(0, dtype=torch.int64, device="cuda"))
+    assert U == 0 and offs.cpu().tolist() == [0]
+
+
+# ------------------------------------------------------------------ push
+PUSH_CASES = [
+    # K, d, n, zipf (None = uniform), G prefilled
+    (1, 4, 1, None, False),
+    (3, 16, 1000, None, False),          # a few keys, long segments (split into chunks)
+    (5000, 16, 4097, 1.1, True),
+    (23_000, 100, 10_006, 1.1, False),
+    (23_000, 100, 300_001, 1.1, True),   # hot key far longer than a chunk
+    (3000, 3, 2000, None, True),         # dim not a multiple of 4
+    (6000, 300, 20_000, 0.75, False),
+    (1 << 16, 64, 212_992, 1.05, False),
+    (4000, 256, 50_000, 1.0, True),
+    (500, 2048, 3000, 1.0, False),
+    (1000, 500, 100_000, None, False),   # every key duplicated ~100x
+]
+
+
+def run_push(K, d, n, zipf, gfill, seed=0):
+    W, G = make_store(K, d, seed, g_fill=gfill)
+    keys, grads = random_push(K, n, d, seed + 1, zipf_s=zipf)
+    Wt, Gt = dev(W), dev(G)
+    s = Store(Wt, Gt, LR, EPS)
+    s.push(dev(keys), dev(grads))
+    assert s.error() == 0
+    Wr, Gr = W.copy(), G.copy()
+    oracle.push(Wr, Gr, keys, grads, LR, EPS)
+    return W, G, Wt.cpu().numpy(), Gt.cpu().numpy(), Wr, Gr, keys
+
+
+@pytest.mark.parametrize("K,d,n,zipf,gfill", PUSH_CASES)
+def test_push_parity(K, d, n, zipf, gfill):
+    say(f"push K={K} d={d} n={n} zipf={zipf}")
+    W0, G0, Wg, Gg, Wr, Gr, keys = run_push(K, d, n, zipf, gfill)
+    assert_close_tables(Wg, Wr, "W")
+    assert_close_tables(Gg, Gr, "G")
+    untouched = np.setdiff1d(np.arange(K), keys)
+    assert_bitwise(Wg[untouched], W0[untouched], "untouched W rows")
+    assert_bitwise(Gg[untouched], G0[untouched], "untouched G rows")
+
+
+def test_push_deterministic():
+    K, d, n = 23_000, 100, 300_001
+    a = run_push(K, d, n, 1.1, True, seed=4)
+    b = run_push(K, d, n, 1.1, True, seed=4)
+    assert_bitwise(a[2], b[2], "W run 1 vs run 2")
+    assert_bitwise(a[3], b[3], "G run 1 vs run 2")
+
+
+def test_push_zero_gradients_then_pull_returns_same_rows():
+    K, d = 3000, 100
+    W, G = make_store(K, d, 5, g_fill=True)
+    G[::3] = 0
+    Wt, Gt = dev(W), dev(G)
+    s = Store(Wt, Gt, LR, EPS)
+    keys = np.random.default_rng(5).integers(0, K, 50_000)
+    s.push(dev(keys), torch.zeros((keys.size, d), dtype=torch.float32, device="cuda"))
+    out = s.pull(dev(np.arange(K)))
+    assert_bitwise(out.cpu().numpy(), W, "W after zero push")
+    assert_bitwise(Gt.cpu().numpy(), G, "G after zero push")
+
+
+def test_push_first_touch_is_exactly_lr():
+    """G = 0 and |sum| >= 2^-9: every touched element moves by exactly lr."""
+    K, d = 2000, 64
+    W, G = make_store(K, d, 6)
+    rng = np.random.default_rng(6)
+    keys = rng.permutation(K)[:1500]
+    grads = (rng.uniform(0.01, 5, (1500, d)) * rng.choice([-1, 1], (1500, d))).astype(np.float32)
+    Wt, Gt = dev(W), dev(G)
+    Store(Wt, Gt, LR, EPS).push(dev(keys), dev(grads))
+    expect = W.copy()
+    expect[keys] = (W[keys] - np.float32(LR) * np.sign(grads)).astype(np.float32)
+    assert_bitwise(Wt.cpu().numpy(), expect, "W after first touch")
+
+
+def test_push_invalid_keys_ignored_and_flagged():
+    K, d = 1000, 16
+    W, G = make_store(K, d, 10)
+    rng = np.random.default_rng(10)
+    keys = rng.integers(-5, K + 5, 5000)
+    grads = rng.standard_normal((5000, d)).astype(np.float32)
+    Wt, Gt = dev(W), dev(G)
+    s = Store(Wt, Gt, LR, EPS)
+    s.push(dev(keys), dev(grads))
+    assert s.error() == -2
+    Wr, Gr = W.copy(), G.copy()
+    oracle.push(Wr, Gr, keys, grads, LR, EPS)
+    assert_close_tables(Wt.cpu().numpy(), Wr, "W")
+    assert_close_tables(Gt.cpu().numpy(), Gr, "G")
+
+
+def test_push_workspace_too_small_is_rejected():
+    import ctypes as C
+    from paper_2206_00470_amd import _lib
+    W, G = make_store(100, 16, 1)
+    s = Store(dev(W), dev(G), LR, EPS)
+    keys = dev(np.arange(50, dtype=np.int64))
+    grads = torch.zeros((50, 16), dtype=torch.float32, device="cuda")
+    need = s.workspace_bytes(_lib.PS_OP_PUSH, 50, 1)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    st = _lib.lib().ps_push(s._h, C.c_void_p(keys.data_ptr()), 50, C.c_void_p(grads.data_ptr()),
+                            C.c_void_p(ws.data_ptr()), need - 1, C.c_void_p(0))
+    assert st == _lib.PS_ERR_WORKSPACE

@@ -1,0 +1,152 @@
+"""GPU parity of the matrix-factorization step against the CPU oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2206_00470_amd import Store
+from paper_2206_00470_amd.workloads import MF_10Mx1M, MF_TINY, MFWorkload, small_variant
+from tests.helpers import assert_bitwise, assert_close_tables, mismatch_fraction, say
+
+pytestmark = pytest.mark.gpu
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def gpu_step(s, cfg, bt):
+    return s.step_mf(dev(bt.row), dev(bt.col), dev(bt.val), cfg.n_rows, cfg.lam)
+
+
+def check_step_from_same_state(cfg, steps):
+    """Every step starts the oracle from the GPU's pre-step state."""
+    wl = MFWorkload(cfg)
+    W = wl.init_table()
+    G = np.zeros_like(W)
+    Wt, Gt = dev(W), dev(G)
+    s = Store(Wt, Gt, cfg.opt.lr, cfg.opt.eps)
+    for step in steps:
+        say(f"{cfg.name} step {step}")
+        bt = wl.batch(step)
+        Wr, Gr = Wt.cpu().numpy(), Gt.cpu().numpy()
+        W0 = Wr.copy()
+        loss = gpu_step(s, cfg, bt)
+        assert s.error() == 0
+        rloss, bad = oracle.step_mf(Wr, Gr, bt.row, bt.col, bt.val, cfg.n_rows, cfg.lam, cfg.opt.lr, cfg.opt.eps)
+        assert bad == 0
+        Wg, Gg = Wt.cpu().numpy(), Gt.cpu().numpy()
+        assert_close_tables(Wg, Wr, f"W after step {step}")
+        assert_close_tables(Gg, Gr, f"G after step {step}")
+        touched = np.zeros(cfg.num_keys, bool)
+        touched[bt.row] = True
+        touched[cfg.n_rows + bt.col] = True
+        assert_bitwise(Wg[~touched], W0[~touched], "untouched rows")
+        assert float(loss.item()) == pytest.approx(rloss, rel=1e-9)
+        say(f"  loss {rloss:.6g}; W words differing from oracle: {mismatch_fraction(Wg, Wr):.2e}")
+    return s, Wt, Gt
+
+
+def test_mf_tiny_every_step_of_one_epoch():
+    cfg = MF_TINY
+    check_step_from_same_state(cfg, range(cfg.steps_per_epoch))
+
+
+def test_mf_tiny_epoch_trajectory():
+    """The whole epoch run independently on both sides stays within tolerance."""
+    cfg = MF_TINY
+    wl = MFWorkload(cfg)
+    W = wl.init_table()
+    G = np.zeros_like(W)
+    Wt, Gt = dev(W), dev(G)
+    s = Store(Wt, Gt, cfg.opt.lr, cfg.opt.eps)
+    Wr, Gr = W.copy(), G.copy()
+    for step in range(cfg.steps_per_epoch):
+        bt = wl.batch(step)
+        gpu_step(s, cfg, bt)
+        oracle.step_mf(Wr, Gr, bt.row, bt.col, bt.val, cfg.n_rows, cfg.lam, cfg.opt.lr, cfg.opt.eps)
+    assert s.error() == 0
+    assert_close_tables(Wt.cpu().numpy(), Wr, "W after one epoch")
+    assert_close_tables(Gt.cpu().numpy(), Gr, "G after one epoch")
+
+
+def test_mf_small_several_tiles_ragged():
+    cfg = small_variant(MF_10Mx1M)
+    check_step_from_same_state(cfg, range(3))
+
+
+def test_mf_invalid_entries_are_skipped_and_flagged():
+    cfg = small_variant(MF_10Mx1M)
+    wl = MFWorkload(cfg)
+    W = wl.init_table()
+    G = np.zeros_like(W)
+    bt = wl.batch(0)
+    bt.row[[3, 100]] = [-1, cfg.n_rows + cfg.n_cols]
+    bt.col[7] = cfg.n_cols        # key = n_rows + n_cols: outside the table
+    Wt, Gt = dev(W), dev(G)
+    s = Store(Wt, Gt, cfg.opt.lr, cfg.opt.eps)
+    loss = gpu_step(s, cfg, bt)
+    assert s.error() == -2
+    Wr, Gr = W.copy(), G.copy()
+    rloss, bad = oracle.step_mf(Wr, Gr, bt.row, bt.col, bt.val, cfg.n_rows, cfg.lam, cfg.opt.lr, cfg.opt.eps)
+    assert bad == 3
+    assert_close_tables(Wt.cpu().numpy(), Wr, "W")
+    assert_close_tables(Gt.cpu().numpy(), Gr, "G")
+    assert float(loss.item()) == pytest.approx(rloss, rel=1e-9)
+
+
+def test_mf_step_equals_pull_host_gradient_push():
+    """The fused step and the composition pull -> oracle gradient -> push agree."""
+    cfg = small_variant(MF_10Mx1M)
+    wl = MFWorkload(cfg)
+    W = wl.init_table()
+    G = np.zeros_like(W)
+    bt = wl.batch(1)
+    Wa, Ga = dev(W), dev(G)
+    sa = Store(Wa, Ga, cfg.opt.lr, cfg.opt.eps)
+    gpu_step(sa, cfg, bt)
+    Wb, Gb = dev(W), dev(G)
+    sb = Store(Wb, Gb, cfg.opt.lr, cfg.opt.eps)
+    keys, grads, loss, _ = oracle.grad_mf(W, bt.row, bt.col, bt.val, cfg.n_rows, cfg.lam)
+    pulled = sb.pull(dev(keys)).cpu().numpy()
+    assert_bitwise(pulled, W[keys], "pulled rows")
+    sb.push(dev(keys), dev(grads))
+    assert_close_tables(Wa.cpu().numpy(), Wb.cpu().numpy(), "W fused vs composed")
+    assert_close_tables(Ga.cpu().numpy(), Gb.cpu().numpy(), "G fused vs composed")
+
+
+def test_mf_deterministic():
+    cfg = small_variant(MF_10Mx1M)
+    wl = MFWorkload(cfg)
+    W = wl.init_table()
+    out = []
+    for _ in range(2):
+        Wt, Gt = dev(W), dev(np.zeros_like(W))
+        s = Store(Wt, Gt, cfg.opt.lr, cfg.opt.eps)
+        l1 = gpu_step(s, cfg, wl.batch(0))
+        l2 = gpu_step(s, cfg, wl.batch(1))
+        out.append((Wt.cpu().numpy(), Gt.cpu().numpy(), float(l1.item()), float(l2.item())))
+    assert_bitwise(out[0][0], out[1][0], "W")
+    assert_bitwise(out[0][1], out[1][1], "G")
+    assert out[0][2:] == out[1][2:]
+
+
+def test_mf_paper_scale_one_step():
+    """10M x 1M, rank 100, 1,048,576 entries: the full table, the bench's launch."""
+    cfg = MF_10Mx1M
+    wl = MFWorkload(cfg)
+    say("generating the 11M x 100 table")
+    W = wl.init_table()
+    G = np.zeros_like(W)
+    Wt, Gt = dev(W), dev(G)
+    s = Store(Wt, Gt, cfg.opt.lr, cfg.opt.eps)
+    bt = wl.batch(0)
+    say("gpu step")
+    loss = gpu_step(s, cfg, bt)
+    assert s.error() == 0
+    say("oracle step")
+    rloss, bad = oracle.step_mf(W, G, bt.row, bt.col, bt.val, cfg.n_rows, cfg.lam, cfg.opt.lr, cfg.opt.eps)
+    say("compare")
+    assert float(loss.item()) == pytest.approx(rloss, rel=1e-9)
+    assert_close_tables(Wt.cpu().numpy(), W, "W")
+    assert_close_tables(Gt.cpu().numpy(), G, "G")
