@@ -213,6 +213,13 @@ struct Plan {
 
 constexpr int64_t LOSS_GRID = 2048;
 
+// MF and CTR steps write each gradient row straight to its sorted position
+// (scattered writes, contiguous merge reads) rather than in occurrence order
+// (contiguous writes, merge reads through the permutation).
+#ifndef ADAPM_SORTED_GRADS
+#define ADAPM_SORTED_GRADS 1
+#endif
+
 bool plan_op(void* ws, int64_t num_keys, int dim, int op, int64_t units, int64_t per_unit, Plan* p) {
   (void)num_keys;
   const int64_t n = units * per_unit;
@@ -325,7 +332,7 @@ ps_status run_reduce(ps_store* s, const SortBufs& b, const uint32_t* ks, Src src
     const int64_t grid = reduce_grid(n, L);
     {
       Timed t(s, PS_KERNEL_SEGREDUCE, st);
-      hipLaunchKernelGGL((k_segreduce<L, NV, VW, Src>), dim3(grid), dim3(BLOCK), 0, st, sv, src, s->W, s->G,
+      hipLaunchKernelGGL((k_segreduce<L, NV, VW, Src>), dim3(grid), dim3(BLOCK), 0, st, sv, src, n, s->W, s->G,
                          s->dim, s->lr, s->eps, b.partial, b.split_list, b.hdr, key_lo, key_hi);
     }
     LAUNCHED(k_segreduce);
@@ -524,7 +531,9 @@ ps_status ps_step_mf(ps_store* s, const int32_t* row, const int32_t* col, const 
   if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
   uint32_t *ks, *perm;
   KeysMF kmf{row, col, col_key_offset, s->num_keys};
-  if (ps_status r = run_sort(s, kmf, n, s->num_keys, p.sb, s->status, nullptr, true, st, &ks, &perm)) return r;
+  const bool sorted_grads = ADAPM_SORTED_GRADS;
+  if (ps_status r = run_sort(s, kmf, n, s->num_keys, p.sb, s->status, nullptr, sorted_grads, st, &ks, &perm))
+    return r;
   if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st)) return r;
   RowShape shape;
   row_shape(s->dim, true, &shape);
@@ -534,7 +543,8 @@ ps_status ps_step_mf(ps_store* s, const int32_t* row, const int32_t* col, const 
     {
       Timed t(s, PS_KERNEL_TASKGRAD, st);
       hipLaunchKernelGGL((k_mf_grad<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->num_keys, s->dim, row,
-                         col, val, B, col_key_offset, lambda, p.sb.rank, p.grads, p.loss_part);
+                         col, val, B, col_key_offset, lambda, sorted_grads ? p.sb.rank : nullptr, p.grads,
+                         p.loss_part);
     }
     LAUNCHED(k_mf_grad);
     if (loss) {
@@ -544,7 +554,8 @@ ps_status ps_step_mf(ps_store* s, const int32_t* row, const int32_t* col, const 
     return PS_OK;
   });
   if (r) return r;
-  return run_reduce(s, p.sb, ks, SrcSorted{p.grads, s->dim}, n, 0u, (uint32_t)s->num_keys, st);
+  if (sorted_grads) return run_reduce(s, p.sb, ks, SrcSorted{p.grads, s->dim}, n, 0u, (uint32_t)s->num_keys, st);
+  return run_reduce(s, p.sb, ks, SrcIndirect{p.grads, perm, s->dim}, n, 0u, (uint32_t)s->num_keys, st);
 }
 
 ps_status ps_step_kge(ps_store* s, const int32_t* head, const int32_t* rel, const int32_t* tail, const int32_t* neg,

@@ -107,14 +107,14 @@ __device__ __forceinline__ int64_t xcd_slot(int64_t block, int64_t nblocks) {
 // block start, and the one starting inside it) for k_seg_finalize; the
 // first chunk of such a segment also appends the segment to split_list.
 template <int L, int NV, int VW, class Src>
-__global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, float* __restrict__ W,
+__global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, int64_t n, float* __restrict__ W,
                                                      float* __restrict__ G, int dim, float lr, float eps,
                                                      double* __restrict__ partial,
                                                      int32_t* __restrict__ split_list, SegHeader* split_hdr,
                                                      uint32_t key_lo, uint32_t key_hi) {
   constexpr int GPB = BLOCK / L;
   constexpr int NE = NV * VW;
-  constexpr int UNROLL = NE <= 4 ? 8 : 4;
+  constexpr int UNROLL = NE <= 4 ? 4 : 2;
   const int gl = threadIdx.x % L;
   const int64_t nchunks = sv.hdr->num_chunks;
   const int64_t stride = (int64_t)gridDim.x * GPB;
@@ -123,10 +123,9 @@ __global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, float*
     const int64_t j1 = sv.chunk_start[c + 1];
     const uint32_t key = sv.keys[j0];
     if (key < key_lo || key >= key_hi) continue;
-    const int32_t u = sv.chunk_seg[c];
-    const int64_t s0 = sv.seg_off[u];
-    const int64_t s1 = sv.seg_off[u + 1];
-    const bool whole = (j0 == s0) && (j1 == s1);
+    // the chunk is a whole segment if its neighbours hold other keys
+    const bool head = j0 == 0 || sv.keys[j0 - 1] != key;
+    const bool whole = head && (j1 >= n || sv.keys[j1] != key);
     float* wrow = W + (int64_t)key * dim;
     float* grow = G + (int64_t)key * dim;
     float wv[NE], gv[NE];
@@ -172,7 +171,7 @@ __global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, float*
         }
       }
     } else {
-      if (j0 == s0 && gl == 0) split_list[atomicAdd(&split_hdr->num_split, 1u)] = u;
+      if (head && gl == 0) split_list[atomicAdd(&split_hdr->num_split, 1u)] = sv.chunk_seg[c];
       const int64_t slot = 2 * (j0 / CHUNK) + ((j0 % CHUNK) != 0);
       double* p = partial + slot * dim;
 #pragma unroll
@@ -212,7 +211,28 @@ __global__ __launch_bounds__(BLOCK) void k_seg_finalize(SegView sv, float* __res
     double acc[NE];
 #pragma unroll
     for (int q = 0; q < NE; ++q) acc[q] = 0.0;
-    for (int64_t k = g; k < m; k += GPB) {
+    constexpr int FU = 8;   // partial rows in flight per group
+    int64_t k = g;
+    for (; k + (FU - 1) * GPB < m; k += FU * GPB) {
+      double x[FU][NE];
+#pragma unroll
+      for (int f = 0; f < FU; ++f) {
+        const int64_t kk = k + f * GPB;
+        const int64_t slot = kk == 0 ? 2 * b0 + ((s0 % CHUNK) != 0) : 2 * (b0 + kk);
+        const double* p = partial + slot * dim;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+          const int col = (gl + v * L) * VW;
+#pragma unroll
+          for (int q = 0; q < VW; ++q) x[f][v * VW + q] = col < dim ? p[col + q] : 0.0;
+        }
+      }
+#pragma unroll
+      for (int f = 0; f < FU; ++f)
+#pragma unroll
+        for (int e = 0; e < NE; ++e) acc[e] += x[f][e];
+    }
+    for (; k < m; k += GPB) {
       const int64_t slot = k == 0 ? 2 * b0 + ((s0 % CHUNK) != 0) : 2 * (b0 + k);
       const double* p = partial + slot * dim;
 #pragma unroll

@@ -1,7 +1,7 @@
 // Duplicate-key merge order: a stable LSD radix sort of (key, occurrence)
 // pairs, then segment and chunk boundaries of the sorted keys.
 //
-// Radix tiles hold TILE = 4096 keys.  Each pass is reduce-then-scan:
+// Radix tiles hold TILE = 2048 keys.  Each pass is reduce-then-scan:
 //   count   : per-tile digit histogram  -> counts[digit][tile]
 //   scan    : one workgroup per digit turns its row of counts into global
 //             offsets, seeded with the digit base from a whole-array

@@ -38,7 +38,8 @@ struct KeysMF {
 // One row group per entry (u = W[row], m = W[col_off + col], e = v - <u,m>):
 //   grad_u = lam u - e m ,  grad_m = lam m - e u     (fp64, rounded to fp32)
 //   loss  += e^2/2 + lam/2 (|u|^2 + |m|^2)
-// The two gradient rows go to the sorted positions rank[2b], rank[2b+1].
+// The two gradient rows go to the sorted positions rank[2b], rank[2b+1], or
+// to occurrence positions 2b, 2b+1 when rank is null.
 template <int L, int NV, int VW>
 __global__ __launch_bounds__(BLOCK) void k_mf_grad(const float* __restrict__ W, int64_t num_keys, int dim,
                                                    const int32_t* __restrict__ row, const int32_t* __restrict__ col,
@@ -87,8 +88,8 @@ __global__ __launch_bounds__(BLOCK) void k_mf_grad(const float* __restrict__ W, 
       gu[e] = (float)(lamd * (double)u[e] - err * (double)m[e]);
       gm[e] = (float)(lamd * (double)m[e] - err * (double)u[e]);
     }
-    float* du = grads + (int64_t)rank[2 * b] * dim;
-    float* dm = grads + (int64_t)rank[2 * b + 1] * dim;
+    float* du = grads + (rank ? (int64_t)rank[2 * b] : 2 * b) * dim;
+    float* dm = grads + (rank ? (int64_t)rank[2 * b + 1] : 2 * b + 1) * dim;
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
       const int c = (gl + v * L) * VW;
