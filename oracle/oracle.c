@@ -400,8 +400,11 @@ ORC_API double orc_grad_sgns(const float* W, int64_t num_keys, int32_t dim,
     for (int64_t b = 0; b < B; ++b) {
         int64_t* kk = okeys + b * per;
         float* gg = ograds + b * per * dim;
+        /* word2vec keeps two tables: centre words index the input vectors
+         * [0, out_off), context and noise words the output vectors
+         * [out_off, num_keys); a unit with an id outside its table is skipped */
         int64_t kc = centre[b];
-        int ok = key_ok(kc, num_keys);
+        int ok = kc >= 0 && kc < out_off && key_ok(kc, num_keys);
         for (int32_t q = 0; q < slots; ++q) {
             int32_t cx = ctx[b * slots + q];
             if (cx == -1) continue;

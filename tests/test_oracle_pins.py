@@ -401,6 +401,14 @@ def test_sgns_zero_output_table_closed_form():
     np.testing.assert_allclose(G[V:], (gsum.astype(np.float32)) ** 2, rtol=1e-6, atol=1e-12)
 
 
+def test_sgns_centre_must_index_the_input_table():
+    W, centre, ctx, neg, w, V = sgns_setup(21)
+    centre[1] = V + 2            # an output-table row used as a centre word
+    keys, grads, loss, bad = oracle.grad_sgns(W, centre, ctx, neg, w, V)
+    per = 1 + 2 * w * (1 + neg.shape[2])
+    assert bad == 1 and np.all(keys[per:2 * per] == -1) and not grads[per:2 * per].any()
+
+
 def test_sgns_occurrence_layout_and_absent_slots():
     W, centre, ctx, neg, w, V = sgns_setup(18)
     keys, grads, loss, _ = oracle.grad_sgns(W, centre, ctx, neg, w, V)
