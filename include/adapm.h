@@ -66,7 +66,7 @@ typedef int32_t ps_status;
 #define PS_OP_STEP_SGNS 5
 #define PS_OP_STEP_CTR  6
 
-/* Limits: num_keys in [1, 2^31-1]; dim in [1, 2048]; key occurrences per
+/* Limits: num_keys in [1, 2^31-1]; dim in [1, 512]; key occurrences per
  * call n < 2^31 - 2^20. */
 
 /* Create a store over caller-owned device tables W (values) and G

@@ -5,6 +5,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <initializer_list>
 #include <string>
 #include <utility>
 #include <vector>
@@ -102,8 +103,7 @@ bool row_shape(int dim, bool vec_ok, RowShape* s) {
     else if (nvec <= 32) { s->L = 32; s->NV = 1; }
     else if (nvec <= 64) { s->L = 64; s->NV = 1; }
     else if (nvec <= 128) { s->L = 64; s->NV = 2; }
-    else if (nvec <= 256) { s->L = 64; s->NV = 4; }
-    else if (nvec <= 512) { s->L = 64; s->NV = 8; }
+    // wider rows are not supported: their register-heavy kernel variants are disabled
     else return false;
     return true;
   }
@@ -127,8 +127,6 @@ ps_status with_shape(const RowShape& s, F&& f) {
   ADAPM_SHAPE(32, 1, 4)
   ADAPM_SHAPE(64, 1, 4)
   ADAPM_SHAPE(64, 2, 4)
-  ADAPM_SHAPE(64, 4, 4)
-  ADAPM_SHAPE(64, 8, 4)
   ADAPM_SHAPE(64, 1, 1)
   ADAPM_SHAPE(64, 2, 1)
   ADAPM_SHAPE(64, 4, 1)
@@ -207,6 +205,10 @@ void carve_sort(Carver& c, int64_t n, int dim, bool want_rank, bool want_segment
 struct Plan {
   SortBufs sb;
   float* grads = nullptr;      // per-occurrence gradient rows (MF, CTR)
+  float* mat = nullptr;        // gradient rows stored per unit (KGE: s, r, o; SGNS: centre)
+  double* base = nullptr;      // KGE: fp64 rows d phi/d s (r,o) and d phi/d o (s,r) per triple
+  double* coef = nullptr;      // KGE, SGNS: fp64 coefficient per occurrence
+  uint8_t* ok = nullptr;       // per-unit validity
   double* loss_part = nullptr;
   size_t bytes = 0;
 };
@@ -236,6 +238,22 @@ bool plan_op(void* ws, int64_t num_keys, int dim, int op, int64_t units, int64_t
       carve_sort(c, n, dim, true, true, &p->sb);
       p->grads = c.take<float>(size_t(n) * dim);
       p->loss_part = c.take<double>(LOSS_GRID);
+      p->ok = c.take<uint8_t>(units);
+      break;
+    case PS_OP_STEP_KGE:
+      carve_sort(c, n, dim, false, true, &p->sb);
+      p->mat = c.take<float>(size_t(3) * units * dim);
+      p->base = c.take<double>(size_t(2) * units * dim);
+      p->coef = c.take<double>(n);
+      p->loss_part = c.take<double>(LOSS_GRID);
+      p->ok = c.take<uint8_t>(units);
+      break;
+    case PS_OP_STEP_SGNS:
+      carve_sort(c, n, dim, false, true, &p->sb);
+      p->mat = c.take<float>(size_t(units) * dim);
+      p->coef = c.take<double>(n);
+      p->loss_part = c.take<double>(LOSS_GRID);
+      p->ok = c.take<uint8_t>(units);
       break;
     default:
       return false;
@@ -320,22 +338,28 @@ int64_t reduce_grid(int64_t n, int L) {
   return g;
 }
 
-// Segmented fp64 reduce of the occurrences' gradients + AdaGrad, for keys in
-// [key_lo, key_hi), then the finalize pass for segments longer than a chunk.
+// Segmented fp64 reduce of the occurrences' gradients + AdaGrad, one launch
+// per key range in the given order (a later range may update rows that an
+// earlier range's source reads), then one finalize pass for all segments
+// longer than a chunk.
+struct KeyRange {
+  uint32_t lo, hi;
+};
+
 template <class Src>
-ps_status run_reduce(ps_store* s, const SortBufs& b, const uint32_t* ks, Src src, int64_t n, uint32_t key_lo,
-                     uint32_t key_hi, hipStream_t st) {
+ps_status run_reduce(ps_store* s, const SortBufs& b, const uint32_t* ks, Src src, int64_t n,
+                     std::initializer_list<KeyRange> ranges, hipStream_t st) {
   RowShape shape;
   if (!row_shape(s->dim, true, &shape)) return fail(PS_ERR_UNSUPPORTED, "dim %d not supported", s->dim);
   SegView sv{ks, b.seg_off, b.chunk_start, b.chunk_seg, b.hdr};
   return with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
     const int64_t grid = reduce_grid(n, L);
-    {
+    for (const KeyRange& r : ranges) {
       Timed t(s, PS_KERNEL_SEGREDUCE, st);
       hipLaunchKernelGGL((k_segreduce<L, NV, VW, Src>), dim3(grid), dim3(BLOCK), 0, st, sv, src, n, s->W, s->G,
-                         s->dim, s->lr, s->eps, b.partial, b.split_list, b.hdr, key_lo, key_hi);
+                         s->dim, s->lr, s->eps, b.partial, b.split_list, b.hdr, r.lo, r.hi);
+      LAUNCHED(k_segreduce);
     }
-    LAUNCHED(k_segreduce);
     int64_t fgrid = n / CHUNK + 1;
     if (fgrid > 1024) fgrid = 1024;
     const size_t lds = size_t(BLOCK / L) * s->dim * sizeof(double);
@@ -344,6 +368,14 @@ ps_status run_reduce(ps_store* s, const SortBufs& b, const uint32_t* ks, Src src
     LAUNCHED(k_seg_finalize);
     return PS_OK;
   });
+}
+
+KeyRange all_keys(const ps_store* s) { return KeyRange{0u, (uint32_t)s->num_keys}; }
+
+int64_t small_grid(int64_t units, int64_t per_block, int64_t cap) {
+  int64_t g = ceil_div(units, per_block);
+  if (g > cap) g = cap;
+  return g < 1 ? 1 : g;
 }
 
 ps_status check_ws(const Plan& p, void* ws, size_t ws_bytes) {
@@ -393,7 +425,7 @@ ps_status ps_create(ps_store** out, int64_t num_keys, int32_t dim, float* values
   if (num_keys < 1 || num_keys > INT32_MAX) return fail(PS_ERR_INVALID, "num_keys %lld outside [1, 2^31-1]", (long long)num_keys);
   RowShape shape;
   if (dim < 1 || !row_shape(dim, true, &shape))
-    return fail(PS_ERR_UNSUPPORTED, "dim %d unsupported (<= 2048 if a multiple of 4, else <= 512)", dim);
+    return fail(PS_ERR_UNSUPPORTED, "dim %d unsupported (at most 512)", dim);
   if (!values || !accum) return fail(PS_ERR_INVALID, "table pointer is NULL");
   if (values == accum) return fail(PS_ERR_INVALID, "values and accumulators alias");
   if (dim % 4 == 0 && (!aligned16(values) || !aligned16(accum)))
@@ -482,7 +514,7 @@ ps_status ps_push(ps_store* s, const int64_t* keys, int64_t n, const float* grad
   if (ps_status r = run_sort(s, KeysInt64{keys}, n, s->num_keys, p.sb, s->status, nullptr, false, st, &ks, &perm))
     return r;
   if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st)) return r;
-  return run_reduce(s, p.sb, ks, SrcIndirect{grads, perm, s->dim}, n, 0u, (uint32_t)s->num_keys, st);
+  return run_reduce(s, p.sb, ks, SrcIndirect{grads, perm, s->dim}, n, {all_keys(s)}, st);
 }
 
 ps_status ps_dedup(int64_t num_keys, const int64_t* keys, int64_t n, int64_t* uniq, int32_t* perm,
@@ -554,30 +586,160 @@ ps_status ps_step_mf(ps_store* s, const int32_t* row, const int32_t* col, const 
     return PS_OK;
   });
   if (r) return r;
-  if (sorted_grads) return run_reduce(s, p.sb, ks, SrcSorted{p.grads, s->dim}, n, 0u, (uint32_t)s->num_keys, st);
-  return run_reduce(s, p.sb, ks, SrcIndirect{p.grads, perm, s->dim}, n, 0u, (uint32_t)s->num_keys, st);
+  if (sorted_grads) return run_reduce(s, p.sb, ks, SrcSorted{p.grads, s->dim}, n, {all_keys(s)}, st);
+  return run_reduce(s, p.sb, ks, SrcIndirect{p.grads, perm, s->dim}, n, {all_keys(s)}, st);
 }
 
 ps_status ps_step_kge(ps_store* s, const int32_t* head, const int32_t* rel, const int32_t* tail, const int32_t* neg,
                       int64_t B, int32_t n_neg, int32_t n_head_neg, int64_t rel_key_offset, double* loss, void* ws,
                       size_t ws_bytes, void* stream) {
-  (void)s; (void)head; (void)rel; (void)tail; (void)neg; (void)B; (void)n_neg; (void)n_head_neg;
-  (void)rel_key_offset; (void)loss; (void)ws; (void)ws_bytes; (void)stream;
-  return fail(PS_ERR_UNSUPPORTED, "ps_step_kge not built yet");
+  if (ps_status st = check_store(s)) return st;
+  if (n_neg < 0 || n_head_neg < 0 || n_head_neg > n_neg)
+    return fail(PS_ERR_INVALID, "need 0 <= n_head_neg <= n_neg");
+  if (ps_status st = check_n(B, 3 + (int64_t)n_neg)) return st;
+  if (s->dim % 2 != 0) return fail(PS_ERR_UNSUPPORTED, "ComplEx rows need an even dim");
+  hipStream_t st = as_stream(stream);
+  if (B == 0) {
+    if (loss) {
+      hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(BLOCK), 0, st, reinterpret_cast<uint32_t*>(loss), int64_t(2));
+      LAUNCHED(k_zero_words);
+    }
+    return PS_OK;
+  }
+  if (!head || !rel || !tail || (n_neg > 0 && !neg)) return fail(PS_ERR_INVALID, "head, rel, tail or neg is NULL");
+  if (rel_key_offset < 0) return fail(PS_ERR_INVALID, "negative rel_key_offset");
+  const int per = 3 + n_neg;
+  const int64_t n = B * per;
+  Plan p;
+  plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_KGE, B, per, &p);
+  if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
+  hipLaunchKernelGGL(k_unit_valid<ValidKGE>, dim3(small_grid(B, BLOCK, 1024)), dim3(BLOCK), 0, st,
+                     ValidKGE{head, rel, tail, neg, n_neg, rel_key_offset, s->num_keys}, B, p.ok, s->status);
+  LAUNCHED(k_unit_valid);
+  uint32_t *ks, *perm;
+  KeysKGE kk{head, rel, tail, neg, per, n_neg, rel_key_offset, p.ok};
+  if (ps_status r = run_sort(s, kk, n, s->num_keys, p.sb, s->status, nullptr, false, st, &ks, &perm)) return r;
+  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st)) return r;
+  const int cdim = s->dim / 2;
+  const int64_t grid = small_grid(B, WAVES_PER_BLOCK, LOSS_GRID);
+  auto launch = [&](auto kernel) -> ps_status {
+    Timed t(s, PS_KERNEL_TASKGRAD, st);
+    hipLaunchKernelGGL(kernel, dim3(grid), dim3(BLOCK), 0, st, s->W, s->dim, head, rel, tail, neg, B, n_neg,
+                       n_head_neg, rel_key_offset, p.ok, p.mat, p.base, p.coef, p.loss_part);
+    LAUNCHED(k_kge_grad);
+    return PS_OK;
+  };
+  ps_status r;
+  if (cdim <= 64) r = launch(k_kge_grad<1>);
+  else if (cdim <= 128) r = launch(k_kge_grad<2>);
+  else r = launch(k_kge_grad<4>);   // cdim <= 256: the store holds rows of at most 512 floats
+  if (r) return r;
+  if (loss) {
+    hipLaunchKernelGGL(k_sum_loss, dim3(1), dim3(BLOCK), 0, st, p.loss_part, grid, loss);
+    LAUNCHED(k_sum_loss);
+  }
+  return run_reduce(s, p.sb, ks, SrcKGE{perm, p.mat, p.base, p.coef, per, n_head_neg, s->dim}, n, {all_keys(s)}, st);
 }
 
 ps_status ps_step_sgns(ps_store* s, const int32_t* centre, const int32_t* ctx, const int32_t* neg, int64_t B,
                        int32_t window, int32_t n_neg, int64_t out_key_offset, double* loss, void* ws,
                        size_t ws_bytes, void* stream) {
-  (void)s; (void)centre; (void)ctx; (void)neg; (void)B; (void)window; (void)n_neg; (void)out_key_offset;
-  (void)loss; (void)ws; (void)ws_bytes; (void)stream;
-  return fail(PS_ERR_UNSUPPORTED, "ps_step_sgns not built yet");
+  if (ps_status st = check_store(s)) return st;
+  if (window < 0 || n_neg < 0) return fail(PS_ERR_INVALID, "negative window or n_neg");
+  const int slots = 2 * window;
+  const int64_t per = 1 + (int64_t)slots * (1 + n_neg);
+  if (ps_status st = check_n(B, per)) return st;
+  if (out_key_offset < 1 || out_key_offset >= s->num_keys)
+    return fail(PS_ERR_INVALID, "out_key_offset must split the table into input and output rows");
+  hipStream_t st = as_stream(stream);
+  if (B == 0) {
+    if (loss) {
+      hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(BLOCK), 0, st, reinterpret_cast<uint32_t*>(loss), int64_t(2));
+      LAUNCHED(k_zero_words);
+    }
+    return PS_OK;
+  }
+  if (!centre || (slots > 0 && !ctx) || (slots > 0 && n_neg > 0 && !neg))
+    return fail(PS_ERR_INVALID, "centre, ctx or neg is NULL");
+  const int64_t n = B * per;
+  Plan p;
+  plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_SGNS, B, per, &p);
+  if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
+  hipLaunchKernelGGL(k_unit_valid<ValidSGNS>, dim3(small_grid(B, BLOCK, 1024)), dim3(BLOCK), 0, st,
+                     ValidSGNS{centre, ctx, neg, slots, n_neg, out_key_offset, s->num_keys}, B, p.ok, s->status);
+  LAUNCHED(k_unit_valid);
+  uint32_t *ks, *perm;
+  KeysSGNS kk{centre, ctx, neg, (int)per, slots, n_neg, out_key_offset, p.ok};
+  if (ps_status r = run_sort(s, kk, n, s->num_keys, p.sb, s->status, nullptr, false, st, &ks, &perm)) return r;
+  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st)) return r;
+  RowShape shape;
+  row_shape(s->dim, true, &shape);
+  ps_status r = with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
+    const int64_t grid = small_grid(B, BLOCK / L, LOSS_GRID);
+    {
+      Timed t(s, PS_KERNEL_TASKGRAD, st);
+      hipLaunchKernelGGL((k_sgns_grad<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->dim, centre, ctx, neg,
+                         B, slots, n_neg, out_key_offset, p.ok, p.mat, p.coef, p.loss_part);
+    }
+    LAUNCHED(k_sgns_grad);
+    if (loss) {
+      hipLaunchKernelGGL(k_sum_loss, dim3(1), dim3(BLOCK), 0, st, p.loss_part, grid, loss);
+      LAUNCHED(k_sum_loss);
+    }
+    return PS_OK;
+  });
+  if (r) return r;
+  // output rows first: their gradients read the input rows, which are updated second
+  SrcSGNS src{perm, p.mat, p.coef, centre, s->W, (int)per, s->dim};
+  return run_reduce(s, p.sb, ks, src, n,
+                    {KeyRange{(uint32_t)out_key_offset, (uint32_t)s->num_keys}, KeyRange{0u, (uint32_t)out_key_offset}},
+                    st);
 }
 
 ps_status ps_step_ctr(ps_store* s, const int64_t* keys, const float* label, int64_t B, int32_t F, double* loss,
                       void* ws, size_t ws_bytes, void* stream) {
-  (void)s; (void)keys; (void)label; (void)B; (void)F; (void)loss; (void)ws; (void)ws_bytes; (void)stream;
-  return fail(PS_ERR_UNSUPPORTED, "ps_step_ctr not built yet");
+  if (ps_status st = check_store(s)) return st;
+  if (F < 1) return fail(PS_ERR_INVALID, "need F >= 1");
+  if (ps_status st = check_n(B, F)) return st;
+  hipStream_t st = as_stream(stream);
+  if (B == 0) {
+    if (loss) {
+      hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(BLOCK), 0, st, reinterpret_cast<uint32_t*>(loss), int64_t(2));
+      LAUNCHED(k_zero_words);
+    }
+    return PS_OK;
+  }
+  if (!keys || !label) return fail(PS_ERR_INVALID, "keys or label is NULL");
+  const int64_t n = B * F;
+  Plan p;
+  plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_CTR, B, F, &p);
+  if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
+  hipLaunchKernelGGL(k_unit_valid<ValidCTR>, dim3(small_grid(B, BLOCK, 1024)), dim3(BLOCK), 0, st,
+                     ValidCTR{keys, F, s->num_keys}, B, p.ok, s->status);
+  LAUNCHED(k_unit_valid);
+  uint32_t *ks, *perm;
+  if (ps_status r = run_sort(s, KeysCTR{keys, F, p.ok}, n, s->num_keys, p.sb, s->status, nullptr, true, st, &ks,
+                             &perm))
+    return r;
+  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st)) return r;
+  RowShape shape;
+  row_shape(s->dim, true, &shape);
+  ps_status r = with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
+    const int64_t grid = small_grid(B, BLOCK / L, LOSS_GRID);
+    {
+      Timed t(s, PS_KERNEL_TASKGRAD, st);
+      hipLaunchKernelGGL((k_ctr_grad<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->dim, keys, label, B, F,
+                         p.ok, p.sb.rank, p.grads, p.loss_part);
+    }
+    LAUNCHED(k_ctr_grad);
+    if (loss) {
+      hipLaunchKernelGGL(k_sum_loss, dim3(1), dim3(BLOCK), 0, st, p.loss_part, grid, loss);
+      LAUNCHED(k_sum_loss);
+    }
+    return PS_OK;
+  });
+  if (r) return r;
+  return run_reduce(s, p.sb, ks, SrcSorted{p.grads, s->dim}, n, {all_keys(s)}, st);
 }
 
 ps_status ps_get_error(ps_store* s, void* stream) {

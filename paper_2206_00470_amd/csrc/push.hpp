@@ -211,7 +211,7 @@ __global__ __launch_bounds__(BLOCK) void k_seg_finalize(SegView sv, float* __res
     double acc[NE];
 #pragma unroll
     for (int q = 0; q < NE; ++q) acc[q] = 0.0;
-    constexpr int FU = 8;   // partial rows in flight per group
+    constexpr int FU = NE <= 4 ? 8 : 4;   // partial rows in flight per group
     int64_t k = g;
     for (; k + (FU - 1) * GPB < m; k += FU * GPB) {
       double x[FU][NE];

@@ -103,4 +103,512 @@ __global__ __launch_bounds__(BLOCK) void k_mf_grad(const float* __restrict__ W, 
   if (threadIdx.x == 0) loss_part[blockIdx.x] = lsum;
 }
 
+// ------------------------------------------------------------------ shared pieces
+__device__ __forceinline__ double sigmoid_d(double x) {
+  if (x >= 0.0) return 1.0 / (1.0 + exp(-x));
+  const double e = exp(x);
+  return e / (1.0 + e);
+}
+
+__device__ __forceinline__ double softplus_d(double x) {
+  return x > 0.0 ? x + log1p(exp(-x)) : log1p(exp(x));
+}
+
+// Per-unit validity: a unit (sample, triple, centre) with any id outside its
+// table is skipped entirely and raises the sticky error flag.
+template <class V>
+__global__ __launch_bounds__(BLOCK) void k_unit_valid(V v, int64_t B, uint8_t* __restrict__ ok,
+                                                      int32_t* __restrict__ err) {
+  int bad = 0;
+  for (int64_t b = (int64_t)blockIdx.x * BLOCK + threadIdx.x; b < B; b += (int64_t)gridDim.x * BLOCK) {
+    const bool o = v(b);
+    ok[b] = o;
+    bad |= !o;
+  }
+  if (__syncthreads_or(bad) && threadIdx.x == 0) atomicOr(err, 1);
+}
+
+// ------------------------------------------------------------------ CTR
+struct ValidCTR {
+  const int64_t* keys;
+  int F;
+  int64_t num_keys;
+  __device__ bool operator()(int64_t b) const {
+    for (int f = 0; f < F; ++f) {
+      const int64_t k = keys[b * F + f];
+      if (k < 0 || k >= num_keys) return false;
+    }
+    return true;
+  }
+};
+
+struct KeysCTR {
+  const int64_t* keys;
+  int F;
+  const uint8_t* ok;
+  __device__ int64_t operator()(int64_t i) const {
+    return ok[(uint32_t)i / (uint32_t)F] ? keys[i] : ABSENT;
+  }
+};
+
+// One row group per sample (e_f = W[keys[b,f]], label y):
+//   S = sum_f e_f ;  z = sum_{f<g} <e_f, e_g> = (|S|^2 - sum_f |e_f|^2) / 2
+//   loss += softplus(z) - y z ;  grad e_f = (sigmoid(z) - y)(S - e_f)
+// Gradient rows go to their sorted positions rank[b*F + f].
+template <int L, int NV, int VW>
+__global__ __launch_bounds__(BLOCK) void k_ctr_grad(const float* __restrict__ W, int dim,
+                                                    const int64_t* __restrict__ keys,
+                                                    const float* __restrict__ label, int64_t B, int F,
+                                                    const uint8_t* __restrict__ ok,
+                                                    const uint32_t* __restrict__ rank, float* __restrict__ grads,
+                                                    double* __restrict__ loss_part) {
+  constexpr int GPB = BLOCK / L;
+  constexpr int NE = NV * VW;
+  __shared__ double sm[WAVES_PER_BLOCK];
+  const int gl = threadIdx.x % L;
+  double lsum = 0.0;
+  for (int64_t b = (int64_t)blockIdx.x * GPB + threadIdx.x / L; b < B; b += (int64_t)gridDim.x * GPB) {
+    if (!ok[b]) continue;
+    double S[NE];
+#pragma unroll
+    for (int e = 0; e < NE; ++e) S[e] = 0.0;
+    double sq = 0.0;
+    for (int f = 0; f < F; ++f) {
+      const float* row = W + keys[b * F + f] * dim;
+      float x[NE];
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int c = (gl + v * L) * VW;
+        if (c < dim) load_frag<VW>(row + c, x + v * VW);
+        else
+#pragma unroll
+          for (int e = 0; e < VW; ++e) x[v * VW + e] = 0.0f;
+      }
+#pragma unroll
+      for (int e = 0; e < NE; ++e) {
+        S[e] += (double)x[e];
+        sq += (double)x[e] * (double)x[e];
+      }
+    }
+    double ss = 0.0;
+#pragma unroll
+    for (int e = 0; e < NE; ++e) ss += S[e] * S[e];
+    ss = group_sum<L>(ss);
+    sq = group_sum<L>(sq);
+    const double z = 0.5 * (ss - sq);
+    const double y = (double)label[b];
+    const double a = sigmoid_d(z) - y;
+    if (gl == 0) lsum += softplus_d(z) - y * z;
+    for (int f = 0; f < F; ++f) {
+      const float* row = W + keys[b * F + f] * dim;
+      float* dst = grads + (int64_t)rank[b * F + f] * dim;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int c = (gl + v * L) * VW;
+        if (c < dim) {
+          float x[VW], g[VW];
+          load_frag<VW>(row + c, x);
+#pragma unroll
+          for (int e = 0; e < VW; ++e) g[e] = (float)(a * (S[v * VW + e] - (double)x[e]));
+          store_frag<VW>(dst + c, g);
+        }
+      }
+    }
+  }
+  lsum = block_sum_double(lsum, sm);
+  if (threadIdx.x == 0) loss_part[blockIdx.x] = lsum;
+}
+
+// ------------------------------------------------------------------ KGE (ComplEx)
+struct ValidKGE {
+  const int32_t *head, *rel, *tail, *neg;
+  int n_neg;
+  int64_t rel_off, num_keys;
+  __device__ bool operator()(int64_t t) const {
+    auto okk = [&](int64_t k) { return k >= 0 && k < num_keys; };
+    if (!okk(head[t]) || !okk(tail[t]) || rel[t] < 0 || !okk(rel_off + rel[t])) return false;
+    for (int j = 0; j < n_neg; ++j)
+      if (!okk(neg[t * n_neg + j])) return false;
+    return true;
+  }
+};
+
+// Occurrences of triple t: 0 = head, 1 = relation, 2 = tail, 3 + j = negative j.
+struct KeysKGE {
+  const int32_t *head, *rel, *tail, *neg;
+  int per, n_neg;
+  int64_t rel_off;
+  const uint8_t* ok;
+  __device__ int64_t operator()(int64_t i) const {
+    const uint32_t t = (uint32_t)i / (uint32_t)per;
+    const uint32_t q = (uint32_t)i - t * (uint32_t)per;
+    if (!ok[t]) return ABSENT;
+    if (q == 0) return head[t];
+    if (q == 1) return rel_off + rel[t];
+    if (q == 2) return tail[t];
+    return neg[(int64_t)t * n_neg + (q - 3)];
+  }
+};
+
+// One wavefront per triple; lane l holds complex components k = l + 64 i.
+// A row is [Re(0..C-1) | Im(0..C-1)].  With f = d phi/d s at (r, o) and
+// h = d phi/d o at (s, r), a head-corrupted triple scores phi(x,r,o) = <x, f>
+// and a tail-corrupted one phi(s,r,x) = <x, h>, so the gradient row of each
+// negative occurrence is (its coefficient) x (f or h): the kernel stores the
+// fp64 rows f, h per triple and one fp64 coefficient per negative, and
+// writes the full fp32 gradient rows of s, r and o.
+template <int KPL>
+__global__ __launch_bounds__(BLOCK) void k_kge_grad(const float* __restrict__ W, int dim,
+                                                    const int32_t* __restrict__ head,
+                                                    const int32_t* __restrict__ rel,
+                                                    const int32_t* __restrict__ tail,
+                                                    const int32_t* __restrict__ neg, int64_t B, int n_neg,
+                                                    int n_head, int64_t rel_off, const uint8_t* __restrict__ ok,
+                                                    float* __restrict__ mat, double* __restrict__ base,
+                                                    double* __restrict__ coef, double* __restrict__ loss_part) {
+  constexpr int JB = 4;   // negatives in flight
+  __shared__ double sm[WAVES_PER_BLOCK];
+  const int cdim = dim / 2;
+  const int lane = lane_id();
+  const int64_t per = 3 + n_neg;
+  double lsum = 0.0;
+  for (int64_t t = (int64_t)blockIdx.x * WAVES_PER_BLOCK + threadIdx.x / WAVE; t < B;
+       t += (int64_t)gridDim.x * WAVES_PER_BLOCK) {
+    if (!ok[t]) continue;
+    const float* sp = W + (int64_t)head[t] * dim;
+    const float* rp = W + (rel_off + rel[t]) * dim;
+    const float* op = W + (int64_t)tail[t] * dim;
+    double sR[KPL], sI[KPL], rR[KPL], rI[KPL], oR[KPL], oI[KPL];
+#pragma unroll
+    for (int i = 0; i < KPL; ++i) {
+      const int k = lane + WAVE * i;
+      const bool in = k < cdim;
+      sR[i] = in ? (double)sp[k] : 0.0; sI[i] = in ? (double)sp[cdim + k] : 0.0;
+      rR[i] = in ? (double)rp[k] : 0.0; rI[i] = in ? (double)rp[cdim + k] : 0.0;
+      oR[i] = in ? (double)op[k] : 0.0; oI[i] = in ? (double)op[cdim + k] : 0.0;
+    }
+    double fR[KPL], fI[KPL], hR[KPL], hI[KPL];
+    double gsR[KPL], gsI[KPL], grR[KPL], grI[KPL], goR[KPL], goI[KPL];
+    double part = 0.0;
+#pragma unroll
+    for (int i = 0; i < KPL; ++i) {
+      fR[i] = rR[i] * oR[i] + rI[i] * oI[i];
+      fI[i] = rR[i] * oI[i] - rI[i] * oR[i];
+      hR[i] = sR[i] * rR[i] - sI[i] * rI[i];
+      hI[i] = sI[i] * rR[i] + sR[i] * rI[i];
+      part += sR[i] * rR[i] * oR[i];
+      part += sI[i] * rR[i] * oI[i];
+      part += sR[i] * rI[i] * oI[i];
+      part -= sI[i] * rI[i] * oR[i];
+    }
+    const double phi = group_sum<WAVE>(part);
+    double c = -sigmoid_d(-phi);
+    if (lane == 0) lsum += softplus_d(-phi);
+#pragma unroll
+    for (int i = 0; i < KPL; ++i) {
+      gsR[i] = c * fR[i];
+      gsI[i] = c * fI[i];
+      grR[i] = c * (sR[i] * oR[i] + sI[i] * oI[i]);
+      grI[i] = c * (sR[i] * oI[i] - sI[i] * oR[i]);
+      goR[i] = c * hR[i];
+      goI[i] = c * hI[i];
+      const int k = lane + WAVE * i;
+      if (k < cdim) {
+        double* fb = base + (2 * t) * dim;
+        double* hb = base + (2 * t + 1) * dim;
+        fb[k] = fR[i]; fb[cdim + k] = fI[i];
+        hb[k] = hR[i]; hb[cdim + k] = hI[i];
+      }
+    }
+    const int32_t* nt = neg + t * n_neg;
+    for (int j0 = 0; j0 < n_neg; j0 += JB) {
+      float xR[JB][KPL], xI[JB][KPL];
+#pragma unroll
+      for (int jj = 0; jj < JB; ++jj) {
+        const int j = j0 + jj;
+        const float* xp = W + (int64_t)(j < n_neg ? nt[j] : 0) * dim;
+#pragma unroll
+        for (int i = 0; i < KPL; ++i) {
+          const int k = lane + WAVE * i;
+          const bool in = k < cdim && j < n_neg;
+          xR[jj][i] = in ? xp[k] : 0.0f;
+          xI[jj][i] = in ? xp[cdim + k] : 0.0f;
+        }
+      }
+      double ph[JB];
+#pragma unroll
+      for (int jj = 0; jj < JB; ++jj) {
+        const bool hd = j0 + jj < n_head;
+        double p = 0.0;
+#pragma unroll
+        for (int i = 0; i < KPL; ++i)
+          p += hd ? ((double)xR[jj][i] * fR[i] + (double)xI[jj][i] * fI[i])
+                  : ((double)xR[jj][i] * hR[i] + (double)xI[jj][i] * hI[i]);
+        ph[jj] = p;
+      }
+#pragma unroll
+      for (int jj = 0; jj < JB; ++jj) ph[jj] = group_sum<WAVE>(ph[jj]);
+#pragma unroll
+      for (int jj = 0; jj < JB; ++jj) {
+        const int j = j0 + jj;
+        if (j >= n_neg) break;
+        const double cj = sigmoid_d(ph[jj]);
+        if (lane == 0) {
+          lsum += softplus_d(ph[jj]);
+          coef[t * per + 3 + j] = cj;
+        }
+        if (j < n_head) {   // (x, r, o): d/dr and d/do
+#pragma unroll
+          for (int i = 0; i < KPL; ++i) {
+            const double x_r = xR[jj][i], x_i = xI[jj][i];
+            grR[i] += cj * (x_r * oR[i] + x_i * oI[i]);
+            grI[i] += cj * (x_r * oI[i] - x_i * oR[i]);
+            goR[i] += cj * (x_r * rR[i] - x_i * rI[i]);
+            goI[i] += cj * (x_i * rR[i] + x_r * rI[i]);
+          }
+        } else {            // (s, r, x): d/ds and d/dr
+#pragma unroll
+          for (int i = 0; i < KPL; ++i) {
+            const double x_r = xR[jj][i], x_i = xI[jj][i];
+            gsR[i] += cj * (rR[i] * x_r + rI[i] * x_i);
+            gsI[i] += cj * (rR[i] * x_i - rI[i] * x_r);
+            grR[i] += cj * (sR[i] * x_r + sI[i] * x_i);
+            grI[i] += cj * (sR[i] * x_i - sI[i] * x_r);
+          }
+        }
+      }
+    }
+    float* ms = mat + (3 * t) * dim;
+#pragma unroll
+    for (int i = 0; i < KPL; ++i) {
+      const int k = lane + WAVE * i;
+      if (k < cdim) {
+        ms[k] = (float)gsR[i];
+        ms[cdim + k] = (float)gsI[i];
+        ms[dim + k] = (float)grR[i];
+        ms[dim + cdim + k] = (float)grI[i];
+        ms[2 * dim + k] = (float)goR[i];
+        ms[2 * dim + cdim + k] = (float)goI[i];
+      }
+    }
+  }
+  lsum = block_sum_double(lsum, sm);
+  if (threadIdx.x == 0) loss_part[blockIdx.x] = lsum;
+}
+
+// Gradient source of the KGE push.
+struct SrcKGE {
+  const uint32_t* perm;
+  const float* mat;
+  const double* base;
+  const double* coef;
+  int per, n_head, dim;
+  template <int L, int NV, int VW>
+  __device__ __forceinline__ void load(int64_t j, int gl, float* x) const {
+    const uint32_t occ = perm[j];
+    const uint32_t t = occ / (uint32_t)per;
+    const uint32_t q = occ - t * (uint32_t)per;
+    if (q < 3) {
+      const float* row = mat + ((int64_t)t * 3 + q) * dim;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int c = (gl + v * L) * VW;
+        if (c < dim) load_frag<VW>(row + c, x + v * VW);
+      }
+    } else {
+      const double cj = coef[occ];
+      const double* row = base + ((int64_t)t * 2 + ((int)q - 3 < n_head ? 0 : 1)) * dim;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int c = (gl + v * L) * VW;
+        if (c < dim)
+#pragma unroll
+          for (int e = 0; e < VW; ++e) x[v * VW + e] = (float)(cj * row[c + e]);
+      }
+    }
+  }
+};
+
+// ------------------------------------------------------------------ SGNS
+struct ValidSGNS {
+  const int32_t *centre, *ctx, *neg;
+  int slots, K;
+  int64_t out_off, num_keys;
+  __device__ bool operator()(int64_t b) const {
+    const int64_t c = centre[b];
+    if (c < 0 || c >= out_off || c >= num_keys) return false;
+    const int64_t vout = num_keys - out_off;
+    for (int q = 0; q < slots; ++q) {
+      const int64_t x = ctx[b * slots + q];
+      if (x == -1) continue;
+      if (x < 0 || x >= vout) return false;
+      for (int k = 0; k < K; ++k) {
+        const int64_t y = neg[(b * slots + q) * K + k];
+        if (y < 0 || y >= vout) return false;
+      }
+    }
+    return true;
+  }
+};
+
+// Occurrences of centre b: 0 = centre (input table), then for slot q the
+// context word and its K negatives (output table); absent slots are ABSENT.
+struct KeysSGNS {
+  const int32_t *centre, *ctx, *neg;
+  int per, slots, K;
+  int64_t out_off;
+  const uint8_t* ok;
+  __device__ int64_t operator()(int64_t i) const {
+    const uint32_t b = (uint32_t)i / (uint32_t)per;
+    const uint32_t q = (uint32_t)i - b * (uint32_t)per;
+    if (!ok[b]) return ABSENT;
+    if (q == 0) return centre[b];
+    const uint32_t r = q - 1;
+    const uint32_t slot = r / (uint32_t)(K + 1);
+    const uint32_t k = r - slot * (uint32_t)(K + 1);
+    const int64_t cx = ctx[(int64_t)b * slots + slot];
+    if (cx == -1) return ABSENT;
+    if (k == 0) return out_off + cx;
+    return out_off + neg[((int64_t)b * slots + slot) * K + (k - 1)];
+  }
+};
+
+// One row group per centre (v = input row of the centre word): for each
+// present slot, the context word (x = <u, v>, a = -sigmoid(-x), loss
+// softplus(-x)) and its negatives (a = sigmoid(x), loss softplus(x)).
+// Stores one fp64 coefficient a per output occurrence (its gradient row is
+// a*v) and the centre's fp32 gradient row sum(a*u).
+template <int L, int NV, int VW>
+__global__ __launch_bounds__(BLOCK) void k_sgns_grad(const float* __restrict__ W, int dim,
+                                                     const int32_t* __restrict__ centre,
+                                                     const int32_t* __restrict__ ctx,
+                                                     const int32_t* __restrict__ neg, int64_t B, int slots, int K,
+                                                     int64_t out_off, const uint8_t* __restrict__ ok,
+                                                     float* __restrict__ mat, double* __restrict__ coef,
+                                                     double* __restrict__ loss_part) {
+  constexpr int GPB = BLOCK / L;
+  constexpr int NE = NV * VW;
+  constexpr int JB = 4;   // output rows in flight
+  __shared__ double sm[WAVES_PER_BLOCK];
+  const int gl = threadIdx.x % L;
+  const int64_t per = 1 + (int64_t)slots * (K + 1);
+  double lsum = 0.0;
+  for (int64_t b = (int64_t)blockIdx.x * GPB + threadIdx.x / L; b < B; b += (int64_t)gridDim.x * GPB) {
+    if (!ok[b]) continue;
+    const float* vp = W + (int64_t)centre[b] * dim;
+    float v[NE];
+    double gv[NE];
+#pragma unroll
+    for (int q = 0; q < NV; ++q) {
+      const int c = (gl + q * L) * VW;
+      if (c < dim) load_frag<VW>(vp + c, v + q * VW);
+      else
+#pragma unroll
+        for (int e = 0; e < VW; ++e) v[q * VW + e] = 0.0f;
+    }
+#pragma unroll
+    for (int e = 0; e < NE; ++e) gv[e] = 0.0;
+    for (int q = 0; q < slots; ++q) {
+      const int64_t cx = ctx[b * slots + q];
+      if (cx == -1) continue;
+      const int32_t* nq = neg + (b * slots + q) * K;
+      for (int k0 = 0; k0 <= K; k0 += JB) {
+        float u[JB][NE];
+#pragma unroll
+        for (int jj = 0; jj < JB; ++jj) {
+          const int k = k0 + jj;
+          const int64_t id = k == 0 ? cx : (k <= K ? nq[k - 1] : cx);
+          const float* up = W + (out_off + id) * dim;
+#pragma unroll
+          for (int q2 = 0; q2 < NV; ++q2) {
+            const int c = (gl + q2 * L) * VW;
+            if (c < dim) load_frag<VW>(up + c, u[jj] + q2 * VW);
+            else
+#pragma unroll
+              for (int e = 0; e < VW; ++e) u[jj][q2 * VW + e] = 0.0f;
+          }
+        }
+        double x[JB];
+#pragma unroll
+        for (int jj = 0; jj < JB; ++jj) {
+          double p = 0.0;
+#pragma unroll
+          for (int e = 0; e < NE; ++e) p += (double)u[jj][e] * (double)v[e];
+          x[jj] = p;
+        }
+#pragma unroll
+        for (int jj = 0; jj < JB; ++jj) x[jj] = group_sum<L>(x[jj]);
+#pragma unroll
+        for (int jj = 0; jj < JB; ++jj) {
+          const int k = k0 + jj;
+          if (k > K) break;
+          double a;
+          if (k == 0) {
+            a = -sigmoid_d(-x[jj]);
+            if (gl == 0) lsum += softplus_d(-x[jj]);
+          } else {
+            a = sigmoid_d(x[jj]);
+            if (gl == 0) lsum += softplus_d(x[jj]);
+          }
+          if (gl == 0) coef[b * per + 1 + (int64_t)q * (K + 1) + k] = a;
+#pragma unroll
+          for (int e = 0; e < NE; ++e) gv[e] += a * (double)u[jj][e];
+        }
+      }
+    }
+    float* dst = mat + b * dim;
+#pragma unroll
+    for (int q = 0; q < NV; ++q) {
+      const int c = (gl + q * L) * VW;
+      if (c < dim) {
+        float g[VW];
+#pragma unroll
+        for (int e = 0; e < VW; ++e) g[e] = (float)gv[q * VW + e];
+        store_frag<VW>(dst + c, g);
+      }
+    }
+  }
+  lsum = block_sum_double(lsum, sm);
+  if (threadIdx.x == 0) loss_part[blockIdx.x] = lsum;
+}
+
+// Gradient source of the SGNS push: the centre occurrence reads its stored
+// row; an output occurrence of centre b is a * v with v the centre's input
+// row, read from the table before the input rows are updated.
+struct SrcSGNS {
+  const uint32_t* perm;
+  const float* mat;
+  const double* coef;
+  const int32_t* centre;
+  const float* W;
+  int per, dim;
+  template <int L, int NV, int VW>
+  __device__ __forceinline__ void load(int64_t j, int gl, float* x) const {
+    const uint32_t occ = perm[j];
+    const uint32_t b = occ / (uint32_t)per;
+    const uint32_t q = occ - b * (uint32_t)per;
+    if (q == 0) {
+      const float* row = mat + (int64_t)b * dim;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int c = (gl + v * L) * VW;
+        if (c < dim) load_frag<VW>(row + c, x + v * VW);
+      }
+    } else {
+      const double a = coef[occ];
+      const float* row = W + (int64_t)centre[b] * dim;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int c = (gl + v * L) * VW;
+        if (c < dim) {
+          float t[VW];
+          load_frag<VW>(row + c, t);
+#pragma unroll
+          for (int e = 0; e < VW; ++e) x[v * VW + e] = (float)(a * (double)t[e]);
+        }
+      }
+    }
+  }
+};
+
 }  // namespace adapm

@@ -242,6 +242,8 @@ class CTRConfig:
         return b * self.n_fields
 
     def vocab_sizes(self) -> list[int]:
+        if self.n_fields == 1:
+            return [self.vocab_max]
         f = np.arange(self.n_fields, dtype=np.float64)
         span = np.log10(self.vocab_max / self.vocab_min)
         return [int(round(self.vocab_min * 10 ** (span * x / (self.n_fields - 1)))) for x in f]

@@ -53,6 +53,9 @@ def test_create_rejects_bad_arguments_on_host():
     assert L.ps_create(C.byref(h), 10, 0, fake, other, 0.1, 0.0, None) == _lib.PS_ERR_UNSUPPORTED
     assert L.ps_create(C.byref(h), 10, 4096, fake, other, 0.1, 0.0, None) == _lib.PS_ERR_UNSUPPORTED
     assert L.ps_create(C.byref(h), 10, 513, fake, other, 0.1, 0.0, None) == _lib.PS_ERR_UNSUPPORTED
+    for wide in (516, 600, 1024, 2048):   # rows wider than 512 floats are not supported
+        assert L.ps_create(C.byref(h), 10, wide, fake, other, 0.1, 0.0, None) == _lib.PS_ERR_UNSUPPORTED
+    assert L.ps_create(C.byref(h), 10, 512, fake, None, 0.1, 0.0, None) == _lib.PS_ERR_INVALID
     assert L.ps_create(C.byref(h), 10, 4, None, other, 0.1, 0.0, None) == _lib.PS_ERR_INVALID
     assert L.ps_create(C.byref(h), 10, 4, fake, fake, 0.1, 0.0, None) == _lib.PS_ERR_INVALID
     assert L.ps_create(C.byref(h), 10, 4, C.c_void_p(0x1004), other, 0.1, 0.0, None) == _lib.PS_ERR_INVALID

@@ -27,7 +27,7 @@ def make_store(K, d, seed, g_fill=False):
 
 # ------------------------------------------------------------------ pull
 @pytest.mark.parametrize("K,d,n", [(1, 4, 1), (5000, 16, 4097), (5000, 100, 100_003), (3000, 3, 777),
-                                   (3000, 300, 5000), (1 << 16, 64, 70_000), (2000, 256, 3000), (700, 2048, 999)])
+                                   (3000, 300, 5000), (1 << 16, 64, 70_000), (2000, 256, 3000), (700, 512, 999)])
 def test_pull_bitexact(K, d, n):
     say(f"pull K={K} d={d} n={n}")
     W, G = make_store(K, d, 7)
@@ -115,7 +115,7 @@ PUSH_CASES = [
     (6000, 300, 20_000, 0.75, False),
     (1 << 16, 64, 212_992, 1.05, False),
     (4000, 256, 50_000, 1.0, True),
-    (500, 2048, 3000, 1.0, False),
+    (500, 512, 3000, 1.0, False),
     (1000, 500, 100_000, None, False),   # every key duplicated ~100x
 ]
 
