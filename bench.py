@@ -1,17 +1,19 @@
 #!/usr/bin/env python3
 """Throughput of the sparse parameter-store training step on one MI355X.
 
-Workload: matrix factorization of a synthetic 10,000,000 x 1,000,000 matrix
-(rows uniform, columns Zipf 1.1), rank-100 fp32 factors with fp32 AdaGrad
-accumulators (11M keys x 100, 8.8 GB of W+G in HBM), 1,048,576 entries per
-step.  One step = ps_step_mf: key intake, stable radix sort of the 2,097,152
-key occurrences, segment boundaries, per-entry gradients from the pulled
-rows, fp64 per-key merge and the AdaGrad row update.
+Default workload: matrix factorization of a synthetic 10,000,000 x 1,000,000
+matrix (rows uniform, columns Zipf 1.1), rank-100 fp32 factors with fp32
+AdaGrad accumulators (11M keys x 100, 8.8 GB of W+G in HBM), 1,048,576
+entries per step.  One step = ps_step_mf: key intake, stable radix sort of
+the 2,097,152 key occurrences, segment boundaries, per-entry gradients from
+the pulled rows, fp64 per-key merge and the AdaGrad row update.
 
-Prints one JSON line: rows pulled + pushed per second (2 x 2,097,152 row
-accesses per step), the roofline of the dominant kernel measured with HIP
-events during the timed steps, the push-only and pull-only rates, and the
-CPU oracle timed on the host.
+--workload selects one of the other task shapes (mf_tiny, kge, sgns, ctr).
+
+Prints one JSON line: rows pulled + pushed per second (2 row accesses per
+key occurrence), the roofline of the dominant kernel measured with HIP
+events during the timed steps, push-only / pull-only rates (MF), and the CPU
+oracle timed on the host.
 """
 from __future__ import annotations
 
@@ -35,9 +37,12 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="mf", choices=["mf", "mf_tiny", "kge", "sgns", "ctr"])
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="bound on the CPU-oracle sample (0 = skip)")
     ap.add_argument("--no-ops", action="store_true", help="skip the pull-only / push-only measurements")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a 4 GiB device-to-device copy (reference for HBM counters)")
     return ap.parse_args()
 
 
@@ -51,10 +56,10 @@ def source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def counter_traffic(kernel: str):
+def counter_traffic(workload: str, kernel: str):
     """HBM bytes per launch from the committed rocprofv3 counter summary, if
     it was taken on the current kernel sources (else None)."""
-    path = os.path.join(ROOT, "profiles", "counters_mf_10Mx1M.json")
+    path = os.path.join(ROOT, "profiles", f"counters_{workload}.json")
     try:
         with open(path) as f:
             data = json.load(f)
@@ -64,6 +69,100 @@ def counter_traffic(kernel: str):
         return None
     k = data.get("kernels", {}).get(kernel)
     return None if k is None else k.get("hbm_bytes_per_launch")
+
+
+# ---------------------------------------------------------------------------- workloads
+class Bench:
+    """One workload: its table, resident step batches, the step call, the
+    algorithmic bytes of its two big kernels and the oracle step."""
+
+    def __init__(self, name, dev, nbatches):
+        import torch
+        from paper_2206_00470_amd import workloads as wls
+
+        self.name = name
+        cfgs = {"mf": wls.MF_10Mx1M, "mf_tiny": wls.MF_TINY, "kge": wls.KGE_COMPLEX,
+                "sgns": wls.SGNS_1M, "ctr": wls.CTR_33M}
+        self.cfg = cfg = cfgs[name]
+        self.wl = wls.workload(cfg)
+        self.dev = dev
+        self.dim = cfg.dim
+        self.R = 4 * cfg.dim
+        self.W = self.wl.init_table()
+        T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+        self.T = T
+        self.batches, self.host_batches, self.occ, self.uniq = [], [], [], []
+        for i in range(nbatches):
+            bt = self.wl.batch(i)
+            self.host_batches.append(bt)
+            self.batches.append({k: T(v) for k, v in bt.__dict__.items()})
+            keys = self.keys_of(bt)
+            self.occ.append(keys.size)
+            self.uniq.append(np.unique(keys).size)
+
+    def keys_of(self, bt):
+        c = self.cfg
+        if self.name in ("mf", "mf_tiny"):
+            return np.concatenate([bt.row.astype(np.int64), c.n_rows + bt.col.astype(np.int64)])
+        if self.name == "kge":
+            return np.concatenate([bt.head, c.n_ent + bt.rel.astype(np.int64), bt.tail, bt.neg.ravel()]).astype(np.int64)
+        if self.name == "sgns":
+            ctx = bt.ctx.astype(np.int64)
+            neg = bt.neg.astype(np.int64)
+            present = ctx >= 0
+            return np.concatenate([bt.centre.astype(np.int64), c.vocab + ctx[present],
+                                   c.vocab + neg[present].ravel()])
+        return bt.keys.ravel()
+
+    def step(self, store, i, loss):
+        c, b = self.cfg, self.batches[i % len(self.batches)]
+        if self.name in ("mf", "mf_tiny"):
+            store.step_mf(b["row"], b["col"], b["val"], c.n_rows, c.lam, loss=loss)
+        elif self.name == "kge":
+            store.step_kge(b["head"], b["rel"], b["tail"], b["neg"], c.n_head_neg, c.n_ent, loss=loss)
+        elif self.name == "sgns":
+            store.step_sgns(b["centre"], b["ctx"], b["neg"], c.window, c.vocab, loss=loss)
+        else:
+            store.step_ctr(b["keys"], b["label"], loss=loss)
+
+    def alg_bytes(self, i):
+        """Algorithmic (useful) bytes per launch of the merge kernel(s) and of
+        the task-gradient kernel for batch i; shared per-unit rows count once."""
+        c, bt = self.cfg, self.host_batches[i % len(self.host_batches)]
+        n, U, R = self.occ[i % len(self.occ)], self.uniq[i % len(self.uniq)], self.R
+        table = 4.0 * U * R                      # W and G read and written once per distinct key
+        if self.name in ("mf", "mf_tiny"):
+            B = bt.row.size
+            return {"segreduce": n * R + table,                   # gradient rows in sorted order
+                    "taskgrad": B * (12.0 + 2 * R + 2 * R + 8.0)}  # inputs, 2 gathers, 2 rows out, ranks
+        if self.name == "ctr":
+            B, F = bt.keys.shape
+            return {"segreduce": n * R + table,
+                    "taskgrad": B * (4.0 + F * (8.0 + R + R + 4.0))}
+        if self.name == "kge":
+            B, nn = bt.neg.shape
+            return {"segreduce": n * 4.0 + 3 * B * R + B * nn * 8.0 + 2 * B * 2 * R + table,
+                    "taskgrad": B * (12.0 + 4 * nn + (3 + nn) * R + 3 * R + 4 * R + 8 * nn)}
+        B = bt.centre.size                       # sgns
+        pairs = int((bt.ctx >= 0).sum())
+        out_occ = pairs * (1 + c.n_neg)
+        return {"segreduce": n * 4.0 + out_occ * 8.0 + 2 * B * R + table,
+                "taskgrad": B * (4.0 + 4 * bt.ctx.shape[1] * (1 + c.n_neg)) + (B + out_occ) * R + B * R
+                            + out_occ * 8.0}
+
+    def oracle_step(self, W, G, i):
+        import oracle
+        c, bt = self.cfg, self.wl.batch(i)
+        lr, eps = c.opt.lr, c.opt.eps
+        if self.name in ("mf", "mf_tiny"):
+            oracle.step_mf(W, G, bt.row, bt.col, bt.val, c.n_rows, c.lam, lr, eps)
+        elif self.name == "kge":
+            oracle.step_kge(W, G, bt.head, bt.rel, bt.tail, bt.neg, c.n_head_neg, c.n_ent, lr, eps)
+        elif self.name == "sgns":
+            oracle.step_sgns(W, G, bt.centre, bt.ctx, bt.neg, c.window, c.vocab, lr, eps)
+        else:
+            oracle.step_ctr(W, G, bt.keys, bt.label, lr, eps)
+        return self.keys_of(bt).size
 
 
 def main():
@@ -76,40 +175,22 @@ def main():
     import torch
 
     from paper_2206_00470_amd import Store, _lib
-    from paper_2206_00470_amd.workloads import MF_10Mx1M, MFWorkload, random_push
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
-    cfg = MF_10Mx1M
-    wl = MFWorkload(cfg)
     dev = torch.device("cuda:0")
-    B = cfg.batch
-    n = 2 * B
-    R = 4 * cfg.dim
-
     t0 = time.time()
-    W = wl.init_table()
-    Wt = torch.from_numpy(W).to(dev)
+    nb = max(1, min(args.steps + args.warmup, 8))
+    wb = Bench(args.workload, dev, nb)
+    cfg = wb.cfg
+    Wt = torch.from_numpy(wb.W).to(dev)
     Gt = torch.zeros_like(Wt)
     store = Store(Wt, Gt, cfg.opt.lr, cfg.opt.eps)
-
-    nb = max(1, min(args.steps + args.warmup, 8))
-    batches, uniq = [], []
-    for i in range(nb):
-        bt = wl.batch(i)
-        batches.append((torch.from_numpy(bt.row).to(dev), torch.from_numpy(bt.col).to(dev),
-                        torch.from_numpy(bt.val).to(dev)))
-        keys = np.concatenate([bt.row.astype(np.int64), cfg.n_rows + bt.col.astype(np.int64)])
-        uniq.append(np.unique(keys).size)
     loss = torch.empty(1, dtype=torch.float64, device=dev)
-    print(f"# setup {time.time() - t0:.1f}s: table {cfg.num_keys}x{cfg.dim}, {nb} batches resident",
+    print(f"# setup {time.time() - t0:.1f}s: {cfg.name}, table {cfg.num_keys}x{cfg.dim}, {nb} batches resident",
           file=sys.stderr, flush=True)
 
-    def step(i):
-        r, c, v = batches[i % nb]
-        store.step_mf(r, c, v, cfg.n_rows, cfg.lam, loss=loss)
-
     for i in range(args.warmup):
-        step(i)
+        wb.step(store, i, loss)
     torch.cuda.synchronize()
     assert store.error() == 0
 
@@ -120,55 +201,60 @@ def main():
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for i in range(args.steps):
-        step(args.warmup + i)
+        wb.step(store, args.warmup + i, loss)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     store.set_timing(False)
     assert store.error() == 0
-    kt = {name: store.read_timing(k) for name, k in
-          (("segreduce", _lib.PS_KERNEL_SEGREDUCE), ("taskgrad", _lib.PS_KERNEL_TASKGRAD),
-           ("scatter", _lib.PS_KERNEL_SCATTER))}
+    kt = {"segreduce": store.read_timing(_lib.PS_KERNEL_SEGREDUCE),
+          "taskgrad": store.read_timing(_lib.PS_KERNEL_TASKGRAD),
+          "scatter": store.read_timing(_lib.PS_KERNEL_SCATTER)}
 
+    idx = [args.warmup + i for i in range(args.steps)]
+    occ = float(np.mean([wb.occ[i % nb] for i in idx]))
+    U_avg = float(np.mean([wb.uniq[i % nb] for i in idx]))
     ms_per_step = elapsed * 1e3 / args.steps
-    rows_per_s = 2.0 * n * args.steps / elapsed
-    U_avg = float(np.mean([uniq[(args.warmup + i) % nb] for i in range(args.steps)]))
-
-    # algorithmic bytes per launch (useful bytes only)
-    alg = {
-        # gradient rows read in sorted order + W and G read and written for each distinct key
-        "segreduce": n * R + 4.0 * U_avg * R,
-        # entry inputs + two gathered rows + two gradient rows written + two rank words
-        "taskgrad": B * (12.0 + 2 * R + 2 * R + 8.0),
-    }
+    rows_per_s = 2.0 * occ / (ms_per_step * 1e-3)
+    alg = {k: float(np.mean([wb.alg_bytes(i)[k] for i in idx])) for k in ("segreduce", "taskgrad")}
+    # launches per step of the merge kernel: SGNS merges output rows, then input rows
+    seg_launches_per_step = 2 if args.workload == "sgns" else 1
     kernels = {}
     for name, nbytes in alg.items():
         ms, cnt = kt[name]
-        avg_ms = ms / max(cnt, 1)
-        kernels[name] = {"avg_ms": avg_ms, "launches": cnt, "alg_bytes": nbytes,
-                         "alg_GBps": nbytes / (avg_ms * 1e-3) / 1e9 if cnt else None}
-    dom = max(kernels, key=lambda k: kernels[k]["avg_ms"])
+        per_step_ms = ms / max(args.steps, 1)
+        nl = seg_launches_per_step if name == "segreduce" else 1
+        kernels[name] = {"avg_ms": ms / max(cnt, 1), "ms_per_step": per_step_ms, "launches": cnt,
+                         "alg_bytes_per_step": nbytes,
+                         "alg_GBps": nbytes / (per_step_ms * 1e-3) / 1e9 if cnt else None,
+                         "launches_per_step": nl}
+    kernels["scatter"] = {"ms_per_step": kt["scatter"][0] / max(args.steps, 1), "launches": kt["scatter"][1]}
+    dom = max(("segreduce", "taskgrad"), key=lambda k: kernels[k]["ms_per_step"])
     dk = kernels[dom]
-    kernel_symbol = {"segreduce": "k_segreduce", "taskgrad": "k_mf_grad"}[dom]
+    symbol = {"segreduce": "k_segreduce",
+              "taskgrad": {"mf": "k_mf_grad", "mf_tiny": "k_mf_grad", "kge": "k_kge_grad", "sgns": "k_sgns_grad",
+                           "ctr": "k_ctr_grad"}[args.workload]}[dom]
+    traffic = counter_traffic(args.workload, symbol)
     roofline = {
         "bound": "hbm",
-        "kernel": kernel_symbol,
+        "kernel": symbol,
         "achieved": round(dk["alg_GBps"], 1),
         "peak": HBM_PEAK_GBPS,
         "unit": "GB/s",
         "frac": round(dk["alg_GBps"] / HBM_PEAK_GBPS, 4),
-        "traffic": counter_traffic(kernel_symbol),
+        "traffic": traffic,
         "avg_ms": round(dk["avg_ms"], 4),
-        "alg_bytes_per_launch": int(dk["alg_bytes"]),
+        "alg_bytes_per_launch": int(dk["alg_bytes_per_step"] / dk["launches_per_step"]),
     }
 
-    # ------------------------------------------------------------ push-only / pull-only
+    # ------------------------------------------------------------ push-only / pull-only (MF)
     ops = {}
-    if not args.no_ops:
-        keys_np, grads_np = random_push(cfg.num_keys, n, cfg.dim, 7)
-        bt = wl.batch(100)
-        keys_np = np.concatenate([bt.row.astype(np.int64)[:, None],
-                                  cfg.n_rows + bt.col.astype(np.int64)[:, None]], axis=1).ravel()
+    if not args.no_ops and args.workload == "mf":
+        from paper_2206_00470_amd.workloads import random_push
+        n = int(wb.occ[0])
+        bt = wb.wl.batch(100)
+        keys_np = wb.keys_of(bt)
         U = np.unique(keys_np).size
+        _, grads_np = random_push(cfg.num_keys, n, cfg.dim, 7)
         keys = torch.from_numpy(keys_np).to(dev)
         grads = torch.from_numpy(grads_np).to(dev)
         del grads_np
@@ -189,6 +275,7 @@ def main():
         torch.cuda.synchronize()
         tl = (time.perf_counter() - t1) / reps
         assert store.error() == 0
+        R = wb.R
         push_alg = 8.0 * n + n * R + 4.0 * U * R
         pull_alg = 8.0 * n + U * R + n * R
         ops = {
@@ -198,25 +285,42 @@ def main():
         }
         del keys, grads, out
 
+    copy = None
+    if args.calibrate_copy:
+        a = torch.empty(1 << 30, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        a.fill_(1.0)
+        for _ in range(2):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for _ in range(5):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        tcp = (time.perf_counter() - t1) / 5
+        copy = {"bytes_read": a.numel() * 4, "bytes_written": b.numel() * 4, "ms": round(tcp * 1e3, 4),
+                "GBps": round(2 * a.numel() * 4 / tcp / 1e9, 1)}
+        del a, b
+
     # ------------------------------------------------------------ CPU oracle on the host
     cpu = None
     if args.cpu_seconds > 0:
-        import oracle
+        W = wb.W
         G = np.zeros_like(W)
-        done, tc0 = 0, time.perf_counter()
+        done, rows, tc0 = 0, 0, time.perf_counter()
         while True:
-            bt = wl.batch(1000 + done)
-            oracle.step_mf(W, G, bt.row, bt.col, bt.val, cfg.n_rows, cfg.lam, cfg.opt.lr, cfg.opt.eps)
+            rows += 2 * wb.oracle_step(W, G, 1000 + done)
             done += 1
             if time.perf_counter() - tc0 >= args.cpu_seconds:
                 break
         tc = time.perf_counter() - tc0
-        cpu = {"value": 2.0 * n * done / tc, "unit": "rows/s", "cores": 1, "kind": "oracle",
-               "sample": f"{done} step(s) of {B} entries on the full {cfg.num_keys}x{cfg.dim} table, "
+        cpu = {"value": rows / tc, "unit": "rows/s", "cores": 1, "kind": "oracle",
+               "sample": f"{done} step(s) of the same workload on the full {cfg.num_keys}x{cfg.dim} table, "
                          f"single-threaded C oracle, {tc:.1f} s"}
 
     line = {
-        "metric": "param rows pulled+pushed/sec (MF 10m x 1m, rank 100)",
+        "metric": "param rows pulled+pushed/sec (MF 10m x 1m, rank 100)" if args.workload == "mf"
+        else f"param rows pulled+pushed/sec ({cfg.name})",
         "value": rows_per_s,
         "unit": "rows/s",
         "n_gpus": 1,
@@ -229,13 +333,13 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": cfg.name, "num_keys": cfg.num_keys, "dim": cfg.dim,
-                   "entries_per_step": B, "key_occurrences_per_step": n,
-                   "avg_unique_keys_per_step": U_avg, "batches_resident": nb},
-        "step_alg_GBps": round((B * 12.0 + 4.0 * U_avg * R) / (ms_per_step * 1e-3) / 1e9, 1),
+                   "key_occurrences_per_step": occ, "avg_unique_keys_per_step": U_avg,
+                   "batches_resident": nb},
         "roofline": roofline,
         "kernels": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv) for kk, vv in v.items()}
                     for k, v in kernels.items()},
         "ops": ops,
+        "copy_calibration": copy,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

@@ -6,15 +6,14 @@ The computation lives in the HIP library ``libadapm_hip.so`` (C ABI in
 it.  Importing this package loads nothing; the library is loaded on first use
 and a missing library is an error, never a fallback.
 """
+import importlib
 
 __all__ = ["Store", "dedup", "workloads"]
 
 
 def __getattr__(name):
     if name in ("Store", "dedup"):
-        from . import store
-        return getattr(store, name)
+        return getattr(importlib.import_module(__name__ + ".store"), name)
     if name == "workloads":
-        from . import workloads
-        return workloads
+        return importlib.import_module(__name__ + ".workloads")
     raise AttributeError(name)
