@@ -45,6 +45,34 @@ __device__ __forceinline__ double group_sum(double v) {
   return v;
 }
 
+// Sums J values over a group of L lanes at once (J <= L, both powers of two):
+// log2(J) halving stages in which each lane keeps half of its values and adds
+// the partner's copy of that half, then a butterfly over the remaining L/J
+// lanes.  Lane gl returns the group total of value gl / (L/J).  The addition
+// tree is fixed, so the result is deterministic.
+template <int L, int J>
+__device__ __forceinline__ double group_multi_sum(double (&v)[J], int gl) {
+  static_assert(J >= 1 && J <= L, "J must not exceed the group width");
+#pragma unroll
+  for (int k = 0; (J >> k) > 1; ++k) {
+    const int half = (J >> k) / 2;
+    const int mask = L >> (k + 1);
+    const bool upper = (gl & mask) != 0;
+#pragma unroll
+    for (int i = 0; i < J / 2; ++i) {
+      if (i < half) {
+        const double keep = upper ? v[i + half] : v[i];
+        const double send = upper ? v[i] : v[i + half];
+        v[i] = keep + __shfl_xor(send, mask, L);
+      }
+    }
+  }
+  double s = v[0];
+#pragma unroll
+  for (int o = L / J / 2; o > 0; o >>= 1) s += __shfl_xor(s, o, L);
+  return s;
+}
+
 // ------------------------------------------------------------------ block scan
 // Exclusive scan of one uint32 per thread over a 256-thread block; returns the
 // thread's exclusive prefix and writes the block total to *total.

@@ -73,9 +73,11 @@ __global__ __launch_bounds__(BLOCK) void k_mf_grad(const float* __restrict__ W, 
     double dot = 0.0, nu = 0.0, nm = 0.0;
 #pragma unroll
     for (int e = 0; e < NE; ++e) {
-      dot += (double)u[e] * (double)m[e];
-      nu += (double)u[e] * (double)u[e];
-      nm += (double)m[e] * (double)m[e];
+      // a product of two floats is exact in fp64, so a fused multiply-add
+      // rounds exactly like the separate multiply and add
+      dot = __builtin_fma((double)u[e], (double)m[e], dot);
+      nu = __builtin_fma((double)u[e], (double)u[e], nu);
+      nm = __builtin_fma((double)m[e], (double)m[e], nm);
     }
     dot = group_sum<L>(dot);
     nu = group_sum<L>(nu);
@@ -112,6 +114,15 @@ __device__ __forceinline__ double sigmoid_d(double x) {
 
 __device__ __forceinline__ double softplus_d(double x) {
   return x > 0.0 ? x + log1p(exp(-x)) : log1p(exp(x));
+}
+
+// sigmoid(x) and softplus(x) from one exp(-|x|), without divergent branches;
+// each result rounds exactly as the two-branch forms above.
+__device__ __forceinline__ void sigmoid_softplus(double x, double* sig, double* sp) {
+  const double e = exp(-fabs(x));
+  *sig = (x >= 0.0 ? 1.0 : e) / (1.0 + e);
+  const double l = log1p(e);
+  *sp = x > 0.0 ? x + l : l;
 }
 
 // Per-unit validity: a unit (sample, triple, centre) with any id outside its
@@ -187,7 +198,7 @@ __global__ __launch_bounds__(BLOCK) void k_ctr_grad(const float* __restrict__ W,
 #pragma unroll
       for (int e = 0; e < NE; ++e) {
         S[e] += (double)x[e];
-        sq += (double)x[e] * (double)x[e];
+        sq = __builtin_fma((double)x[e], (double)x[e], sq);   // exact product: same rounding as mul + add
       }
     }
     double ss = 0.0;
@@ -266,7 +277,7 @@ __global__ __launch_bounds__(BLOCK) void k_kge_grad(const float* __restrict__ W,
                                                     int n_head, int64_t rel_off, const uint8_t* __restrict__ ok,
                                                     float* __restrict__ mat, double* __restrict__ base,
                                                     double* __restrict__ coef, double* __restrict__ loss_part) {
-  constexpr int JB = 4;   // negatives in flight
+  constexpr int JB = 4;   // negatives in flight, scored together (8 costs occupancy)
   __shared__ double sm[WAVES_PER_BLOCK];
   const int cdim = dim / 2;
   const int lane = lane_id();
@@ -346,17 +357,23 @@ __global__ __launch_bounds__(BLOCK) void k_kge_grad(const float* __restrict__ W,
                   : ((double)xR[jj][i] * hR[i] + (double)xI[jj][i] * hI[i]);
         ph[jj] = p;
       }
-#pragma unroll
-      for (int jj = 0; jj < JB; ++jj) ph[jj] = group_sum<WAVE>(ph[jj]);
+      // lane finishes the score of negative j0 + lane / (WAVE / JB) and its coefficient
+      const double phi_my = group_multi_sum<WAVE, JB>(ph, lane);
+      const int j_my = j0 + lane / (WAVE / JB);
+      double c_my = 0.0;
+      if (j_my < n_neg) {
+        double sp;
+        sigmoid_softplus(phi_my, &c_my, &sp);
+        if (lane % (WAVE / JB) == 0) {
+          lsum += sp;
+          coef[t * per + 3 + j_my] = c_my;
+        }
+      }
 #pragma unroll
       for (int jj = 0; jj < JB; ++jj) {
         const int j = j0 + jj;
+        const double cj = __shfl(c_my, jj * (WAVE / JB), WAVE);
         if (j >= n_neg) break;
-        const double cj = sigmoid_d(ph[jj]);
-        if (lane == 0) {
-          lsum += softplus_d(ph[jj]);
-          coef[t * per + 3 + j] = cj;
-        }
         if (j < n_head) {   // (x, r, o): d/dr and d/do
 #pragma unroll
           for (int i = 0; i < KPL; ++i) {
@@ -488,7 +505,7 @@ __global__ __launch_bounds__(BLOCK) void k_sgns_grad(const float* __restrict__ W
                                                      double* __restrict__ loss_part) {
   constexpr int GPB = BLOCK / L;
   constexpr int NE = NV * VW;
-  constexpr int JB = 4;   // output rows in flight
+  constexpr int JB = L >= 4 ? 4 : L;   // output rows scored together (power of two <= L)
   __shared__ double sm[WAVES_PER_BLOCK];
   const int gl = threadIdx.x % L;
   const int64_t per = 1 + (int64_t)slots * (K + 1);
@@ -508,52 +525,61 @@ __global__ __launch_bounds__(BLOCK) void k_sgns_grad(const float* __restrict__ W
     }
 #pragma unroll
     for (int e = 0; e < NE; ++e) gv[e] = 0.0;
-    for (int q = 0; q < slots; ++q) {
-      const int64_t cx = ctx[b * slots + q];
-      if (cx == -1) continue;
-      const int32_t* nq = neg + (b * slots + q) * K;
-      for (int k0 = 0; k0 <= K; k0 += JB) {
-        float u[JB][NE];
+    // all output rows of the centre in occurrence order: row r is slot r / (K+1),
+    // position r % (K+1) (0 = the context word, then the negatives)
+    const int rows = slots * (K + 1);
+    for (int r0 = 0; r0 < rows; r0 += JB) {
+      float u[JB][NE];
+      bool live[JB];
 #pragma unroll
-        for (int jj = 0; jj < JB; ++jj) {
-          const int k = k0 + jj;
-          const int64_t id = k == 0 ? cx : (k <= K ? nq[k - 1] : cx);
-          const float* up = W + (out_off + id) * dim;
+      for (int jj = 0; jj < JB; ++jj) {
+        const int r = r0 + jj;
+        const int q = r / (K + 1);
+        const int k = r - q * (K + 1);
+        const int64_t cx = r < rows ? (int64_t)ctx[b * slots + q] : -1;
+        live[jj] = cx != -1;
+        const int64_t id = !live[jj] ? 0 : (k == 0 ? cx : (int64_t)neg[(b * slots + q) * K + (k - 1)]);
+        const float* up = W + (out_off + id) * dim;
 #pragma unroll
-          for (int q2 = 0; q2 < NV; ++q2) {
-            const int c = (gl + q2 * L) * VW;
-            if (c < dim) load_frag<VW>(up + c, u[jj] + q2 * VW);
-            else
+        for (int q2 = 0; q2 < NV; ++q2) {
+          const int c = (gl + q2 * L) * VW;
+          if (c < dim) load_frag<VW>(up + c, u[jj] + q2 * VW);
+          else
 #pragma unroll
-              for (int e = 0; e < VW; ++e) u[jj][q2 * VW + e] = 0.0f;
-          }
+            for (int e = 0; e < VW; ++e) u[jj][q2 * VW + e] = 0.0f;
         }
-        double x[JB];
+      }
+      double x[JB];
 #pragma unroll
-        for (int jj = 0; jj < JB; ++jj) {
-          double p = 0.0;
+      for (int jj = 0; jj < JB; ++jj) {
+        double p = 0.0;
 #pragma unroll
-          for (int e = 0; e < NE; ++e) p += (double)u[jj][e] * (double)v[e];
-          x[jj] = p;
+        for (int e = 0; e < NE; ++e) p = __builtin_fma((double)u[jj][e], (double)v[e], p);   // exact product
+        x[jj] = p;
+      }
+      // lane finishes the score of row r0 + gl / (L / JB) and its coefficient
+      const double x_my = group_multi_sum<L, JB>(x, gl);
+      const int r_my = r0 + gl / (L / JB);
+      const int q_my = r_my / (K + 1);
+      const int k_my = r_my - q_my * (K + 1);
+      double a_my = 0.0;
+      if (r_my < rows && ctx[b * slots + q_my] != -1) {
+        // context word: a = -sigmoid(-x), loss softplus(-x); negative: a = sigmoid(x), loss softplus(x)
+        const double sgn = k_my == 0 ? -1.0 : 1.0;
+        double sig, sp;
+        sigmoid_softplus(sgn * x_my, &sig, &sp);
+        a_my = sgn * sig;
+        if (gl % (L / JB) == 0) {
+          lsum += sp;
+          coef[b * per + 1 + r_my] = a_my;
         }
+      }
 #pragma unroll
-        for (int jj = 0; jj < JB; ++jj) x[jj] = group_sum<L>(x[jj]);
+      for (int jj = 0; jj < JB; ++jj) {
+        const double aj = __shfl(a_my, jj * (L / JB), L);
+        if (live[jj])
 #pragma unroll
-        for (int jj = 0; jj < JB; ++jj) {
-          const int k = k0 + jj;
-          if (k > K) break;
-          double a;
-          if (k == 0) {
-            a = -sigmoid_d(-x[jj]);
-            if (gl == 0) lsum += softplus_d(-x[jj]);
-          } else {
-            a = sigmoid_d(x[jj]);
-            if (gl == 0) lsum += softplus_d(x[jj]);
-          }
-          if (gl == 0) coef[b * per + 1 + (int64_t)q * (K + 1) + k] = a;
-#pragma unroll
-          for (int e = 0; e < NE; ++e) gv[e] += a * (double)u[jj][e];
-        }
+          for (int e = 0; e < NE; ++e) gv[e] += aj * (double)u[jj][e];
       }
     }
     float* dst = mat + b * dim;
