@@ -41,6 +41,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="bound on the CPU-oracle sample (0 = skip)")
     ap.add_argument("--no-ops", action="store_true", help="skip the pull-only / push-only measurements")
+    ap.add_argument("--layout", default="interleaved", choices=["interleaved", "dense"],
+                    help="W and G rows of a key side by side in one allocation, or two dense tables")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a 4 GiB device-to-device copy (reference for HBM counters)")
     return ap.parse_args()
@@ -182,8 +184,12 @@ def main():
     nb = max(1, min(args.steps + args.warmup, 8))
     wb = Bench(args.workload, dev, nb)
     cfg = wb.cfg
-    Wt = torch.from_numpy(wb.W).to(dev)
-    Gt = torch.zeros_like(Wt)
+    if args.layout == "interleaved":
+        from paper_2206_00470_amd.store import interleaved_tables
+        Wt, Gt = interleaved_tables(torch.from_numpy(wb.W).to(dev))
+    else:
+        Wt = torch.from_numpy(wb.W).to(dev)
+        Gt = torch.zeros_like(Wt)
     store = Store(Wt, Gt, cfg.opt.lr, cfg.opt.eps)
     loss = torch.empty(1, dtype=torch.float64, device=dev)
     print(f"# setup {time.time() - t0:.1f}s: {cfg.name}, table {cfg.num_keys}x{cfg.dim}, {nb} batches resident",
@@ -332,7 +338,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": cfg.name, "num_keys": cfg.num_keys, "dim": cfg.dim,
+        "config": {"workload": cfg.name, "num_keys": cfg.num_keys, "dim": cfg.dim, "layout": args.layout,
                    "key_occurrences_per_step": occ, "avg_unique_keys_per_step": U_avg,
                    "batches_resident": nb},
         "roofline": roofline,

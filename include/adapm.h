@@ -76,6 +76,16 @@ typedef int32_t ps_status;
 ps_status ps_create(ps_store** out, int64_t num_keys, int32_t dim, float* values, float* accum,
                     float lr, float eps, void* stream);
 
+/* As ps_create, with a row stride: row k of W starts at values + k*row_stride
+ * and row k of G at accum + k*row_stride (row_stride >= dim floats; a
+ * multiple of 4 when dim is).  ps_create is the dense case row_stride = dim.
+ * One allocation of [num_keys][2*dim] floats with accum = values + dim keeps
+ * each key's value and accumulator rows side by side, so an update touches
+ * one 8*dim-byte region of HBM instead of two.  Rows of W and G must not
+ * overlap (PS_ERR_INVALID otherwise).  Pulled rows are always dense. */
+ps_status ps_create_strided(ps_store** out, int64_t num_keys, int32_t dim, int64_t row_stride,
+                            float* values, float* accum, float lr, float eps, void* stream);
+
 /* Free the handle and its status block (not the tables).  NULL is a no-op.
  * Synchronizes the device before freeing. */
 ps_status ps_destroy(ps_store* s);

@@ -49,6 +49,7 @@ constexpr size_t MAX_TIMED_LAUNCHES = 1 << 14;
 // ======================================================================== store
 struct ps_store {
   int64_t num_keys;
+  int64_t ld;        // row stride (floats) of both tables
   int32_t dim;
   float* W;
   float* G;
@@ -356,14 +357,14 @@ ps_status run_reduce(ps_store* s, const SortBufs& b, const uint32_t* ks, Src src
     const int64_t grid = reduce_grid(n, L);
     for (const KeyRange& r : ranges) {
       Timed t(s, PS_KERNEL_SEGREDUCE, st);
-      hipLaunchKernelGGL((k_segreduce<L, NV, VW, Src>), dim3(grid), dim3(BLOCK), 0, st, sv, src, n, s->W, s->G,
+      hipLaunchKernelGGL((k_segreduce<L, NV, VW, Src>), dim3(grid), dim3(BLOCK), 0, st, sv, src, n, s->W, s->G, s->ld,
                          s->dim, s->lr, s->eps, b.partial, b.split_list, b.hdr, r.lo, r.hi);
       LAUNCHED(k_segreduce);
     }
     int64_t fgrid = n / CHUNK + 1;
     if (fgrid > 1024) fgrid = 1024;
     const size_t lds = size_t(BLOCK / L) * s->dim * sizeof(double);
-    hipLaunchKernelGGL((k_seg_finalize<L, NV, VW>), dim3(fgrid), dim3(BLOCK), lds, st, sv, s->W, s->G, s->dim,
+    hipLaunchKernelGGL((k_seg_finalize<L, NV, VW>), dim3(fgrid), dim3(BLOCK), lds, st, sv, s->W, s->G, s->ld, s->dim,
                        s->lr, s->eps, b.partial, b.split_list);
     LAUNCHED(k_seg_finalize);
     return PS_OK;
@@ -420,19 +421,35 @@ const char* ps_last_error_message(void) { return g_last_error.c_str(); }
 
 ps_status ps_create(ps_store** out, int64_t num_keys, int32_t dim, float* values, float* accum, float lr,
                     float eps, void* stream) {
+  return ps_create_strided(out, num_keys, dim, dim, values, accum, lr, eps, stream);
+}
+
+ps_status ps_create_strided(ps_store** out, int64_t num_keys, int32_t dim, int64_t row_stride, float* values,
+                            float* accum, float lr, float eps, void* stream) {
   if (!out) return fail(PS_ERR_INVALID, "out is NULL");
   *out = nullptr;
   if (num_keys < 1 || num_keys > INT32_MAX) return fail(PS_ERR_INVALID, "num_keys %lld outside [1, 2^31-1]", (long long)num_keys);
   RowShape shape;
   if (dim < 1 || !row_shape(dim, true, &shape))
     return fail(PS_ERR_UNSUPPORTED, "dim %d unsupported (at most 512)", dim);
+  if (row_stride < dim) return fail(PS_ERR_INVALID, "row_stride %lld < dim %d", (long long)row_stride, dim);
   if (!values || !accum) return fail(PS_ERR_INVALID, "table pointer is NULL");
-  if (values == accum) return fail(PS_ERR_INVALID, "values and accumulators alias");
-  if (dim % 4 == 0 && (!aligned16(values) || !aligned16(accum)))
-    return fail(PS_ERR_INVALID, "tables must be 16-byte aligned");
+  {
+    // rows of W and G must not overlap: either two separate tables, or rows
+    // interleaved in one allocation with a gap of at least dim on each side
+    const int64_t d = (int64_t)(accum - values);
+    const int64_t ad = d < 0 ? -d : d;
+    const bool separate = ad >= num_keys * row_stride;
+    const int64_t r = ((d % row_stride) + row_stride) % row_stride;
+    const bool interleaved = row_stride >= 2 * (int64_t)dim && r >= dim && r <= row_stride - dim;
+    if (!separate && !interleaved) return fail(PS_ERR_INVALID, "values and accumulator rows overlap");
+  }
+  if (dim % 4 == 0 && (!aligned16(values) || !aligned16(accum) || row_stride % 4 != 0))
+    return fail(PS_ERR_INVALID, "tables must be 16-byte aligned with a row stride that is a multiple of 4");
   if (!(lr > 0.0f) || !(eps >= 0.0f)) return fail(PS_ERR_INVALID, "need lr > 0 and eps >= 0");
   ps_store* s = new ps_store();
   s->num_keys = num_keys;
+  s->ld = row_stride;
   s->dim = dim;
   s->W = values;
   s->G = accum;
@@ -492,7 +509,7 @@ ps_status ps_pull(ps_store* s, const int64_t* keys, int64_t n, float* out, void*
     int64_t grid = ceil_div(n, BLOCK / L);
     if (grid > 65536) grid = 65536;
     Timed t(s, PS_KERNEL_PULL, st);
-    hipLaunchKernelGGL((k_pull<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->num_keys, s->dim, keys, n,
+    hipLaunchKernelGGL((k_pull<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->ld, s->num_keys, s->dim, keys, n,
                        out, s->status);
     LAUNCHED(k_pull);
     return PS_OK;
@@ -574,7 +591,7 @@ ps_status ps_step_mf(ps_store* s, const int32_t* row, const int32_t* col, const 
     if (grid > LOSS_GRID) grid = LOSS_GRID;
     {
       Timed t(s, PS_KERNEL_TASKGRAD, st);
-      hipLaunchKernelGGL((k_mf_grad<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->num_keys, s->dim, row,
+      hipLaunchKernelGGL((k_mf_grad<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->ld, s->num_keys, s->dim, row,
                          col, val, B, col_key_offset, lambda, sorted_grads ? p.sb.rank : nullptr, p.grads,
                          p.loss_part);
     }
@@ -624,7 +641,7 @@ ps_status ps_step_kge(ps_store* s, const int32_t* head, const int32_t* rel, cons
   const int64_t grid = small_grid(B, WAVES_PER_BLOCK, LOSS_GRID);
   auto launch = [&](auto kernel) -> ps_status {
     Timed t(s, PS_KERNEL_TASKGRAD, st);
-    hipLaunchKernelGGL(kernel, dim3(grid), dim3(BLOCK), 0, st, s->W, s->dim, head, rel, tail, neg, B, n_neg,
+    hipLaunchKernelGGL(kernel, dim3(grid), dim3(BLOCK), 0, st, s->W, s->ld, s->dim, head, rel, tail, neg, B, n_neg,
                        n_head_neg, rel_key_offset, p.ok, p.mat, p.base, p.coef, p.loss_part);
     LAUNCHED(k_kge_grad);
     return PS_OK;
@@ -678,7 +695,7 @@ ps_status ps_step_sgns(ps_store* s, const int32_t* centre, const int32_t* ctx, c
     const int64_t grid = small_grid(B, BLOCK / L, LOSS_GRID);
     {
       Timed t(s, PS_KERNEL_TASKGRAD, st);
-      hipLaunchKernelGGL((k_sgns_grad<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->dim, centre, ctx, neg,
+      hipLaunchKernelGGL((k_sgns_grad<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->ld, s->dim, centre, ctx, neg,
                          B, slots, n_neg, out_key_offset, p.ok, p.mat, p.coef, p.loss_part);
     }
     LAUNCHED(k_sgns_grad);
@@ -690,7 +707,7 @@ ps_status ps_step_sgns(ps_store* s, const int32_t* centre, const int32_t* ctx, c
   });
   if (r) return r;
   // output rows first: their gradients read the input rows, which are updated second
-  SrcSGNS src{perm, p.mat, p.coef, centre, s->W, (int)per, s->dim};
+  SrcSGNS src{perm, p.mat, p.coef, centre, s->W, s->ld, (int)per, s->dim};
   return run_reduce(s, p.sb, ks, src, n,
                     {KeyRange{(uint32_t)out_key_offset, (uint32_t)s->num_keys}, KeyRange{0u, (uint32_t)out_key_offset}},
                     st);
@@ -728,7 +745,7 @@ ps_status ps_step_ctr(ps_store* s, const int64_t* keys, const float* label, int6
     const int64_t grid = small_grid(B, BLOCK / L, LOSS_GRID);
     {
       Timed t(s, PS_KERNEL_TASKGRAD, st);
-      hipLaunchKernelGGL((k_ctr_grad<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->dim, keys, label, B, F,
+      hipLaunchKernelGGL((k_ctr_grad<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->ld, s->dim, keys, label, B, F,
                          p.ok, p.sb.rank, p.grads, p.loss_part);
     }
     LAUNCHED(k_ctr_grad);

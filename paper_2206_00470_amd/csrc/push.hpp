@@ -18,7 +18,7 @@ struct RowShape {
 
 // ------------------------------------------------------------------ pull
 template <int L, int NV, int VW>
-__global__ __launch_bounds__(BLOCK) void k_pull(const float* __restrict__ W, int64_t num_keys, int dim,
+__global__ __launch_bounds__(BLOCK) void k_pull(const float* __restrict__ W, int64_t ld, int64_t num_keys, int dim,
                                                 const int64_t* __restrict__ keys, int64_t n,
                                                 float* __restrict__ out, int32_t* __restrict__ err) {
   constexpr int GPB = BLOCK / L;
@@ -28,7 +28,7 @@ __global__ __launch_bounds__(BLOCK) void k_pull(const float* __restrict__ W, int
     const int64_t key = keys[i];
     const bool ok = key >= 0 && key < num_keys;
     bad |= !ok;
-    const float* src = W + (ok ? key : 0) * (int64_t)dim;
+    const float* src = W + (ok ? key : 0) * ld;
     float* dst = out + i * (int64_t)dim;
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
@@ -108,7 +108,7 @@ __device__ __forceinline__ int64_t xcd_slot(int64_t block, int64_t nblocks) {
 // first chunk of such a segment also appends the segment to split_list.
 template <int L, int NV, int VW, class Src>
 __global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, int64_t n, float* __restrict__ W,
-                                                     float* __restrict__ G, int dim, float lr, float eps,
+                                                     float* __restrict__ G, int64_t ld, int dim, float lr, float eps,
                                                      double* __restrict__ partial,
                                                      int32_t* __restrict__ split_list, SegHeader* split_hdr,
                                                      uint32_t key_lo, uint32_t key_hi) {
@@ -126,8 +126,8 @@ __global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, int64_
     // the chunk is a whole segment if its neighbours hold other keys
     const bool head = j0 == 0 || sv.keys[j0 - 1] != key;
     const bool whole = head && (j1 >= n || sv.keys[j1] != key);
-    float* wrow = W + (int64_t)key * dim;
-    float* grow = G + (int64_t)key * dim;
+    float* wrow = W + (int64_t)key * ld;
+    float* grow = G + (int64_t)key * ld;
     float wv[NE], gv[NE];
     if (whole) {   // issue the table reads early, they do not depend on the sum
 #pragma unroll
@@ -192,7 +192,7 @@ __global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, int64_
 // deterministic.
 template <int L, int NV, int VW>
 __global__ __launch_bounds__(BLOCK) void k_seg_finalize(SegView sv, float* __restrict__ W, float* __restrict__ G,
-                                                        int dim, float lr, float eps,
+                                                        int64_t ld, int dim, float lr, float eps,
                                                         const double* __restrict__ partial,
                                                         const int32_t* __restrict__ split_list) {
   constexpr int GPB = BLOCK / L;
@@ -251,8 +251,8 @@ __global__ __launch_bounds__(BLOCK) void k_seg_finalize(SegView sv, float* __res
         for (int q = 0; q < VW; ++q) lds[g * dim + col + q] = acc[v * VW + q];
     }
     __syncthreads();
-    float* wrow = W + (int64_t)key * dim;
-    float* grow = G + (int64_t)key * dim;
+    float* wrow = W + (int64_t)key * ld;
+    float* grow = G + (int64_t)key * ld;
     for (int col = threadIdx.x; col < dim; col += BLOCK) {
       double s = 0.0;
       for (int gg = 0; gg < GPB; ++gg) s += lds[gg * dim + col];

@@ -41,7 +41,7 @@ struct KeysMF {
 // The two gradient rows go to the sorted positions rank[2b], rank[2b+1], or
 // to occurrence positions 2b, 2b+1 when rank is null.
 template <int L, int NV, int VW>
-__global__ __launch_bounds__(BLOCK) void k_mf_grad(const float* __restrict__ W, int64_t num_keys, int dim,
+__global__ __launch_bounds__(BLOCK) void k_mf_grad(const float* __restrict__ W, int64_t ld, int64_t num_keys, int dim,
                                                    const int32_t* __restrict__ row, const int32_t* __restrict__ col,
                                                    const float* __restrict__ val, int64_t B, int64_t col_off,
                                                    float lam, const uint32_t* __restrict__ rank,
@@ -56,8 +56,8 @@ __global__ __launch_bounds__(BLOCK) void k_mf_grad(const float* __restrict__ W, 
     const int64_t ku = row[b];
     const int64_t km = col_off + (int64_t)col[b];
     if (!(ku >= 0 && ku < num_keys && col[b] >= 0 && km < num_keys)) continue;
-    const float* up = W + ku * dim;
-    const float* mp = W + km * dim;
+    const float* up = W + ku * ld;
+    const float* mp = W + km * ld;
     float u[NE], m[NE];
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
@@ -167,7 +167,7 @@ struct KeysCTR {
 //   loss += softplus(z) - y z ;  grad e_f = (sigmoid(z) - y)(S - e_f)
 // Gradient rows go to their sorted positions rank[b*F + f].
 template <int L, int NV, int VW>
-__global__ __launch_bounds__(BLOCK) void k_ctr_grad(const float* __restrict__ W, int dim,
+__global__ __launch_bounds__(BLOCK) void k_ctr_grad(const float* __restrict__ W, int64_t ld, int dim,
                                                     const int64_t* __restrict__ keys,
                                                     const float* __restrict__ label, int64_t B, int F,
                                                     const uint8_t* __restrict__ ok,
@@ -185,7 +185,7 @@ __global__ __launch_bounds__(BLOCK) void k_ctr_grad(const float* __restrict__ W,
     for (int e = 0; e < NE; ++e) S[e] = 0.0;
     double sq = 0.0;
     for (int f = 0; f < F; ++f) {
-      const float* row = W + keys[b * F + f] * dim;
+      const float* row = W + keys[b * F + f] * ld;
       float x[NE];
 #pragma unroll
       for (int v = 0; v < NV; ++v) {
@@ -211,7 +211,7 @@ __global__ __launch_bounds__(BLOCK) void k_ctr_grad(const float* __restrict__ W,
     const double a = sigmoid_d(z) - y;
     if (gl == 0) lsum += softplus_d(z) - y * z;
     for (int f = 0; f < F; ++f) {
-      const float* row = W + keys[b * F + f] * dim;
+      const float* row = W + keys[b * F + f] * ld;
       float* dst = grads + (int64_t)rank[b * F + f] * dim;
 #pragma unroll
       for (int v = 0; v < NV; ++v) {
@@ -269,7 +269,7 @@ struct KeysKGE {
 // fp64 rows f, h per triple and one fp64 coefficient per negative, and
 // writes the full fp32 gradient rows of s, r and o.
 template <int KPL>
-__global__ __launch_bounds__(BLOCK) void k_kge_grad(const float* __restrict__ W, int dim,
+__global__ __launch_bounds__(BLOCK) void k_kge_grad(const float* __restrict__ W, int64_t ld, int dim,
                                                     const int32_t* __restrict__ head,
                                                     const int32_t* __restrict__ rel,
                                                     const int32_t* __restrict__ tail,
@@ -286,9 +286,9 @@ __global__ __launch_bounds__(BLOCK) void k_kge_grad(const float* __restrict__ W,
   for (int64_t t = (int64_t)blockIdx.x * WAVES_PER_BLOCK + threadIdx.x / WAVE; t < B;
        t += (int64_t)gridDim.x * WAVES_PER_BLOCK) {
     if (!ok[t]) continue;
-    const float* sp = W + (int64_t)head[t] * dim;
-    const float* rp = W + (rel_off + rel[t]) * dim;
-    const float* op = W + (int64_t)tail[t] * dim;
+    const float* sp = W + (int64_t)head[t] * ld;
+    const float* rp = W + (rel_off + rel[t]) * ld;
+    const float* op = W + (int64_t)tail[t] * ld;
     double sR[KPL], sI[KPL], rR[KPL], rI[KPL], oR[KPL], oI[KPL];
 #pragma unroll
     for (int i = 0; i < KPL; ++i) {
@@ -337,7 +337,7 @@ __global__ __launch_bounds__(BLOCK) void k_kge_grad(const float* __restrict__ W,
 #pragma unroll
       for (int jj = 0; jj < JB; ++jj) {
         const int j = j0 + jj;
-        const float* xp = W + (int64_t)(j < n_neg ? nt[j] : 0) * dim;
+        const float* xp = W + (int64_t)(j < n_neg ? nt[j] : 0) * ld;
 #pragma unroll
         for (int i = 0; i < KPL; ++i) {
           const int k = lane + WAVE * i;
@@ -496,7 +496,7 @@ struct KeysSGNS {
 // Stores one fp64 coefficient a per output occurrence (its gradient row is
 // a*v) and the centre's fp32 gradient row sum(a*u).
 template <int L, int NV, int VW>
-__global__ __launch_bounds__(BLOCK) void k_sgns_grad(const float* __restrict__ W, int dim,
+__global__ __launch_bounds__(BLOCK) void k_sgns_grad(const float* __restrict__ W, int64_t ld, int dim,
                                                      const int32_t* __restrict__ centre,
                                                      const int32_t* __restrict__ ctx,
                                                      const int32_t* __restrict__ neg, int64_t B, int slots, int K,
@@ -512,7 +512,7 @@ __global__ __launch_bounds__(BLOCK) void k_sgns_grad(const float* __restrict__ W
   double lsum = 0.0;
   for (int64_t b = (int64_t)blockIdx.x * GPB + threadIdx.x / L; b < B; b += (int64_t)gridDim.x * GPB) {
     if (!ok[b]) continue;
-    const float* vp = W + (int64_t)centre[b] * dim;
+    const float* vp = W + (int64_t)centre[b] * ld;
     float v[NE];
     double gv[NE];
 #pragma unroll
@@ -539,7 +539,7 @@ __global__ __launch_bounds__(BLOCK) void k_sgns_grad(const float* __restrict__ W
         const int64_t cx = r < rows ? (int64_t)ctx[b * slots + q] : -1;
         live[jj] = cx != -1;
         const int64_t id = !live[jj] ? 0 : (k == 0 ? cx : (int64_t)neg[(b * slots + q) * K + (k - 1)]);
-        const float* up = W + (out_off + id) * dim;
+        const float* up = W + (out_off + id) * ld;
 #pragma unroll
         for (int q2 = 0; q2 < NV; ++q2) {
           const int c = (gl + q2 * L) * VW;
@@ -607,6 +607,7 @@ struct SrcSGNS {
   const double* coef;
   const int32_t* centre;
   const float* W;
+  int64_t ld;
   int per, dim;
   template <int L, int NV, int VW>
   __device__ __forceinline__ void load(int64_t j, int gl, float* x) const {
@@ -622,7 +623,7 @@ struct SrcSGNS {
       }
     } else {
       const double a = coef[occ];
-      const float* row = W + (int64_t)centre[b] * dim;
+      const float* row = W + (int64_t)centre[b] * ld;
 #pragma unroll
       for (int v = 0; v < NV; ++v) {
         const int c = (gl + v * L) * VW;

@@ -44,21 +44,42 @@ class Workspace:
         return C.c_void_p(self.buf.data_ptr()), self.buf.numel()
 
 
+def interleaved_tables(W0: torch.Tensor, G0: torch.Tensor | None = None):
+    """Copy [num_keys, dim] tables into one [num_keys, 2*dim] allocation and
+    return the (W, G) row-strided views: each key's value row and
+    accumulator row then sit side by side in HBM."""
+    K, d = W0.shape
+    T = torch.empty((K, 2 * d), dtype=torch.float32, device=W0.device)
+    T[:, :d].copy_(W0)
+    if G0 is None:
+        T[:, d:].zero_()
+    else:
+        T[:, d:].copy_(G0)
+    return T[:, :d], T[:, d:]
+
+
 class Store:
     """A parameter store over caller-owned tables W (values) and G (AdaGrad
-    accumulators), float32 [num_keys, dim] CUDA tensors."""
+    accumulators), float32 [num_keys, dim] CUDA tensors.  W and G may be
+    dense, or row-strided views with one common row stride (for example the
+    two halves of a [num_keys, 2*dim] tensor, see interleaved_tables)."""
 
     def __init__(self, W: torch.Tensor, G: torch.Tensor, lr: float = 0.1, eps: float = 1e-10, stream=None):
-        _dev(W, torch.float32, "W")
-        _dev(G, torch.float32, "G")
-        if W.shape != G.shape or W.dim() != 2:
-            raise ValueError("W and G must be [num_keys, dim] tensors of one shape")
+        for t, nm in ((W, "W"), (G, "G")):
+            if not (t.is_cuda and t.dtype == torch.float32 and t.dim() == 2 and t.stride(1) == 1):
+                raise TypeError(f"{nm} must be a float32 CUDA tensor [num_keys, dim] with unit column stride")
+        if W.shape != G.shape:
+            raise ValueError("W and G must have one shape")
+        if W.shape[0] > 1 and W.stride(0) != G.stride(0):
+            raise ValueError("W and G must share one row stride")
         self.W, self.G = W, G
         self.num_keys, self.dim = W.shape
+        self.row_stride = W.stride(0) if W.shape[0] > 1 else self.dim
         self.lr, self.eps = lr, eps
         self.ws = Workspace(W.device)
         h = C.c_void_p()
-        check(lib().ps_create(C.byref(h), self.num_keys, self.dim, _ptr(W), _ptr(G), lr, eps, _stream(stream)))
+        check(lib().ps_create_strided(C.byref(h), self.num_keys, self.dim, self.row_stride, _ptr(W), _ptr(G), lr,
+                                      eps, _stream(stream)))
         self._h = h
 
     def close(self):

@@ -64,6 +64,22 @@ def test_create_rejects_bad_arguments_on_host():
     assert b"lr" in L.ps_last_error_message()
 
 
+def test_create_strided_rejects_overlapping_or_misaligned_rows():
+    L = _lib.lib()
+    h = C.c_void_p(1)
+    base = 0x100000
+    K, d = 1000, 100
+    P = lambda off_floats: C.c_void_p(base + 4 * off_floats)
+    # interleaved [K][2d]: accum = values + d, stride 2d is fine (host checks only, so expect no
+    # argument error before the device allocation; we stop at the overlap checks here)
+    assert L.ps_create_strided(C.byref(h), K, d, d - 1, P(0), P(d), 0.1, 0.0, None) == _lib.PS_ERR_INVALID
+    assert L.ps_create_strided(C.byref(h), K, d, 2 * d, P(0), P(d // 2), 0.1, 0.0, None) == _lib.PS_ERR_INVALID
+    assert L.ps_create_strided(C.byref(h), K, d, d, P(0), P(d), 0.1, 0.0, None) == _lib.PS_ERR_INVALID
+    assert L.ps_create_strided(C.byref(h), K, d, 2 * d + 2, P(0), P(d), 0.1, 0.0, None) == _lib.PS_ERR_INVALID
+    assert L.ps_create_strided(C.byref(h), K, d, 2 * d, P(1), P(d + 1), 0.1, 0.0, None) == _lib.PS_ERR_INVALID
+    assert h.value is None
+
+
 def test_calls_on_null_store_are_rejected():
     L = _lib.lib()
     p = C.c_void_p(0x1000)
