@@ -207,7 +207,8 @@ ORC_API double orc_grad_mf(const float* W, int64_t num_keys, int32_t dim,
         int64_t km = col_off + (int64_t)col[b];
         float* gu = ograds + (2 * b) * dim;
         float* gm = ograds + (2 * b + 1) * dim;
-        if (!key_ok(ku, num_keys) || !key_ok(km, num_keys) || row[b] < 0 || col[b] < 0) {
+        /* row factors occupy keys [0, col_off), column factors [col_off, num_keys) */
+        if (!key_ok(ku, num_keys) || ku >= col_off || !key_ok(km, num_keys) || row[b] < 0 || col[b] < 0) {
             okeys[2 * b] = -1;
             okeys[2 * b + 1] = -1;
             memset(gu, 0, sizeof(float) * (size_t)dim);

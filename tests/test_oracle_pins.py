@@ -271,6 +271,13 @@ def test_mf_invalid_entry_is_skipped():
     assert bad == 1 and keys[6] == -1 and keys[7] == -1 and not grads[6:8].any()
 
 
+def test_mf_row_id_must_index_the_row_factors():
+    W, row, col, val, R = mf_setup()
+    row[2] = R            # a column-factor key used as a row id
+    keys, grads, loss, bad = oracle.grad_mf(W, row, col, val, R, 1e-2)
+    assert bad == 1 and keys[4] == -1 and keys[5] == -1
+
+
 def test_mf_step_is_grad_then_push():
     W, row, col, val, R = mf_setup(10)
     G = np.zeros_like(W)
