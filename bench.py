@@ -135,8 +135,13 @@ class Bench:
         table = 4.0 * U * R                      # W and G read and written once per distinct key
         if self.name in ("mf", "mf_tiny"):
             B = bt.row.size
-            return {"segreduce": n * R + table,                   # gradient rows in sorted order
-                    "taskgrad": B * (12.0 + 2 * R + 2 * R + 8.0)}  # inputs, 2 gathers, 2 rows out, ranks
+            Ucol = np.unique(bt.col).size
+            # merge: column keys read their stored gradient rows; row keys read a 16-byte record
+            # and the snapshot of their entry's column row (one read per distinct column key)
+            return {"segreduce": B * R + B * 16.0 + Ucol * R + table,
+                    # inputs, 2 gathered rows, 1 gradient row + 1 record out, ranks, segment ids,
+                    # one snapshot row per distinct column key
+                    "taskgrad": B * (12.0 + 2 * R + R + 16.0 + 8.0 + 4.0) + Ucol * R}
         if self.name == "ctr":
             B, F = bt.keys.shape
             return {"segreduce": n * R + table,
@@ -222,8 +227,9 @@ def main():
     ms_per_step = elapsed * 1e3 / args.steps
     rows_per_s = 2.0 * occ / (ms_per_step * 1e-3)
     alg = {k: float(np.mean([wb.alg_bytes(i)[k] for i in idx])) for k in ("segreduce", "taskgrad")}
-    # launches per step of the merge kernel: SGNS merges output rows, then input rows
-    seg_launches_per_step = 2 if args.workload == "sgns" else 1
+    # launches per step of the merge kernel: MF merges column keys then row keys,
+    # SGNS output rows then input rows
+    seg_launches_per_step = 2 if args.workload in ("sgns", "mf", "mf_tiny") else 1
     kernels = {}
     for name, nbytes in alg.items():
         ms, cnt = kt[name]
@@ -237,7 +243,7 @@ def main():
     dom = max(("segreduce", "taskgrad"), key=lambda k: kernels[k]["ms_per_step"])
     dk = kernels[dom]
     symbol = {"segreduce": "k_segreduce",
-              "taskgrad": {"mf": "k_mf_grad", "mf_tiny": "k_mf_grad", "kge": "k_kge_grad", "sgns": "k_sgns_grad",
+              "taskgrad": {"mf": "k_mf_err", "mf_tiny": "k_mf_err", "kge": "k_kge_grad", "sgns": "k_sgns_grad",
                            "ctr": "k_ctr_grad"}[args.workload]}[dom]
     traffic = counter_traffic(args.workload, symbol)
     roofline = {

@@ -210,18 +210,13 @@ struct Plan {
   double* base = nullptr;      // KGE: fp64 rows d phi/d s (r,o) and d phi/d o (s,r) per triple
   double* coef = nullptr;      // KGE, SGNS: fp64 coefficient per occurrence
   uint8_t* ok = nullptr;       // per-unit validity
+  int32_t* seg_of_pos = nullptr;   // MF: segment of each sorted position
+  MFMeta* pm = nullptr;            // MF: e and partner row per sorted position
   double* loss_part = nullptr;
   size_t bytes = 0;
 };
 
 constexpr int64_t LOSS_GRID = 2048;
-
-// MF and CTR steps write each gradient row straight to its sorted position
-// (scattered writes, contiguous merge reads) rather than in occurrence order
-// (contiguous writes, merge reads through the permutation).
-#ifndef ADAPM_SORTED_GRADS
-#define ADAPM_SORTED_GRADS 1
-#endif
 
 bool plan_op(void* ws, int64_t num_keys, int dim, int op, int64_t units, int64_t per_unit, Plan* p) {
   (void)num_keys;
@@ -235,6 +230,13 @@ bool plan_op(void* ws, int64_t num_keys, int dim, int op, int64_t units, int64_t
       carve_sort(c, n, dim, false, false, &p->sb);
       break;
     case PS_OP_STEP_MF:
+      carve_sort(c, n, dim, true, true, &p->sb);
+      p->seg_of_pos = c.take<int32_t>(n);
+      p->pm = c.take<MFMeta>(n);                     // per sorted position: e and the partner row
+      p->mat = c.take<float>(size_t(units) * dim);   // column-row snapshot (at most one per entry)
+      p->grads = c.take<float>(size_t(n) * dim);     // column-occurrence gradient rows, sorted positions
+      p->loss_part = c.take<double>(LOSS_GRID);
+      break;
     case PS_OP_STEP_CTR:
       carve_sort(c, n, dim, true, true, &p->sb);
       p->grads = c.take<float>(size_t(n) * dim);
@@ -319,14 +321,14 @@ ps_status run_sort(ps_store* s, KS ks, int64_t n, int64_t num_keys, SortBufs& b,
 }
 
 ps_status run_segments(const SortBufs& b, const uint32_t* ks, int64_t n, int64_t num_keys, int32_t* seg_off,
-                       int64_t* uniq64, hipStream_t st) {
+                       int64_t* uniq64, hipStream_t st, int32_t* seg_of_pos = nullptr, uint32_t split_key = 0) {
   const int tiles = (int)b.tiles;
   hipLaunchKernelGGL(k_seg_count, dim3(tiles), dim3(BLOCK), 0, st, ks, n, (uint32_t)num_keys, b.tstat, tiles);
   LAUNCHED(k_seg_count);
   hipLaunchKernelGGL(k_seg_scan, dim3(1), dim3(BLOCK), 0, st, b.tstat, tiles, b.hdr, seg_off, b.chunk_start);
   LAUNCHED(k_seg_scan);
   hipLaunchKernelGGL(k_seg_write, dim3(tiles), dim3(BLOCK), 0, st, ks, n, (uint32_t)num_keys, b.tstat, tiles,
-                     seg_off, uniq64, b.chunk_start, b.chunk_seg);
+                     seg_off, uniq64, b.chunk_start, b.chunk_seg, seg_of_pos, split_key, b.hdr);
   LAUNCHED(k_seg_write);
   return PS_OK;
 }
@@ -340,27 +342,33 @@ int64_t reduce_grid(int64_t n, int L) {
 }
 
 // Segmented fp64 reduce of the occurrences' gradients + AdaGrad, one launch
-// per key range in the given order (a later range may update rows that an
-// earlier range's source reads), then one finalize pass for all segments
-// longer than a chunk.
-struct KeyRange {
-  uint32_t lo, hi;
-};
+// per part of the chunk list in the given order (a later part may update
+// rows that an earlier part's source reads), then one finalize pass for all
+// segments longer than a chunk.  Parts split the sorted keys at the split key
+// given to run_segments: PART_UPPER = keys >= split, PART_LOWER = keys below.
+enum { PART_ALL = 0, PART_UPPER = 1, PART_LOWER = 2 };
 
 template <class Src>
-ps_status run_reduce(ps_store* s, const SortBufs& b, const uint32_t* ks, Src src, int64_t n,
-                     std::initializer_list<KeyRange> ranges, hipStream_t st) {
+ps_status launch_segreduce(ps_store* s, const SortBufs& b, const uint32_t* ks, Src src, int64_t n, int part,
+                           hipStream_t st) {
   RowShape shape;
   if (!row_shape(s->dim, true, &shape)) return fail(PS_ERR_UNSUPPORTED, "dim %d not supported", s->dim);
   SegView sv{ks, b.seg_off, b.chunk_start, b.chunk_seg, b.hdr};
   return with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
     const int64_t grid = reduce_grid(n, L);
-    for (const KeyRange& r : ranges) {
-      Timed t(s, PS_KERNEL_SEGREDUCE, st);
-      hipLaunchKernelGGL((k_segreduce<L, NV, VW, Src>), dim3(grid), dim3(BLOCK), 0, st, sv, src, n, s->W, s->G, s->ld,
-                         s->dim, s->lr, s->eps, b.partial, b.split_list, b.hdr, r.lo, r.hi);
-      LAUNCHED(k_segreduce);
-    }
+    Timed t(s, PS_KERNEL_SEGREDUCE, st);
+    hipLaunchKernelGGL((k_segreduce<L, NV, VW, Src>), dim3(grid), dim3(BLOCK), 0, st, sv, src, n, s->W, s->G, s->ld,
+                       s->dim, s->lr, s->eps, b.partial, b.split_list, b.hdr, part);
+    LAUNCHED(k_segreduce);
+    return PS_OK;
+  });
+}
+
+ps_status launch_finalize(ps_store* s, const SortBufs& b, const uint32_t* ks, int64_t n, hipStream_t st) {
+  RowShape shape;
+  if (!row_shape(s->dim, true, &shape)) return fail(PS_ERR_UNSUPPORTED, "dim %d not supported", s->dim);
+  SegView sv{ks, b.seg_off, b.chunk_start, b.chunk_seg, b.hdr};
+  return with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
     int64_t fgrid = n / CHUNK + 1;
     if (fgrid > 1024) fgrid = 1024;
     const size_t lds = size_t(BLOCK / L) * s->dim * sizeof(double);
@@ -371,7 +379,14 @@ ps_status run_reduce(ps_store* s, const SortBufs& b, const uint32_t* ks, Src src
   });
 }
 
-KeyRange all_keys(const ps_store* s) { return KeyRange{0u, (uint32_t)s->num_keys}; }
+template <class Src>
+ps_status run_reduce(ps_store* s, const SortBufs& b, const uint32_t* ks, Src src, int64_t n,
+                     std::initializer_list<int> parts, hipStream_t st) {
+  for (int part : parts)
+    if (ps_status r = launch_segreduce(s, b, ks, src, n, part, st)) return r;
+  return launch_finalize(s, b, ks, n, st);
+}
+
 
 int64_t small_grid(int64_t units, int64_t per_block, int64_t cap) {
   int64_t g = ceil_div(units, per_block);
@@ -531,7 +546,7 @@ ps_status ps_push(ps_store* s, const int64_t* keys, int64_t n, const float* grad
   if (ps_status r = run_sort(s, KeysInt64{keys}, n, s->num_keys, p.sb, s->status, nullptr, false, st, &ks, &perm))
     return r;
   if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st)) return r;
-  return run_reduce(s, p.sb, ks, SrcIndirect{grads, perm, s->dim}, n, {all_keys(s)}, st);
+  return run_reduce(s, p.sb, ks, SrcIndirect{grads, perm, s->dim}, n, {PART_ALL}, st);
 }
 
 ps_status ps_dedup(int64_t num_keys, const int64_t* keys, int64_t n, int64_t* uniq, int32_t* perm,
@@ -580,10 +595,9 @@ ps_status ps_step_mf(ps_store* s, const int32_t* row, const int32_t* col, const 
   if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
   uint32_t *ks, *perm;
   KeysMF kmf{row, col, col_key_offset, s->num_keys};
-  const bool sorted_grads = ADAPM_SORTED_GRADS;
-  if (ps_status r = run_sort(s, kmf, n, s->num_keys, p.sb, s->status, nullptr, sorted_grads, st, &ks, &perm))
-    return r;
-  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st)) return r;
+  if (ps_status r = run_sort(s, kmf, n, s->num_keys, p.sb, s->status, nullptr, true, st, &ks, &perm)) return r;
+  const uint32_t split = (uint32_t)(col_key_offset < s->num_keys ? col_key_offset : s->num_keys);
+  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st, p.seg_of_pos, split)) return r;
   RowShape shape;
   row_shape(s->dim, true, &shape);
   ps_status r = with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
@@ -591,11 +605,11 @@ ps_status ps_step_mf(ps_store* s, const int32_t* row, const int32_t* col, const 
     if (grid > LOSS_GRID) grid = LOSS_GRID;
     {
       Timed t(s, PS_KERNEL_TASKGRAD, st);
-      hipLaunchKernelGGL((k_mf_grad<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->ld, s->num_keys, s->dim, row,
-                         col, val, B, col_key_offset, lambda, sorted_grads ? p.sb.rank : nullptr, p.grads,
-                         p.loss_part);
+      hipLaunchKernelGGL((k_mf_err<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->ld, s->num_keys, s->dim, row,
+                         col, val, B, col_key_offset, lambda, p.sb.rank, ks, p.seg_of_pos, p.sb.hdr, p.pm, p.mat,
+                         p.grads, p.loss_part);
     }
-    LAUNCHED(k_mf_grad);
+    LAUNCHED(k_mf_err);
     if (loss) {
       hipLaunchKernelGGL(k_sum_loss, dim3(1), dim3(BLOCK), 0, st, p.loss_part, grid, loss);
       LAUNCHED(k_sum_loss);
@@ -603,8 +617,11 @@ ps_status ps_step_mf(ps_store* s, const int32_t* row, const int32_t* col, const 
     return PS_OK;
   });
   if (r) return r;
-  if (sorted_grads) return run_reduce(s, p.sb, ks, SrcSorted{p.grads, s->dim}, n, {all_keys(s)}, st);
-  return run_reduce(s, p.sb, ks, SrcIndirect{p.grads, perm, s->dim}, n, {all_keys(s)}, st);
+  // column keys merge the stored rows; row keys form theirs from the column-row snapshot
+  if (ps_status r = launch_segreduce(s, p.sb, ks, SrcSorted{p.grads, s->dim}, n, PART_UPPER, st)) return r;
+  SrcMF src{p.pm, p.mat, s->W, s->ld, (double)lambda, s->dim};
+  if (ps_status r = launch_segreduce(s, p.sb, ks, src, n, PART_LOWER, st)) return r;
+  return launch_finalize(s, p.sb, ks, n, st);
 }
 
 ps_status ps_step_kge(ps_store* s, const int32_t* head, const int32_t* rel, const int32_t* tail, const int32_t* neg,
@@ -655,7 +672,7 @@ ps_status ps_step_kge(ps_store* s, const int32_t* head, const int32_t* rel, cons
     hipLaunchKernelGGL(k_sum_loss, dim3(1), dim3(BLOCK), 0, st, p.loss_part, grid, loss);
     LAUNCHED(k_sum_loss);
   }
-  return run_reduce(s, p.sb, ks, SrcKGE{perm, p.mat, p.base, p.coef, per, n_head_neg, s->dim}, n, {all_keys(s)}, st);
+  return run_reduce(s, p.sb, ks, SrcKGE{perm, p.mat, p.base, p.coef, per, n_head_neg, s->dim}, n, {PART_ALL}, st);
 }
 
 ps_status ps_step_sgns(ps_store* s, const int32_t* centre, const int32_t* ctx, const int32_t* neg, int64_t B,
@@ -688,7 +705,9 @@ ps_status ps_step_sgns(ps_store* s, const int32_t* centre, const int32_t* ctx, c
   uint32_t *ks, *perm;
   KeysSGNS kk{centre, ctx, neg, (int)per, slots, n_neg, out_key_offset, p.ok};
   if (ps_status r = run_sort(s, kk, n, s->num_keys, p.sb, s->status, nullptr, false, st, &ks, &perm)) return r;
-  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st)) return r;
+  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st, nullptr,
+                                 (uint32_t)out_key_offset))
+    return r;
   RowShape shape;
   row_shape(s->dim, true, &shape);
   ps_status r = with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
@@ -708,9 +727,7 @@ ps_status ps_step_sgns(ps_store* s, const int32_t* centre, const int32_t* ctx, c
   if (r) return r;
   // output rows first: their gradients read the input rows, which are updated second
   SrcSGNS src{perm, p.mat, p.coef, centre, s->W, s->ld, (int)per, s->dim};
-  return run_reduce(s, p.sb, ks, src, n,
-                    {KeyRange{(uint32_t)out_key_offset, (uint32_t)s->num_keys}, KeyRange{0u, (uint32_t)out_key_offset}},
-                    st);
+  return run_reduce(s, p.sb, ks, src, n, {PART_UPPER, PART_LOWER}, st);
 }
 
 ps_status ps_step_ctr(ps_store* s, const int64_t* keys, const float* label, int64_t B, int32_t F, double* loss,
@@ -756,7 +773,7 @@ ps_status ps_step_ctr(ps_store* s, const int64_t* keys, const float* label, int6
     return PS_OK;
   });
   if (r) return r;
-  return run_reduce(s, p.sb, ks, SrcSorted{p.grads, s->dim}, n, {all_keys(s)}, st);
+  return run_reduce(s, p.sb, ks, SrcSorted{p.grads, s->dim}, n, {PART_ALL}, st);
 }
 
 ps_status ps_get_error(ps_store* s, void* stream) {

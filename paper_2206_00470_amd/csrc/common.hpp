@@ -26,6 +26,9 @@ struct SegHeader {
   uint32_t num_chunks;   // reduce work items
   uint32_t num_valid;    // occurrences with a valid key (a prefix of the sorted order)
   uint32_t num_split;    // segments longer than one chunk, listed for the finalize pass
+  uint32_t num_lo;       // segments whose key is below the split key given to k_seg_write
+  uint32_t chunk_lo;     // chunks whose key is below that split key (they come first)
+  uint32_t pad[2];
 };
 
 // ------------------------------------------------------------------ lanes

@@ -47,36 +47,62 @@ __global__ __launch_bounds__(BLOCK) void k_pull(const float* __restrict__ W, int
 }
 
 // ------------------------------------------------------------------ gradient sources
-// A source yields the fp32 gradient fragment of the occurrence at sorted
-// position j (the fragment of lane gl of its row group).
+// A source describes the fp32 gradient row of the occurrence at sorted
+// position j in two steps:
+//   meta(j)            the per-occurrence indirections (loaded by one lane,
+//                      for up to L consecutive positions at once)
+//   load(m, own, ...)  the lane's fragment of the gradient row, given the
+//                      broadcast metadata and, for sources that need it
+//                      (kNeedsOwn), the pre-step row of the segment's key.
+// Metadata travels between lanes word by word.
+template <class T>
+__device__ __forceinline__ T shfl_pod(const T& v, int src, int width) {
+  static_assert(sizeof(T) % 4 == 0, "metadata must be whole words");
+  union U {
+    T t;
+    uint32_t w[sizeof(T) / 4];
+  } in, out;
+  in.t = v;
+#pragma unroll
+  for (int i = 0; i < (int)(sizeof(T) / 4); ++i) out.w[i] = __shfl(in.w[i], src, width);
+  return out.t;
+}
 
 // Gradient rows in occurrence order, read through the sort permutation.
 struct SrcIndirect {
+  static constexpr bool kNeedsOwn = false;
   const float* grads;
   const uint32_t* perm;
   int dim;
+  struct Meta {
+    const float* row;
+  };
+  __device__ __forceinline__ Meta meta(int64_t j) const { return {grads + (int64_t)perm[j] * dim}; }
   template <int L, int NV, int VW>
-  __device__ __forceinline__ void load(int64_t j, int gl, float* x) const {
-    const float* row = grads + (int64_t)perm[j] * dim;
+  __device__ __forceinline__ void load(const Meta& m, const float*, int gl, float* x) const {
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
       const int c = (gl + v * L) * VW;
-      if (c < dim) load_frag<VW>(row + c, x + v * VW);
+      if (c < dim) load_frag<VW>(m.row + c, x + v * VW);
     }
   }
 };
 
 // Gradient rows already stored at their sorted positions.
 struct SrcSorted {
+  static constexpr bool kNeedsOwn = false;
   const float* grads;
   int dim;
+  struct Meta {
+    const float* row;
+  };
+  __device__ __forceinline__ Meta meta(int64_t j) const { return {grads + j * dim}; }
   template <int L, int NV, int VW>
-  __device__ __forceinline__ void load(int64_t j, int gl, float* x) const {
-    const float* row = grads + j * dim;
+  __device__ __forceinline__ void load(const Meta& m, const float*, int gl, float* x) const {
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
       const int c = (gl + v * L) * VW;
-      if (c < dim) load_frag<VW>(row + c, x + v * VW);
+      if (c < dim) load_frag<VW>(m.row + c, x + v * VW);
     }
   }
 };
@@ -100,63 +126,73 @@ __device__ __forceinline__ int64_t xcd_slot(int64_t block, int64_t nblocks) {
 }
 
 // Chunk c covers sorted positions [chunk_start[c], chunk_start[c+1]) of one
-// segment.  The group sums its gradient rows in position order in fp64.  If
-// the chunk is the whole segment it rounds the sum to fp32 and applies
-// AdaGrad to the key's row; otherwise it stores the fp64 partial in the slot
-// of its CHUNK-aligned block (2 slots per block: the chunk starting at the
-// block start, and the one starting inside it) for k_seg_finalize; the
-// first chunk of such a segment also appends the segment to split_list.
+// segment.  The group sums its gradient rows in position order in fp64: the
+// metadata of up to L positions is loaded at once (one lane each) and
+// broadcast, so each row load depends on one round trip only.  If the chunk
+// is the whole segment the group rounds the sum to fp32 and applies AdaGrad
+// to the key's row; otherwise it stores the fp64 partial in the slot of its
+// CHUNK-aligned block (2 slots per block: the chunk starting at the block
+// start, and the one starting inside it) for k_seg_finalize; the first chunk
+// of such a segment also appends the segment to split_list.
 template <int L, int NV, int VW, class Src>
 __global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, int64_t n, float* __restrict__ W,
                                                      float* __restrict__ G, int64_t ld, int dim, float lr, float eps,
                                                      double* __restrict__ partial,
                                                      int32_t* __restrict__ split_list, SegHeader* split_hdr,
-                                                     uint32_t key_lo, uint32_t key_hi) {
+                                                     int part) {
   constexpr int GPB = BLOCK / L;
   constexpr int NE = NV * VW;
   constexpr int UNROLL = NE <= 4 ? 4 : 2;
+  using Meta = typename Src::Meta;
   const int gl = threadIdx.x % L;
-  const int64_t nchunks = sv.hdr->num_chunks;
+  // part 0: every chunk; 1: chunks whose key reaches the split key; 2: the others
+  int64_t cbeg = 0, cend = sv.hdr->num_chunks;
+  if (part == 1) cbeg = sv.hdr->chunk_lo;
+  if (part == 2) cend = sv.hdr->chunk_lo;
   const int64_t stride = (int64_t)gridDim.x * GPB;
-  for (int64_t c = xcd_slot(blockIdx.x, gridDim.x) * GPB + threadIdx.x / L; c < nchunks; c += stride) {
+  for (int64_t c = cbeg + xcd_slot(blockIdx.x, gridDim.x) * GPB + threadIdx.x / L; c < cend; c += stride) {
     const int64_t j0 = sv.chunk_start[c];
     const int64_t j1 = sv.chunk_start[c + 1];
     const uint32_t key = sv.keys[j0];
-    if (key < key_lo || key >= key_hi) continue;
     // the chunk is a whole segment if its neighbours hold other keys
     const bool head = j0 == 0 || sv.keys[j0 - 1] != key;
     const bool whole = head && (j1 >= n || sv.keys[j1] != key);
     float* wrow = W + (int64_t)key * ld;
     float* grow = G + (int64_t)key * ld;
     float wv[NE], gv[NE];
-    if (whole) {   // issue the table reads early, they do not depend on the sum
+    if (whole || Src::kNeedsOwn) {   // issue the table reads early, they do not depend on the sum
 #pragma unroll
       for (int v = 0; v < NV; ++v) {
         const int col = (gl + v * L) * VW;
         if (col < dim) {
           load_frag<VW>(wrow + col, wv + v * VW);
-          load_frag<VW>(grow + col, gv + v * VW);
+          if (whole) load_frag<VW>(grow + col, gv + v * VW);
         }
       }
     }
     double acc[NE];
 #pragma unroll
     for (int e = 0; e < NE; ++e) acc[e] = 0.0;
-    int64_t j = j0;
-    for (; j + UNROLL <= j1; j += UNROLL) {
-      float x[UNROLL][NE];
+    for (int64_t jb = j0; jb < j1; jb += L) {
+      const int cnt = (int)((j1 - jb) < L ? (j1 - jb) : L);
+      Meta mine{};
+      if (gl < cnt) mine = src.meta(jb + gl);
+      int q = 0;
+      for (; q + UNROLL <= cnt; q += UNROLL) {
+        float x[UNROLL][NE];
 #pragma unroll
-      for (int q = 0; q < UNROLL; ++q) src.template load<L, NV, VW>(j + q, gl, x[q]);
+        for (int u = 0; u < UNROLL; ++u) src.template load<L, NV, VW>(shfl_pod(mine, q + u, L), wv, gl, x[u]);
 #pragma unroll
-      for (int q = 0; q < UNROLL; ++q)
+        for (int u = 0; u < UNROLL; ++u)
 #pragma unroll
-        for (int e = 0; e < NE; ++e) acc[e] += (double)x[q][e];
-    }
-    for (; j < j1; ++j) {
-      float x[NE];
-      src.template load<L, NV, VW>(j, gl, x);
+          for (int e = 0; e < NE; ++e) acc[e] += (double)x[u][e];
+      }
+      for (; q < cnt; ++q) {
+        float x[NE];
+        src.template load<L, NV, VW>(shfl_pod(mine, q, L), wv, gl, x);
 #pragma unroll
-      for (int e = 0; e < NE; ++e) acc[e] += (double)x[e];
+        for (int e = 0; e < NE; ++e) acc[e] += (double)x[e];
+      }
     }
     if (whole) {
 #pragma unroll
@@ -230,7 +266,7 @@ __global__ __launch_bounds__(BLOCK) void k_seg_finalize(SegView sv, float* __res
 #pragma unroll
       for (int f = 0; f < FU; ++f)
 #pragma unroll
-        for (int e = 0; e < NE; ++e) acc[e] += x[f][e];
+        for (int q = 0; q < NE; ++q) acc[q] += x[f][q];
     }
     for (; k < m; k += GPB) {
       const int64_t slot = k == 0 ? 2 * b0 + ((s0 % CHUNK) != 0) : 2 * (b0 + k);

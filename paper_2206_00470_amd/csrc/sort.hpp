@@ -256,19 +256,24 @@ __global__ __launch_bounds__(BLOCK) void k_seg_scan(uint32_t* __restrict__ tstat
     hdr->num_unique = ch;
     hdr->num_chunks = cc;
     hdr->num_valid = cv;
+    hdr->num_lo = ch;   // k_seg_write lowers these if some key reaches the split key
+    hdr->chunk_lo = cc;
     seg_off[ch] = (int32_t)cv;
     chunk_start[cc] = (int32_t)cv;
   }
 }
 
-// Per tile (blocked: thread t owns positions base + t*16 .. +15): write the
-// segment offsets (and optionally the distinct keys as int64) and the chunk
-// list (start position and segment of each chunk).
+// Per tile (blocked: thread t owns positions base + t*SORT_ITEMS ..): write
+// the segment offsets (and optionally the distinct keys as int64), the chunk
+// list (start position and segment of each chunk), optionally the segment of
+// every valid position, and the number of segments with key < split_key.
 __global__ __launch_bounds__(BLOCK) void k_seg_write(const uint32_t* __restrict__ ks, int64_t n, uint32_t sentinel,
                                                      const uint32_t* __restrict__ tstat, int tiles,
                                                      int32_t* __restrict__ seg_off, int64_t* __restrict__ uniq64,
                                                      int32_t* __restrict__ chunk_start,
-                                                     int32_t* __restrict__ chunk_seg) {
+                                                     int32_t* __restrict__ chunk_seg,
+                                                     int32_t* __restrict__ seg_of_pos, uint32_t split_key,
+                                                     SegHeader* hdr) {
   __shared__ uint32_t smem[WAVES_PER_BLOCK + 1];
   const int64_t base = (int64_t)blockIdx.x * TILE + (int64_t)threadIdx.x * SORT_ITEMS;
   uint32_t k[SORT_ITEMS];
@@ -303,9 +308,15 @@ __global__ __launch_bounds__(BLOCK) void k_seg_write(const uint32_t* __restrict_
     if ((hf >> q) & 1u) {
       seg_off[hi] = (int32_t)j;
       if (uniq64) uniq64[hi] = (int64_t)k[q];
+      const uint32_t pk = q == 0 ? prev : k[q - 1];
+      if (k[q] >= split_key && (j == 0 || pk < split_key)) {
+        hdr->num_lo = hi;
+        hdr->chunk_lo = ci;   // a segment head is always a chunk head
+      }
       cur = hi;
       ++hi;
     }
+    if (seg_of_pos && j < n && k[q] < sentinel) seg_of_pos[j] = (int32_t)cur;
     if ((cf >> q) & 1u) {
       chunk_start[ci] = (int32_t)j;
       chunk_seg[ci] = (int32_t)cur;

@@ -18,8 +18,13 @@ __global__ __launch_bounds__(BLOCK) void k_sum_loss(const double* __restrict__ p
 }
 
 // ------------------------------------------------------------------ MF
-// Key occurrences of entry b: 2b = row key, 2b+1 = column key.  An entry with
-// a key outside the table yields the (invalid) key -1 for both occurrences.
+// Key occurrences of entry b: 2b = row key, 2b+1 = column key.  Row factors
+// are keys [0, col_off), column factors [col_off, num_keys); an entry with a
+// key outside its range yields the (invalid) key -1 for both occurrences.
+__device__ __forceinline__ bool mf_entry_ok(int64_t ku, int32_t c, int64_t col_off, int64_t num_keys) {
+  return ku >= 0 && ku < col_off && c >= 0 && col_off + (int64_t)c < num_keys;
+}
+
 struct KeysMF {
   const int32_t* row;
   const int32_t* col;
@@ -27,35 +32,50 @@ struct KeysMF {
   int64_t num_keys;
   __device__ int64_t operator()(int64_t i) const {
     const int64_t b = i >> 1;
-    const int64_t ku = row[b];
-    const int64_t km = col_off + (int64_t)col[b];
-    const bool ok = ku >= 0 && ku < num_keys && col[b] >= 0 && km < num_keys;
-    if (!ok) return -1;
-    return (i & 1) ? km : ku;
+    if (!mf_entry_ok(row[b], col[b], col_off, num_keys)) return -1;
+    return (i & 1) ? col_off + (int64_t)col[b] : (int64_t)row[b];
   }
 };
 
-// One row group per entry (u = W[row], m = W[col_off + col], e = v - <u,m>):
-//   grad_u = lam u - e m ,  grad_m = lam m - e u     (fp64, rounded to fp32)
-//   loss  += e^2/2 + lam/2 (|u|^2 + |m|^2)
-// The two gradient rows go to the sorted positions rank[2b], rank[2b+1], or
-// to occurrence positions 2b, 2b+1 when rank is null.
+// What the merge needs of one MF occurrence, stored at its sorted position:
+// e of its entry and its partner row (idx >= 0: row-factor key idx of the
+// table; idx < 0: row -idx-1 of the column-row snapshot).
+struct MFMeta {
+  double e;
+  int32_t idx;
+  int32_t pad;
+};
+
+// One row group per entry (u = W[row], m = W[col_off + col]):
+//   e = v - <u,m>   (fp64)
+//   loss += e^2/2 + lam/2 (|u|^2 + |m|^2)
+// The column occurrence's gradient row lam*m - e*u (fp32) is written to its
+// sorted position in grads: column keys are few and hot, so their merge reads
+// these rows contiguously instead of gathering u again.  The row occurrence
+// (about one per row key) gets an MFMeta at its sorted position and its
+// gradient is formed inside the merge (SrcMF) from the snapshot of m: the
+// entry whose column occurrence is first in its segment copies the pre-step
+// row m to snap[segment - num_lo], one copy per distinct column key.
 template <int L, int NV, int VW>
-__global__ __launch_bounds__(BLOCK) void k_mf_grad(const float* __restrict__ W, int64_t ld, int64_t num_keys, int dim,
-                                                   const int32_t* __restrict__ row, const int32_t* __restrict__ col,
-                                                   const float* __restrict__ val, int64_t B, int64_t col_off,
-                                                   float lam, const uint32_t* __restrict__ rank,
-                                                   float* __restrict__ grads, double* __restrict__ loss_part) {
+__global__ __launch_bounds__(BLOCK) void k_mf_err(const float* __restrict__ W, int64_t ld, int64_t num_keys, int dim,
+                                                  const int32_t* __restrict__ row, const int32_t* __restrict__ col,
+                                                  const float* __restrict__ val, int64_t B, int64_t col_off,
+                                                  float lam, const uint32_t* __restrict__ rank,
+                                                  const uint32_t* __restrict__ ks,
+                                                  const int32_t* __restrict__ seg_of_pos, const SegHeader* hdr,
+                                                  MFMeta* __restrict__ pm, float* __restrict__ snap,
+                                                  float* __restrict__ grads, double* __restrict__ loss_part) {
   constexpr int GPB = BLOCK / L;
   constexpr int NE = NV * VW;
   __shared__ double sm[WAVES_PER_BLOCK];
   const int gl = threadIdx.x % L;
   const double lamd = (double)lam;
+  const int64_t num_lo = hdr->num_lo;
   double lsum = 0.0;
   for (int64_t b = (int64_t)blockIdx.x * GPB + threadIdx.x / L; b < B; b += (int64_t)gridDim.x * GPB) {
+    if (!mf_entry_ok(row[b], col[b], col_off, num_keys)) continue;
     const int64_t ku = row[b];
     const int64_t km = col_off + (int64_t)col[b];
-    if (!(ku >= 0 && ku < num_keys && col[b] >= 0 && km < num_keys)) continue;
     const float* up = W + ku * ld;
     const float* mp = W + km * ld;
     float u[NE], m[NE];
@@ -83,27 +103,76 @@ __global__ __launch_bounds__(BLOCK) void k_mf_grad(const float* __restrict__ W, 
     nu = group_sum<L>(nu);
     nm = group_sum<L>(nm);
     const double err = (double)val[b] - dot;
-    if (gl == 0) lsum += 0.5 * err * err + 0.5 * lamd * (nu + nm);
-    float gu[NE], gm[NE];
-#pragma unroll
-    for (int e = 0; e < NE; ++e) {
-      gu[e] = (float)(lamd * (double)u[e] - err * (double)m[e]);
-      gm[e] = (float)(lamd * (double)m[e] - err * (double)u[e]);
+    const uint32_t pos = rank[2 * b + 1];
+    const int64_t si = (int64_t)seg_of_pos[pos] - num_lo;
+    if (gl == 0) {
+      lsum += 0.5 * err * err + 0.5 * lamd * (nu + nm);
+      pm[rank[2 * b]] = MFMeta{err, (int32_t)(-si - 1), 0};   // row occurrence: partner m (snapshot)
     }
-    float* du = grads + (rank ? (int64_t)rank[2 * b] : 2 * b) * dim;
-    float* dm = grads + (rank ? (int64_t)rank[2 * b + 1] : 2 * b + 1) * dim;
+    float* gm = grads + (int64_t)pos * dim;                    // column occurrence: lam*m - e*u
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
       const int c = (gl + v * L) * VW;
       if (c < dim) {
-        store_frag<VW>(du + c, gu + v * VW);
-        store_frag<VW>(dm + c, gm + v * VW);
+        float g[VW];
+#pragma unroll
+        for (int q = 0; q < VW; ++q) g[q] = (float)(lamd * (double)m[v * VW + q] - err * (double)u[v * VW + q]);
+        store_frag<VW>(gm + c, g);
+      }
+    }
+    if (pos == 0 || ks[pos - 1] != ks[pos]) {   // first occurrence of this column key
+      float* dst = snap + si * dim;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int c = (gl + v * L) * VW;
+        if (c < dim) store_frag<VW>(dst + c, m + v * VW);
       }
     }
   }
   lsum = block_sum_double(lsum, sm);
   if (threadIdx.x == 0) loss_part[blockIdx.x] = lsum;
 }
+
+// Gradient source of the MF merge.  Occurrence 2b (row key) has gradient
+// lam*u - e*m, occurrence 2b+1 (column key) lam*m - e*u, each rounded once
+// to fp32 as a materialized row would be.  "own" is the segment key's row,
+// read before its update; the partner is read from a table that is still
+// pre-step when the merge runs in two launches: column keys first (their
+// partners u are row-factor rows, not yet updated), then row keys (their
+// partners m come from the column-row snapshot taken before any update).
+struct SrcMF {
+  static constexpr bool kNeedsOwn = true;
+  const MFMeta* pm;
+  const float* snap;
+  const float* W;
+  int64_t ld;
+  double lam;
+  int dim;
+  struct Meta {
+    const float* partner;
+    double e;
+  };
+  __device__ __forceinline__ Meta meta(int64_t j) const {
+    const MFMeta r = pm[j];
+    const float* partner = r.idx >= 0 ? W + (int64_t)r.idx * ld : snap + (int64_t)(-(int64_t)r.idx - 1) * dim;
+    return {partner, r.e};
+  }
+  // own: the lane's fragment of the segment key's pre-step row
+  template <int L, int NV, int VW>
+  __device__ __forceinline__ void load(const Meta& m, const float* own, int gl, float* x) const {
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int c = (gl + v * L) * VW;
+      if (c < dim) {
+        float p[VW];
+        load_frag<VW>(m.partner + c, p);
+#pragma unroll
+        for (int q = 0; q < VW; ++q)
+          x[v * VW + q] = (float)(lam * (double)own[v * VW + q] - m.e * (double)p[q]);
+      }
+    }
+  }
+};
 
 // ------------------------------------------------------------------ shared pieces
 __device__ __forceinline__ double sigmoid_d(double x) {
@@ -415,32 +484,42 @@ __global__ __launch_bounds__(BLOCK) void k_kge_grad(const float* __restrict__ W,
 
 // Gradient source of the KGE push.
 struct SrcKGE {
+  static constexpr bool kNeedsOwn = false;
   const uint32_t* perm;
   const float* mat;
   const double* base;
   const double* coef;
   int per, n_head, dim;
-  template <int L, int NV, int VW>
-  __device__ __forceinline__ void load(int64_t j, int gl, float* x) const {
+  struct Meta {
+    const void* row;    // fp32 stored row (s, r, o) or fp64 base row (negatives)
+    double c;           // coefficient of a negative
+    uint32_t scaled;    // 1: row is fp64 and scaled by c
+    uint32_t pad;
+  };
+  __device__ __forceinline__ Meta meta(int64_t j) const {
     const uint32_t occ = perm[j];
     const uint32_t t = occ / (uint32_t)per;
     const uint32_t q = occ - t * (uint32_t)per;
-    if (q < 3) {
-      const float* row = mat + ((int64_t)t * 3 + q) * dim;
+    if (q < 3) return {mat + ((int64_t)t * 3 + q) * dim, 0.0, 0u, 0u};
+    return {base + ((int64_t)t * 2 + ((int)q - 3 < n_head ? 0 : 1)) * dim, coef[occ], 1u, 0u};
+  }
+  template <int L, int NV, int VW>
+  __device__ __forceinline__ void load(const Meta& m, const float*, int gl, float* x) const {
+    if (!m.scaled) {
+      const float* row = static_cast<const float*>(m.row);
 #pragma unroll
       for (int v = 0; v < NV; ++v) {
         const int c = (gl + v * L) * VW;
         if (c < dim) load_frag<VW>(row + c, x + v * VW);
       }
     } else {
-      const double cj = coef[occ];
-      const double* row = base + ((int64_t)t * 2 + ((int)q - 3 < n_head ? 0 : 1)) * dim;
+      const double* row = static_cast<const double*>(m.row);
 #pragma unroll
       for (int v = 0; v < NV; ++v) {
         const int c = (gl + v * L) * VW;
         if (c < dim)
 #pragma unroll
-          for (int e = 0; e < VW; ++e) x[v * VW + e] = (float)(cj * row[c + e]);
+          for (int e = 0; e < VW; ++e) x[v * VW + e] = (float)(m.c * row[c + e]);
       }
     }
   }
@@ -602,6 +681,7 @@ __global__ __launch_bounds__(BLOCK) void k_sgns_grad(const float* __restrict__ W
 // row; an output occurrence of centre b is a * v with v the centre's input
 // row, read from the table before the input rows are updated.
 struct SrcSGNS {
+  static constexpr bool kNeedsOwn = false;
   const uint32_t* perm;
   const float* mat;
   const double* coef;
@@ -609,30 +689,29 @@ struct SrcSGNS {
   const float* W;
   int64_t ld;
   int per, dim;
-  template <int L, int NV, int VW>
-  __device__ __forceinline__ void load(int64_t j, int gl, float* x) const {
+  struct Meta {
+    const float* row;   // the centre's stored gradient row, or its input row
+    double a;           // coefficient of an output occurrence
+    uint32_t scaled;    // 1: row is the input row, scaled by a
+    uint32_t pad;
+  };
+  __device__ __forceinline__ Meta meta(int64_t j) const {
     const uint32_t occ = perm[j];
     const uint32_t b = occ / (uint32_t)per;
     const uint32_t q = occ - b * (uint32_t)per;
-    if (q == 0) {
-      const float* row = mat + (int64_t)b * dim;
+    if (q == 0) return {mat + (int64_t)b * dim, 1.0, 0u, 0u};
+    return {W + (int64_t)centre[b] * ld, coef[occ], 1u, 0u};
+  }
+  template <int L, int NV, int VW>
+  __device__ __forceinline__ void load(const Meta& m, const float*, int gl, float* x) const {
 #pragma unroll
-      for (int v = 0; v < NV; ++v) {
-        const int c = (gl + v * L) * VW;
-        if (c < dim) load_frag<VW>(row + c, x + v * VW);
-      }
-    } else {
-      const double a = coef[occ];
-      const float* row = W + (int64_t)centre[b] * ld;
+    for (int v = 0; v < NV; ++v) {
+      const int c = (gl + v * L) * VW;
+      if (c < dim) {
+        float t[VW];
+        load_frag<VW>(m.row + c, t);
 #pragma unroll
-      for (int v = 0; v < NV; ++v) {
-        const int c = (gl + v * L) * VW;
-        if (c < dim) {
-          float t[VW];
-          load_frag<VW>(row + c, t);
-#pragma unroll
-          for (int e = 0; e < VW; ++e) x[v * VW + e] = (float)(a * (double)t[e]);
-        }
+        for (int e = 0; e < VW; ++e) x[v * VW + e] = m.scaled ? (float)(m.a * (double)t[e]) : t[e];
       }
     }
   }
