@@ -335,6 +335,7 @@ ps_status run_segments(const SortBufs& b, const uint32_t* ks, int64_t n, int64_t
 
 int64_t reduce_grid(int64_t n, int L) {
   const int64_t gpb = BLOCK / L;
+  // one row group per chunk up to a cap (there are at most n + n/CHUNK + 1 chunks)
   int64_t g = ceil_div(n + n / CHUNK + 1, gpb);
   if (g > 8192) g = 8192;
   g = ceil_div(g, NUM_XCD) * NUM_XCD;

@@ -149,14 +149,35 @@ __global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, int64_
   int64_t cbeg = 0, cend = sv.hdr->num_chunks;
   if (part == 1) cbeg = sv.hdr->chunk_lo;
   if (part == 2) cend = sv.hdr->chunk_lo;
-  const int64_t stride = (int64_t)gridDim.x * GPB;
-  for (int64_t c = cbeg + xcd_slot(blockIdx.x, gridDim.x) * GPB + threadIdx.x / L; c < cend; c += stride) {
-    const int64_t j0 = sv.chunk_start[c];
-    const int64_t j1 = sv.chunk_start[c + 1];
-    const uint32_t key = sv.keys[j0];
-    // the chunk is a whole segment if its neighbours hold other keys
-    const bool head = j0 == 0 || sv.keys[j0 - 1] != key;
-    const bool whole = head && (j1 >= n || sv.keys[j1] != key);
+  // chunks are dealt round-robin over the S row groups of the grid (hot keys'
+  // chunks spread out); lane i prefetches the bounds and keys of the group's
+  // i-th next chunk, so one round of loads serves L chunks
+  const int64_t S = (int64_t)gridDim.x * GPB;
+  for (int64_t cb = cbeg + xcd_slot(blockIdx.x, gridDim.x) * GPB + threadIdx.x / L; cb < cend; cb += S * L) {
+    const int64_t left = (cend - cb + S - 1) / S;
+    const int ccount = (int)(left < L ? left : L);
+    int32_t my_j0 = 0, my_j1 = 0;
+    uint32_t my_key = 0, my_flags = 0;
+    Meta my_first{};   // metadata of the chunk's first occurrence
+    if (gl < ccount) {
+      my_j0 = sv.chunk_start[cb + gl * S];
+      my_j1 = sv.chunk_start[cb + gl * S + 1];
+      my_first = src.meta(my_j0);
+      my_key = sv.keys[my_j0];
+      // the chunk is a whole segment if its neighbours hold other keys
+      const bool hd = my_j0 == 0 || sv.keys[my_j0 - 1] != my_key;
+      const bool wh = hd && (my_j1 >= n || sv.keys[my_j1] != my_key);
+      my_flags = (hd ? 1u : 0u) | (wh ? 2u : 0u);
+    }
+  for (int ci = 0; ci < ccount; ++ci) {
+    const int64_t c = cb + ci * S;
+    const int64_t j0 = __shfl(my_j0, ci, L);
+    const int64_t j1 = __shfl(my_j1, ci, L);
+    const uint32_t key = __shfl(my_key, ci, L);
+    const uint32_t flags = __shfl(my_flags, ci, L);
+    const bool head = flags & 1u;
+    const bool whole = flags & 2u;
+    const Meta first = shfl_pod(my_first, ci, L);
     float* wrow = W + (int64_t)key * ld;
     float* grow = G + (int64_t)key * ld;
     float wv[NE], gv[NE];
@@ -176,7 +197,8 @@ __global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, int64_
     for (int64_t jb = j0; jb < j1; jb += L) {
       const int cnt = (int)((j1 - jb) < L ? (j1 - jb) : L);
       Meta mine{};
-      if (gl < cnt) mine = src.meta(jb + gl);
+      if (jb == j0 && gl == 0) mine = first;            // prefetched with the chunk bounds
+      else if (gl < cnt) mine = src.meta(jb + gl);
       int q = 0;
       for (; q + UNROLL <= cnt; q += UNROLL) {
         float x[UNROLL][NE];
@@ -218,6 +240,7 @@ __global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, int64_
           for (int e = 0; e < VW; ++e) p[col + e] = acc[v * VW + e];
       }
     }
+  }
   }
 }
 
