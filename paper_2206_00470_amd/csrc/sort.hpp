@@ -130,8 +130,13 @@ __global__ __launch_bounds__(BLOCK) void k_radix_scatter(const uint32_t* __restr
                                                          int bits, const uint32_t* __restrict__ offs, int tiles,
                                                          uint32_t* __restrict__ kout, uint32_t* __restrict__ vout,
                                                          uint32_t* __restrict__ rank) {
+  static_assert(BLOCK == MAX_BINS, "one thread per digit in the tile scan");
   __shared__ uint32_t wc[WAVES_PER_BLOCK][MAX_BINS];
   __shared__ uint32_t toff[MAX_BINS];
+  __shared__ uint32_t dstart[MAX_BINS];
+  __shared__ uint32_t scan_smem[WAVES_PER_BLOCK + 1];
+  __shared__ uint32_t sk[TILE];
+  __shared__ uint32_t sv[TILE];
   const int bins = 1 << bits;
   const uint32_t mask = (uint32_t)bins - 1u;
   for (int i = threadIdx.x; i < WAVES_PER_BLOCK * MAX_BINS; i += BLOCK) (&wc[0][0])[i] = 0u;
@@ -173,25 +178,45 @@ __global__ __launch_bounds__(BLOCK) void k_radix_scatter(const uint32_t* __restr
     rk[it] = r;
   }
   __syncthreads();
-  for (int d = threadIdx.x; d < bins; d += BLOCK) {
-    uint32_t run = 0;
-    for (int ww = 0; ww < WAVES_PER_BLOCK; ++ww) {
-      const uint32_t t = wc[ww][d];
-      wc[ww][d] = run;
-      run += t;
+  // per digit: offsets of the 4 waves inside the tile's run, and the run's
+  // start within the tile (exclusive scan over digits)
+  uint32_t tot = 0;
+  {
+    const int d = threadIdx.x;   // BLOCK == MAX_BINS
+    if (d < bins) {
+      for (int ww = 0; ww < WAVES_PER_BLOCK; ++ww) {
+        const uint32_t t = wc[ww][d];
+        wc[ww][d] = tot;
+        tot += t;
+      }
     }
+    uint32_t all;
+    dstart[d] = block_exclusive_scan(d < bins ? tot : 0u, scan_smem, &all);
   }
   __syncthreads();
+  // stage the tile in LDS in digit order ...
 #pragma unroll
   for (int it = 0; it < SORT_ITEMS; ++it) {
     const int64_t i = base + it * WAVE + lane;
     if (i < n) {
       const uint32_t d = (key[it] >> shift) & mask;
-      const uint32_t pos = toff[d] + wc[w][d] + rk[it];
-      kout[pos] = key[it];
-      vout[pos] = val[it];
-      if constexpr (RANK) rank[val[it]] = pos;
+      const uint32_t p = dstart[d] + wc[w][d] + rk[it];
+      sk[p] = key[it];
+      sv[p] = val[it];
     }
+  }
+  __syncthreads();
+  // ... and write it out: consecutive threads write consecutive positions of a digit run
+  const int64_t tile_base = (int64_t)blockIdx.x * TILE;
+  const int cnt = (int)((n - tile_base) < TILE ? (n - tile_base) : TILE);
+  for (int p = threadIdx.x; p < cnt; p += BLOCK) {
+    const uint32_t k = sk[p];
+    const uint32_t v = sv[p];
+    const uint32_t d = (k >> shift) & mask;
+    const uint32_t pos = toff[d] + (uint32_t)p - dstart[d];
+    kout[pos] = k;
+    vout[pos] = v;
+    if constexpr (RANK) rank[v] = pos;
   }
 }
 
