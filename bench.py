@@ -136,12 +136,14 @@ class Bench:
         if self.name in ("mf", "mf_tiny"):
             B = bt.row.size
             Ucol = np.unique(bt.col).size
-            # merge: column keys read their stored gradient rows; row keys read a 16-byte record
-            # and the snapshot of their entry's column row (one read per distinct column key)
-            return {"segreduce": B * R + B * 16.0 + Ucol * R + table,
-                    # inputs, 2 gathered rows, 1 gradient row + 1 record out, ranks, segment ids,
-                    # one snapshot row per distinct column key
-                    "taskgrad": B * (12.0 + 2 * R + R + 16.0 + 8.0 + 4.0) + Ucol * R}
+            Urow = U - Ucol
+            # row-key merge: a 16-byte record per entry, the entry's column row (one read per
+            # distinct column key), the column-occurrence gradient row out, and the row keys'
+            # W and G; column-key merge: the stored gradient rows and the column keys' W and G;
+            # record scatter: col, val, two ranks in, one record out
+            return {"rowmerge": B * (16.0 + R) + Ucol * R + 4.0 * Urow * R,
+                    "segreduce": B * R + 4.0 * Ucol * R,
+                    "taskgrad": B * (4.0 + 4.0 + 8.0 + 16.0)}
         if self.name == "ctr":
             B, F = bt.keys.shape
             return {"segreduce": n * R + table,
@@ -206,7 +208,7 @@ def main():
     assert store.error() == 0
 
     # ------------------------------------------------------------ timed steps
-    for k in range(4):
+    for k in range(5):
         store.read_timing(k)            # reset
     store.set_timing(True)
     torch.cuda.synchronize()
@@ -219,6 +221,7 @@ def main():
     assert store.error() == 0
     kt = {"segreduce": store.read_timing(_lib.PS_KERNEL_SEGREDUCE),
           "taskgrad": store.read_timing(_lib.PS_KERNEL_TASKGRAD),
+          "rowmerge": store.read_timing(_lib.PS_KERNEL_MF_ROWMERGE),
           "scatter": store.read_timing(_lib.PS_KERNEL_SCATTER)}
 
     idx = [args.warmup + i for i in range(args.steps)]
@@ -226,10 +229,10 @@ def main():
     U_avg = float(np.mean([wb.uniq[i % nb] for i in idx]))
     ms_per_step = elapsed * 1e3 / args.steps
     rows_per_s = 2.0 * occ / (ms_per_step * 1e-3)
-    alg = {k: float(np.mean([wb.alg_bytes(i)[k] for i in idx])) for k in ("segreduce", "taskgrad")}
-    # launches per step of the merge kernel: MF merges column keys then row keys,
-    # SGNS output rows then input rows
-    seg_launches_per_step = 2 if args.workload in ("sgns", "mf", "mf_tiny") else 1
+    alg = {k: float(np.mean([wb.alg_bytes(i)[k] for i in idx])) for k in wb.alg_bytes(idx[0])}
+    # launches per step of the merge kernel: SGNS merges output rows, then input rows
+    # (MF's row-key merge is timed on its own, "rowmerge")
+    seg_launches_per_step = 2 if args.workload == "sgns" else 1
     kernels = {}
     for name, nbytes in alg.items():
         ms, cnt = kt[name]
@@ -240,10 +243,12 @@ def main():
                          "alg_GBps": nbytes / (per_step_ms * 1e-3) / 1e9 if cnt else None,
                          "launches_per_step": nl}
     kernels["scatter"] = {"ms_per_step": kt["scatter"][0] / max(args.steps, 1), "launches": kt["scatter"][1]}
-    dom = max(("segreduce", "taskgrad"), key=lambda k: kernels[k]["ms_per_step"])
+    dom = max(alg, key=lambda k: kernels[k]["ms_per_step"])
     dk = kernels[dom]
-    symbol = {"segreduce": "k_segreduce",
-              "taskgrad": {"mf": "k_mf_err", "mf_tiny": "k_mf_err", "kge": "k_kge_grad", "sgns": "k_sgns_grad",
+    symbol = {"segreduce": "k_segreduce<%s>" % {"mf": "SrcSorted", "mf_tiny": "SrcSorted", "kge": "SrcKGE",
+                                                 "sgns": "SrcSGNS", "ctr": "SrcSorted"}[args.workload],
+              "rowmerge": "k_segreduce<SrcMFRow>",
+              "taskgrad": {"mf": "k_mf_pack", "mf_tiny": "k_mf_pack", "kge": "k_kge_grad", "sgns": "k_sgns_grad",
                            "ctr": "k_ctr_grad"}[args.workload]}[dom]
     traffic = counter_traffic(args.workload, symbol)
     roofline = {

@@ -41,7 +41,7 @@ ps_status fail(ps_status st, const char* fmt, ...) {
 #define LAUNCHED(name) HIP_TRY(hipGetLastError())
 
 constexpr int64_t MAX_OCC = (int64_t(1) << 31) - (int64_t(1) << 20);
-constexpr int NUM_TIMED = 4;
+constexpr int NUM_TIMED = 5;
 constexpr size_t MAX_TIMED_LAUNCHES = 1 << 14;
 
 }  // namespace
@@ -58,7 +58,7 @@ struct ps_store {
   int32_t* status;   // device: [0] sticky key-range flag
   bool timing = false;
   std::vector<std::pair<hipEvent_t, hipEvent_t>> events[NUM_TIMED];
-  size_t used[NUM_TIMED] = {0, 0, 0, 0};
+  size_t used[NUM_TIMED] = {};
 };
 
 namespace {
@@ -210,13 +210,13 @@ struct Plan {
   double* base = nullptr;      // KGE: fp64 rows d phi/d s (r,o) and d phi/d o (s,r) per triple
   double* coef = nullptr;      // KGE, SGNS: fp64 coefficient per occurrence
   uint8_t* ok = nullptr;       // per-unit validity
-  int32_t* seg_of_pos = nullptr;   // MF: segment of each sorted position
-  MFMeta* pm = nullptr;            // MF: e and partner row per sorted position
+  MFEntry* pe = nullptr;       // MF: entry data at the sorted position of its row occurrence
   double* loss_part = nullptr;
   size_t bytes = 0;
 };
 
 constexpr int64_t LOSS_GRID = 2048;
+constexpr int64_t MERGE_GRID_MAX = 8192;   // largest merge grid (see reduce_grid)
 
 bool plan_op(void* ws, int64_t num_keys, int dim, int op, int64_t units, int64_t per_unit, Plan* p) {
   (void)num_keys;
@@ -231,11 +231,10 @@ bool plan_op(void* ws, int64_t num_keys, int dim, int op, int64_t units, int64_t
       break;
     case PS_OP_STEP_MF:
       carve_sort(c, n, dim, true, true, &p->sb);
-      p->seg_of_pos = c.take<int32_t>(n);
-      p->pm = c.take<MFMeta>(n);                     // per sorted position: e and the partner row
-      p->mat = c.take<float>(size_t(units) * dim);   // column-row snapshot (at most one per entry)
+      // row keys sort below column keys, so row occurrences hold positions [0, units)
+      p->pe = c.take<MFEntry>(units);
       p->grads = c.take<float>(size_t(n) * dim);     // column-occurrence gradient rows, sorted positions
-      p->loss_part = c.take<double>(LOSS_GRID);
+      p->loss_part = c.take<double>(MERGE_GRID_MAX);   // written by the row-key merge
       break;
     case PS_OP_STEP_CTR:
       carve_sort(c, n, dim, true, true, &p->sb);
@@ -321,14 +320,14 @@ ps_status run_sort(ps_store* s, KS ks, int64_t n, int64_t num_keys, SortBufs& b,
 }
 
 ps_status run_segments(const SortBufs& b, const uint32_t* ks, int64_t n, int64_t num_keys, int32_t* seg_off,
-                       int64_t* uniq64, hipStream_t st, int32_t* seg_of_pos = nullptr, uint32_t split_key = 0) {
+                       int64_t* uniq64, hipStream_t st, uint32_t split_key = 0) {
   const int tiles = (int)b.tiles;
   hipLaunchKernelGGL(k_seg_count, dim3(tiles), dim3(BLOCK), 0, st, ks, n, (uint32_t)num_keys, b.tstat, tiles);
   LAUNCHED(k_seg_count);
   hipLaunchKernelGGL(k_seg_scan, dim3(1), dim3(BLOCK), 0, st, b.tstat, tiles, b.hdr, seg_off, b.chunk_start);
   LAUNCHED(k_seg_scan);
   hipLaunchKernelGGL(k_seg_write, dim3(tiles), dim3(BLOCK), 0, st, ks, n, (uint32_t)num_keys, b.tstat, tiles,
-                     seg_off, uniq64, b.chunk_start, b.chunk_seg, seg_of_pos, split_key, b.hdr);
+                     seg_off, uniq64, b.chunk_start, b.chunk_seg, split_key, b.hdr);
   LAUNCHED(k_seg_write);
   return PS_OK;
 }
@@ -337,7 +336,7 @@ int64_t reduce_grid(int64_t n, int L) {
   const int64_t gpb = BLOCK / L;
   // one row group per chunk up to a cap (there are at most n + n/CHUNK + 1 chunks)
   int64_t g = ceil_div(n + n / CHUNK + 1, gpb);
-  if (g > 8192) g = 8192;
+  if (g > MERGE_GRID_MAX) g = MERGE_GRID_MAX;
   g = ceil_div(g, NUM_XCD) * NUM_XCD;
   return g;
 }
@@ -351,13 +350,13 @@ enum { PART_ALL = 0, PART_UPPER = 1, PART_LOWER = 2 };
 
 template <class Src>
 ps_status launch_segreduce(ps_store* s, const SortBufs& b, const uint32_t* ks, Src src, int64_t n, int part,
-                           hipStream_t st) {
+                           hipStream_t st, int timing_id = PS_KERNEL_SEGREDUCE) {
   RowShape shape;
   if (!row_shape(s->dim, true, &shape)) return fail(PS_ERR_UNSUPPORTED, "dim %d not supported", s->dim);
   SegView sv{ks, b.seg_off, b.chunk_start, b.chunk_seg, b.hdr};
   return with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
     const int64_t grid = reduce_grid(n, L);
-    Timed t(s, PS_KERNEL_SEGREDUCE, st);
+    Timed t(s, timing_id, st);
     hipLaunchKernelGGL((k_segreduce<L, NV, VW, Src>), dim3(grid), dim3(BLOCK), 0, st, sv, src, n, s->W, s->G, s->ld,
                        s->dim, s->lr, s->eps, b.partial, b.split_list, b.hdr, part);
     LAUNCHED(k_segreduce);
@@ -598,30 +597,25 @@ ps_status ps_step_mf(ps_store* s, const int32_t* row, const int32_t* col, const 
   KeysMF kmf{row, col, col_key_offset, s->num_keys};
   if (ps_status r = run_sort(s, kmf, n, s->num_keys, p.sb, s->status, nullptr, true, st, &ks, &perm)) return r;
   const uint32_t split = (uint32_t)(col_key_offset < s->num_keys ? col_key_offset : s->num_keys);
-  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st, p.seg_of_pos, split)) return r;
-  RowShape shape;
-  row_shape(s->dim, true, &shape);
-  ps_status r = with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
-    int64_t grid = ceil_div(B, BLOCK / L);
-    if (grid > LOSS_GRID) grid = LOSS_GRID;
-    {
-      Timed t(s, PS_KERNEL_TASKGRAD, st);
-      hipLaunchKernelGGL((k_mf_err<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->ld, s->num_keys, s->dim, row,
-                         col, val, B, col_key_offset, lambda, p.sb.rank, ks, p.seg_of_pos, p.sb.hdr, p.pm, p.mat,
-                         p.grads, p.loss_part);
-    }
-    LAUNCHED(k_mf_err);
-    if (loss) {
-      hipLaunchKernelGGL(k_sum_loss, dim3(1), dim3(BLOCK), 0, st, p.loss_part, grid, loss);
-      LAUNCHED(k_sum_loss);
-    }
-    return PS_OK;
-  });
-  if (r) return r;
-  // column keys merge the stored rows; row keys form theirs from the column-row snapshot
+  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st, split)) return r;
+  {
+    Timed t(s, PS_KERNEL_TASKGRAD, st);
+    hipLaunchKernelGGL(k_mf_pack, dim3(small_grid(B, BLOCK, MERGE_GRID_MAX)), dim3(BLOCK), 0, st, row, col, val, B,
+                       col_key_offset, s->num_keys, p.sb.rank, p.pe);
+  }
+  LAUNCHED(k_mf_pack);
+  // Row keys first: their source reads the column rows before any column
+  // update, forms e, the loss and the column-occurrence gradients; then the
+  // column keys merge those stored rows.
+  SrcMFRow src{p.pe, s->W, s->ld, p.grads, p.loss_part, (double)lambda, s->dim};
+  if (ps_status r = launch_segreduce(s, p.sb, ks, src, n, PART_LOWER, st, PS_KERNEL_MF_ROWMERGE)) return r;
+  if (loss) {
+    RowShape shape;
+    row_shape(s->dim, true, &shape);
+    hipLaunchKernelGGL(k_sum_loss, dim3(1), dim3(BLOCK), 0, st, p.loss_part, reduce_grid(n, shape.L), loss);
+    LAUNCHED(k_sum_loss);
+  }
   if (ps_status r = launch_segreduce(s, p.sb, ks, SrcSorted{p.grads, s->dim}, n, PART_UPPER, st)) return r;
-  SrcMF src{p.pm, p.mat, s->W, s->ld, (double)lambda, s->dim};
-  if (ps_status r = launch_segreduce(s, p.sb, ks, src, n, PART_LOWER, st)) return r;
   return launch_finalize(s, p.sb, ks, n, st);
 }
 
@@ -706,8 +700,7 @@ ps_status ps_step_sgns(ps_store* s, const int32_t* centre, const int32_t* ctx, c
   uint32_t *ks, *perm;
   KeysSGNS kk{centre, ctx, neg, (int)per, slots, n_neg, out_key_offset, p.ok};
   if (ps_status r = run_sort(s, kk, n, s->num_keys, p.sb, s->status, nullptr, false, st, &ks, &perm)) return r;
-  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st, nullptr,
-                                 (uint32_t)out_key_offset))
+  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st, (uint32_t)out_key_offset))
     return r;
   RowShape shape;
   row_shape(s->dim, true, &shape);

@@ -107,6 +107,22 @@ struct SrcSorted {
   }
 };
 
+// Sources with kLoss = true also add each occurrence's loss term to a
+// per-thread sum (load takes it as a last argument); the merge writes the
+// workgroup totals to src.loss_part[workgroup].
+template <class Src>
+constexpr bool src_has_loss() {
+  if constexpr (requires { Src::kLoss; }) return Src::kLoss;
+  else return false;
+}
+
+template <int L, int NV, int VW, class Src>
+__device__ __forceinline__ void src_load(const Src& src, const typename Src::Meta& m, const float* own, int gl,
+                                         float* x, double& lsum) {
+  if constexpr (src_has_loss<Src>()) src.template load<L, NV, VW>(m, own, gl, x, lsum);
+  else src.template load<L, NV, VW>(m, own, gl, x);
+}
+
 // ------------------------------------------------------------------ reduce
 struct SegView {
   const uint32_t* keys;        // sorted u32 keys
@@ -142,7 +158,7 @@ __global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, int64_
                                                      int part) {
   constexpr int GPB = BLOCK / L;
   constexpr int NE = NV * VW;
-  constexpr int UNROLL = NE <= 4 ? 4 : 2;
+  constexpr int UNROLL = src_has_loss<Src>() ? 1 : (NE <= 4 ? 4 : 2);
   using Meta = typename Src::Meta;
   const int gl = threadIdx.x % L;
   // part 0: every chunk; 1: chunks whose key reaches the split key; 2: the others
@@ -153,6 +169,7 @@ __global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, int64_
   // chunks spread out); lane i prefetches the bounds and keys of the group's
   // i-th next chunk, so one round of loads serves L chunks
   const int64_t S = (int64_t)gridDim.x * GPB;
+  double lsum = 0.0;
   for (int64_t cb = cbeg + xcd_slot(blockIdx.x, gridDim.x) * GPB + threadIdx.x / L; cb < cend; cb += S * L) {
     const int64_t left = (cend - cb + S - 1) / S;
     const int ccount = (int)(left < L ? left : L);
@@ -203,7 +220,7 @@ __global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, int64_
       for (; q + UNROLL <= cnt; q += UNROLL) {
         float x[UNROLL][NE];
 #pragma unroll
-        for (int u = 0; u < UNROLL; ++u) src.template load<L, NV, VW>(shfl_pod(mine, q + u, L), wv, gl, x[u]);
+        for (int u = 0; u < UNROLL; ++u) src_load<L, NV, VW>(src, shfl_pod(mine, q + u, L), wv, gl, x[u], lsum);
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u)
 #pragma unroll
@@ -211,7 +228,7 @@ __global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, int64_
       }
       for (; q < cnt; ++q) {
         float x[NE];
-        src.template load<L, NV, VW>(shfl_pod(mine, q, L), wv, gl, x);
+        src_load<L, NV, VW>(src, shfl_pod(mine, q, L), wv, gl, x, lsum);
 #pragma unroll
         for (int e = 0; e < NE; ++e) acc[e] += (double)x[e];
       }
@@ -241,6 +258,11 @@ __global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, int64_
       }
     }
   }
+  }
+  if constexpr (src_has_loss<Src>()) {
+    __shared__ double sm[WAVES_PER_BLOCK];
+    lsum = block_sum_double(lsum, sm);
+    if (threadIdx.x == 0) src.loss_part[blockIdx.x] = lsum;
   }
 }
 

@@ -290,14 +290,14 @@ __global__ __launch_bounds__(BLOCK) void k_seg_scan(uint32_t* __restrict__ tstat
 
 // Per tile (blocked: thread t owns positions base + t*SORT_ITEMS ..): write
 // the segment offsets (and optionally the distinct keys as int64), the chunk
-// list (start position and segment of each chunk), optionally the segment of
-// every valid position, and the number of segments with key < split_key.
+// list (start position and segment of each chunk) and the number of segments
+// with key < split_key.
 __global__ __launch_bounds__(BLOCK) void k_seg_write(const uint32_t* __restrict__ ks, int64_t n, uint32_t sentinel,
                                                      const uint32_t* __restrict__ tstat, int tiles,
                                                      int32_t* __restrict__ seg_off, int64_t* __restrict__ uniq64,
                                                      int32_t* __restrict__ chunk_start,
                                                      int32_t* __restrict__ chunk_seg,
-                                                     int32_t* __restrict__ seg_of_pos, uint32_t split_key,
+                                                     uint32_t split_key,
                                                      SegHeader* hdr) {
   __shared__ uint32_t smem[WAVES_PER_BLOCK + 1];
   const int64_t base = (int64_t)blockIdx.x * TILE + (int64_t)threadIdx.x * SORT_ITEMS;
@@ -341,7 +341,6 @@ __global__ __launch_bounds__(BLOCK) void k_seg_write(const uint32_t* __restrict_
       cur = hi;
       ++hi;
     }
-    if (seg_of_pos && j < n && k[q] < sentinel) seg_of_pos[j] = (int32_t)cur;
     if ((cf >> q) & 1u) {
       chunk_start[ci] = (int32_t)j;
       chunk_seg[ci] = (int32_t)cur;

@@ -37,138 +37,95 @@ struct KeysMF {
   }
 };
 
-// What the merge needs of one MF occurrence, stored at its sorted position:
-// e of its entry and its partner row (idx >= 0: row-factor key idx of the
-// table; idx < 0: row -idx-1 of the column-row snapshot).
-struct MFMeta {
-  double e;
-  int32_t idx;
-  int32_t pad;
+// What the row-key merge needs of one MF entry, stored at the sorted
+// position of its row occurrence: the column key, the observed value and the
+// sorted position of the column occurrence.
+struct MFEntry {
+  uint32_t col_key;
+  float y;
+  uint32_t col_pos;
+  uint32_t pad;
 };
 
-// One row group per entry (u = W[row], m = W[col_off + col]):
-//   e = v - <u,m>   (fp64)
+// Entry b -> its MFEntry at the row occurrence's sorted position (rank[2b]);
+// reads are in entry order, the write is one 16-byte scatter.
+__global__ __launch_bounds__(BLOCK) void k_mf_pack(const int32_t* __restrict__ row, const int32_t* __restrict__ col,
+                                                   const float* __restrict__ val, int64_t B, int64_t col_off,
+                                                   int64_t num_keys, const uint32_t* __restrict__ rank,
+                                                   MFEntry* __restrict__ pe) {
+  for (int64_t b = (int64_t)blockIdx.x * BLOCK + threadIdx.x; b < B; b += (int64_t)gridDim.x * BLOCK) {
+    const int32_t c = col[b];
+    if (!mf_entry_ok(row[b], c, col_off, num_keys)) continue;
+    const uint2 rk = *reinterpret_cast<const uint2*>(rank + 2 * b);
+    pe[rk.x] = MFEntry{(uint32_t)(col_off + (int64_t)c), val[b], rk.y, 0u};
+  }
+}
+
+// MF row keys, merged before any column key is updated.  For the row
+// occurrence of entry (u = W[row], m = W[col_off + col], y) the merge has the
+// pre-step row u of the segment key; this source reads m and forms
+//   e = y - <u,m>   (fp64)
+//   row gradient      lam*u - e*m   (returned, fp32)
+//   column gradient   lam*m - e*u   (fp32, stored at the column occurrence's
+//                                    sorted position for the column-key merge)
 //   loss += e^2/2 + lam/2 (|u|^2 + |m|^2)
-// The column occurrence's gradient row lam*m - e*u (fp32) is written to its
-// sorted position in grads: column keys are few and hot, so their merge reads
-// these rows contiguously instead of gathering u again.  The row occurrence
-// (about one per row key) gets an MFMeta at its sorted position and its
-// gradient is formed inside the merge (SrcMF) from the snapshot of m: the
-// entry whose column occurrence is first in its segment copies the pre-step
-// row m to snap[segment - num_lo], one copy per distinct column key.
-template <int L, int NV, int VW>
-__global__ __launch_bounds__(BLOCK) void k_mf_err(const float* __restrict__ W, int64_t ld, int64_t num_keys, int dim,
-                                                  const int32_t* __restrict__ row, const int32_t* __restrict__ col,
-                                                  const float* __restrict__ val, int64_t B, int64_t col_off,
-                                                  float lam, const uint32_t* __restrict__ rank,
-                                                  const uint32_t* __restrict__ ks,
-                                                  const int32_t* __restrict__ seg_of_pos, const SegHeader* hdr,
-                                                  MFMeta* __restrict__ pm, float* __restrict__ snap,
-                                                  float* __restrict__ grads, double* __restrict__ loss_part) {
-  constexpr int GPB = BLOCK / L;
-  constexpr int NE = NV * VW;
-  __shared__ double sm[WAVES_PER_BLOCK];
-  const int gl = threadIdx.x % L;
-  const double lamd = (double)lam;
-  const int64_t num_lo = hdr->num_lo;
-  double lsum = 0.0;
-  for (int64_t b = (int64_t)blockIdx.x * GPB + threadIdx.x / L; b < B; b += (int64_t)gridDim.x * GPB) {
-    if (!mf_entry_ok(row[b], col[b], col_off, num_keys)) continue;
-    const int64_t ku = row[b];
-    const int64_t km = col_off + (int64_t)col[b];
-    const float* up = W + ku * ld;
-    const float* mp = W + km * ld;
-    float u[NE], m[NE];
+struct SrcMFRow {
+  static constexpr bool kNeedsOwn = true;
+  static constexpr bool kLoss = true;
+  const MFEntry* pe;
+  const float* W;
+  int64_t ld;
+  float* grads;
+  double* loss_part;
+  double lam;
+  int dim;
+  struct Meta {
+    const float* partner;
+    float y;
+    uint32_t col_pos;
+  };
+  __device__ __forceinline__ Meta meta(int64_t j) const {
+    const MFEntry r = pe[j];
+    return {W + (int64_t)r.col_key * ld, r.y, r.col_pos};
+  }
+  template <int L, int NV, int VW>
+  __device__ __forceinline__ void load(const Meta& m, const float* own, int gl, float* x, double& lsum) const {
+    float p[NV * VW];
+    double dot = 0.0, nu = 0.0, nm = 0.0;
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
       const int c = (gl + v * L) * VW;
       if (c < dim) {
-        load_frag<VW>(up + c, u + v * VW);
-        load_frag<VW>(mp + c, m + v * VW);
-      } else {
+        load_frag<VW>(m.partner + c, p + v * VW);
 #pragma unroll
-        for (int e = 0; e < VW; ++e) u[v * VW + e] = m[v * VW + e] = 0.0f;
+        for (int q = 0; q < VW; ++q) {
+          // a product of two floats is exact in fp64, so a fused multiply-add
+          // rounds exactly like the separate multiply and add
+          const double uq = (double)own[v * VW + q], mq = (double)p[v * VW + q];
+          dot = __builtin_fma(uq, mq, dot);
+          nu = __builtin_fma(uq, uq, nu);
+          nm = __builtin_fma(mq, mq, nm);
+        }
       }
-    }
-    double dot = 0.0, nu = 0.0, nm = 0.0;
-#pragma unroll
-    for (int e = 0; e < NE; ++e) {
-      // a product of two floats is exact in fp64, so a fused multiply-add
-      // rounds exactly like the separate multiply and add
-      dot = __builtin_fma((double)u[e], (double)m[e], dot);
-      nu = __builtin_fma((double)u[e], (double)u[e], nu);
-      nm = __builtin_fma((double)m[e], (double)m[e], nm);
     }
     dot = group_sum<L>(dot);
     nu = group_sum<L>(nu);
     nm = group_sum<L>(nm);
-    const double err = (double)val[b] - dot;
-    const uint32_t pos = rank[2 * b + 1];
-    const int64_t si = (int64_t)seg_of_pos[pos] - num_lo;
-    if (gl == 0) {
-      lsum += 0.5 * err * err + 0.5 * lamd * (nu + nm);
-      pm[rank[2 * b]] = MFMeta{err, (int32_t)(-si - 1), 0};   // row occurrence: partner m (snapshot)
-    }
-    float* gm = grads + (int64_t)pos * dim;                    // column occurrence: lam*m - e*u
+    const double err = (double)m.y - dot;
+    if (gl == 0) lsum += 0.5 * err * err + 0.5 * lam * (nu + nm);
+    float* gc = grads + (int64_t)m.col_pos * dim;
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
       const int c = (gl + v * L) * VW;
       if (c < dim) {
         float g[VW];
 #pragma unroll
-        for (int q = 0; q < VW; ++q) g[q] = (float)(lamd * (double)m[v * VW + q] - err * (double)u[v * VW + q]);
-        store_frag<VW>(gm + c, g);
-      }
-    }
-    if (pos == 0 || ks[pos - 1] != ks[pos]) {   // first occurrence of this column key
-      float* dst = snap + si * dim;
-#pragma unroll
-      for (int v = 0; v < NV; ++v) {
-        const int c = (gl + v * L) * VW;
-        if (c < dim) store_frag<VW>(dst + c, m + v * VW);
-      }
-    }
-  }
-  lsum = block_sum_double(lsum, sm);
-  if (threadIdx.x == 0) loss_part[blockIdx.x] = lsum;
-}
-
-// Gradient source of the MF merge.  Occurrence 2b (row key) has gradient
-// lam*u - e*m, occurrence 2b+1 (column key) lam*m - e*u, each rounded once
-// to fp32 as a materialized row would be.  "own" is the segment key's row,
-// read before its update; the partner is read from a table that is still
-// pre-step when the merge runs in two launches: column keys first (their
-// partners u are row-factor rows, not yet updated), then row keys (their
-// partners m come from the column-row snapshot taken before any update).
-struct SrcMF {
-  static constexpr bool kNeedsOwn = true;
-  const MFMeta* pm;
-  const float* snap;
-  const float* W;
-  int64_t ld;
-  double lam;
-  int dim;
-  struct Meta {
-    const float* partner;
-    double e;
-  };
-  __device__ __forceinline__ Meta meta(int64_t j) const {
-    const MFMeta r = pm[j];
-    const float* partner = r.idx >= 0 ? W + (int64_t)r.idx * ld : snap + (int64_t)(-(int64_t)r.idx - 1) * dim;
-    return {partner, r.e};
-  }
-  // own: the lane's fragment of the segment key's pre-step row
-  template <int L, int NV, int VW>
-  __device__ __forceinline__ void load(const Meta& m, const float* own, int gl, float* x) const {
-#pragma unroll
-    for (int v = 0; v < NV; ++v) {
-      const int c = (gl + v * L) * VW;
-      if (c < dim) {
-        float p[VW];
-        load_frag<VW>(m.partner + c, p);
-#pragma unroll
-        for (int q = 0; q < VW; ++q)
-          x[v * VW + q] = (float)(lam * (double)own[v * VW + q] - m.e * (double)p[q]);
+        for (int q = 0; q < VW; ++q) {
+          const double uq = (double)own[v * VW + q], mq = (double)p[v * VW + q];
+          x[v * VW + q] = (float)(lam * uq - err * mq);
+          g[q] = (float)(lam * mq - err * uq);
+        }
+        store_frag<VW>(gc + c, g);
       }
     }
   }
