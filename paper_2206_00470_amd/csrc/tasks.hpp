@@ -12,7 +12,16 @@ __global__ __launch_bounds__(BLOCK) void k_sum_loss(const double* __restrict__ p
                                                     double* __restrict__ out) {
   __shared__ double sm[WAVES_PER_BLOCK];
   double s = 0.0;
-  for (int64_t i = threadIdx.x; i < n; i += BLOCK) s += part[i];
+  int64_t i = threadIdx.x;
+  // eight independent loads per round, added in index order
+  for (; i + 7 * BLOCK < n; i += 8 * BLOCK) {
+    double x[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) x[k] = part[i + k * BLOCK];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) s += x[k];
+  }
+  for (; i < n; i += BLOCK) s += part[i];
   s = block_sum_double(s, sm);
   if (threadIdx.x == 0) *out = s;
 }
