@@ -571,20 +571,33 @@ __global__ __launch_bounds__(BLOCK) void k_sgns_grad(const float* __restrict__ W
 #pragma unroll
     for (int e = 0; e < NE; ++e) gv[e] = 0.0;
     // all output rows of the centre in occurrence order: row r is slot r / (K+1),
-    // position r % (K+1) (0 = the context word, then the negatives)
+    // position r % (K+1) (0 = the context word, then the negatives).  Lane i
+    // holds the table id of row t*L + i of the current tile t of L rows (-1:
+    // absent slot or past the end); the next tile's ids are loaded one tile
+    // ahead, so the row loads never wait for an id load.
     const int rows = slots * (K + 1);
+    auto row_id = [&](int r) -> int64_t {
+      if (r >= rows) return -1;
+      const int q = r / (K + 1);
+      const int k = r - q * (K + 1);
+      const int64_t cx = ctx[b * slots + q];
+      const int64_t ng = k == 0 ? 0 : (int64_t)neg[(b * slots + q) * K + (k - 1)];
+      return cx == -1 ? -1 : (k == 0 ? cx : ng);
+    };
+    int64_t id_cur = row_id(gl);
+    int64_t id_nxt = row_id(L + gl);
     for (int r0 = 0; r0 < rows; r0 += JB) {
+      if (r0 > 0 && r0 % L == 0) {
+        id_cur = id_nxt;
+        id_nxt = row_id(r0 + L + gl);
+      }
       float u[JB][NE];
       bool live[JB];
 #pragma unroll
       for (int jj = 0; jj < JB; ++jj) {
-        const int r = r0 + jj;
-        const int q = r / (K + 1);
-        const int k = r - q * (K + 1);
-        const int64_t cx = r < rows ? (int64_t)ctx[b * slots + q] : -1;
-        live[jj] = cx != -1;
-        const int64_t id = !live[jj] ? 0 : (k == 0 ? cx : (int64_t)neg[(b * slots + q) * K + (k - 1)]);
-        const float* up = W + (out_off + id) * ld;
+        const int64_t id = __shfl(id_cur, r0 % L + jj, L);
+        live[jj] = id != -1;
+        const float* up = W + (out_off + (live[jj] ? id : 0)) * ld;
 #pragma unroll
         for (int q2 = 0; q2 < NV; ++q2) {
           const int c = (gl + q2 * L) * VW;
@@ -607,8 +620,9 @@ __global__ __launch_bounds__(BLOCK) void k_sgns_grad(const float* __restrict__ W
       const int r_my = r0 + gl / (L / JB);
       const int q_my = r_my / (K + 1);
       const int k_my = r_my - q_my * (K + 1);
+      const bool live_my = __shfl(id_cur, r0 % L + gl / (L / JB), L) != -1;   // also false past the end
       double a_my = 0.0;
-      if (r_my < rows && ctx[b * slots + q_my] != -1) {
+      if (live_my) {
         // context word: a = -sigmoid(-x), loss softplus(-x); negative: a = sigmoid(x), loss softplus(x)
         const double sgn = k_my == 0 ? -1.0 : 1.0;
         double sig, sp;
