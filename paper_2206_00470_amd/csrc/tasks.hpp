@@ -366,13 +366,23 @@ __global__ __launch_bounds__(BLOCK) void k_kge_grad(const float* __restrict__ W,
         hb[k] = hR[i]; hb[cdim + k] = hI[i];
       }
     }
+    // lane l holds the id of negative 64 i + l of the current tile i; the
+    // next tile's ids are loaded one tile ahead, so the row loads of a batch
+    // never wait for an id load
     const int32_t* nt = neg + t * n_neg;
+    int32_t id_cur = lane < n_neg ? nt[lane] : 0;
+    int32_t id_nxt = WAVE + lane < n_neg ? nt[WAVE + lane] : 0;
     for (int j0 = 0; j0 < n_neg; j0 += JB) {
+      if (j0 > 0 && j0 % WAVE == 0) {
+        id_cur = id_nxt;
+        id_nxt = j0 + WAVE + lane < n_neg ? nt[j0 + WAVE + lane] : 0;
+      }
       float xR[JB][KPL], xI[JB][KPL];
 #pragma unroll
       for (int jj = 0; jj < JB; ++jj) {
         const int j = j0 + jj;
-        const float* xp = W + (int64_t)(j < n_neg ? nt[j] : 0) * ld;
+        const int32_t id = __shfl(id_cur, j0 % WAVE + jj, WAVE);
+        const float* xp = W + (int64_t)(j < n_neg ? id : 0) * ld;
 #pragma unroll
         for (int i = 0; i < KPL; ++i) {
           const int k = lane + WAVE * i;
