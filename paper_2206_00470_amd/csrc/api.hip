@@ -171,7 +171,7 @@ RadixPlan radix_plan(int64_t num_keys) {
 // Buffers of the sort + segment pipeline, carved from the workspace.
 struct SortBufs {
   SegHeader* hdr;
-  uint32_t* ghist;        // [MAX_PASSES][MAX_BINS]
+  uint32_t* ghist;        // [MAX_PASSES][GH_COPIES][MAX_BINS]
   uint32_t* counts;       // [MAX_BINS][tiles]
   uint32_t* k[2];
   uint32_t* v[2];
@@ -188,7 +188,7 @@ struct SortBufs {
 void carve_sort(Carver& c, int64_t n, int dim, bool want_rank, bool want_segments, SortBufs* b) {
   b->tiles = ceil_div(n, TILE);
   b->hdr = c.take<SegHeader>(16);   // header and histogram are cleared together
-  b->ghist = c.take<uint32_t>(MAX_PASSES * MAX_BINS);
+  b->ghist = c.take<uint32_t>(MAX_PASSES * GH_COPIES * MAX_BINS);
   b->counts = c.take<uint32_t>(size_t(MAX_BINS) * b->tiles);
   b->k[0] = c.take<uint32_t>(n);
   b->k[1] = c.take<uint32_t>(n);
@@ -266,9 +266,10 @@ bool plan_op(void* ws, int64_t num_keys, int dim, int op, int64_t units, int64_t
 
 // ------------------------------------------------------------------ pipeline pieces
 void clear_header(const SortBufs& b, hipStream_t st) {
-  const int64_t words = (reinterpret_cast<char*>(b.ghist + MAX_PASSES * MAX_BINS) -
+  const int64_t words = (reinterpret_cast<char*>(b.ghist + MAX_PASSES * GH_COPIES * MAX_BINS) -
                          reinterpret_cast<char*>(b.hdr)) / 4;
-  hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(BLOCK), 0, st, reinterpret_cast<uint32_t*>(b.hdr), words);
+  hipLaunchKernelGGL(k_zero_words, dim3(ceil_div(words, 4 * BLOCK)), dim3(BLOCK), 0, st,
+                     reinterpret_cast<uint32_t*>(b.hdr), words);
 }
 
 // Stable radix sort of the keys produced by `ks`.  Returns the sorted keys;
@@ -294,7 +295,8 @@ ps_status run_sort(ps_store* s, KS ks, int64_t n, int64_t num_keys, SortBufs& b,
                          plan.bits[p], b.counts, tiles);
       LAUNCHED(k_radix_count);
     }
-    hipLaunchKernelGGL(k_radix_scan, dim3(bins), dim3(BLOCK), 0, st, b.counts, tiles, b.ghist + p * MAX_BINS);
+    hipLaunchKernelGGL(k_radix_scan, dim3(bins), dim3(BLOCK), 0, st, b.counts, tiles,
+                       b.ghist + p * GH_COPIES * MAX_BINS);
     LAUNCHED(k_radix_scan);
     uint32_t* vout = (last && perm_out) ? perm_out : b.v[1 - src];
     uint32_t* rank = (last && want_rank) ? b.rank : nullptr;
@@ -332,11 +334,11 @@ ps_status run_segments(const SortBufs& b, const uint32_t* ks, int64_t n, int64_t
   return PS_OK;
 }
 
-int64_t reduce_grid(int64_t n, int L) {
+int64_t reduce_grid(int64_t n, int L, int64_t cap = MERGE_GRID_MAX) {
   const int64_t gpb = BLOCK / L;
   // one row group per chunk up to a cap (there are at most n + n/CHUNK + 1 chunks)
   int64_t g = ceil_div(n + n / CHUNK + 1, gpb);
-  if (g > MERGE_GRID_MAX) g = MERGE_GRID_MAX;
+  if (g > cap) g = cap;
   g = ceil_div(g, NUM_XCD) * NUM_XCD;
   return g;
 }
@@ -350,12 +352,12 @@ enum { PART_ALL = 0, PART_UPPER = 1, PART_LOWER = 2 };
 
 template <class Src>
 ps_status launch_segreduce(ps_store* s, const SortBufs& b, const uint32_t* ks, Src src, int64_t n, int part,
-                           hipStream_t st, int timing_id = PS_KERNEL_SEGREDUCE) {
+                           hipStream_t st, int timing_id = PS_KERNEL_SEGREDUCE, int64_t grid_cap = MERGE_GRID_MAX) {
   RowShape shape;
   if (!row_shape(s->dim, true, &shape)) return fail(PS_ERR_UNSUPPORTED, "dim %d not supported", s->dim);
   SegView sv{ks, b.seg_off, b.chunk_start, b.chunk_seg, b.hdr};
   return with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
-    const int64_t grid = reduce_grid(n, L);
+    const int64_t grid = reduce_grid(n, L, grid_cap);
     Timed t(s, timing_id, st);
     hipLaunchKernelGGL((k_segreduce<L, NV, VW, Src>), dim3(grid), dim3(BLOCK), 0, st, sv, src, n, s->W, s->G, s->ld,
                        s->dim, s->lr, s->eps, b.partial, b.split_list, b.hdr, part);
@@ -608,11 +610,16 @@ ps_status ps_step_mf(ps_store* s, const int32_t* row, const int32_t* col, const 
   // update, forms e, the loss and the column-occurrence gradients; then the
   // column keys merge those stored rows.
   SrcMFRow src{p.pe, s->W, s->ld, p.grads, p.loss_part, (double)lambda, s->dim};
-  if (ps_status r = launch_segreduce(s, p.sb, ks, src, n, PART_LOWER, st, PS_KERNEL_MF_ROWMERGE)) return r;
+  // (about one key per chunk here: a smaller grid gives each group a longer
+  // run of chunks whose metadata it prefetches together)
+  constexpr int64_t kRowMergeGrid = 2048;
+  if (ps_status r = launch_segreduce(s, p.sb, ks, src, n, PART_LOWER, st, PS_KERNEL_MF_ROWMERGE, kRowMergeGrid))
+    return r;
   if (loss) {
     RowShape shape;
     row_shape(s->dim, true, &shape);
-    hipLaunchKernelGGL(k_sum_loss, dim3(1), dim3(BLOCK), 0, st, p.loss_part, reduce_grid(n, shape.L), loss);
+    hipLaunchKernelGGL(k_sum_loss, dim3(1), dim3(BLOCK), 0, st, p.loss_part, reduce_grid(n, shape.L, kRowMergeGrid),
+                       loss);
     LAUNCHED(k_sum_loss);
   }
   if (ps_status r = launch_segreduce(s, p.sb, ks, SrcSorted{p.grads, s->dim}, n, PART_UPPER, st)) return r;

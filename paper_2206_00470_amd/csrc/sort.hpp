@@ -37,7 +37,9 @@ struct KeysInt64 {
 
 // Reads every occurrence key once: range check (invalid -> sentinel and the
 // sticky error flag), narrow to u32, digit-0 histogram of this tile, and the
-// whole-array histograms of every pass.
+// whole-array histograms of every pass.  Those are kept in GH_COPIES copies,
+// tile t adding to copy t % GH_COPIES, so that no histogram word takes more
+// than tiles / GH_COPIES atomic adds.
 template <class KS>
 __global__ __launch_bounds__(BLOCK) void k_keyprep(KS ks, int64_t n, uint32_t sentinel, RadixPlan plan,
                                                    uint32_t* __restrict__ kout, uint32_t* __restrict__ counts0,
@@ -71,10 +73,11 @@ __global__ __launch_bounds__(BLOCK) void k_keyprep(KS ks, int64_t n, uint32_t se
   if (bad && threadIdx.x == 0 && err) atomicOr(err, 1);
   const int bins0 = 1 << plan.bits[0];
   for (int d = threadIdx.x; d < bins0; d += BLOCK) counts0[(int64_t)d * tiles + blockIdx.x] = h[0][d];
+  uint32_t* gh = ghist + (int64_t)(blockIdx.x % GH_COPIES) * MAX_BINS;
   for (int p = 0; p < plan.passes; ++p) {
     const int bins = 1 << plan.bits[p];
     for (int d = threadIdx.x; d < bins; d += BLOCK)
-      if (h[p][d]) atomicAdd(&ghist[p * MAX_BINS + d], h[p][d]);
+      if (h[p][d]) atomicAdd(&gh[(int64_t)p * GH_COPIES * MAX_BINS + d], h[p][d]);
   }
 }
 
@@ -97,14 +100,23 @@ __global__ __launch_bounds__(BLOCK) void k_radix_count(const uint32_t* __restric
 
 // ------------------------------------------------------------------ scan
 // One workgroup per digit d: offsets[d][t] = sum_{d'<d} total[d'] + sum_{t'<t} counts[d][t'].
+// ghist_pass holds the pass's GH_COPIES histogram copies ([GH_COPIES][MAX_BINS]).
 __global__ __launch_bounds__(BLOCK) void k_radix_scan(uint32_t* __restrict__ counts, int tiles,
                                                       const uint32_t* __restrict__ ghist_pass) {
   __shared__ uint32_t smem[WAVES_PER_BLOCK + 1];
   __shared__ double dsm[WAVES_PER_BLOCK];
   const int d = blockIdx.x;
-  // digit base (exact in double: the sum is below 2^31)
-  double part = 0.0;
-  for (int i = threadIdx.x; i < d; i += BLOCK) part += (double)ghist_pass[i];
+  // digit base: thread i sums digit i's count over the copies (independent
+  // loads), then the block adds the digits below d (exact in double: the sum
+  // is below 2^31)
+  static_assert(BLOCK == MAX_BINS, "one thread per digit");
+  uint32_t x[GH_COPIES];
+#pragma unroll
+  for (int c = 0; c < GH_COPIES; ++c) x[c] = ghist_pass[c * MAX_BINS + threadIdx.x];
+  uint32_t tot = 0;
+#pragma unroll
+  for (int c = 0; c < GH_COPIES; ++c) tot += x[c];
+  double part = (int)threadIdx.x < d ? (double)tot : 0.0;
   double b = block_sum_double(part, dsm);
   __shared__ uint32_t sbase;
   if (threadIdx.x == 0) sbase = (uint32_t)b;
