@@ -182,6 +182,7 @@ struct SortBufs {
   int32_t* chunk_seg;     // [n]
   int32_t* split_list;    // [n/CHUNK + 2]
   double* partial;        // [2*(n/CHUNK+1)][dim]
+  double* fold;           // [n/(FOLD_SB*CHUNK)+1][dim]
   int64_t tiles;
 };
 
@@ -201,6 +202,7 @@ void carve_sort(Carver& c, int64_t n, int dim, bool want_rank, bool want_segment
   b->chunk_seg = c.take<int32_t>(n);
   b->split_list = c.take<int32_t>(n / CHUNK + 2);
   b->partial = c.take<double>(size_t(2) * (n / CHUNK + 1) * dim);
+  b->fold = c.take<double>(size_t(n / (FOLD_SB * CHUNK) + 1) * dim);
 }
 
 struct Plan {
@@ -371,11 +373,17 @@ ps_status launch_finalize(ps_store* s, const SortBufs& b, const uint32_t* ks, in
   if (!row_shape(s->dim, true, &shape)) return fail(PS_ERR_UNSUPPORTED, "dim %d not supported", s->dim);
   SegView sv{ks, b.seg_off, b.chunk_start, b.chunk_seg, b.hdr};
   return with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
+    const size_t lds = size_t(BLOCK / L) * s->dim * sizeof(double);
+    const int64_t nsb = n / (FOLD_SB * CHUNK);   // super-blocks wholly inside [0, n)
+    if (nsb > 0) {
+      hipLaunchKernelGGL((k_seg_fold<L, NV, VW>), dim3(nsb < 1024 ? nsb : 1024), dim3(BLOCK), lds, st, sv, nsb,
+                         (uint32_t)s->num_keys, s->dim, b.partial, b.fold);
+      LAUNCHED(k_seg_fold);
+    }
     int64_t fgrid = n / CHUNK + 1;
     if (fgrid > 1024) fgrid = 1024;
-    const size_t lds = size_t(BLOCK / L) * s->dim * sizeof(double);
     hipLaunchKernelGGL((k_seg_finalize<L, NV, VW>), dim3(fgrid), dim3(BLOCK), lds, st, sv, s->W, s->G, s->ld, s->dim,
-                       s->lr, s->eps, b.partial, b.split_list);
+                       s->lr, s->eps, b.partial, b.fold, b.split_list);
     LAUNCHED(k_seg_finalize);
     return PS_OK;
   });

@@ -266,21 +266,103 @@ __global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, int64_
   }
 }
 
+// Block-wide fixed-order sum of `count` fp64 rows of dim values: row group g
+// adds rows g, g + GPB, g + 2 GPB, ... (FU rows in flight), in that order,
+// and leaves its sum in lds[g][*]; the caller adds the GPB group sums in
+// group order.  row(i) returns the address of row i.
+template <int L, int NV, int VW, class RowAt>
+__device__ __forceinline__ void group_sum_rows(RowAt row, int64_t count, int dim, double* lds) {
+  constexpr int GPB = BLOCK / L;
+  constexpr int NE = NV * VW;
+  constexpr int FU = NE <= 4 ? 8 : 4;
+  const int gl = threadIdx.x % L;
+  const int g = threadIdx.x / L;
+  double acc[NE];
+#pragma unroll
+  for (int q = 0; q < NE; ++q) acc[q] = 0.0;
+  int64_t k = g;
+  for (; k + (FU - 1) * GPB < count; k += FU * GPB) {
+    double x[FU][NE];
+#pragma unroll
+    for (int f = 0; f < FU; ++f) {
+      const double* p = row(k + f * GPB);
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int col = (gl + v * L) * VW;
+#pragma unroll
+        for (int q = 0; q < VW; ++q) x[f][v * VW + q] = col < dim ? p[col + q] : 0.0;
+      }
+    }
+#pragma unroll
+    for (int f = 0; f < FU; ++f)
+#pragma unroll
+      for (int q = 0; q < NE; ++q) acc[q] += x[f][q];
+  }
+  for (; k < count; k += GPB) {
+    const double* p = row(k);
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int col = (gl + v * L) * VW;
+      if (col < dim)
+#pragma unroll
+        for (int q = 0; q < VW; ++q) acc[v * VW + q] += p[col + q];
+    }
+  }
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    const int col = (gl + v * L) * VW;
+    if (col < dim)
+#pragma unroll
+      for (int q = 0; q < VW; ++q) lds[g * dim + col + q] = acc[v * VW + q];
+  }
+}
+
+// Chunk partials of a long segment are folded ahead of the finalize in runs
+// of FOLD_SB CHUNK-aligned blocks ("super-blocks"): super-block s covers
+// sorted positions [s*FOLD_SB*CHUNK, (s+1)*FOLD_SB*CHUNK).  When all of it
+// holds one key, every block in it starts a chunk of that key's segment and
+// its partial sits in the block's even slot; one workgroup adds those FOLD_SB
+// partials in fixed order into fold[s].  A hot key's segment then needs a few
+// fold rows plus the partials at its two ragged ends instead of one partial
+// per chunk.
+constexpr int FOLD_SB = 64;
+
+template <int L, int NV, int VW>
+__global__ __launch_bounds__(BLOCK) void k_seg_fold(SegView sv, int64_t nsb, uint32_t sentinel, int dim,
+                                                    const double* __restrict__ partial,
+                                                    double* __restrict__ fold) {
+  constexpr int GPB = BLOCK / L;
+  extern __shared__ double lds[];   // [GPB][dim]
+  for (int64_t s = blockIdx.x; s < nsb; s += gridDim.x) {
+    const int64_t p0 = s * FOLD_SB * CHUNK;
+    const uint32_t key = sv.keys[p0];
+    if (key >= sentinel || sv.keys[p0 + FOLD_SB * CHUNK - 1] != key) continue;   // uniform over the block
+    const int64_t b0 = s * FOLD_SB;
+    group_sum_rows<L, NV, VW>([&](int64_t k) { return partial + 2 * (b0 + k) * dim; }, FOLD_SB, dim, lds);
+    __syncthreads();
+    for (int col = threadIdx.x; col < dim; col += BLOCK) {
+      double t = 0.0;
+      for (int gg = 0; gg < GPB; ++gg) t += lds[gg * dim + col];
+      fold[s * dim + col] = t;
+    }
+    __syncthreads();
+  }
+}
+
 // Segments longer than one chunk: one workgroup per split segment (listed by
-// k_segreduce).  Its BLOCK/L row groups each add every (BLOCK/L)-th chunk
-// partial in order, the group results are added in group order, rounded once
-// and applied with AdaGrad.  The order is fixed, so the result is
-// deterministic.
+// k_segreduce).  The segment's rows are, in position order: the partials of
+// the blocks before its first whole super-block, the fold rows of its whole
+// super-blocks, then the partials of the blocks after them.  They are added
+// by group_sum_rows, the group results in group order, rounded once and
+// applied with AdaGrad.  The order is fixed, so the result is deterministic.
 template <int L, int NV, int VW>
 __global__ __launch_bounds__(BLOCK) void k_seg_finalize(SegView sv, float* __restrict__ W, float* __restrict__ G,
                                                         int64_t ld, int dim, float lr, float eps,
                                                         const double* __restrict__ partial,
+                                                        const double* __restrict__ fold,
                                                         const int32_t* __restrict__ split_list) {
   constexpr int GPB = BLOCK / L;
-  constexpr int NE = NV * VW;
   extern __shared__ double lds[];   // [GPB][dim]
-  const int gl = threadIdx.x % L;
-  const int g = threadIdx.x / L;
   const int64_t nsplit = sv.hdr->num_split;
   for (int64_t e = blockIdx.x; e < nsplit; e += gridDim.x) {
     const int32_t u = split_list[e];
@@ -288,57 +370,27 @@ __global__ __launch_bounds__(BLOCK) void k_seg_finalize(SegView sv, float* __res
     const int64_t s1 = sv.seg_off[u + 1];
     const uint32_t key = sv.keys[s0];
     const int64_t b0 = s0 / CHUNK;
-    const int64_t m = (s1 - 1) / CHUNK - b0 + 1;   // number of chunk partials
-    double acc[NE];
-#pragma unroll
-    for (int q = 0; q < NE; ++q) acc[q] = 0.0;
-    constexpr int FU = NE <= 4 ? 8 : 4;   // partial rows in flight per group
-    int64_t k = g;
-    for (; k + (FU - 1) * GPB < m; k += FU * GPB) {
-      double x[FU][NE];
-#pragma unroll
-      for (int f = 0; f < FU; ++f) {
-        const int64_t kk = k + f * GPB;
-        const int64_t slot = kk == 0 ? 2 * b0 + ((s0 % CHUNK) != 0) : 2 * (b0 + kk);
-        const double* p = partial + slot * dim;
-#pragma unroll
-        for (int v = 0; v < NV; ++v) {
-          const int col = (gl + v * L) * VW;
-#pragma unroll
-          for (int q = 0; q < VW; ++q) x[f][v * VW + q] = col < dim ? p[col + q] : 0.0;
-        }
-      }
-#pragma unroll
-      for (int f = 0; f < FU; ++f)
-#pragma unroll
-        for (int q = 0; q < NE; ++q) acc[q] += x[f][q];
-    }
-    for (; k < m; k += GPB) {
-      const int64_t slot = k == 0 ? 2 * b0 + ((s0 % CHUNK) != 0) : 2 * (b0 + k);
-      const double* p = partial + slot * dim;
-#pragma unroll
-      for (int v = 0; v < NV; ++v) {
-        const int col = (gl + v * L) * VW;
-        if (col < dim)
-#pragma unroll
-          for (int q = 0; q < VW; ++q) acc[v * VW + q] += p[col + q];
-      }
-    }
-#pragma unroll
-    for (int v = 0; v < NV; ++v) {
-      const int col = (gl + v * L) * VW;
-      if (col < dim)
-#pragma unroll
-        for (int q = 0; q < VW; ++q) lds[g * dim + col + q] = acc[v * VW + q];
-    }
+    const int64_t m = (s1 - 1) / CHUNK - b0 + 1;        // CHUNK blocks the segment touches
+    const int64_t bf = (s0 + CHUNK - 1) / CHUNK;        // first block starting inside it
+    const int64_t sa = (bf + FOLD_SB - 1) / FOLD_SB;    // whole super-blocks: [sa, sb)
+    const int64_t sb = s1 / (FOLD_SB * CHUNK);
+    const int64_t nf = sb > sa ? sb - sa : 0;
+    const int64_t nh = nf ? sa * FOLD_SB - b0 : m;      // partial rows before the folds
+    const int64_t nt = nf ? b0 + m - sb * FOLD_SB : 0;  // partial rows after them
+    auto row = [&](int64_t i) -> const double* {
+      if (i < nh) return partial + (i == 0 ? 2 * b0 + ((s0 % CHUNK) != 0) : 2 * (b0 + i)) * dim;
+      if (i < nh + nf) return fold + (sa + (i - nh)) * dim;
+      return partial + 2 * (sb * FOLD_SB + (i - nh - nf)) * dim;
+    };
+    group_sum_rows<L, NV, VW>(row, nh + nf + nt, dim, lds);
     __syncthreads();
     float* wrow = W + (int64_t)key * ld;
     float* grow = G + (int64_t)key * ld;
     for (int col = threadIdx.x; col < dim; col += BLOCK) {
-      double s = 0.0;
-      for (int gg = 0; gg < GPB; ++gg) s += lds[gg * dim + col];
+      double t = 0.0;
+      for (int gg = 0; gg < GPB; ++gg) t += lds[gg * dim + col];
       float w = wrow[col], a = grow[col];
-      adagrad_elem(w, a, (float)s, lr, eps);
+      adagrad_elem(w, a, (float)t, lr, eps);
       wrow[col] = w;
       grow[col] = a;
     }

@@ -143,6 +143,39 @@ def test_push_parity(K, d, n, zipf, gfill):
     assert_bitwise(Gg[untouched], G0[untouched], "untouched G rows")
 
 
+# Segment lengths around multiples of the fold run (64 chunk blocks; chunks of
+# 32, 64 or 128 occurrences): segments that start or end exactly on a run
+# boundary, runs wholly inside a segment, ragged ends, and a segment that
+# fills the whole batch.
+FOLD_COUNTS = [
+    [8192, 16384, 3, 2],
+    [100, 20000, 8192, 1],
+    [2048, 4096, 6144, 12288],
+    [1, 8191, 8193, 16383],
+    [24576],
+    [5, 2047, 2049, 4095, 4097, 30000],
+]
+
+
+@pytest.mark.parametrize("counts", FOLD_COUNTS)
+def test_push_long_segments_fold_boundaries(counts):
+    say(f"push long segments {counts}")
+    K, d = len(counts) + 3, 16
+    W, G = make_store(K, d, 21, g_fill=True)
+    rng = np.random.default_rng(21)
+    keys = rng.permutation(np.repeat(np.arange(len(counts)), counts)).astype(np.int64)
+    grads = rng.standard_normal((keys.size, d)).astype(np.float32)
+    Wt, Gt = dev(W), dev(G)
+    s = Store(Wt, Gt, LR, EPS)
+    s.push(dev(keys), dev(grads))
+    assert s.error() == 0
+    Wr, Gr = W.copy(), G.copy()
+    oracle.push(Wr, Gr, keys, grads, LR, EPS)
+    assert_close_tables(Wt.cpu().numpy(), Wr, "W")
+    assert_close_tables(Gt.cpu().numpy(), Gr, "G")
+    assert_bitwise(Wt.cpu().numpy()[len(counts):], W[len(counts):], "untouched W rows")
+
+
 def test_push_deterministic():
     K, d, n = 23_000, 100, 300_001
     a = run_push(K, d, n, 1.1, True, seed=4)
