@@ -177,11 +177,13 @@ const char* ps_status_string(ps_status st);
 /* Message of the last error raised on the calling thread ("" if none). */
 const char* ps_last_error_message(void);
 
-/* Kernel timing (instrumentation).  While enabled, the store brackets each
- * launch of the listed kernels with HIP events on the launch stream.
- * ps_read_timing() synchronizes those events and returns the summed
- * duration (ms) and launch count of one kernel since the last reset, then
- * resets it.  kernel_id: 0 = segmented reduce + AdaGrad, 1 = task gradient
+/* Kernel timing (instrumentation).  ps_set_timing(s, mask): bit k of mask
+ * turns on timing of kernel id k (PS_TIMING_ALL: every id; 0: off).  The
+ * store then brackets each launch of those kernels with HIP events on the
+ * launch stream; each event costs a few microseconds of GPU idle time, so a
+ * measurement should time only the kernels it reports.  ps_read_timing()
+ * synchronizes those events and returns the summed duration (ms) and launch
+ * count of one kernel since the last reset, then resets it.  kernel_id: 0 = segmented reduce + AdaGrad, 1 = task gradient
  * (MF: the per-entry record scatter), 2 = radix scatter, 3 = pull, 4 = MF
  * row-key merge that also forms the MF gradients and loss (timed under 4,
  * not 0). */
@@ -190,7 +192,8 @@ const char* ps_last_error_message(void);
 #define PS_KERNEL_SCATTER   2
 #define PS_KERNEL_PULL      3
 #define PS_KERNEL_MF_ROWMERGE 4
-ps_status ps_set_timing(ps_store* s, int32_t enable);
+#define PS_TIMING_ALL (-1)
+ps_status ps_set_timing(ps_store* s, int32_t mask);
 ps_status ps_read_timing(ps_store* s, int32_t kernel_id, double* total_ms, int64_t* launches);
 
 #ifdef __cplusplus

@@ -22,6 +22,7 @@ PS_OP_PULL, PS_OP_PUSH, PS_OP_DEDUP = 0, 1, 2
 PS_OP_STEP_MF, PS_OP_STEP_KGE, PS_OP_STEP_SGNS, PS_OP_STEP_CTR = 3, 4, 5, 6
 
 PS_KERNEL_SEGREDUCE, PS_KERNEL_TASKGRAD, PS_KERNEL_SCATTER, PS_KERNEL_PULL, PS_KERNEL_MF_ROWMERGE = 0, 1, 2, 3, 4
+PS_TIMING_ALL = -1
 
 _p, _i64, _i32, _f32, _sz = C.c_void_p, C.c_int64, C.c_int32, C.c_float, C.c_size_t
 

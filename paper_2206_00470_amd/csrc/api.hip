@@ -56,7 +56,7 @@ struct ps_store {
   float lr;
   float eps;
   int32_t* status;   // device: [0] sticky key-range flag
-  bool timing = false;
+  uint32_t timing = 0;   // bit k: bracket launches of kernel id k
   std::vector<std::pair<hipEvent_t, hipEvent_t>> events[NUM_TIMED];
   size_t used[NUM_TIMED] = {};
 };
@@ -70,7 +70,7 @@ struct Timed {
   hipStream_t st;
   hipEvent_t end = nullptr;
   Timed(ps_store* s_, int id_, hipStream_t st_) : s(s_), id(id_), st(st_) {
-    if (!s || !s->timing || s->used[id] >= MAX_TIMED_LAUNCHES) return;
+    if (!s || !((s->timing >> id) & 1u) || s->used[id] >= MAX_TIMED_LAUNCHES) return;
     auto& v = s->events[id];
     if (s->used[id] == v.size()) {
       hipEvent_t a, b;
@@ -798,9 +798,9 @@ ps_status ps_get_error(ps_store* s, void* stream) {
   return PS_OK;
 }
 
-ps_status ps_set_timing(ps_store* s, int32_t enable) {
+ps_status ps_set_timing(ps_store* s, int32_t mask) {
   if (ps_status st = check_store(s)) return st;
-  s->timing = enable != 0;
+  s->timing = (uint32_t)mask;
   return PS_OK;
 }
 

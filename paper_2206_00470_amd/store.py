@@ -170,8 +170,10 @@ class Store:
         """Synchronize, then return and clear the sticky device status."""
         return int(lib().ps_get_error(self._h, _stream(stream)))
 
-    def set_timing(self, on: bool):
-        check(lib().ps_set_timing(self._h, 1 if on else 0))
+    def set_timing(self, on):
+        """True: time every kernel id; False: off; an int: bit mask of kernel ids."""
+        mask = -1 if on is True else (0 if on is False else int(on))
+        check(lib().ps_set_timing(self._h, mask))
 
     def read_timing(self, kernel_id: int):
         ms, n = C.c_double(0.0), C.c_int64(0)

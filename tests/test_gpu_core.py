@@ -227,6 +227,26 @@ def test_push_invalid_keys_ignored_and_flagged():
     assert_close_tables(Gt.cpu().numpy(), Gr, "G")
 
 
+def test_timing_mask_brackets_only_selected_kernels():
+    from paper_2206_00470_amd import _lib
+    K, d = 5000, 16
+    W, G = make_store(K, d, 30)
+    keys, grads = random_push(K, 20_000, d, 31, zipf_s=1.1)
+    s = Store(dev(W), dev(G), LR, EPS)
+    s.set_timing(1 << _lib.PS_KERNEL_SEGREDUCE)
+    s.push(dev(keys), dev(grads))
+    s.push(dev(keys), dev(grads))
+    s.set_timing(False)
+    ms, n = s.read_timing(_lib.PS_KERNEL_SEGREDUCE)
+    assert n == 2 and ms > 0
+    assert s.read_timing(_lib.PS_KERNEL_SCATTER)[1] == 0
+    s.set_timing(True)
+    s.push(dev(keys), dev(grads))
+    s.set_timing(False)
+    assert s.read_timing(_lib.PS_KERNEL_SEGREDUCE)[1] == 1   # the read above reset the count
+    assert s.read_timing(_lib.PS_KERNEL_SCATTER)[1] >= 1
+
+
 def test_push_workspace_too_small_is_rejected():
     import ctypes as C
     from paper_2206_00470_amd import _lib
