@@ -562,6 +562,8 @@ __global__ __launch_bounds__(BLOCK) void k_sgns_grad(const float* __restrict__ W
   constexpr int NE = NV * VW;
   constexpr int JB = L >= 4 ? 4 : L;   // output rows scored together (power of two <= L)
   __shared__ double sm[WAVES_PER_BLOCK];
+  __shared__ float ustash[JB * NE][BLOCK];   // one batch of rows, lane-major
+  __shared__ double gacc[NE][BLOCK];
   const int gl = threadIdx.x % L;
   const int64_t per = 1 + (int64_t)slots * (K + 1);
   double lsum = 0.0;
@@ -569,7 +571,7 @@ __global__ __launch_bounds__(BLOCK) void k_sgns_grad(const float* __restrict__ W
     if (!ok[b]) continue;
     const float* vp = W + (int64_t)centre[b] * ld;
     float v[NE];
-    double gv[NE];
+    double* gv = gacc[0] + threadIdx.x;   // gv[e] is gacc[e][thread]: the centre gradient in fp64
 #pragma unroll
     for (int q = 0; q < NV; ++q) {
       const int c = (gl + q * L) * VW;
@@ -579,7 +581,7 @@ __global__ __launch_bounds__(BLOCK) void k_sgns_grad(const float* __restrict__ W
         for (int e = 0; e < VW; ++e) v[q * VW + e] = 0.0f;
     }
 #pragma unroll
-    for (int e = 0; e < NE; ++e) gv[e] = 0.0;
+    for (int e = 0; e < NE; ++e) gv[e * BLOCK] = 0.0;
     // all output rows of the centre in occurrence order: row r is slot r / (K+1),
     // position r % (K+1) (0 = the context word, then the negatives).  Lane i
     // holds the table id of row t*L + i of the current tile t of L rows (-1:
@@ -619,12 +621,20 @@ __global__ __launch_bounds__(BLOCK) void k_sgns_grad(const float* __restrict__ W
       }
       double x[JB];
 #pragma unroll
+      for (int e = 0; e < NE; ++e) asm volatile("" : "+v"(v[e]));   // convert v per batch, not once for the loop
+#pragma unroll
       for (int jj = 0; jj < JB; ++jj) {
         double p = 0.0;
 #pragma unroll
         for (int e = 0; e < NE; ++e) p = __builtin_fma((double)u[jj][e], (double)v[e], p);   // exact product
         x[jj] = p;
       }
+      // park the rows in LDS while the coefficients are computed (the fp64
+      // transcendentals need many registers; the rows come back for the update)
+#pragma unroll
+      for (int jj = 0; jj < JB; ++jj)
+#pragma unroll
+        for (int e = 0; e < NE; ++e) ustash[jj * NE + e][threadIdx.x] = u[jj][e];
       // lane finishes the score of row r0 + gl / (L / JB) and its coefficient
       const double x_my = group_multi_sum<L, JB>(x, gl);
       const int r_my = r0 + gl / (L / JB);
@@ -648,7 +658,7 @@ __global__ __launch_bounds__(BLOCK) void k_sgns_grad(const float* __restrict__ W
         const double aj = __shfl(a_my, jj * (L / JB), L);
         if (live[jj])
 #pragma unroll
-          for (int e = 0; e < NE; ++e) gv[e] += aj * (double)u[jj][e];
+          for (int e = 0; e < NE; ++e) gv[e * BLOCK] += aj * (double)ustash[jj * NE + e][threadIdx.x];
       }
     }
     float* dst = mat + b * dim;
@@ -658,7 +668,7 @@ __global__ __launch_bounds__(BLOCK) void k_sgns_grad(const float* __restrict__ W
       if (c < dim) {
         float g[VW];
 #pragma unroll
-        for (int e = 0; e < VW; ++e) g[e] = (float)gv[q * VW + e];
+        for (int e = 0; e < VW; ++e) g[e] = (float)gv[(q * VW + e) * BLOCK];
         store_frag<VW>(dst + c, g);
       }
     }
