@@ -314,6 +314,11 @@ __global__ __launch_bounds__(BLOCK) void k_kge_grad(const float* __restrict__ W,
                                                     double* __restrict__ coef, double* __restrict__ loss_part) {
   constexpr int JB = 4;   // negatives in flight, scored together (8 costs occupancy)
   __shared__ double sm[WAVES_PER_BLOCK];
+  // per-thread fp64 gradient accumulators of s, r, o (Re, Im), and the
+  // current batch of negative rows, kept in LDS: the coefficient's fp64
+  // transcendentals would otherwise run with all of them in registers
+  __shared__ double gacc[6 * KPL][BLOCK];
+  __shared__ float xstash[2 * JB * KPL][BLOCK];
   const int cdim = dim / 2;
   const int lane = lane_id();
   const int64_t per = 3 + n_neg;
@@ -324,40 +329,46 @@ __global__ __launch_bounds__(BLOCK) void k_kge_grad(const float* __restrict__ W,
     const float* sp = W + (int64_t)head[t] * ld;
     const float* rp = W + (rel_off + rel[t]) * ld;
     const float* op = W + (int64_t)tail[t] * ld;
-    double sR[KPL], sI[KPL], rR[KPL], rI[KPL], oR[KPL], oI[KPL];
+    // the rows as loaded (fp32; each use converts exactly to fp64)
+    float sRf[KPL], sIf[KPL], rRf[KPL], rIf[KPL], oRf[KPL], oIf[KPL];
 #pragma unroll
     for (int i = 0; i < KPL; ++i) {
       const int k = lane + WAVE * i;
       const bool in = k < cdim;
-      sR[i] = in ? (double)sp[k] : 0.0; sI[i] = in ? (double)sp[cdim + k] : 0.0;
-      rR[i] = in ? (double)rp[k] : 0.0; rI[i] = in ? (double)rp[cdim + k] : 0.0;
-      oR[i] = in ? (double)op[k] : 0.0; oI[i] = in ? (double)op[cdim + k] : 0.0;
+      sRf[i] = in ? sp[k] : 0.0f; sIf[i] = in ? sp[cdim + k] : 0.0f;
+      rRf[i] = in ? rp[k] : 0.0f; rIf[i] = in ? rp[cdim + k] : 0.0f;
+      oRf[i] = in ? op[k] : 0.0f; oIf[i] = in ? op[cdim + k] : 0.0f;
     }
     double fR[KPL], fI[KPL], hR[KPL], hI[KPL];
-    double gsR[KPL], gsI[KPL], grR[KPL], grI[KPL], goR[KPL], goI[KPL];
+    double* const gsR = gacc[0 * KPL] + threadIdx.x;   // element i at [i * BLOCK]
+    double* const gsI = gacc[1 * KPL] + threadIdx.x;
+    double* const grR = gacc[2 * KPL] + threadIdx.x;
+    double* const grI = gacc[3 * KPL] + threadIdx.x;
+    double* const goR = gacc[4 * KPL] + threadIdx.x;
+    double* const goI = gacc[5 * KPL] + threadIdx.x;
     double part = 0.0;
 #pragma unroll
     for (int i = 0; i < KPL; ++i) {
-      fR[i] = rR[i] * oR[i] + rI[i] * oI[i];
-      fI[i] = rR[i] * oI[i] - rI[i] * oR[i];
-      hR[i] = sR[i] * rR[i] - sI[i] * rI[i];
-      hI[i] = sI[i] * rR[i] + sR[i] * rI[i];
-      part += sR[i] * rR[i] * oR[i];
-      part += sI[i] * rR[i] * oI[i];
-      part += sR[i] * rI[i] * oI[i];
-      part -= sI[i] * rI[i] * oR[i];
+      fR[i] = (double)rRf[i] * (double)oRf[i] + (double)rIf[i] * (double)oIf[i];
+      fI[i] = (double)rRf[i] * (double)oIf[i] - (double)rIf[i] * (double)oRf[i];
+      hR[i] = (double)sRf[i] * (double)rRf[i] - (double)sIf[i] * (double)rIf[i];
+      hI[i] = (double)sIf[i] * (double)rRf[i] + (double)sRf[i] * (double)rIf[i];
+      part += (double)sRf[i] * (double)rRf[i] * (double)oRf[i];
+      part += (double)sIf[i] * (double)rRf[i] * (double)oIf[i];
+      part += (double)sRf[i] * (double)rIf[i] * (double)oIf[i];
+      part -= (double)sIf[i] * (double)rIf[i] * (double)oRf[i];
     }
     const double phi = group_sum<WAVE>(part);
     double c = -sigmoid_d(-phi);
     if (lane == 0) lsum += softplus_d(-phi);
 #pragma unroll
     for (int i = 0; i < KPL; ++i) {
-      gsR[i] = c * fR[i];
-      gsI[i] = c * fI[i];
-      grR[i] = c * (sR[i] * oR[i] + sI[i] * oI[i]);
-      grI[i] = c * (sR[i] * oI[i] - sI[i] * oR[i]);
-      goR[i] = c * hR[i];
-      goI[i] = c * hI[i];
+      gsR[i * BLOCK] = c * fR[i];
+      gsI[i * BLOCK] = c * fI[i];
+      grR[i * BLOCK] = c * ((double)sRf[i] * (double)oRf[i] + (double)sIf[i] * (double)oIf[i]);
+      grI[i * BLOCK] = c * ((double)sRf[i] * (double)oIf[i] - (double)sIf[i] * (double)oRf[i]);
+      goR[i * BLOCK] = c * hR[i];
+      goI[i * BLOCK] = c * hI[i];
       const int k = lane + WAVE * i;
       if (k < cdim) {
         double* fb = base + (2 * t) * dim;
@@ -373,6 +384,10 @@ __global__ __launch_bounds__(BLOCK) void k_kge_grad(const float* __restrict__ W,
     int32_t id_cur = lane < n_neg ? nt[lane] : 0;
     int32_t id_nxt = WAVE + lane < n_neg ? nt[WAVE + lane] : 0;
     for (int j0 = 0; j0 < n_neg; j0 += JB) {
+      // convert s, r, o per batch instead of holding fp64 copies across the loop
+#pragma unroll
+      for (int i = 0; i < KPL; ++i)
+        asm volatile("" : "+v"(sRf[i]), "+v"(sIf[i]), "+v"(rRf[i]), "+v"(rIf[i]), "+v"(oRf[i]), "+v"(oIf[i]));
       if (j0 > 0 && j0 % WAVE == 0) {
         id_cur = id_nxt;
         id_nxt = j0 + WAVE + lane < n_neg ? nt[j0 + WAVE + lane] : 0;
@@ -402,6 +417,14 @@ __global__ __launch_bounds__(BLOCK) void k_kge_grad(const float* __restrict__ W,
                   : ((double)xR[jj][i] * hR[i] + (double)xI[jj][i] * hI[i]);
         ph[jj] = p;
       }
+#pragma unroll
+      for (int jj = 0; jj < JB; ++jj)
+#pragma unroll
+        for (int i = 0; i < KPL; ++i) {
+          xstash[(jj * KPL + i) * 2][threadIdx.x] = xR[jj][i];
+          xstash[(jj * KPL + i) * 2 + 1][threadIdx.x] = xI[jj][i];
+        }
+      asm volatile("" ::: "memory");   // read them back from LDS, not from registers
       // lane finishes the score of negative j0 + lane / (WAVE / JB) and its coefficient
       const double phi_my = group_multi_sum<WAVE, JB>(ph, lane);
       const int j_my = j0 + lane / (WAVE / JB);
@@ -422,20 +445,22 @@ __global__ __launch_bounds__(BLOCK) void k_kge_grad(const float* __restrict__ W,
         if (j < n_head) {   // (x, r, o): d/dr and d/do
 #pragma unroll
           for (int i = 0; i < KPL; ++i) {
-            const double x_r = xR[jj][i], x_i = xI[jj][i];
-            grR[i] += cj * (x_r * oR[i] + x_i * oI[i]);
-            grI[i] += cj * (x_r * oI[i] - x_i * oR[i]);
-            goR[i] += cj * (x_r * rR[i] - x_i * rI[i]);
-            goI[i] += cj * (x_i * rR[i] + x_r * rI[i]);
+            const double x_r = xstash[(jj * KPL + i) * 2][threadIdx.x];
+            const double x_i = xstash[(jj * KPL + i) * 2 + 1][threadIdx.x];
+            grR[i * BLOCK] += cj * (x_r * (double)oRf[i] + x_i * (double)oIf[i]);
+            grI[i * BLOCK] += cj * (x_r * (double)oIf[i] - x_i * (double)oRf[i]);
+            goR[i * BLOCK] += cj * (x_r * (double)rRf[i] - x_i * (double)rIf[i]);
+            goI[i * BLOCK] += cj * (x_i * (double)rRf[i] + x_r * (double)rIf[i]);
           }
         } else {            // (s, r, x): d/ds and d/dr
 #pragma unroll
           for (int i = 0; i < KPL; ++i) {
-            const double x_r = xR[jj][i], x_i = xI[jj][i];
-            gsR[i] += cj * (rR[i] * x_r + rI[i] * x_i);
-            gsI[i] += cj * (rR[i] * x_i - rI[i] * x_r);
-            grR[i] += cj * (sR[i] * x_r + sI[i] * x_i);
-            grI[i] += cj * (sR[i] * x_i - sI[i] * x_r);
+            const double x_r = xstash[(jj * KPL + i) * 2][threadIdx.x];
+            const double x_i = xstash[(jj * KPL + i) * 2 + 1][threadIdx.x];
+            gsR[i * BLOCK] += cj * ((double)rRf[i] * x_r + (double)rIf[i] * x_i);
+            gsI[i * BLOCK] += cj * ((double)rRf[i] * x_i - (double)rIf[i] * x_r);
+            grR[i * BLOCK] += cj * ((double)sRf[i] * x_r + (double)sIf[i] * x_i);
+            grI[i * BLOCK] += cj * ((double)sRf[i] * x_i - (double)sIf[i] * x_r);
           }
         }
       }
@@ -445,12 +470,12 @@ __global__ __launch_bounds__(BLOCK) void k_kge_grad(const float* __restrict__ W,
     for (int i = 0; i < KPL; ++i) {
       const int k = lane + WAVE * i;
       if (k < cdim) {
-        ms[k] = (float)gsR[i];
-        ms[cdim + k] = (float)gsI[i];
-        ms[dim + k] = (float)grR[i];
-        ms[dim + cdim + k] = (float)grI[i];
-        ms[2 * dim + k] = (float)goR[i];
-        ms[2 * dim + cdim + k] = (float)goI[i];
+        ms[k] = (float)gsR[i * BLOCK];
+        ms[cdim + k] = (float)gsI[i * BLOCK];
+        ms[dim + k] = (float)grR[i * BLOCK];
+        ms[dim + cdim + k] = (float)grI[i * BLOCK];
+        ms[2 * dim + k] = (float)goR[i * BLOCK];
+        ms[2 * dim + cdim + k] = (float)goI[i * BLOCK];
       }
     }
   }
