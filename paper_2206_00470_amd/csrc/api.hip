@@ -380,8 +380,9 @@ ps_status launch_finalize(ps_store* s, const SortBufs& b, const uint32_t* ks, in
                          (uint32_t)s->num_keys, s->dim, b.partial, b.fold);
       LAUNCHED(k_seg_fold);
     }
+    // at most n / CHUNK + 1 split segments; blocks beyond their count exit at once
     int64_t fgrid = n / CHUNK + 1;
-    if (fgrid > 1024) fgrid = 1024;
+    if (fgrid > 16384) fgrid = 16384;
     hipLaunchKernelGGL((k_seg_finalize<L, NV, VW>), dim3(fgrid), dim3(BLOCK), lds, st, sv, s->W, s->G, s->ld, s->dim,
                        s->lr, s->eps, b.partial, b.fold, b.split_list);
     LAUNCHED(k_seg_finalize);
@@ -657,7 +658,7 @@ ps_status ps_step_kge(ps_store* s, const int32_t* head, const int32_t* rel, cons
   Plan p;
   plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_KGE, B, per, &p);
   if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
-  hipLaunchKernelGGL(k_unit_valid<ValidKGE>, dim3(small_grid(B, BLOCK, 1024)), dim3(BLOCK), 0, st,
+  hipLaunchKernelGGL(k_unit_valid<ValidKGE>, dim3(small_grid(B, WAVES_PER_BLOCK, 4096)), dim3(BLOCK), 0, st,
                      ValidKGE{head, rel, tail, neg, n_neg, rel_key_offset, s->num_keys}, B, p.ok, s->status);
   LAUNCHED(k_unit_valid);
   uint32_t *ks, *perm;
@@ -709,7 +710,7 @@ ps_status ps_step_sgns(ps_store* s, const int32_t* centre, const int32_t* ctx, c
   Plan p;
   plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_SGNS, B, per, &p);
   if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
-  hipLaunchKernelGGL(k_unit_valid<ValidSGNS>, dim3(small_grid(B, BLOCK, 1024)), dim3(BLOCK), 0, st,
+  hipLaunchKernelGGL(k_unit_valid<ValidSGNS>, dim3(small_grid(B, WAVES_PER_BLOCK, 4096)), dim3(BLOCK), 0, st,
                      ValidSGNS{centre, ctx, neg, slots, n_neg, out_key_offset, s->num_keys}, B, p.ok, s->status);
   LAUNCHED(k_unit_valid);
   uint32_t *ks, *perm;
@@ -757,7 +758,7 @@ ps_status ps_step_ctr(ps_store* s, const int64_t* keys, const float* label, int6
   Plan p;
   plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_CTR, B, F, &p);
   if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
-  hipLaunchKernelGGL(k_unit_valid<ValidCTR>, dim3(small_grid(B, BLOCK, 1024)), dim3(BLOCK), 0, st,
+  hipLaunchKernelGGL(k_unit_valid<ValidCTR>, dim3(small_grid(B, WAVES_PER_BLOCK, 4096)), dim3(BLOCK), 0, st,
                      ValidCTR{keys, F, s->num_keys}, B, p.ok, s->status);
   LAUNCHED(k_unit_valid);
   uint32_t *ks, *perm;

@@ -16,7 +16,7 @@ constexpr int TILE = BLOCK * SORT_ITEMS; // keys per radix tile (2048)
 constexpr int MAX_PASSES = 4;            // 32-bit keys, at most 8 bits per pass
 constexpr int MAX_BINS = 256;
 constexpr int GH_COPIES = 32;             // copies of the whole-array histograms (spreads the atomics)
-constexpr int CHUNK = 64;               // longest run of occurrences one group reduces alone
+constexpr int CHUNK = 32;               // cut length of long segments (chunks hold < 2*CHUNK occurrences)
 constexpr int NUM_XCD = 8;               // MI355X: 8 accelerator dies, each with its own L2
 constexpr int64_t ABSENT = INT64_MIN;    // a key source's "no occurrence here" marker
 

@@ -319,12 +319,12 @@ __device__ __forceinline__ void group_sum_rows(RowAt row, int64_t count, int dim
 
 // Chunk partials of a long segment are folded ahead of the finalize in runs
 // of FOLD_SB CHUNK-aligned blocks ("super-blocks"): super-block s covers
-// sorted positions [s*FOLD_SB*CHUNK, (s+1)*FOLD_SB*CHUNK).  When all of it
-// holds one key, every block in it starts a chunk of that key's segment and
-// its partial sits in the block's even slot; one workgroup adds those FOLD_SB
-// partials in fixed order into fold[s].  A hot key's segment then needs a few
-// fold rows plus the partials at its two ragged ends instead of one partial
-// per chunk.
+// sorted positions [P0, P1) = [s*FOLD_SB*CHUNK, (s+1)*FOLD_SB*CHUNK).  When
+// positions P0 - CHUNK .. P1 - 1 all hold one key, the start of every block
+// in it is a cut of that key's segment, whose partial sits in the block's
+// even slot; one workgroup adds those FOLD_SB partials in fixed order into
+// fold[s].  A hot key's segment then needs a few fold rows plus the partials
+// at its two ragged ends instead of one partial per chunk.
 constexpr int FOLD_SB = 64;
 
 template <int L, int NV, int VW>
@@ -335,8 +335,10 @@ __global__ __launch_bounds__(BLOCK) void k_seg_fold(SegView sv, int64_t nsb, uin
   extern __shared__ double lds[];   // [GPB][dim]
   for (int64_t s = blockIdx.x; s < nsb; s += gridDim.x) {
     const int64_t p0 = s * FOLD_SB * CHUNK;
+    if (p0 < CHUNK) continue;
     const uint32_t key = sv.keys[p0];
-    if (key >= sentinel || sv.keys[p0 + FOLD_SB * CHUNK - 1] != key) continue;   // uniform over the block
+    // uniform over the block
+    if (key >= sentinel || sv.keys[p0 - CHUNK] != key || sv.keys[p0 + FOLD_SB * CHUNK - 1] != key) continue;
     const int64_t b0 = s * FOLD_SB;
     group_sum_rows<L, NV, VW>([&](int64_t k) { return partial + 2 * (b0 + k) * dim; }, FOLD_SB, dim, lds);
     __syncthreads();
@@ -349,12 +351,13 @@ __global__ __launch_bounds__(BLOCK) void k_seg_fold(SegView sv, int64_t nsb, uin
   }
 }
 
-// Segments longer than one chunk: one workgroup per split segment (listed by
-// k_segreduce).  The segment's rows are, in position order: the partials of
-// the blocks before its first whole super-block, the fold rows of its whole
-// super-blocks, then the partials of the blocks after them.  They are added
-// by group_sum_rows, the group results in group order, rounded once and
-// applied with AdaGrad.  The order is fixed, so the result is deterministic.
+// Segments cut into several chunks: one workgroup per such segment (listed by
+// k_segreduce).  The segment's rows are, in position order: the partial of
+// its first chunk, the partials of its cuts before its first foldable
+// super-block, the fold rows of its foldable super-blocks, then the partials
+// of the cuts after them.  They are added by group_sum_rows, the group
+// results in group order, rounded once and applied with AdaGrad.  The order
+// is fixed, so the result is deterministic.
 template <int L, int NV, int VW>
 __global__ __launch_bounds__(BLOCK) void k_seg_finalize(SegView sv, float* __restrict__ W, float* __restrict__ G,
                                                         int64_t ld, int dim, float lr, float eps,
@@ -370,19 +373,20 @@ __global__ __launch_bounds__(BLOCK) void k_seg_finalize(SegView sv, float* __res
     const int64_t s1 = sv.seg_off[u + 1];
     const uint32_t key = sv.keys[s0];
     const int64_t b0 = s0 / CHUNK;
-    const int64_t m = (s1 - 1) / CHUNK - b0 + 1;        // CHUNK blocks the segment touches
-    const int64_t bf = (s0 + CHUNK - 1) / CHUNK;        // first block starting inside it
-    const int64_t sa = (bf + FOLD_SB - 1) / FOLD_SB;    // whole super-blocks: [sa, sb)
+    const int64_t f = (s0 + 2 * CHUNK - 1) / CHUNK;     // block of the first cut
+    const int64_t bl = (s1 - 1) / CHUNK;                // block of the last cut
+    const int64_t sa = (f + FOLD_SB - 1) / FOLD_SB;     // foldable super-blocks: [sa, sb)
     const int64_t sb = s1 / (FOLD_SB * CHUNK);
     const int64_t nf = sb > sa ? sb - sa : 0;
-    const int64_t nh = nf ? sa * FOLD_SB - b0 : m;      // partial rows before the folds
-    const int64_t nt = nf ? b0 + m - sb * FOLD_SB : 0;  // partial rows after them
+    const int64_t n1 = nf ? sa * FOLD_SB - f : bl - f + 1;   // cut partials before the folds
+    const int64_t n3 = nf ? bl - sb * FOLD_SB + 1 : 0;       // cut partials after them
     auto row = [&](int64_t i) -> const double* {
-      if (i < nh) return partial + (i == 0 ? 2 * b0 + ((s0 % CHUNK) != 0) : 2 * (b0 + i)) * dim;
-      if (i < nh + nf) return fold + (sa + (i - nh)) * dim;
-      return partial + 2 * (sb * FOLD_SB + (i - nh - nf)) * dim;
+      if (i == 0) return partial + (2 * b0 + ((s0 % CHUNK) != 0)) * dim;
+      if (i <= n1) return partial + 2 * (f + (i - 1)) * dim;
+      if (i <= n1 + nf) return fold + (sa + (i - 1 - n1)) * dim;
+      return partial + 2 * (sb * FOLD_SB + (i - 1 - n1 - nf)) * dim;
     };
-    group_sum_rows<L, NV, VW>(row, nh + nf + nt, dim, lds);
+    group_sum_rows<L, NV, VW>(row, 1 + n1 + nf + n3, dim, lds);
     __syncthreads();
     float* wrow = W + (int64_t)key * ld;
     float* grow = G + (int64_t)key * ld;

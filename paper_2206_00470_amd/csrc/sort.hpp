@@ -234,7 +234,16 @@ __global__ __launch_bounds__(BLOCK) void k_radix_scatter(const uint32_t* __restr
 
 // ------------------------------------------------------------------ segments
 // Sorted position j (valid key) starts a segment if its key differs from
-// position j-1, and starts a chunk if it starts a segment or j % CHUNK == 0.
+// position j-1.  It starts a chunk if it starts a segment, or if j is a
+// multiple of CHUNK and position j - CHUNK holds the same key ("cut"): a
+// segment of at most CHUNK occurrences is never cut, a longer one is cut at
+// the multiples of CHUNK at least CHUNK past its start, so a chunk holds at
+// most 2*CHUNK-1 occurrences and a CHUNK-aligned block holds at most two
+// chunk starts of cut segments (a cut at its start, a segment head inside).
+__device__ __forceinline__ bool chunk_cut(const uint32_t* __restrict__ ks, int64_t j, uint32_t k) {
+  return (j % CHUNK) == 0 && j >= CHUNK && ks[j - CHUNK] == k;
+}
+
 // Per tile: number of segment heads, chunk heads and valid positions.
 __global__ __launch_bounds__(BLOCK) void k_seg_count(const uint32_t* __restrict__ ks, int64_t n, uint32_t sentinel,
                                                      uint32_t* __restrict__ tstat /*[3][tiles]*/, int tiles) {
@@ -250,7 +259,7 @@ __global__ __launch_bounds__(BLOCK) void k_seg_count(const uint32_t* __restrict_
         const bool head = (j == 0) || ks[j - 1] != k;
         nv += 1;
         nh += head;
-        nc += head || (j % CHUNK) == 0;
+        nc += head || chunk_cut(ks, j, k);
       }
     }
   }
@@ -271,19 +280,37 @@ __global__ __launch_bounds__(BLOCK) void k_seg_scan(uint32_t* __restrict__ tstat
                                                     int32_t* __restrict__ seg_off,
                                                     int32_t* __restrict__ chunk_start) {
   __shared__ uint32_t smem[WAVES_PER_BLOCK + 1];
+  constexpr int IPT = 16;   // consecutive tiles per thread and round
   uint32_t ch = 0, cc = 0, cv = 0;
-  for (int t0 = 0; t0 < tiles; t0 += BLOCK) {
-    const int t = t0 + threadIdx.x;
-    const uint32_t h = t < tiles ? tstat[t] : 0u;
-    const uint32_t c = t < tiles ? tstat[tiles + t] : 0u;
-    const uint32_t v = t < tiles ? tstat[2 * tiles + t] : 0u;
+  for (int t0 = 0; t0 < tiles; t0 += BLOCK * IPT) {
+    const int tb = t0 + threadIdx.x * IPT;
+    uint32_t h[IPT], c[IPT];
+    uint32_t sh = 0, sc = 0, sv = 0;
+#pragma unroll
+    for (int q = 0; q < IPT; ++q) {
+      const int t = tb + q;
+      h[q] = t < tiles ? tstat[t] : 0u;
+      c[q] = t < tiles ? tstat[tiles + t] : 0u;
+      sv += t < tiles ? tstat[2 * tiles + t] : 0u;
+    }
+#pragma unroll
+    for (int q = 0; q < IPT; ++q) {
+      sh += h[q];
+      sc += c[q];
+    }
     uint32_t th, tc, tv;
-    const uint32_t eh = block_exclusive_scan(h, smem, &th);
-    const uint32_t ec = block_exclusive_scan(c, smem, &tc);
-    block_exclusive_scan(v, smem, &tv);
-    if (t < tiles) {
-      tstat[t] = ch + eh;
-      tstat[tiles + t] = cc + ec;
+    uint32_t eh = block_exclusive_scan(sh, smem, &th) + ch;
+    uint32_t ec = block_exclusive_scan(sc, smem, &tc) + cc;
+    block_exclusive_scan(sv, smem, &tv);
+#pragma unroll
+    for (int q = 0; q < IPT; ++q) {
+      const int t = tb + q;
+      if (t < tiles) {
+        tstat[t] = eh;
+        tstat[tiles + t] = ec;
+      }
+      eh += h[q];
+      ec += c[q];
     }
     ch += th;
     cc += tc;
@@ -328,7 +355,7 @@ __global__ __launch_bounds__(BLOCK) void k_seg_write(const uint32_t* __restrict_
     const uint32_t p = q == 0 ? prev : k[q - 1];
     const bool valid = j < n && k[q] < sentinel;
     const bool head = valid && (j == 0 || p != k[q]);
-    const bool chead = valid && (head || (j % CHUNK) == 0);
+    const bool chead = valid && (head || chunk_cut(ks, j, k[q]));
     hf |= (uint32_t)head << q;
     cf |= (uint32_t)chead << q;
     nh += head;

@@ -163,13 +163,20 @@ __device__ __forceinline__ void sigmoid_softplus(double x, double* sig, double* 
 // Per-unit validity: a unit (sample, triple, centre) with any id outside its
 // table is skipped entirely and raises the sticky error flag.
 template <class V>
+// One wavefront per unit: its lanes check the unit's ids (V::ids, V::id_ok)
+// side by side.
 __global__ __launch_bounds__(BLOCK) void k_unit_valid(V v, int64_t B, uint8_t* __restrict__ ok,
                                                       int32_t* __restrict__ err) {
+  const int lane = lane_id();
   int bad = 0;
-  for (int64_t b = (int64_t)blockIdx.x * BLOCK + threadIdx.x; b < B; b += (int64_t)gridDim.x * BLOCK) {
-    const bool o = v(b);
-    ok[b] = o;
-    bad |= !o;
+  for (int64_t b = (int64_t)blockIdx.x * WAVES_PER_BLOCK + threadIdx.x / WAVE; b < B;
+       b += (int64_t)gridDim.x * WAVES_PER_BLOCK) {
+    const int n = v.ids(b);
+    bool good = true;
+    for (int i = lane; i < n; i += WAVE) good = good && v.id_ok(b, i);
+    const bool all = __ballot(!good) == 0;
+    if (lane == 0) ok[b] = all;
+    bad |= !all;
   }
   if (__syncthreads_or(bad) && threadIdx.x == 0) atomicOr(err, 1);
 }
@@ -179,12 +186,10 @@ struct ValidCTR {
   const int64_t* keys;
   int F;
   int64_t num_keys;
-  __device__ bool operator()(int64_t b) const {
-    for (int f = 0; f < F; ++f) {
-      const int64_t k = keys[b * F + f];
-      if (k < 0 || k >= num_keys) return false;
-    }
-    return true;
+  __device__ int ids(int64_t) const { return F; }
+  __device__ bool id_ok(int64_t b, int f) const {
+    const int64_t k = keys[b * F + f];
+    return k >= 0 && k < num_keys;
   }
 };
 
@@ -270,12 +275,14 @@ struct ValidKGE {
   const int32_t *head, *rel, *tail, *neg;
   int n_neg;
   int64_t rel_off, num_keys;
-  __device__ bool operator()(int64_t t) const {
+  __device__ int ids(int64_t) const { return 3 + n_neg; }
+  // id 0 = head, 1 = tail, 2 = relation, 3 + j = negative j
+  __device__ bool id_ok(int64_t t, int i) const {
     auto okk = [&](int64_t k) { return k >= 0 && k < num_keys; };
-    if (!okk(head[t]) || !okk(tail[t]) || rel[t] < 0 || !okk(rel_off + rel[t])) return false;
-    for (int j = 0; j < n_neg; ++j)
-      if (!okk(neg[t * n_neg + j])) return false;
-    return true;
+    if (i == 0) return okk(head[t]);
+    if (i == 1) return okk(tail[t]);
+    if (i == 2) return rel[t] >= 0 && okk(rel_off + rel[t]);
+    return okk(neg[t * n_neg + (i - 3)]);
   }
 };
 
@@ -531,20 +538,21 @@ struct ValidSGNS {
   const int32_t *centre, *ctx, *neg;
   int slots, K;
   int64_t out_off, num_keys;
-  __device__ bool operator()(int64_t b) const {
-    const int64_t c = centre[b];
-    if (c < 0 || c >= out_off || c >= num_keys) return false;
-    const int64_t vout = num_keys - out_off;
-    for (int q = 0; q < slots; ++q) {
-      const int64_t x = ctx[b * slots + q];
-      if (x == -1) continue;
-      if (x < 0 || x >= vout) return false;
-      for (int k = 0; k < K; ++k) {
-        const int64_t y = neg[(b * slots + q) * K + k];
-        if (y < 0 || y >= vout) return false;
-      }
+  __device__ int ids(int64_t) const { return 1 + slots * (K + 1); }
+  // id 0 = centre; then per slot q the context word and its K negatives
+  // (an absent slot, context -1, passes)
+  __device__ bool id_ok(int64_t b, int i) const {
+    if (i == 0) {
+      const int64_t c = centre[b];
+      return c >= 0 && c < out_off && c < num_keys;
     }
-    return true;
+    const int q = (i - 1) / (K + 1);
+    const int k = (i - 1) - q * (K + 1);
+    const int64_t x = ctx[b * slots + q];
+    if (x == -1) return true;
+    const int64_t vout = num_keys - out_off;
+    const int64_t y = k == 0 ? x : (int64_t)neg[(b * slots + q) * K + (k - 1)];
+    return y >= 0 && y < vout;
   }
 };
 
