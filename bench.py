@@ -47,6 +47,9 @@ def parse():
                     help="W and G rows of a key side by side in one allocation, or two dense tables")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a 4 GiB device-to-device copy (reference for HBM counters)")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture the timed steps in one HIP graph and time its replay (for the launch-bound "
+                         "small configurations); the roofline then comes from the eager breakdown steps")
     return ap.parse_args()
 
 
@@ -231,7 +234,21 @@ def main():
     # ------------------------------------------------------------ timed steps
     # Each HIP event costs the GPU a few microseconds, so only the dominant
     # kernel is bracketed while the step time is measured.
-    elapsed, kt = run_steps(args.warmup, args.steps, 1 << KID[dom])
+    if args.graph:
+        # the same steps, captured once (the workspace is already sized) and replayed
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(args.steps):
+                wb.step(store, args.warmup + i, loss)
+        g.replay()                          # untimed first replay
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        g.replay()
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t
+        assert store.error() == 0
+    else:
+        elapsed, kt = run_steps(args.warmup, args.steps, 1 << KID[dom])
     # per-kernel breakdown from a few more steps with every big kernel timed
     # (instrumentation only, not part of the timed figure)
     nprof = max(1, min(args.steps, 5))
@@ -256,8 +273,9 @@ def main():
                 "alg_GBps": nbytes / (per_step_ms * 1e-3) / 1e9 if cnt else None,
                 "launches_per_step": seg_launches_per_step if name == "segreduce" else 1}
 
-    dk = kernel_entry(dom, kt[dom], args.steps, idx)          # from the timed steps
     kernels = {name: kernel_entry(name, kt_all[name], nprof, idx_prof) for name in names}
+    # from the timed steps (graph mode: from the eager breakdown steps)
+    dk = kernels[dom] if args.graph else kernel_entry(dom, kt[dom], args.steps, idx)
     kernels["scatter"] = {"ms_per_step": kt_all["scatter"][0] / nprof, "launches": kt_all["scatter"][1]}
     symbol = {"segreduce": "k_segreduce<%s>" % {"mf": "SrcSorted", "mf_tiny": "SrcSorted", "kge": "SrcKGE",
                                                  "sgns": "SrcSGNS", "ctr": "SrcSorted"}[args.workload],
@@ -364,12 +382,15 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": cfg.name, "num_keys": cfg.num_keys, "dim": cfg.dim, "layout": args.layout,
+                   "launch": "hip graph replay" if args.graph else "eager",
                    "key_occurrences_per_step": occ, "avg_unique_keys_per_step": U_avg,
                    "batches_resident": nb},
         "roofline": roofline,
         "kernels": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv) for kk, vv in v.items()}
                     for k, v in kernels.items()},
-        "kernels_from": f"{nprof} extra steps with every big kernel timed (the timed steps time only {dom})",
+        "kernels_from": f"{nprof} extra steps with every big kernel timed (the timed steps time only {dom})"
+                        if not args.graph else f"{nprof} eager steps with every big kernel timed; the timed steps "
+                                               f"are one HIP-graph replay",
         "ops": ops,
         "copy_calibration": copy,
         "cpu_baseline": cpu,
