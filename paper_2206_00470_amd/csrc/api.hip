@@ -184,10 +184,23 @@ struct SortBufs {
   double* partial;        // [2*(n/CHUNK+1)][dim]
   double* fold;           // [n/(FOLD_SB*CHUNK)+1][dim]
   int64_t tiles;
+  int items;              // keys per thread of a radix tile (tile = BLOCK * items keys)
 };
 
+// Keys per thread of the radix tiles: small sorts get more, smaller tiles
+// (more workgroups), large ones bigger tiles (fewer per-tile counts).
+int sort_items(int64_t n) { return n < (int64_t(1) << 19) ? 4 : (n > (int64_t(1) << 23) ? 16 : 8); }
+
+template <class F>
+ps_status with_items(int items, F&& f) {
+  if (items == 4) return f.template operator()<4>();
+  if (items == 16) return f.template operator()<16>();
+  return f.template operator()<8>();
+}
+
 void carve_sort(Carver& c, int64_t n, int dim, bool want_rank, bool want_segments, SortBufs* b) {
-  b->tiles = ceil_div(n, TILE);
+  b->items = sort_items(n);
+  b->tiles = ceil_div(n, int64_t(BLOCK) * b->items);
   b->hdr = c.take<SegHeader>(16);   // header and histogram are cleared together
   b->ghist = c.take<uint32_t>(MAX_PASSES * GH_COPIES * MAX_BINS);
   b->counts = c.take<uint32_t>(size_t(MAX_BINS) * b->tiles);
@@ -285,55 +298,59 @@ ps_status run_sort(ps_store* s, KS ks, int64_t n, int64_t num_keys, SortBufs& b,
   const int tiles = (int)b.tiles;
   clear_header(b, st);
   LAUNCHED(k_zero_words);
-  hipLaunchKernelGGL(k_keyprep<KS>, dim3(tiles), dim3(BLOCK), 0, st, ks, n, (uint32_t)num_keys, plan, b.k[0],
-                     b.counts, tiles, b.ghist, err);
-  LAUNCHED(k_keyprep);
-  int src = 0;
-  for (int p = 0; p < plan.passes; ++p) {
-    const int bins = 1 << plan.bits[p];
-    const bool last = p == plan.passes - 1;
-    if (p > 0) {
-      hipLaunchKernelGGL(k_radix_count, dim3(tiles), dim3(BLOCK), 0, st, b.k[src], n, plan.shift[p],
-                         plan.bits[p], b.counts, tiles);
-      LAUNCHED(k_radix_count);
+  return with_items(b.items, [&]<int IT>() -> ps_status {
+    hipLaunchKernelGGL((k_keyprep<KS, IT>), dim3(tiles), dim3(BLOCK), 0, st, ks, n, (uint32_t)num_keys, plan, b.k[0],
+                       b.counts, tiles, b.ghist, err);
+    LAUNCHED(k_keyprep);
+    int src = 0;
+    for (int p = 0; p < plan.passes; ++p) {
+      const int bins = 1 << plan.bits[p];
+      const bool last = p == plan.passes - 1;
+      if (p > 0) {
+        hipLaunchKernelGGL(k_radix_count<IT>, dim3(tiles), dim3(BLOCK), 0, st, b.k[src], n, plan.shift[p],
+                           plan.bits[p], b.counts, tiles);
+        LAUNCHED(k_radix_count);
+      }
+      hipLaunchKernelGGL(k_radix_scan, dim3(bins), dim3(BLOCK), 0, st, b.counts, tiles,
+                         b.ghist + p * GH_COPIES * MAX_BINS);
+      LAUNCHED(k_radix_scan);
+      uint32_t* vout = (last && perm_out) ? perm_out : b.v[1 - src];
+      uint32_t* rank = (last && want_rank) ? b.rank : nullptr;
+      Timed t(s, PS_KERNEL_SCATTER, st);
+      if (p == 0 && rank)
+        hipLaunchKernelGGL((k_radix_scatter<true, true, IT>), dim3(tiles), dim3(BLOCK), 0, st, b.k[src], nullptr, n,
+                           plan.shift[p], plan.bits[p], b.counts, tiles, b.k[1 - src], vout, rank);
+      else if (p == 0)
+        hipLaunchKernelGGL((k_radix_scatter<true, false, IT>), dim3(tiles), dim3(BLOCK), 0, st, b.k[src], nullptr, n,
+                           plan.shift[p], plan.bits[p], b.counts, tiles, b.k[1 - src], vout, nullptr);
+      else if (rank)
+        hipLaunchKernelGGL((k_radix_scatter<false, true, IT>), dim3(tiles), dim3(BLOCK), 0, st, b.k[src], b.v[src], n,
+                           plan.shift[p], plan.bits[p], b.counts, tiles, b.k[1 - src], vout, rank);
+      else
+        hipLaunchKernelGGL((k_radix_scatter<false, false, IT>), dim3(tiles), dim3(BLOCK), 0, st, b.k[src], b.v[src],
+                           n, plan.shift[p], plan.bits[p], b.counts, tiles, b.k[1 - src], vout, nullptr);
+      LAUNCHED(k_radix_scatter);
+      src = 1 - src;
+      if (last) *perm = vout;
     }
-    hipLaunchKernelGGL(k_radix_scan, dim3(bins), dim3(BLOCK), 0, st, b.counts, tiles,
-                       b.ghist + p * GH_COPIES * MAX_BINS);
-    LAUNCHED(k_radix_scan);
-    uint32_t* vout = (last && perm_out) ? perm_out : b.v[1 - src];
-    uint32_t* rank = (last && want_rank) ? b.rank : nullptr;
-    Timed t(s, PS_KERNEL_SCATTER, st);
-    if (p == 0 && rank)
-      hipLaunchKernelGGL((k_radix_scatter<true, true>), dim3(tiles), dim3(BLOCK), 0, st, b.k[src], nullptr, n,
-                         plan.shift[p], plan.bits[p], b.counts, tiles, b.k[1 - src], vout, rank);
-    else if (p == 0)
-      hipLaunchKernelGGL((k_radix_scatter<true, false>), dim3(tiles), dim3(BLOCK), 0, st, b.k[src], nullptr, n,
-                         plan.shift[p], plan.bits[p], b.counts, tiles, b.k[1 - src], vout, nullptr);
-    else if (rank)
-      hipLaunchKernelGGL((k_radix_scatter<false, true>), dim3(tiles), dim3(BLOCK), 0, st, b.k[src], b.v[src], n,
-                         plan.shift[p], plan.bits[p], b.counts, tiles, b.k[1 - src], vout, rank);
-    else
-      hipLaunchKernelGGL((k_radix_scatter<false, false>), dim3(tiles), dim3(BLOCK), 0, st, b.k[src], b.v[src],
-                         n, plan.shift[p], plan.bits[p], b.counts, tiles, b.k[1 - src], vout, nullptr);
-    LAUNCHED(k_radix_scatter);
-    src = 1 - src;
-    if (last) *perm = vout;
-  }
-  *keys_sorted = b.k[src];
-  return PS_OK;
+    *keys_sorted = b.k[src];
+    return PS_OK;
+  });
 }
 
 ps_status run_segments(const SortBufs& b, const uint32_t* ks, int64_t n, int64_t num_keys, int32_t* seg_off,
                        int64_t* uniq64, hipStream_t st, uint32_t split_key = 0) {
   const int tiles = (int)b.tiles;
-  hipLaunchKernelGGL(k_seg_count, dim3(tiles), dim3(BLOCK), 0, st, ks, n, (uint32_t)num_keys, b.tstat, tiles);
-  LAUNCHED(k_seg_count);
-  hipLaunchKernelGGL(k_seg_scan, dim3(1), dim3(BLOCK), 0, st, b.tstat, tiles, b.hdr, seg_off, b.chunk_start);
-  LAUNCHED(k_seg_scan);
-  hipLaunchKernelGGL(k_seg_write, dim3(tiles), dim3(BLOCK), 0, st, ks, n, (uint32_t)num_keys, b.tstat, tiles,
-                     seg_off, uniq64, b.chunk_start, b.chunk_seg, split_key, b.hdr);
-  LAUNCHED(k_seg_write);
-  return PS_OK;
+  return with_items(b.items, [&]<int IT>() -> ps_status {
+    hipLaunchKernelGGL(k_seg_count<IT>, dim3(tiles), dim3(BLOCK), 0, st, ks, n, (uint32_t)num_keys, b.tstat, tiles);
+    LAUNCHED(k_seg_count);
+    hipLaunchKernelGGL(k_seg_scan, dim3(1), dim3(BLOCK), 0, st, b.tstat, tiles, b.hdr, seg_off, b.chunk_start);
+    LAUNCHED(k_seg_scan);
+    hipLaunchKernelGGL(k_seg_write<IT>, dim3(tiles), dim3(BLOCK), 0, st, ks, n, (uint32_t)num_keys, b.tstat, tiles,
+                       seg_off, uniq64, b.chunk_start, b.chunk_seg, split_key, b.hdr);
+    LAUNCHED(k_seg_write);
+    return PS_OK;
+  });
 }
 
 int64_t reduce_grid(int64_t n, int L, int64_t cap = MERGE_GRID_MAX) {

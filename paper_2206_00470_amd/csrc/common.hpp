@@ -11,8 +11,6 @@ namespace adapm {
 constexpr int WAVE = 64;                 // CDNA wavefront width
 constexpr int BLOCK = 256;               // threads per workgroup for every kernel here
 constexpr int WAVES_PER_BLOCK = BLOCK / WAVE;
-constexpr int SORT_ITEMS = 8;            // keys per thread in the radix tiles
-constexpr int TILE = BLOCK * SORT_ITEMS; // keys per radix tile (2048)
 constexpr int MAX_PASSES = 4;            // 32-bit keys, at most 8 bits per pass
 constexpr int MAX_BINS = 256;
 constexpr int GH_COPIES = 32;             // copies of the whole-array histograms (spreads the atomics)

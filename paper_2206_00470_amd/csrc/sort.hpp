@@ -1,7 +1,8 @@
 // Duplicate-key merge order: a stable LSD radix sort of (key, occurrence)
 // pairs, then segment and chunk boundaries of the sorted keys.
 //
-// Radix tiles hold TILE = 2048 keys.  Each pass is reduce-then-scan:
+// Radix tiles hold BLOCK * IT keys (IT = 4, 8 or 16 keys per thread, chosen
+// per call from the number of keys).  Each pass is reduce-then-scan:
 //   count   : per-tile digit histogram  -> counts[digit][tile]
 //   scan    : one workgroup per digit turns its row of counts into global
 //             offsets, seeded with the digit base from a whole-array
@@ -40,7 +41,7 @@ struct KeysInt64 {
 // whole-array histograms of every pass.  Those are kept in GH_COPIES copies,
 // tile t adding to copy t % GH_COPIES, so that no histogram word takes more
 // than tiles / GH_COPIES atomic adds.
-template <class KS>
+template <class KS, int IT>
 __global__ __launch_bounds__(BLOCK) void k_keyprep(KS ks, int64_t n, uint32_t sentinel, RadixPlan plan,
                                                    uint32_t* __restrict__ kout, uint32_t* __restrict__ counts0,
                                                    int tiles, uint32_t* __restrict__ ghist,
@@ -48,10 +49,10 @@ __global__ __launch_bounds__(BLOCK) void k_keyprep(KS ks, int64_t n, uint32_t se
   __shared__ uint32_t h[MAX_PASSES][MAX_BINS];
   for (int i = threadIdx.x; i < MAX_PASSES * MAX_BINS; i += BLOCK) (&h[0][0])[i] = 0u;
   __syncthreads();
-  const int64_t base = (int64_t)blockIdx.x * TILE;
+  const int64_t base = (int64_t)blockIdx.x * (BLOCK * IT);
   int bad = 0;
 #pragma unroll 4
-  for (int it = 0; it < SORT_ITEMS; ++it) {
+  for (int it = 0; it < IT; ++it) {
     const int64_t i = base + (int64_t)it * BLOCK + threadIdx.x;
     if (i < n) {
       const int64_t key = ks(i);
@@ -82,15 +83,16 @@ __global__ __launch_bounds__(BLOCK) void k_keyprep(KS ks, int64_t n, uint32_t se
 }
 
 // ------------------------------------------------------------------ count
+template <int IT>
 __global__ __launch_bounds__(BLOCK) void k_radix_count(const uint32_t* __restrict__ keys, int64_t n, int shift,
                                                        int bits, uint32_t* __restrict__ counts, int tiles) {
   __shared__ uint32_t h[MAX_BINS];
   const int bins = 1 << bits;
   for (int d = threadIdx.x; d < bins; d += BLOCK) h[d] = 0u;
   __syncthreads();
-  const int64_t base = (int64_t)blockIdx.x * TILE;
+  const int64_t base = (int64_t)blockIdx.x * (BLOCK * IT);
 #pragma unroll 4
-  for (int it = 0; it < SORT_ITEMS; ++it) {
+  for (int it = 0; it < IT; ++it) {
     const int64_t i = base + (int64_t)it * BLOCK + threadIdx.x;
     if (i < n) atomicAdd(&h[(keys[i] >> shift) & (bins - 1)], 1u);
   }
@@ -136,7 +138,7 @@ __global__ __launch_bounds__(BLOCK) void k_radix_scan(uint32_t* __restrict__ cou
 // ------------------------------------------------------------------ scatter
 // FIRST: the values are the occurrence indices themselves (no value input).
 // RANK : also write rank[value] = destination (the inverse permutation).
-template <bool FIRST, bool RANK>
+template <bool FIRST, bool RANK, int IT>
 __global__ __launch_bounds__(BLOCK) void k_radix_scatter(const uint32_t* __restrict__ kin,
                                                          const uint32_t* __restrict__ vin, int64_t n, int shift,
                                                          int bits, const uint32_t* __restrict__ offs, int tiles,
@@ -147,8 +149,8 @@ __global__ __launch_bounds__(BLOCK) void k_radix_scatter(const uint32_t* __restr
   __shared__ uint32_t toff[MAX_BINS];
   __shared__ uint32_t dstart[MAX_BINS];
   __shared__ uint32_t scan_smem[WAVES_PER_BLOCK + 1];
-  __shared__ uint32_t sk[TILE];
-  __shared__ uint32_t sv[TILE];
+  __shared__ uint32_t sk[(BLOCK * IT)];
+  __shared__ uint32_t sv[(BLOCK * IT)];
   const int bins = 1 << bits;
   const uint32_t mask = (uint32_t)bins - 1u;
   for (int i = threadIdx.x; i < WAVES_PER_BLOCK * MAX_BINS; i += BLOCK) (&wc[0][0])[i] = 0u;
@@ -158,10 +160,10 @@ __global__ __launch_bounds__(BLOCK) void k_radix_scatter(const uint32_t* __restr
   const int w = threadIdx.x / WAVE;
   const int lane = lane_id();
   const uint64_t lt = lanemask_lt();
-  const int64_t base = (int64_t)blockIdx.x * TILE + (int64_t)w * (WAVE * SORT_ITEMS);
-  uint32_t key[SORT_ITEMS], val[SORT_ITEMS], rk[SORT_ITEMS];
+  const int64_t base = (int64_t)blockIdx.x * (BLOCK * IT) + (int64_t)w * (WAVE * IT);
+  uint32_t key[IT], val[IT], rk[IT];
 #pragma unroll
-  for (int it = 0; it < SORT_ITEMS; ++it) {
+  for (int it = 0; it < IT; ++it) {
     const int64_t i = base + it * WAVE + lane;
     const bool valid = i < n;
     key[it] = valid ? kin[i] : 0u;
@@ -169,7 +171,7 @@ __global__ __launch_bounds__(BLOCK) void k_radix_scatter(const uint32_t* __restr
     else val[it] = valid ? vin[i] : 0u;
   }
 #pragma unroll
-  for (int it = 0; it < SORT_ITEMS; ++it) {
+  for (int it = 0; it < IT; ++it) {
     const int64_t i = base + it * WAVE + lane;
     const bool valid = i < n;
     const uint32_t d = (key[it] >> shift) & mask;
@@ -208,7 +210,7 @@ __global__ __launch_bounds__(BLOCK) void k_radix_scatter(const uint32_t* __restr
   __syncthreads();
   // stage the tile in LDS in digit order ...
 #pragma unroll
-  for (int it = 0; it < SORT_ITEMS; ++it) {
+  for (int it = 0; it < IT; ++it) {
     const int64_t i = base + it * WAVE + lane;
     if (i < n) {
       const uint32_t d = (key[it] >> shift) & mask;
@@ -219,8 +221,8 @@ __global__ __launch_bounds__(BLOCK) void k_radix_scatter(const uint32_t* __restr
   }
   __syncthreads();
   // ... and write it out: consecutive threads write consecutive positions of a digit run
-  const int64_t tile_base = (int64_t)blockIdx.x * TILE;
-  const int cnt = (int)((n - tile_base) < TILE ? (n - tile_base) : TILE);
+  const int64_t tile_base = (int64_t)blockIdx.x * (BLOCK * IT);
+  const int cnt = (int)((n - tile_base) < (BLOCK * IT) ? (n - tile_base) : (BLOCK * IT));
   for (int p = threadIdx.x; p < cnt; p += BLOCK) {
     const uint32_t k = sk[p];
     const uint32_t v = sv[p];
@@ -245,13 +247,14 @@ __device__ __forceinline__ bool chunk_cut(const uint32_t* __restrict__ ks, int64
 }
 
 // Per tile: number of segment heads, chunk heads and valid positions.
+template <int IT>
 __global__ __launch_bounds__(BLOCK) void k_seg_count(const uint32_t* __restrict__ ks, int64_t n, uint32_t sentinel,
                                                      uint32_t* __restrict__ tstat /*[3][tiles]*/, int tiles) {
   __shared__ uint32_t smem[WAVES_PER_BLOCK + 1];
-  const int64_t base = (int64_t)blockIdx.x * TILE;
+  const int64_t base = (int64_t)blockIdx.x * (BLOCK * IT);
   uint32_t nh = 0, nc = 0, nv = 0;
 #pragma unroll 4
-  for (int it = 0; it < SORT_ITEMS; ++it) {
+  for (int it = 0; it < IT; ++it) {
     const int64_t j = base + (int64_t)it * BLOCK + threadIdx.x;
     if (j < n) {
       const uint32_t k = ks[j];
@@ -327,10 +330,11 @@ __global__ __launch_bounds__(BLOCK) void k_seg_scan(uint32_t* __restrict__ tstat
   }
 }
 
-// Per tile (blocked: thread t owns positions base + t*SORT_ITEMS ..): write
+// Per tile (blocked: thread t owns positions base + t*IT ..): write
 // the segment offsets (and optionally the distinct keys as int64), the chunk
 // list (start position and segment of each chunk) and the number of segments
 // with key < split_key.
+template <int IT>
 __global__ __launch_bounds__(BLOCK) void k_seg_write(const uint32_t* __restrict__ ks, int64_t n, uint32_t sentinel,
                                                      const uint32_t* __restrict__ tstat, int tiles,
                                                      int32_t* __restrict__ seg_off, int64_t* __restrict__ uniq64,
@@ -339,18 +343,18 @@ __global__ __launch_bounds__(BLOCK) void k_seg_write(const uint32_t* __restrict_
                                                      uint32_t split_key,
                                                      SegHeader* hdr) {
   __shared__ uint32_t smem[WAVES_PER_BLOCK + 1];
-  const int64_t base = (int64_t)blockIdx.x * TILE + (int64_t)threadIdx.x * SORT_ITEMS;
-  uint32_t k[SORT_ITEMS];
+  const int64_t base = (int64_t)blockIdx.x * (BLOCK * IT) + (int64_t)threadIdx.x * IT;
+  uint32_t k[IT];
   uint32_t prev = (base > 0 && base - 1 < n) ? ks[base - 1] : 0xFFFFFFFFu;
 #pragma unroll
-  for (int q = 0; q < SORT_ITEMS; ++q) {
+  for (int q = 0; q < IT; ++q) {
     const int64_t j = base + q;
     k[q] = j < n ? ks[j] : sentinel;
   }
   uint32_t hf = 0, cf = 0;   // bit q: position base+q starts a segment / chunk
   uint32_t nh = 0, nc = 0;
 #pragma unroll
-  for (int q = 0; q < SORT_ITEMS; ++q) {
+  for (int q = 0; q < IT; ++q) {
     const int64_t j = base + q;
     const uint32_t p = q == 0 ? prev : k[q - 1];
     const bool valid = j < n && k[q] < sentinel;
@@ -367,7 +371,7 @@ __global__ __launch_bounds__(BLOCK) void k_seg_write(const uint32_t* __restrict_
   // segment index of the position before this thread's first one
   int64_t cur = (int64_t)hi - 1;
 #pragma unroll
-  for (int q = 0; q < SORT_ITEMS; ++q) {
+  for (int q = 0; q < IT; ++q) {
     const int64_t j = base + q;
     if ((hf >> q) & 1u) {
       seg_off[hi] = (int32_t)j;
