@@ -327,12 +327,29 @@ def main():
         R = wb.R
         push_alg = 8.0 * n + n * R + 4.0 * U * R
         pull_alg = 8.0 * n + U * R + n * R
+        # the bare read-modify-write pattern through the merge kernel: U distinct
+        # random keys, one contiguous gradient row each (no duplicates to merge)
+        ukeys = torch.from_numpy(np.sort(np.random.default_rng(11).choice(cfg.num_keys, int(U), replace=False))).to(dev)
+        ugrads = grads[:int(U)]
+        store.push(ukeys, ugrads)
+        store.read_timing(_lib.PS_KERNEL_SEGREDUCE)
+        store.set_timing(1 << _lib.PS_KERNEL_SEGREDUCE)
+        for _ in range(reps):
+            store.push(ukeys, ugrads)
+        store.set_timing(False)
+        mms, mcnt = store.read_timing(_lib.PS_KERNEL_SEGREDUCE)
+        merge_ms = mms / max(mcnt, 1)
+        rmw_alg = U * R + 4.0 * U * R
         ops = {
             "push": {"ms": round(tp * 1e3, 4), "rows_per_s": n / tp, "alg_GBps": round(push_alg / tp / 1e9, 1),
                      "frac_of_peak": round(push_alg / tp / 1e9 / HBM_PEAK_GBPS, 4), "unique_keys": int(U)},
             "pull": {"ms": round(tl * 1e3, 4), "rows_per_s": n / tl, "alg_GBps": round(pull_alg / tl / 1e9, 1)},
+            "merge_distinct_keys": {"keys": int(U), "merge_ms": round(merge_ms, 4),
+                                    "alg_GBps": round(rmw_alg / (merge_ms * 1e-3) / 1e9, 1),
+                                    "what": "merge kernel alone on a push of distinct random keys: W and G "
+                                            "read-modify-write plus one gradient row per key"},
         }
-        del keys, grads, out
+        del keys, grads, out, ukeys, ugrads
 
     copy = None
     if args.calibrate_copy:
