@@ -39,7 +39,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="mf", choices=["mf", "mf_tiny", "kge", "sgns", "ctr"])
+    ap.add_argument("--workload", default="mf", choices=["mf", "mf_tiny", "kge", "kge2x100", "sgns", "ctr"])
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="bound on the CPU-oracle sample (0 = skip)")
     ap.add_argument("--no-ops", action="store_true", help="skip the pull-only / push-only measurements")
@@ -88,8 +88,9 @@ class Bench:
         from paper_2206_00470_amd import workloads as wls
 
         self.name = name
+        self.task = {"mf_tiny": "mf", "kge2x100": "kge"}.get(name, name)
         cfgs = {"mf": wls.MF_10Mx1M, "mf_tiny": wls.MF_TINY, "kge": wls.KGE_COMPLEX,
-                "sgns": wls.SGNS_1M, "ctr": wls.CTR_33M}
+                "kge2x100": wls.KGE_COMPLEX_2x100, "sgns": wls.SGNS_1M, "ctr": wls.CTR_33M}
         self.cfg = cfg = cfgs[name]
         self.wl = wls.workload(cfg)
         self.dev = dev
@@ -109,11 +110,11 @@ class Bench:
 
     def keys_of(self, bt):
         c = self.cfg
-        if self.name in ("mf", "mf_tiny"):
+        if self.task == "mf":
             return np.concatenate([bt.row.astype(np.int64), c.n_rows + bt.col.astype(np.int64)])
-        if self.name == "kge":
+        if self.task == "kge":
             return np.concatenate([bt.head, c.n_ent + bt.rel.astype(np.int64), bt.tail, bt.neg.ravel()]).astype(np.int64)
-        if self.name == "sgns":
+        if self.task == "sgns":
             ctx = bt.ctx.astype(np.int64)
             neg = bt.neg.astype(np.int64)
             present = ctx >= 0
@@ -123,11 +124,11 @@ class Bench:
 
     def step(self, store, i, loss):
         c, b = self.cfg, self.batches[i % len(self.batches)]
-        if self.name in ("mf", "mf_tiny"):
+        if self.task == "mf":
             store.step_mf(b["row"], b["col"], b["val"], c.n_rows, c.lam, loss=loss)
-        elif self.name == "kge":
+        elif self.task == "kge":
             store.step_kge(b["head"], b["rel"], b["tail"], b["neg"], c.n_head_neg, c.n_ent, loss=loss)
-        elif self.name == "sgns":
+        elif self.task == "sgns":
             store.step_sgns(b["centre"], b["ctx"], b["neg"], c.window, c.vocab, loss=loss)
         else:
             store.step_ctr(b["keys"], b["label"], loss=loss)
@@ -138,7 +139,7 @@ class Bench:
         c, bt = self.cfg, self.host_batches[i % len(self.host_batches)]
         n, U, R = self.occ[i % len(self.occ)], self.uniq[i % len(self.uniq)], self.R
         table = 4.0 * U * R                      # W and G read and written once per distinct key
-        if self.name in ("mf", "mf_tiny"):
+        if self.task == "mf":
             B = bt.row.size
             Ucol = np.unique(bt.col).size
             Urow = U - Ucol
@@ -149,11 +150,11 @@ class Bench:
             return {"rowmerge": B * (16.0 + R) + Ucol * R + 4.0 * Urow * R,
                     "segreduce": B * R + 4.0 * Ucol * R,
                     "taskgrad": B * (4.0 + 4.0 + 8.0 + 16.0)}
-        if self.name == "ctr":
+        if self.task == "ctr":
             B, F = bt.keys.shape
             return {"segreduce": n * R + table,
                     "taskgrad": B * (4.0 + F * (8.0 + R + R + 4.0))}
-        if self.name == "kge":
+        if self.task == "kge":
             B, nn = bt.neg.shape
             return {"segreduce": n * 4.0 + 3 * B * R + B * nn * 8.0 + 2 * B * 2 * R + table,
                     "taskgrad": B * (12.0 + 4 * nn + (3 + nn) * R + 3 * R + 4 * R + 8 * nn)}
@@ -168,11 +169,11 @@ class Bench:
         import oracle
         c, bt = self.cfg, self.wl.batch(i)
         lr, eps = c.opt.lr, c.opt.eps
-        if self.name in ("mf", "mf_tiny"):
+        if self.task == "mf":
             oracle.step_mf(W, G, bt.row, bt.col, bt.val, c.n_rows, c.lam, lr, eps)
-        elif self.name == "kge":
+        elif self.task == "kge":
             oracle.step_kge(W, G, bt.head, bt.rel, bt.tail, bt.neg, c.n_head_neg, c.n_ent, lr, eps)
-        elif self.name == "sgns":
+        elif self.task == "sgns":
             oracle.step_sgns(W, G, bt.centre, bt.ctx, bt.neg, c.window, c.vocab, lr, eps)
         else:
             oracle.step_ctr(W, G, bt.keys, bt.label, lr, eps)
@@ -277,11 +278,11 @@ def main():
     # from the timed steps (graph mode: from the eager breakdown steps)
     dk = kernels[dom] if args.graph else kernel_entry(dom, kt[dom], args.steps, idx)
     kernels["scatter"] = {"ms_per_step": kt_all["scatter"][0] / nprof, "launches": kt_all["scatter"][1]}
-    symbol = {"segreduce": "k_segreduce<%s>" % {"mf": "SrcSorted", "mf_tiny": "SrcSorted", "kge": "SrcKGE",
-                                                 "sgns": "SrcSGNS", "ctr": "SrcSorted"}[args.workload],
+    symbol = {"segreduce": "k_segreduce<%s>" % {"mf": "SrcSorted", "kge": "SrcKGE", "sgns": "SrcSGNS",
+                                                 "ctr": "SrcSorted"}[wb.task],
               "rowmerge": "k_segreduce<SrcMFRow>",
-              "taskgrad": {"mf": "k_mf_pack", "mf_tiny": "k_mf_pack", "kge": "k_kge_grad", "sgns": "k_sgns_grad",
-                           "ctr": "k_ctr_grad"}[args.workload]}[dom]
+              "taskgrad": {"mf": "k_mf_pack", "kge": "k_kge_grad", "sgns": "k_sgns_grad",
+                           "ctr": "k_ctr_grad"}[wb.task]}[dom]
     traffic = counter_traffic(args.workload, symbol)
     roofline = {
         "bound": "hbm",

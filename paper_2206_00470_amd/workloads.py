@@ -262,6 +262,11 @@ CTR_33M = CTRConfig("ctr_26f_2^25_d64", n_fields=26, table_rows=1 << 25, dim=64,
 
 CONFIGS = [MF_TINY, MF_10Mx1M, KGE_COMPLEX, SGNS_1M, CTR_33M]
 
+# The paper corrupts both the subject and the object n_neg = 100 times each
+# (Appendix C, "Knowledge graph embeddings"): 100 head- then 100
+# tail-corrupted negatives per triple.
+KGE_COMPLEX_2x100 = replace(KGE_COMPLEX, name="kge_complex_4.6M_d128_2x100neg", n_neg=200, n_head_neg=100)
+
 
 def small_variant(cfg, scale: str = "small"):
     """Reduced sizes of the same workload for oracle-speed parity tests: the

@@ -5,7 +5,7 @@ import torch
 
 import oracle
 from paper_2206_00470_amd import Store
-from paper_2206_00470_amd.workloads import (CTR_33M, KGE_COMPLEX, SGNS_1M, CTRWorkload, KGEWorkload,
+from paper_2206_00470_amd.workloads import (CTR_33M, KGE_COMPLEX, KGE_COMPLEX_2x100, SGNS_1M, CTRWorkload, KGEWorkload,
                                             SGNSWorkload, small_variant)
 from tests.helpers import assert_bitwise, assert_close_tables, mismatch_fraction, say
 
@@ -183,10 +183,16 @@ def test_deterministic(task):
     assert res[0][2:] == res[1][2:]
 
 
+def test_kge_two_times_100_negatives_small():
+    """100 head- and 100 tail-corrupted negatives per triple (four id tiles of 64)."""
+    run_steps("kge", small_variant(KGE_COMPLEX_2x100), range(3))
+
+
 # ------------------------------------------------------------------ full sizes, one step each
-@pytest.mark.parametrize("task", ["kge", "ctr", "sgns"])
-def test_paper_scale_one_step(task):
-    cfg, WL, gpu, ref = TASKS[task]
+@pytest.mark.parametrize("task,cfg", [("kge", KGE_COMPLEX), ("ctr", CTR_33M), ("sgns", SGNS_1M),
+                                      ("kge", KGE_COMPLEX_2x100)])
+def test_paper_scale_one_step(task, cfg):
+    _, WL, gpu, ref = TASKS[task]
     wl = WL(cfg)
     say(f"{cfg.name}: generating the {cfg.num_keys} x {cfg.dim if hasattr(cfg, 'dim') else ''} table")
     W = wl.init_table()
