@@ -47,6 +47,9 @@ def parse():
                     help="W and G rows of a key side by side in one allocation, or two dense tables")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a 4 GiB device-to-device copy (reference for HBM counters)")
+    ap.add_argument("--no-overlap", action="store_true",
+                    help="MF: one ps_step_mf call per step instead of overlapping the next batch's key work "
+                         "(sort, segments, records) on a second stream with this batch's table update")
     ap.add_argument("--graph", action="store_true",
                     help="capture the timed steps in one HIP graph and time its replay (for the launch-bound "
                          "small configurations); the roofline then comes from the eager breakdown steps")
@@ -133,6 +136,38 @@ class Bench:
         else:
             store.step_ctr(b["keys"], b["label"], loss=loss)
 
+    def run_overlapped(self, store, first, count, loss):
+        """MF steps first .. first+count-1 with the two-phase step: the key work
+        of batch i+1 (sort, segments, records) runs on a second stream while
+        batch i updates the table on the current one; two workspaces, events
+        for the order.  The results equal those of ps_step_mf step by step."""
+        import torch
+        c = self.cfg
+        main = torch.cuda.current_stream()
+        if not hasattr(self, "_ovl"):
+            nB = self.batches[0]["row"].numel()
+            self._ovl = (torch.cuda.Stream(), [store.mf_workspace(nB), store.mf_workspace(nB)],
+                         [torch.cuda.Event(), torch.cuda.Event()], [torch.cuda.Event(), torch.cuda.Event()],
+                         torch.cuda.Event())
+            self._ovl[4].record(main)   # creates the event, whose handle the library records into
+        side, ws, prepared, applied, rows_done = self._ovl
+        b = lambda i: self.batches[i % len(self.batches)]
+        side.wait_stream(main)
+        store.step_mf_prepare(b(first)["row"], b(first)["col"], b(first)["val"], c.n_rows, ws[0], stream=side)
+        prepared[0].record(side)
+        for k in range(count):
+            bt = b(first + k)
+            main.wait_event(prepared[k % 2])
+            store.step_mf_apply(bt["row"].numel(), c.lam, ws[k % 2], loss=loss, stream=main, rows_done=rows_done)
+            applied[k % 2].record(main)
+            if k + 1 < count:
+                nx = b(first + k + 1)
+                if k >= 1:
+                    side.wait_event(applied[(k + 1) % 2])
+                side.wait_event(rows_done)   # overlap the column-key merge, not the row-key merge
+                store.step_mf_prepare(nx["row"], nx["col"], nx["val"], c.n_rows, ws[(k + 1) % 2], stream=side)
+                prepared[(k + 1) % 2].record(side)
+
     def alg_bytes(self, i):
         """Algorithmic (useful) bytes per launch of the merge kernel(s) and of
         the task-gradient kernel for batch i; shared per-unit rows count once."""
@@ -212,6 +247,8 @@ def main():
            "rowmerge": _lib.PS_KERNEL_MF_ROWMERGE, "scatter": _lib.PS_KERNEL_SCATTER}
     names = list(wb.alg_bytes(0))                 # kernels with algorithmic bytes for this workload
 
+    overlap = wb.task == "mf" and not args.no_overlap and not args.graph
+
     def run_steps(first, count, mask):
         """count steps from batch `first` with the kernels in `mask` bracketed by HIP
         events; returns host seconds and {name: (total ms, launches)}."""
@@ -220,8 +257,11 @@ def main():
         store.set_timing(mask)
         torch.cuda.synchronize()
         t = time.perf_counter()
-        for i in range(count):
-            wb.step(store, first + i, loss)
+        if overlap:
+            wb.run_overlapped(store, first, count, loss)
+        else:
+            for i in range(count):
+                wb.step(store, first + i, loss)
         torch.cuda.synchronize()
         secs = time.perf_counter() - t
         store.set_timing(False)
@@ -401,6 +441,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": cfg.name, "num_keys": cfg.num_keys, "dim": cfg.dim, "layout": args.layout,
                    "launch": "hip graph replay" if args.graph else "eager",
+                   "mf_key_work_overlapped": overlap,
                    "key_occurrences_per_step": occ, "avg_unique_keys_per_step": U_avg,
                    "batches_resident": nb},
         "roofline": roofline,

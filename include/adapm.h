@@ -135,6 +135,25 @@ ps_status ps_step_mf(ps_store* s, const int32_t* row, const int32_t* col, const 
                      int64_t B, int64_t col_key_offset, float lambda, double* loss,
                      void* ws, size_t ws_bytes, void* stream);
 
+/* ps_step_mf in two phases, for callers that overlap the key work of the
+ * next batch with the table update of this one (two workspaces, two
+ * streams).  ps_step_mf_prepare reads only the batch and writes the
+ * workspace (sorted keys, segments, one record per entry); it reads no
+ * table row, so it may run while another workspace's apply updates W and G.
+ * ps_step_mf_apply then updates W and G from that workspace (and writes
+ * the loss); it no longer reads row, col or val.  ws must hold the
+ * result of ps_step_mf_prepare for this store and the same B, unmodified;
+ * ordering prepare before apply (and an apply before the next prepare into
+ * the same workspace) is the caller's, e.g. with events.  Prepare then
+ * apply on one stream is exactly ps_step_mf.  rows_done (a hipEvent_t, may
+ * be NULL) is recorded on the stream once the row-key merge has been
+ * enqueued: a prepare that waits for it overlaps the rest of the apply
+ * (column-key merge, finalize) instead of the bandwidth-bound row merge. */
+ps_status ps_step_mf_prepare(ps_store* s, const int32_t* row, const int32_t* col, const float* val,
+                             int64_t B, int64_t col_key_offset, void* ws, size_t ws_bytes, void* stream);
+ps_status ps_step_mf_apply(ps_store* s, int64_t B, float lambda, double* loss, void* ws,
+                           size_t ws_bytes, void* stream, void* rows_done);
+
 /* One ComplEx knowledge-graph-embedding step with negative sampling
  * (Appendix C, "Knowledge graph embeddings").  Rows hold [Re | Im] of a
  * complex vector of dim/2 components (dim must be even).  Triple t uses

@@ -36,6 +36,8 @@ SIGNATURES = {
     "ps_push": (_i32, [_p, _p, _i64, _p, _p, _sz, _p]),
     "ps_dedup": (_i32, [_i64, _p, _i64, _p, _p, _p, _p, _p, _p, _sz, _p]),
     "ps_step_mf": (_i32, [_p, _p, _p, _p, _i64, _i64, _f32, _p, _p, _sz, _p]),
+    "ps_step_mf_prepare": (_i32, [_p, _p, _p, _p, _i64, _i64, _p, _sz, _p]),
+    "ps_step_mf_apply": (_i32, [_p, _i64, _f32, _p, _p, _sz, _p, _p]),
     "ps_step_kge": (_i32, [_p, _p, _p, _p, _p, _i64, _i32, _i32, _i64, _p, _p, _sz, _p]),
     "ps_step_sgns": (_i32, [_p, _p, _p, _p, _i64, _i32, _i32, _i64, _p, _p, _sz, _p]),
     "ps_step_ctr": (_i32, [_p, _p, _p, _i64, _i32, _p, _p, _sz, _p]),

@@ -443,6 +443,58 @@ ps_status check_n(int64_t n, int64_t per_unit) {
 
 hipStream_t as_stream(void* p) { return static_cast<hipStream_t>(p); }
 
+// The MF step in two phases.  Prepare reads only the batch: the key sort,
+// segments and the per-entry records, all in the workspace.  Apply reads the
+// workspace and W: the row-key merge (with the loss), the column-key merge
+// and the long-segment finalize.
+ps_status mf_prepare(ps_store* s, const int32_t* row, const int32_t* col, const float* val, int64_t B,
+                     int64_t col_key_offset, Plan& p, hipStream_t st) {
+  const int64_t n = 2 * B;
+  uint32_t *ks, *perm;
+  KeysMF kmf{row, col, col_key_offset, s->num_keys};
+  if (ps_status r = run_sort(s, kmf, n, s->num_keys, p.sb, s->status, nullptr, true, st, &ks, &perm)) return r;
+  const uint32_t split = (uint32_t)(col_key_offset < s->num_keys ? col_key_offset : s->num_keys);
+  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st, split)) return r;
+  Timed t(s, PS_KERNEL_TASKGRAD, st);
+  hipLaunchKernelGGL(k_mf_pack, dim3(small_grid(B, BLOCK, MERGE_GRID_MAX)), dim3(BLOCK), 0, st, row, col, val, B,
+                     col_key_offset, s->num_keys, p.sb.rank, p.pe);
+  LAUNCHED(k_mf_pack);
+  return PS_OK;
+}
+
+ps_status mf_apply(ps_store* s, int64_t B, float lambda, double* loss, Plan& p, hipStream_t st,
+                   hipEvent_t rows_done = nullptr) {
+  const int64_t n = 2 * B;
+  const uint32_t* ks = p.sb.k[radix_plan(s->num_keys).passes % 2];   // where the sort left the keys
+  // Row keys first: their source reads the column rows before any column
+  // update, forms e, the loss and the column-occurrence gradients; then the
+  // column keys merge those stored rows.
+  SrcMFRow src{p.pe, s->W, s->ld, p.grads, p.loss_part, (double)lambda, s->dim};
+  // (about one key per chunk here: a smaller grid gives each group a longer
+  // run of chunks whose metadata it prefetches together)
+  constexpr int64_t kRowMergeGrid = 2048;
+  if (ps_status r = launch_segreduce(s, p.sb, ks, src, n, PART_LOWER, st, PS_KERNEL_MF_ROWMERGE, kRowMergeGrid))
+    return r;
+  if (rows_done) HIP_TRY(hipEventRecord(rows_done, st));
+  if (loss) {
+    RowShape shape;
+    row_shape(s->dim, true, &shape);
+    hipLaunchKernelGGL(k_sum_loss, dim3(1), dim3(BLOCK), 0, st, p.loss_part, reduce_grid(n, shape.L, kRowMergeGrid),
+                       loss);
+    LAUNCHED(k_sum_loss);
+  }
+  if (ps_status r = launch_segreduce(s, p.sb, ks, SrcSorted{p.grads, s->dim}, n, PART_UPPER, st)) return r;
+  return launch_finalize(s, p.sb, ks, n, st);
+}
+
+ps_status zero_loss(double* loss, hipStream_t st) {
+  if (loss) {
+    hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(BLOCK), 0, st, reinterpret_cast<uint32_t*>(loss), int64_t(2));
+    LAUNCHED(k_zero_words);
+  }
+  return PS_OK;
+}
+
 }  // namespace
 
 // ======================================================================== C ABI
@@ -608,48 +660,39 @@ ps_status ps_step_mf(ps_store* s, const int32_t* row, const int32_t* col, const 
   if (ps_status st = check_store(s)) return st;
   if (ps_status st = check_n(B, 2)) return st;
   hipStream_t st = as_stream(stream);
-  if (B == 0) {
-    if (loss) {
-      hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(BLOCK), 0, st, reinterpret_cast<uint32_t*>(loss), int64_t(2));
-      LAUNCHED(k_zero_words);
-    }
-    return PS_OK;
-  }
+  if (B == 0) return zero_loss(loss, st);
   if (!row || !col || !val) return fail(PS_ERR_INVALID, "row, col or val is NULL");
   if (col_key_offset < 0) return fail(PS_ERR_INVALID, "negative col_key_offset");
-  const int64_t n = 2 * B;
   Plan p;
   plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_MF, B, 2, &p);
   if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
-  uint32_t *ks, *perm;
-  KeysMF kmf{row, col, col_key_offset, s->num_keys};
-  if (ps_status r = run_sort(s, kmf, n, s->num_keys, p.sb, s->status, nullptr, true, st, &ks, &perm)) return r;
-  const uint32_t split = (uint32_t)(col_key_offset < s->num_keys ? col_key_offset : s->num_keys);
-  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st, split)) return r;
-  {
-    Timed t(s, PS_KERNEL_TASKGRAD, st);
-    hipLaunchKernelGGL(k_mf_pack, dim3(small_grid(B, BLOCK, MERGE_GRID_MAX)), dim3(BLOCK), 0, st, row, col, val, B,
-                       col_key_offset, s->num_keys, p.sb.rank, p.pe);
-  }
-  LAUNCHED(k_mf_pack);
-  // Row keys first: their source reads the column rows before any column
-  // update, forms e, the loss and the column-occurrence gradients; then the
-  // column keys merge those stored rows.
-  SrcMFRow src{p.pe, s->W, s->ld, p.grads, p.loss_part, (double)lambda, s->dim};
-  // (about one key per chunk here: a smaller grid gives each group a longer
-  // run of chunks whose metadata it prefetches together)
-  constexpr int64_t kRowMergeGrid = 2048;
-  if (ps_status r = launch_segreduce(s, p.sb, ks, src, n, PART_LOWER, st, PS_KERNEL_MF_ROWMERGE, kRowMergeGrid))
-    return r;
-  if (loss) {
-    RowShape shape;
-    row_shape(s->dim, true, &shape);
-    hipLaunchKernelGGL(k_sum_loss, dim3(1), dim3(BLOCK), 0, st, p.loss_part, reduce_grid(n, shape.L, kRowMergeGrid),
-                       loss);
-    LAUNCHED(k_sum_loss);
-  }
-  if (ps_status r = launch_segreduce(s, p.sb, ks, SrcSorted{p.grads, s->dim}, n, PART_UPPER, st)) return r;
-  return launch_finalize(s, p.sb, ks, n, st);
+  if (ps_status r = mf_prepare(s, row, col, val, B, col_key_offset, p, st)) return r;
+  return mf_apply(s, B, lambda, loss, p, st);
+}
+
+ps_status ps_step_mf_prepare(ps_store* s, const int32_t* row, const int32_t* col, const float* val, int64_t B,
+                             int64_t col_key_offset, void* ws, size_t ws_bytes, void* stream) {
+  if (ps_status st = check_store(s)) return st;
+  if (ps_status st = check_n(B, 2)) return st;
+  if (B == 0) return PS_OK;
+  if (!row || !col || !val) return fail(PS_ERR_INVALID, "row, col or val is NULL");
+  if (col_key_offset < 0) return fail(PS_ERR_INVALID, "negative col_key_offset");
+  Plan p;
+  plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_MF, B, 2, &p);
+  if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
+  return mf_prepare(s, row, col, val, B, col_key_offset, p, as_stream(stream));
+}
+
+ps_status ps_step_mf_apply(ps_store* s, int64_t B, float lambda, double* loss, void* ws, size_t ws_bytes,
+                           void* stream, void* rows_done) {
+  if (ps_status st = check_store(s)) return st;
+  if (ps_status st = check_n(B, 2)) return st;
+  hipStream_t st = as_stream(stream);
+  if (B == 0) return zero_loss(loss, st);
+  Plan p;
+  plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_MF, B, 2, &p);
+  if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
+  return mf_apply(s, B, lambda, loss, p, st, static_cast<hipEvent_t>(rows_done));
 }
 
 ps_status ps_step_kge(ps_store* s, const int32_t* head, const int32_t* rel, const int32_t* tail, const int32_t* neg,

@@ -134,6 +134,23 @@ class Store:
                                ws, wsb, _stream(stream)))
         return loss
 
+    def mf_workspace(self, B: int) -> torch.Tensor:
+        """A workspace of its own for the two-phase MF step (one per batch in flight)."""
+        return torch.empty(self.workspace_bytes(_lib.PS_OP_STEP_MF, B, 2), dtype=torch.uint8, device=self.W.device)
+
+    def step_mf_prepare(self, row, col, val, col_key_offset: int, ws: torch.Tensor, stream=None):
+        _dev(row, torch.int32, "row"), _dev(col, torch.int32, "col"), _dev(val, torch.float32, "val")
+        B = row.numel()
+        check(lib().ps_step_mf_prepare(self._h, _ptr(row), _ptr(col), _ptr(val), B, col_key_offset, _ptr(ws),
+                                       ws.numel(), _stream(stream)))
+
+    def step_mf_apply(self, B: int, lam: float, ws: torch.Tensor, loss=None, stream=None, rows_done=None):
+        """rows_done: a torch.cuda.Event recorded once the row-key merge is enqueued."""
+        loss = self._loss(loss)
+        ev = C.c_void_p(rows_done.cuda_event) if rows_done is not None else C.c_void_p(0)
+        check(lib().ps_step_mf_apply(self._h, B, lam, _ptr(loss), _ptr(ws), ws.numel(), _stream(stream), ev))
+        return loss
+
     def step_kge(self, head, rel, tail, neg, n_head_neg: int, rel_key_offset: int, loss=None, stream=None):
         for t, nm in ((head, "head"), (rel, "rel"), (tail, "tail"), (neg, "neg")):
             _dev(t, torch.int32, nm)

@@ -150,3 +150,57 @@ def test_mf_paper_scale_one_step():
     assert float(loss.item()) == pytest.approx(rloss, rel=1e-9)
     assert_close_tables(Wt.cpu().numpy(), W, "W")
     assert_close_tables(Gt.cpu().numpy(), G, "G")
+
+
+def run_two_phase(cfg, steps, seed_table=None):
+    """Sequential ps_step_mf on one store; on a twin store the same steps as
+    prepare (second stream, alternating workspaces) overlapped with apply
+    (first stream), ordered by events.  Tables and losses must agree bit for bit."""
+    wl = MFWorkload(cfg)
+    W0 = wl.init_table() if seed_table is None else seed_table
+    WA, GA = dev(W0), torch.zeros(W0.shape, dtype=torch.float32, device="cuda")
+    WB, GB = dev(W0), torch.zeros(W0.shape, dtype=torch.float32, device="cuda")
+    A = Store(WA, GA, cfg.opt.lr, cfg.opt.eps)
+    Bs = Store(WB, GB, cfg.opt.lr, cfg.opt.eps)
+    batches = []
+    for step in steps:
+        bt = wl.batch(step)
+        batches.append((dev(bt.row), dev(bt.col), dev(bt.val)))
+    lossA = [A.step_mf(r, c, v, cfg.n_rows, cfg.lam).clone() for r, c, v in batches]
+    main = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    nB = batches[0][0].numel()
+    assert all(b[0].numel() == nB for b in batches)
+    ws = [Bs.mf_workspace(nB), Bs.mf_workspace(nB)]
+    prepared = [torch.cuda.Event(), torch.cuda.Event()]
+    applied = [torch.cuda.Event(), torch.cuda.Event()]
+    rows_done = torch.cuda.Event()
+    rows_done.record(main)
+    lossB = []
+    side.wait_stream(main)
+    Bs.step_mf_prepare(*batches[0], cfg.n_rows, ws[0], stream=side)
+    prepared[0].record(side)
+    for i in range(len(batches)):
+        main.wait_event(prepared[i % 2])
+        lossB.append(Bs.step_mf_apply(nB, cfg.lam, ws[i % 2], stream=main, rows_done=rows_done))
+        applied[i % 2].record(main)
+        if i + 1 < len(batches):
+            if i >= 1:
+                side.wait_event(applied[(i + 1) % 2])   # the apply that last used this workspace
+            side.wait_event(rows_done)
+            Bs.step_mf_prepare(*batches[i + 1], cfg.n_rows, ws[(i + 1) % 2], stream=side)
+            prepared[(i + 1) % 2].record(side)
+    torch.cuda.synchronize()
+    assert A.error() == 0 and Bs.error() == 0
+    assert_bitwise(WB.cpu().numpy(), WA.cpu().numpy(), "W two-phase vs one call")
+    assert_bitwise(GB.cpu().numpy(), GA.cpu().numpy(), "G two-phase vs one call")
+    assert [l.item() for l in lossB] == [l.item() for l in lossA]
+
+
+def test_mf_two_phase_overlapped_matches_one_call():
+    run_two_phase(small_variant(MF_10Mx1M), range(6))
+
+
+def test_mf_two_phase_paper_scale():
+    say("10M x 1M two-phase steps")
+    run_two_phase(MF_10Mx1M, range(3))
