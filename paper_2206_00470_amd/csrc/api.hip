@@ -57,6 +57,10 @@ struct ps_store {
   float eps;
   int32_t* status;   // device: [0] sticky key-range flag
   uint32_t timing = 0;   // bit k: bracket launches of kernel id k
+  // a second stream for key work that runs beside a step's task kernel
+  hipStream_t aux = nullptr;
+  hipEvent_t fork_ev = nullptr;
+  hipEvent_t join_ev = nullptr;
   std::vector<std::pair<hipEvent_t, hipEvent_t>> events[NUM_TIMED];
   size_t used[NUM_TIMED] = {};
 };
@@ -443,6 +447,22 @@ ps_status check_n(int64_t n, int64_t per_unit) {
 
 hipStream_t as_stream(void* p) { return static_cast<hipStream_t>(p); }
 
+// Fork/join with the store's second stream: work enqueued on s->aux after
+// fork() runs beside what the caller then enqueues on st; join() makes st
+// wait for it.  Both are event record/wait pairs, so a step stays capturable
+// in a HIP graph.
+ps_status fork_aux(ps_store* s, hipStream_t st) {
+  HIP_TRY(hipEventRecord(s->fork_ev, st));
+  HIP_TRY(hipStreamWaitEvent(s->aux, s->fork_ev, 0));
+  return PS_OK;
+}
+
+ps_status join_aux(ps_store* s, hipStream_t st) {
+  HIP_TRY(hipEventRecord(s->join_ev, s->aux));
+  HIP_TRY(hipStreamWaitEvent(st, s->join_ev, 0));
+  return PS_OK;
+}
+
 // The MF step in two phases.  Prepare reads only the batch: the key sort,
 // segments and the per-entry records, all in the workspace.  Apply reads the
 // workspace and W: the row-key merge (with the loss), the column-key merge
@@ -559,10 +579,16 @@ ps_status ps_create_strided(ps_store** out, int64_t num_keys, int32_t dim, int64
   hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(BLOCK), 0, st, reinterpret_cast<uint32_t*>(s->status), int64_t(64));
   e = hipGetLastError();
   if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e == hipSuccess) e = hipStreamCreateWithFlags(&s->aux, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&s->fork_ev, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&s->join_ev, hipEventDisableTiming);
   if (e != hipSuccess) {
+    if (s->join_ev) (void)hipEventDestroy(s->join_ev);
+    if (s->fork_ev) (void)hipEventDestroy(s->fork_ev);
+    if (s->aux) (void)hipStreamDestroy(s->aux);
     (void)hipFree(s->status);
     delete s;
-    return fail(PS_ERR_DEVICE, "status clear: %s", hipGetErrorString(e));
+    return fail(PS_ERR_DEVICE, "store set-up: %s", hipGetErrorString(e));
   }
   *out = s;
   return PS_OK;
@@ -576,6 +602,9 @@ ps_status ps_destroy(ps_store* s) {
       (void)hipEventDestroy(pr.first);
       (void)hipEventDestroy(pr.second);
     }
+  (void)hipEventDestroy(s->join_ev);
+  (void)hipEventDestroy(s->fork_ev);
+  (void)hipStreamDestroy(s->aux);
   hipError_t f = hipFree(s->status);
   delete s;
   if (e != hipSuccess) return fail(PS_ERR_DEVICE, "hipDeviceSynchronize: %s", hipGetErrorString(e));
@@ -721,10 +750,13 @@ ps_status ps_step_kge(ps_store* s, const int32_t* head, const int32_t* rel, cons
   hipLaunchKernelGGL(k_unit_valid<ValidKGE>, dim3(small_grid(B, WAVES_PER_BLOCK, 4096)), dim3(BLOCK), 0, st,
                      ValidKGE{head, rel, tail, neg, n_neg, rel_key_offset, s->num_keys}, B, p.ok, s->status);
   LAUNCHED(k_unit_valid);
+  // the key sort and segments (workspace only) run on the second stream
+  // beside the gradient kernel (table reads, per-unit rows)
+  if (ps_status r = fork_aux(s, st)) return r;
   uint32_t *ks, *perm;
   KeysKGE kk{head, rel, tail, neg, per, n_neg, rel_key_offset, p.ok};
-  if (ps_status r = run_sort(s, kk, n, s->num_keys, p.sb, s->status, nullptr, false, st, &ks, &perm)) return r;
-  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st)) return r;
+  if (ps_status r = run_sort(s, kk, n, s->num_keys, p.sb, s->status, nullptr, false, s->aux, &ks, &perm)) return r;
+  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, s->aux)) return r;
   const int cdim = s->dim / 2;
   const int64_t grid = small_grid(B, WAVES_PER_BLOCK, LOSS_GRID);
   auto launch = [&](auto kernel) -> ps_status {
@@ -743,6 +775,7 @@ ps_status ps_step_kge(ps_store* s, const int32_t* head, const int32_t* rel, cons
     hipLaunchKernelGGL(k_sum_loss, dim3(1), dim3(BLOCK), 0, st, p.loss_part, grid, loss);
     LAUNCHED(k_sum_loss);
   }
+  if (ps_status r = join_aux(s, st)) return r;
   return run_reduce(s, p.sb, ks, SrcKGE{perm, p.mat, p.base, p.coef, per, n_head_neg, s->dim}, n, {PART_ALL}, st);
 }
 
@@ -773,10 +806,14 @@ ps_status ps_step_sgns(ps_store* s, const int32_t* centre, const int32_t* ctx, c
   hipLaunchKernelGGL(k_unit_valid<ValidSGNS>, dim3(small_grid(B, WAVES_PER_BLOCK, 4096)), dim3(BLOCK), 0, st,
                      ValidSGNS{centre, ctx, neg, slots, n_neg, out_key_offset, s->num_keys}, B, p.ok, s->status);
   LAUNCHED(k_unit_valid);
+  // the key sort and segments (workspace only) run on the second stream
+  // beside the gradient kernel (table reads, per-unit rows)
+  if (ps_status r = fork_aux(s, st)) return r;
   uint32_t *ks, *perm;
   KeysSGNS kk{centre, ctx, neg, (int)per, slots, n_neg, out_key_offset, p.ok};
-  if (ps_status r = run_sort(s, kk, n, s->num_keys, p.sb, s->status, nullptr, false, st, &ks, &perm)) return r;
-  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st, (uint32_t)out_key_offset))
+  if (ps_status r = run_sort(s, kk, n, s->num_keys, p.sb, s->status, nullptr, false, s->aux, &ks, &perm)) return r;
+  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, s->aux,
+                                 (uint32_t)out_key_offset))
     return r;
   RowShape shape;
   row_shape(s->dim, true, &shape);
@@ -795,6 +832,7 @@ ps_status ps_step_sgns(ps_store* s, const int32_t* centre, const int32_t* ctx, c
     return PS_OK;
   });
   if (r) return r;
+  if (ps_status r = join_aux(s, st)) return r;
   // output rows first: their gradients read the input rows, which are updated second
   SrcSGNS src{perm, p.mat, p.coef, centre, s->W, s->ld, (int)per, s->dim};
   return run_reduce(s, p.sb, ks, src, n, {PART_UPPER, PART_LOWER}, st);
