@@ -247,7 +247,8 @@ def main():
            "rowmerge": _lib.PS_KERNEL_MF_ROWMERGE, "scatter": _lib.PS_KERNEL_SCATTER}
     names = list(wb.alg_bytes(0))                 # kernels with algorithmic bytes for this workload
 
-    overlap = wb.task == "mf" and not args.no_overlap and not args.graph
+    # (MF tiny is launch-bound: the extra events of the overlap cost more than it hides)
+    overlap = args.workload == "mf" and not args.no_overlap and not args.graph
 
     def run_steps(first, count, mask):
         """count steps from batch `first` with the kernels in `mask` bracketed by HIP
