@@ -47,6 +47,8 @@ def lib():
             "orc_dedup": (i64, [i64, p, i64, p, p, p, p]),
             "orc_adagrad_row": (None, [p, p, p, i32, f32, f32]),
             "orc_push": (i64, [p, p, i64, i32, f32, f32, p, i64, p]),
+            "orc_adagrad_rowwise": (None, [p, p, p, i32, f32, f32]),
+            "orc_push_rowwise": (i64, [p, p, i64, i32, f32, f32, p, i64, p]),
             "orc_complex_score": (f64, [p, p, p, i32]),
             "orc_grad_mf": (f64, [p, i64, i32, p, p, p, i64, i64, f32, p, p, p]),
             "orc_grad_kge": (f64, [p, i64, i32, p, p, p, p, i64, i32, i32, i64, p, p, p]),
@@ -111,6 +113,33 @@ def push(W, G, keys, grads, lr, eps):
     grads = _c(grads, np.float32).reshape(keys.size, W.shape[1])
     return int(lib().orc_push(_p(W), _p(G), W.shape[0], W.shape[1], lr, eps, _p(keys), keys.size,
                               _p(grads)))
+
+
+def adagrad_rowwise(w, acc, g, lr, eps):
+    """Row-wise AdaGrad on one row; acc is the row's single accumulator."""
+    w, g = _c(w, np.float32), _c(g, np.float32)
+    a = np.array([acc], np.float32)
+    lib().orc_adagrad_rowwise(_p(w), _p(a), _p(g), w.size, lr, eps)
+    return w, a[0]
+
+
+def push_rowwise(W, Gr, keys, grads, lr, eps):
+    """The merged push with row-wise AdaGrad; Gr holds one accumulator per key."""
+    W = _table(W)
+    assert Gr.dtype == np.float32 and Gr.flags.c_contiguous and Gr.shape == (W.shape[0],)
+    keys = _c(keys, np.int64)
+    grads = _c(grads, np.float32).reshape(keys.size, W.shape[1])
+    return int(lib().orc_push_rowwise(_p(W), _p(Gr), W.shape[0], W.shape[1], lr, eps, _p(keys), keys.size,
+                                      _p(grads)))
+
+
+def step_rowwise(task, W, Gr, batch, lr, eps, **kw):
+    """A task step with row-wise AdaGrad: the task's per-occurrence gradients
+    from the pre-step table, then push_rowwise.  Returns (loss, bad)."""
+    grad = {"mf": grad_mf, "kge": grad_kge, "sgns": grad_sgns, "ctr": grad_ctr}[task]
+    keys, grads, loss, bad = grad(W, *batch, **kw)
+    push_rowwise(W, Gr, keys, grads, lr, eps)
+    return loss, bad
 
 
 def complex_score(s, r, o):

@@ -157,6 +157,30 @@ ORC_API void orc_adagrad_row(float* w, float* acc, const float* g, int32_t dim, 
 }
 
 /* ------------------------------------------------------------------------ */
+/* Row-wise AdaGrad, an update variant with one accumulator per row instead  */
+/* of one per element (a reading: the paper names AdaGrad only).  For the    */
+/* merged gradient row g of a key, with its accumulator a (fp32):            */
+/*   t = fp32( (sum_c g_c*g_c) / dim )   (products exact, sum in fp64)       */
+/*   a <- a + t ;  then per element  W <- W - lr * ( g / (sqrt(a) + eps) )   */
+/* in the same fp32 operation order as the per-element form.                 */
+/* ------------------------------------------------------------------------ */
+ORC_API void orc_adagrad_rowwise(float* w, float* acc, const float* g, int32_t dim, float lr, float eps)
+{
+    double sq = 0.0;
+    for (int32_t c = 0; c < dim; ++c) sq += (double)g[c] * (double)g[c];
+    float t = (float)(sq / (double)dim);
+    float a = *acc + t;
+    float s = sqrtf(a);
+    float den = s + eps;
+    for (int32_t c = 0; c < dim; ++c) {
+        float q = g[c] / den;
+        float step = lr * q;
+        w[c] = w[c] - step;
+    }
+    *acc = a;
+}
+
+/* ------------------------------------------------------------------------ */
 /* write access with merging: per distinct key, the fp64 sum of its          */
 /* occurrences' gradient rows in occurrence order, rounded once to fp32,     */
 /* then one AdaGrad step.  Invalid keys are ignored and counted.             */
@@ -178,6 +202,31 @@ ORC_API int64_t orc_push(float* W, float* G, int64_t num_keys, int32_t dim, floa
         }
         for (int32_t c = 0; c < dim; ++c) g32[c] = (float)sum[c];
         orc_adagrad_row(W + key * dim, G + key * dim, g32, dim, lr, eps);
+    }
+    free(g32);
+    free(sum);
+    free(occ);
+    return bad;
+}
+
+/* The same merge with row-wise AdaGrad: Gr holds one accumulator per key.   */
+ORC_API int64_t orc_push_rowwise(float* W, float* Gr, int64_t num_keys, int32_t dim, float lr, float eps,
+                                 const int64_t* keys, int64_t n, const float* grads)
+{
+    occ_t* occ = (occ_t*)malloc(sizeof(occ_t) * (size_t)(n > 0 ? n : 1));
+    double* sum = (double*)malloc(sizeof(double) * (size_t)dim);
+    float* g32 = (float*)malloc(sizeof(float) * (size_t)dim);
+    int64_t bad = sort_occurrences(num_keys, keys, n, occ);
+    int64_t j = 0;
+    while (j < n && occ[j].key < num_keys) {
+        int64_t key = occ[j].key;
+        for (int32_t c = 0; c < dim; ++c) sum[c] = 0.0;
+        for (; j < n && occ[j].key == key; ++j) {
+            const float* row = grads + occ[j].idx * dim;
+            for (int32_t c = 0; c < dim; ++c) sum[c] += (double)row[c];
+        }
+        for (int32_t c = 0; c < dim; ++c) g32[c] = (float)sum[c];
+        orc_adagrad_rowwise(W + key * dim, Gr + key, g32, dim, lr, eps);
     }
     free(g32);
     free(sum);

@@ -222,6 +222,117 @@ def test_push_small_sum_uses_fp64_not_fp32():
     assert W[0, 0] < 0
 
 
+# ---------------------------------------------------------------- row-wise AdaGrad (update variant)
+def test_rowwise_first_touch_constant_magnitude_closed_form():
+    """Every |g_c| = x: the row mean of g^2 is fl(x*x) exactly (fp64 products and
+    sum of dim equal terms are exact), sqrt of it is x, so each step is exactly
+    -lr*sign(g_c) and the accumulator is fl(x*x).  A dropped 1/dim, a sum in
+    place of the mean or the old accumulator in the denominator all fail here."""
+    rng = np.random.default_rng(40)
+    for dim in (1, 3, 64, 100, 129):
+        x = np.float32(rng.uniform(2.0 ** -9, 40.0))
+        g = (x * rng.choice([-1, 1], dim)).astype(np.float32)
+        w0 = rng.standard_normal(dim).astype(np.float32)
+        w, a = oracle.adagrad_rowwise(w0.copy(), np.float32(0), g, LR, EPS)
+        assert a == np.float32(x * x)
+        assert np.array_equal(w, (w0 - np.float32(LR) * np.sign(g).astype(np.float32)).astype(np.float32))
+
+
+def test_rowwise_dim1_is_elementwise_adagrad():
+    """With one element per row the two forms coincide bit for bit; the
+    element-wise form is pinned to torch.optim.Adagrad above."""
+    rng = np.random.default_rng(41)
+    w, a = np.float32(0.3), np.float32(0)
+    we, ae = np.array([0.3], np.float32), np.zeros(1, np.float32)
+    for _ in range(20):
+        g = rng.standard_normal(1).astype(np.float32)
+        wv, a = oracle.adagrad_rowwise(np.array([w], np.float32), a, g, LR, EPS)
+        w = wv[0]
+        we, ae = oracle.adagrad_row(we, ae, g, LR, EPS)
+        assert w == we[0] and a == ae[0]
+
+
+def test_rowwise_repeated_pushes_closed_form():
+    """k pushes of the same row g: a_k = k*mean(g^2), so
+    W_k = W_0 - lr * g/rms(g) * sum_{j<=k} j^-1/2, and every step is parallel to g."""
+    rng = np.random.default_rng(42)
+    g = rng.standard_normal(37).astype(np.float32)
+    ms = float(np.mean(g.astype(np.float64) ** 2))
+    w, a = np.zeros(37, np.float32), np.float32(0)
+    for _ in range(25):
+        w, a = oracle.adagrad_rowwise(w, a, g, LR, EPS)
+    expect = -LR * g.astype(np.float64) / math.sqrt(ms) * sum(j ** -0.5 for j in range(1, 26))
+    np.testing.assert_allclose(w, expect, rtol=3e-6)
+    np.testing.assert_allclose(a, 25 * ms, rtol=3e-6)
+
+
+def test_rowwise_matches_torch_on_a_row_mean_accumulator():
+    """torch reference built from separate pieces: the accumulator is the running
+    sum of g.pow(2).mean(); the update divides by its square root plus eps."""
+    rng = np.random.default_rng(43)
+    d = 50
+    w0 = rng.standard_normal(d).astype(np.float32)
+    wt, at = torch.from_numpy(w0.copy()).double(), torch.zeros((), dtype=torch.float64)
+    w, a = w0.copy(), np.float32(0)
+    for _ in range(8):
+        g = (rng.standard_normal(d) * rng.uniform(0.01, 10)).astype(np.float32)
+        gt = torch.from_numpy(g).double()
+        at = at + gt.pow(2).mean()
+        wt = wt - LR * gt / (at.sqrt() + EPS)
+        w, a = oracle.adagrad_rowwise(w, a, g, LR, EPS)
+    np.testing.assert_allclose(w, wt.numpy(), rtol=2e-6, atol=1e-6)
+    np.testing.assert_allclose(a, at.item(), rtol=2e-6)
+
+
+def test_push_rowwise_brute_force_merge():
+    """Each touched key gets one row-wise step on the fp64 sum of its occurrences
+    rounded once to fp32; untouched rows and accumulators are bit-unchanged."""
+    rng = np.random.default_rng(44)
+    K, d, n = 30, 7, 250
+    W0 = rng.standard_normal((K, d)).astype(np.float32)
+    A0 = rng.uniform(0, 2, K).astype(np.float32)
+    keys = rng.integers(-2, K + 2, n)
+    grads = rng.standard_normal((n, d)).astype(np.float32)
+    W, A = W0.copy(), A0.copy()
+    bad = oracle.push_rowwise(W, A, keys, grads, LR, EPS)
+    assert bad == int(((keys < 0) | (keys >= K)).sum())
+    for k in range(K):
+        rows = [grads[i].astype(np.float64) for i in range(n) if keys[i] == k]
+        if not rows:
+            assert np.array_equal(W[k], W0[k]) and A[k] == A0[k]
+            continue
+        g = np.sum(rows, axis=0).astype(np.float32)
+        acc = np.float64(A0[k]) + np.mean(g.astype(np.float64) ** 2)
+        np.testing.assert_allclose(A[k], acc, rtol=2e-7)
+        np.testing.assert_allclose(W[k], W0[k] - LR * g / (np.sqrt(acc) + EPS), rtol=1e-6, atol=1e-7)
+
+
+def test_push_rowwise_zero_push_and_cancellation_leave_state_unchanged():
+    rng = np.random.default_rng(45)
+    W0 = rng.standard_normal((6, 9)).astype(np.float32)
+    A0 = np.where(rng.random(6) < 0.5, 0, rng.uniform(0, 3, 6)).astype(np.float32)
+    W, A = W0.copy(), A0.copy()
+    oracle.push_rowwise(W, A, rng.integers(0, 6, 20), np.zeros((20, 9), np.float32), LR, EPS)
+    x = rng.standard_normal(9).astype(np.float32)
+    oracle.push_rowwise(W, A, np.array([2, 4, 2]), np.stack([x, np.zeros(9, np.float32), -x]), LR, EPS)
+    assert np.array_equal(W.view(np.uint32), W0.view(np.uint32))
+    assert np.array_equal(A.view(np.uint32), A0.view(np.uint32))
+
+
+def test_step_rowwise_on_one_column_table_is_the_elementwise_step():
+    """A task step with the row-wise update on a one-column table is the
+    element-wise step bit for bit (the merge and gradients are shared)."""
+    W, row, col, val, R = mf_setup(46)
+    W = np.ascontiguousarray(W[:, :1])
+    G = np.zeros_like(W)
+    Wr, Ar = W.copy(), np.zeros(W.shape[0], np.float32)
+    for _ in range(3):
+        loss, _ = oracle.step_mf(W, G, row, col, val, R, 1e-2, LR, EPS)
+        loss_r, _ = oracle.step_rowwise("mf", Wr, Ar, (row, col, val, R, 1e-2), LR, EPS)
+        assert loss == loss_r
+        assert np.array_equal(W, Wr) and np.array_equal(G[:, 0], Ar)
+
+
 # ---------------------------------------------------------------- MF
 def mf_setup(seed=8):
     rng = np.random.default_rng(seed)
