@@ -44,7 +44,11 @@ def parse():
                     help="bound on the CPU-oracle sample (0 = skip)")
     ap.add_argument("--no-ops", action="store_true", help="skip the pull-only / push-only measurements")
     ap.add_argument("--layout", default="interleaved", choices=["interleaved", "dense"],
-                    help="W and G rows of a key side by side in one allocation, or two dense tables")
+                    help="W and G rows of a key side by side in one allocation, or two dense tables "
+                         "(row-wise update: the accumulator in each W row's padding, or a separate vector)")
+    ap.add_argument("--update", default="elementwise", choices=["elementwise", "rowwise"],
+                    help="AdaGrad with one accumulator per element (the paper's), or per key (an update "
+                         "variant with half the table traffic)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a 4 GiB device-to-device copy (reference for HBM counters)")
     ap.add_argument("--no-overlap", action="store_true",
@@ -86,11 +90,12 @@ class Bench:
     """One workload: its table, resident step batches, the step call, the
     algorithmic bytes of its two big kernels and the oracle step."""
 
-    def __init__(self, name, dev, nbatches):
+    def __init__(self, name, dev, nbatches, rowwise=False):
         import torch
         from paper_2206_00470_amd import workloads as wls
 
         self.name = name
+        self.rowwise = rowwise
         self.task = {"mf_tiny": "mf", "kge2x100": "kge"}.get(name, name)
         cfgs = {"mf": wls.MF_10Mx1M, "mf_tiny": wls.MF_TINY, "kge": wls.KGE_COMPLEX,
                 "kge2x100": wls.KGE_COMPLEX_2x100, "sgns": wls.SGNS_1M, "ctr": wls.CTR_33M}
@@ -173,7 +178,9 @@ class Bench:
         the task-gradient kernel for batch i; shared per-unit rows count once."""
         c, bt = self.cfg, self.host_batches[i % len(self.host_batches)]
         n, U, R = self.occ[i % len(self.occ)], self.uniq[i % len(self.uniq)], self.R
-        table = 4.0 * U * R                      # W and G read and written once per distinct key
+        # per distinct key: W read and written, and G (a row, or one value when row-wise)
+        tab = 2.0 * R + 8.0 if self.rowwise else 4.0 * R
+        table = tab * U
         if self.task == "mf":
             B = bt.row.size
             Ucol = np.unique(bt.col).size
@@ -182,8 +189,8 @@ class Bench:
             # distinct column key), the column-occurrence gradient row out, and the row keys'
             # W and G; column-key merge: the stored gradient rows and the column keys' W and G;
             # record scatter: col, val, two ranks in, one record out
-            return {"rowmerge": B * (16.0 + R) + Ucol * R + 4.0 * Urow * R,
-                    "segreduce": B * R + 4.0 * Ucol * R,
+            return {"rowmerge": B * (16.0 + R) + Ucol * R + tab * Urow,
+                    "segreduce": B * R + tab * Ucol,
                     "taskgrad": B * (4.0 + 4.0 + 8.0 + 16.0)}
         if self.task == "ctr":
             B, F = bt.keys.shape
@@ -204,7 +211,13 @@ class Bench:
         import oracle
         c, bt = self.cfg, self.wl.batch(i)
         lr, eps = c.opt.lr, c.opt.eps
-        if self.task == "mf":
+        if self.rowwise:
+            args = {"mf": (bt.row, bt.col, bt.val, c.n_rows, c.lam),
+                    "kge": (bt.head, bt.rel, bt.tail, bt.neg, c.n_head_neg, c.n_ent),
+                    "sgns": (bt.centre, bt.ctx, bt.neg, c.window, c.vocab),
+                    "ctr": (bt.keys, bt.label)}[self.task]
+            oracle.step_rowwise(self.task, W, G, args, lr, eps)
+        elif self.task == "mf":
             oracle.step_mf(W, G, bt.row, bt.col, bt.val, c.n_rows, c.lam, lr, eps)
         elif self.task == "kge":
             oracle.step_kge(W, G, bt.head, bt.rel, bt.tail, bt.neg, c.n_head_neg, c.n_ent, lr, eps)
@@ -230,9 +243,16 @@ def main():
     dev = torch.device("cuda:0")
     t0 = time.time()
     nb = max(1, min(args.steps + args.warmup, 8))
-    wb = Bench(args.workload, dev, nb)
+    rowwise = args.update == "rowwise"
+    wb = Bench(args.workload, dev, nb, rowwise)
     cfg = wb.cfg
-    if args.layout == "interleaved":
+    if rowwise and args.layout == "interleaved":
+        from paper_2206_00470_amd.store import padded_rowwise_table
+        Wt, Gt = padded_rowwise_table(torch.from_numpy(wb.W).to(dev))
+    elif rowwise:
+        Wt = torch.from_numpy(wb.W).to(dev)
+        Gt = torch.zeros(cfg.num_keys, dtype=torch.float32, device=dev)
+    elif args.layout == "interleaved":
         from paper_2206_00470_amd.store import interleaved_tables
         Wt, Gt = interleaved_tables(torch.from_numpy(wb.W).to(dev))
     else:
@@ -324,7 +344,7 @@ def main():
               "rowmerge": "k_segreduce<SrcMFRow>",
               "taskgrad": {"mf": "k_mf_pack", "kge": "k_kge_grad", "sgns": "k_sgns_grad",
                            "ctr": "k_ctr_grad"}[wb.task]}[dom]
-    traffic = counter_traffic(args.workload, symbol)
+    traffic = counter_traffic(args.workload + ("_rowwise" if rowwise else ""), symbol)
     roofline = {
         "bound": "hbm",
         "kernel": symbol,
@@ -367,7 +387,8 @@ def main():
         tl = (time.perf_counter() - t1) / reps
         assert store.error() == 0
         R = wb.R
-        push_alg = 8.0 * n + n * R + 4.0 * U * R
+        tab = 2.0 * R + 8.0 if rowwise else 4.0 * R
+        push_alg = 8.0 * n + n * R + tab * U
         pull_alg = 8.0 * n + U * R + n * R
         # the bare read-modify-write pattern through the merge kernel: U distinct
         # random keys, one contiguous gradient row each (no duplicates to merge)
@@ -381,7 +402,7 @@ def main():
         store.set_timing(False)
         mms, mcnt = store.read_timing(_lib.PS_KERNEL_SEGREDUCE)
         merge_ms = mms / max(mcnt, 1)
-        rmw_alg = U * R + 4.0 * U * R
+        rmw_alg = U * R + tab * U
         ops = {
             "push": {"ms": round(tp * 1e3, 4), "rows_per_s": n / tp, "alg_GBps": round(push_alg / tp / 1e9, 1),
                      "frac_of_peak": round(push_alg / tp / 1e9 / HBM_PEAK_GBPS, 4), "unique_keys": int(U)},
@@ -414,7 +435,7 @@ def main():
     cpu = None
     if args.cpu_seconds > 0:
         W = wb.W
-        G = np.zeros_like(W)
+        G = np.zeros(W.shape[0], np.float32) if rowwise else np.zeros_like(W)
         done, rows, tc0 = 0, 0, time.perf_counter()
         while True:
             rows += 2 * wb.oracle_step(W, G, 1000 + done)
@@ -427,8 +448,8 @@ def main():
                          f"single-threaded C oracle, {tc:.1f} s"}
 
     line = {
-        "metric": "param rows pulled+pushed/sec (MF 10m x 1m, rank 100)" if args.workload == "mf"
-        else f"param rows pulled+pushed/sec ({cfg.name})",
+        "metric": ("param rows pulled+pushed/sec (MF 10m x 1m, rank 100)" if args.workload == "mf"
+                   else f"param rows pulled+pushed/sec ({cfg.name})") + (", row-wise AdaGrad" if rowwise else ""),
         "value": rows_per_s,
         "unit": "rows/s",
         "n_gpus": 1,
@@ -441,6 +462,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": cfg.name, "num_keys": cfg.num_keys, "dim": cfg.dim, "layout": args.layout,
+                   "update": args.update,
                    "launch": "hip graph replay" if args.graph else "eager",
                    "mf_key_work_overlapped": overlap,
                    "key_occurrences_per_step": occ, "avg_unique_keys_per_step": U_avg,

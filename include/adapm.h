@@ -86,6 +86,23 @@ ps_status ps_create(ps_store** out, int64_t num_keys, int32_t dim, float* values
 ps_status ps_create_strided(ps_store** out, int64_t num_keys, int32_t dim, int64_t row_stride,
                             float* values, float* accum, float lr, float eps, void* stream);
 
+/* As ps_create_strided, with row-wise AdaGrad: one accumulator per key
+ * instead of one per element, an update variant (the paper's tasks use
+ * per-element AdaGrad, Appendix C) that halves the update's table traffic.
+ * For the merged gradient row g of a key (fp32) and its accumulator a:
+ *   a <- a + fp32( (sum_c g_c*g_c) / dim )   (squares and sum in fp64)
+ *   W <- W - lr * ( g / (sqrt(a) + eps) )    (fp32, per element, in this order)
+ * Merging and all other semantics are those of the per-element store.
+ * The accumulator of key k is accum[k*accum_stride] (device, caller-owned,
+ * accum_stride >= 1).  It may be a separate vector (accum_stride = 1) or
+ * sit in the padding of each value row (accum = values + c with
+ * dim <= c < row_stride and accum_stride = row_stride), so that a key's
+ * update touches one region of HBM.  An accumulator inside a value row is
+ * PS_ERR_INVALID. */
+ps_status ps_create_rowwise(ps_store** out, int64_t num_keys, int32_t dim, int64_t row_stride,
+                            float* values, float* accum, int64_t accum_stride, float lr, float eps,
+                            void* stream);
+
 /* Free the handle and its status block (not the tables).  NULL is a no-op.
  * Synchronizes the device before freeing. */
 ps_status ps_destroy(ps_store* s);

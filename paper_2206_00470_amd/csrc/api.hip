@@ -49,8 +49,10 @@ constexpr size_t MAX_TIMED_LAUNCHES = 1 << 14;
 // ======================================================================== store
 struct ps_store {
   int64_t num_keys;
-  int64_t ld;        // row stride (floats) of both tables
+  int64_t ld;        // row stride (floats) of W
+  int64_t gld;       // stride (floats) between consecutive keys' accumulator rows or values
   int32_t dim;
+  bool rowwise = false;   // one AdaGrad accumulator per key instead of per element
   float* W;
   float* G;
   float lr;
@@ -382,8 +384,12 @@ ps_status launch_segreduce(ps_store* s, const SortBufs& b, const uint32_t* ks, S
   return with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
     const int64_t grid = reduce_grid(n, L, grid_cap);
     Timed t(s, timing_id, st);
-    hipLaunchKernelGGL((k_segreduce<L, NV, VW, Src>), dim3(grid), dim3(BLOCK), 0, st, sv, src, n, s->W, s->G, s->ld,
-                       s->dim, s->lr, s->eps, b.partial, b.split_list, b.hdr, part);
+    if (s->rowwise)
+      hipLaunchKernelGGL((k_segreduce<L, NV, VW, Src, true>), dim3(grid), dim3(BLOCK), 0, st, sv, src, n, s->W, s->G,
+                         s->ld, s->gld, s->dim, s->lr, s->eps, b.partial, b.split_list, b.hdr, part);
+    else
+      hipLaunchKernelGGL((k_segreduce<L, NV, VW, Src, false>), dim3(grid), dim3(BLOCK), 0, st, sv, src, n, s->W, s->G,
+                         s->ld, s->gld, s->dim, s->lr, s->eps, b.partial, b.split_list, b.hdr, part);
     LAUNCHED(k_segreduce);
     return PS_OK;
   });
@@ -404,8 +410,12 @@ ps_status launch_finalize(ps_store* s, const SortBufs& b, const uint32_t* ks, in
     // at most n / CHUNK + 1 split segments; blocks beyond their count exit at once
     int64_t fgrid = n / CHUNK + 1;
     if (fgrid > 16384) fgrid = 16384;
-    hipLaunchKernelGGL((k_seg_finalize<L, NV, VW>), dim3(fgrid), dim3(BLOCK), lds, st, sv, s->W, s->G, s->ld, s->dim,
-                       s->lr, s->eps, b.partial, b.fold, b.split_list);
+    if (s->rowwise)
+      hipLaunchKernelGGL((k_seg_finalize<L, NV, VW, true>), dim3(fgrid), dim3(BLOCK), lds, st, sv, s->W, s->G, s->ld,
+                         s->gld, s->dim, s->lr, s->eps, b.partial, b.fold, b.split_list);
+    else
+      hipLaunchKernelGGL((k_seg_finalize<L, NV, VW, false>), dim3(fgrid), dim3(BLOCK), lds, st, sv, s->W, s->G, s->ld,
+                         s->gld, s->dim, s->lr, s->eps, b.partial, b.fold, b.split_list);
     LAUNCHED(k_seg_finalize);
     return PS_OK;
   });
@@ -515,6 +525,59 @@ ps_status zero_loss(double* loss, hipStream_t st) {
   return PS_OK;
 }
 
+// Checks shared by the store constructors: key count, row shape, value
+// table, learning rate.
+ps_status check_values(int64_t num_keys, int32_t dim, int64_t row_stride, const float* values, float lr, float eps) {
+  if (num_keys < 1 || num_keys > INT32_MAX) return fail(PS_ERR_INVALID, "num_keys %lld outside [1, 2^31-1]", (long long)num_keys);
+  RowShape shape;
+  if (dim < 1 || !row_shape(dim, true, &shape))
+    return fail(PS_ERR_UNSUPPORTED, "dim %d unsupported (at most 512)", dim);
+  if (row_stride < dim) return fail(PS_ERR_INVALID, "row_stride %lld < dim %d", (long long)row_stride, dim);
+  if (!values) return fail(PS_ERR_INVALID, "table pointer is NULL");
+  if (dim % 4 == 0 && (!aligned16(values) || row_stride % 4 != 0))
+    return fail(PS_ERR_INVALID, "tables must be 16-byte aligned with a row stride that is a multiple of 4");
+  if (!(lr > 0.0f) || !(eps >= 0.0f)) return fail(PS_ERR_INVALID, "need lr > 0 and eps >= 0");
+  return PS_OK;
+}
+
+// Allocates the store, its status block (cleared on `stream`), second stream
+// and events.
+ps_status make_store(ps_store** out, int64_t num_keys, int32_t dim, int64_t row_stride, float* values, float* accum,
+                     int64_t accum_stride, bool rowwise, float lr, float eps, void* stream) {
+  ps_store* s = new ps_store();
+  s->num_keys = num_keys;
+  s->ld = row_stride;
+  s->gld = accum_stride;
+  s->dim = dim;
+  s->rowwise = rowwise;
+  s->W = values;
+  s->G = accum;
+  s->lr = lr;
+  s->eps = eps;
+  hipError_t e = hipMalloc(&s->status, 256);
+  if (e != hipSuccess) {
+    delete s;
+    return fail(PS_ERR_DEVICE, "hipMalloc(status): %s", hipGetErrorString(e));
+  }
+  hipStream_t st = as_stream(stream);
+  hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(BLOCK), 0, st, reinterpret_cast<uint32_t*>(s->status), int64_t(64));
+  e = hipGetLastError();
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e == hipSuccess) e = hipStreamCreateWithFlags(&s->aux, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&s->fork_ev, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&s->join_ev, hipEventDisableTiming);
+  if (e != hipSuccess) {
+    if (s->join_ev) (void)hipEventDestroy(s->join_ev);
+    if (s->fork_ev) (void)hipEventDestroy(s->fork_ev);
+    if (s->aux) (void)hipStreamDestroy(s->aux);
+    (void)hipFree(s->status);
+    delete s;
+    return fail(PS_ERR_DEVICE, "store set-up: %s", hipGetErrorString(e));
+  }
+  *out = s;
+  return PS_OK;
+}
+
 }  // namespace
 
 // ======================================================================== C ABI
@@ -543,12 +606,8 @@ ps_status ps_create_strided(ps_store** out, int64_t num_keys, int32_t dim, int64
                             float* accum, float lr, float eps, void* stream) {
   if (!out) return fail(PS_ERR_INVALID, "out is NULL");
   *out = nullptr;
-  if (num_keys < 1 || num_keys > INT32_MAX) return fail(PS_ERR_INVALID, "num_keys %lld outside [1, 2^31-1]", (long long)num_keys);
-  RowShape shape;
-  if (dim < 1 || !row_shape(dim, true, &shape))
-    return fail(PS_ERR_UNSUPPORTED, "dim %d unsupported (at most 512)", dim);
-  if (row_stride < dim) return fail(PS_ERR_INVALID, "row_stride %lld < dim %d", (long long)row_stride, dim);
-  if (!values || !accum) return fail(PS_ERR_INVALID, "table pointer is NULL");
+  if (ps_status r = check_values(num_keys, dim, row_stride, values, lr, eps)) return r;
+  if (!accum) return fail(PS_ERR_INVALID, "table pointer is NULL");
   {
     // rows of W and G must not overlap: either two separate tables, or rows
     // interleaved in one allocation with a gap of at least dim on each side
@@ -559,39 +618,30 @@ ps_status ps_create_strided(ps_store** out, int64_t num_keys, int32_t dim, int64
     const bool interleaved = row_stride >= 2 * (int64_t)dim && r >= dim && r <= row_stride - dim;
     if (!separate && !interleaved) return fail(PS_ERR_INVALID, "values and accumulator rows overlap");
   }
-  if (dim % 4 == 0 && (!aligned16(values) || !aligned16(accum) || row_stride % 4 != 0))
-    return fail(PS_ERR_INVALID, "tables must be 16-byte aligned with a row stride that is a multiple of 4");
-  if (!(lr > 0.0f) || !(eps >= 0.0f)) return fail(PS_ERR_INVALID, "need lr > 0 and eps >= 0");
-  ps_store* s = new ps_store();
-  s->num_keys = num_keys;
-  s->ld = row_stride;
-  s->dim = dim;
-  s->W = values;
-  s->G = accum;
-  s->lr = lr;
-  s->eps = eps;
-  hipError_t e = hipMalloc(&s->status, 256);
-  if (e != hipSuccess) {
-    delete s;
-    return fail(PS_ERR_DEVICE, "hipMalloc(status): %s", hipGetErrorString(e));
+  if (dim % 4 == 0 && !aligned16(accum)) return fail(PS_ERR_INVALID, "accumulator table must be 16-byte aligned");
+  return make_store(out, num_keys, dim, row_stride, values, accum, row_stride, false, lr, eps, stream);
+}
+
+ps_status ps_create_rowwise(ps_store** out, int64_t num_keys, int32_t dim, int64_t row_stride, float* values,
+                            float* accum, int64_t accum_stride, float lr, float eps, void* stream) {
+  if (!out) return fail(PS_ERR_INVALID, "out is NULL");
+  *out = nullptr;
+  if (ps_status r = check_values(num_keys, dim, row_stride, values, lr, eps)) return r;
+  if (!accum) return fail(PS_ERR_INVALID, "accumulator pointer is NULL");
+  if (accum_stride < 1) return fail(PS_ERR_INVALID, "accum_stride %lld < 1", (long long)accum_stride);
+  {
+    // no accumulator may lie inside a value row: either the accumulators
+    // are wholly outside W's extent, or they sit in the rows' padding
+    // (accum_stride == row_stride, offset within the row in [dim, row_stride))
+    const int64_t d = (int64_t)(accum - values);
+    const int64_t w_end = (num_keys - 1) * row_stride + dim;        // W spans [0, w_end)
+    const int64_t a_last = d + (num_keys - 1) * accum_stride;       // last accumulator
+    const bool separate = a_last < 0 || d >= w_end;
+    const int64_t r = ((d % row_stride) + row_stride) % row_stride;
+    const bool padded = accum_stride == row_stride && r >= dim;
+    if (!separate && !padded) return fail(PS_ERR_INVALID, "accumulators overlap the value rows");
   }
-  hipStream_t st = as_stream(stream);
-  hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(BLOCK), 0, st, reinterpret_cast<uint32_t*>(s->status), int64_t(64));
-  e = hipGetLastError();
-  if (e == hipSuccess) e = hipStreamSynchronize(st);
-  if (e == hipSuccess) e = hipStreamCreateWithFlags(&s->aux, hipStreamNonBlocking);
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&s->fork_ev, hipEventDisableTiming);
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&s->join_ev, hipEventDisableTiming);
-  if (e != hipSuccess) {
-    if (s->join_ev) (void)hipEventDestroy(s->join_ev);
-    if (s->fork_ev) (void)hipEventDestroy(s->fork_ev);
-    if (s->aux) (void)hipStreamDestroy(s->aux);
-    (void)hipFree(s->status);
-    delete s;
-    return fail(PS_ERR_DEVICE, "store set-up: %s", hipGetErrorString(e));
-  }
-  *out = s;
-  return PS_OK;
+  return make_store(out, num_keys, dim, row_stride, values, accum, accum_stride, true, lr, eps, stream);
 }
 
 ps_status ps_destroy(ps_store* s) {

@@ -136,6 +136,24 @@ __device__ __forceinline__ void adagrad_elem(float& w, float& acc, float g, floa
   w = w - step;
 }
 
+// Row-wise AdaGrad: one accumulator per row, advanced by the row mean of the
+// squared merged gradient (fp32 values, squared and summed in fp64, the mean
+// rounded once); every element of the row then steps with the row's shared
+// denominator, in the element-wise order q = g/den, step = lr*q, w - step.
+__device__ __forceinline__ float rowwise_den(float& acc, double sumsq, int dim, float eps) {
+  const float t = (float)(sumsq / (double)dim);
+  const float a = acc + t;
+  acc = a;
+  const float s = __builtin_sqrtf(a);
+  return s + eps;
+}
+
+__device__ __forceinline__ void rowwise_elem(float& w, float g, float den, float lr) {
+  float q = g / den;
+  float step = lr * q;
+  w = w - step;
+}
+
 // ------------------------------------------------------------------ row fragments
 // A group of L lanes covers one row of `dim` floats: lane `gl` owns the
 // VW-wide vectors at columns (gl + v*L)*VW for v < NV.

@@ -150,9 +150,12 @@ __device__ __forceinline__ int64_t xcd_slot(int64_t block, int64_t nblocks) {
 // CHUNK-aligned block (2 slots per block: the chunk starting at the block
 // start, and the one starting inside it) for k_seg_finalize; the first chunk
 // of such a segment also appends the segment to split_list.
-template <int L, int NV, int VW, class Src>
+// RW selects row-wise AdaGrad: G then holds one accumulator per key, at
+// G[key * gld]; otherwise G is a table of rows at G + key * gld.
+template <int L, int NV, int VW, class Src, bool RW>
 __global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, int64_t n, float* __restrict__ W,
-                                                     float* __restrict__ G, int64_t ld, int dim, float lr, float eps,
+                                                     float* __restrict__ G, int64_t ld, int64_t gld, int dim,
+                                                     float lr, float eps,
                                                      double* __restrict__ partial,
                                                      int32_t* __restrict__ split_list, SegHeader* split_hdr,
                                                      int part) {
@@ -196,17 +199,19 @@ __global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, int64_
     const bool whole = flags & 2u;
     const Meta first = shfl_pod(my_first, ci, L);
     float* wrow = W + (int64_t)key * ld;
-    float* grow = G + (int64_t)key * ld;
+    float* grow = G + (int64_t)key * gld;
     float wv[NE], gv[NE];
+    float gacc = 0.0f;   // RW: the key's accumulator
     if (whole || Src::kNeedsOwn) {   // issue the table reads early, they do not depend on the sum
 #pragma unroll
       for (int v = 0; v < NV; ++v) {
         const int col = (gl + v * L) * VW;
         if (col < dim) {
           load_frag<VW>(wrow + col, wv + v * VW);
-          if (whole) load_frag<VW>(grow + col, gv + v * VW);
+          if (!RW && whole) load_frag<VW>(grow + col, gv + v * VW);
         }
       }
+      if (RW && whole) gacc = *grow;
     }
     double acc[NE];
 #pragma unroll
@@ -233,7 +238,31 @@ __global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, int64_
         for (int e = 0; e < NE; ++e) acc[e] += (double)x[e];
       }
     }
-    if (whole) {
+    if (whole && RW) {
+      float g[NE];
+      double sq = 0.0;
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int col = (gl + v * L) * VW;
+#pragma unroll
+        for (int e = 0; e < VW; ++e) {
+          g[v * VW + e] = (float)acc[v * VW + e];
+          if (col < dim) sq += (double)g[v * VW + e] * (double)g[v * VW + e];
+        }
+      }
+      sq = group_sum<L>(sq);
+      const float den = rowwise_den(gacc, sq, dim, eps);
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        const int col = (gl + v * L) * VW;
+        if (col < dim) {
+#pragma unroll
+          for (int e = 0; e < VW; ++e) rowwise_elem(wv[v * VW + e], g[v * VW + e], den, lr);
+          store_frag<VW>(wrow + col, wv + v * VW);
+        }
+      }
+      if (gl == 0) *grow = gacc;
+    } else if (whole) {
 #pragma unroll
       for (int v = 0; v < NV; ++v) {
         const int col = (gl + v * L) * VW;
@@ -356,16 +385,19 @@ __global__ __launch_bounds__(BLOCK) void k_seg_fold(SegView sv, int64_t nsb, uin
 // its first chunk, the partials of its cuts before its first foldable
 // super-block, the fold rows of its foldable super-blocks, then the partials
 // of the cuts after them.  They are added by group_sum_rows, the group
-// results in group order, rounded once and applied with AdaGrad.  The order
-// is fixed, so the result is deterministic.
-template <int L, int NV, int VW>
+// results in group order, rounded once and applied with AdaGrad (row-wise
+// when RW, with the accumulator at G[key * gld]).  The order is fixed, so
+// the result is deterministic.
+template <int L, int NV, int VW, bool RW>
 __global__ __launch_bounds__(BLOCK) void k_seg_finalize(SegView sv, float* __restrict__ W, float* __restrict__ G,
-                                                        int64_t ld, int dim, float lr, float eps,
+                                                        int64_t ld, int64_t gld, int dim, float lr, float eps,
                                                         const double* __restrict__ partial,
                                                         const double* __restrict__ fold,
                                                         const int32_t* __restrict__ split_list) {
   constexpr int GPB = BLOCK / L;
   extern __shared__ double lds[];   // [GPB][dim]
+  __shared__ double sm[WAVES_PER_BLOCK];
+  __shared__ float den_sh;
   const int64_t nsplit = sv.hdr->num_split;
   for (int64_t e = blockIdx.x; e < nsplit; e += gridDim.x) {
     const int32_t u = split_list[e];
@@ -389,14 +421,39 @@ __global__ __launch_bounds__(BLOCK) void k_seg_finalize(SegView sv, float* __res
     group_sum_rows<L, NV, VW>(row, 1 + n1 + nf + n3, dim, lds);
     __syncthreads();
     float* wrow = W + (int64_t)key * ld;
-    float* grow = G + (int64_t)key * ld;
-    for (int col = threadIdx.x; col < dim; col += BLOCK) {
-      double t = 0.0;
-      for (int gg = 0; gg < GPB; ++gg) t += lds[gg * dim + col];
-      float w = wrow[col], a = grow[col];
-      adagrad_elem(w, a, (float)t, lr, eps);
-      wrow[col] = w;
-      grow[col] = a;
+    float* grow = G + (int64_t)key * gld;
+    if constexpr (RW) {
+      // each thread keeps the fp32 sums of its own columns in lds[col]
+      double sq = 0.0;
+      for (int col = threadIdx.x; col < dim; col += BLOCK) {
+        double t = 0.0;
+        for (int gg = 0; gg < GPB; ++gg) t += lds[gg * dim + col];
+        const float g = (float)t;
+        lds[col] = g;
+        sq += (double)g * (double)g;
+      }
+      sq = block_sum_double(sq, sm);
+      if (threadIdx.x == 0) {
+        float a = *grow;
+        den_sh = rowwise_den(a, sq, dim, eps);
+        *grow = a;
+      }
+      __syncthreads();
+      const float den = den_sh;
+      for (int col = threadIdx.x; col < dim; col += BLOCK) {
+        float w = wrow[col];
+        rowwise_elem(w, (float)lds[col], den, lr);
+        wrow[col] = w;
+      }
+    } else {
+      for (int col = threadIdx.x; col < dim; col += BLOCK) {
+        double t = 0.0;
+        for (int gg = 0; gg < GPB; ++gg) t += lds[gg * dim + col];
+        float w = wrow[col], a = grow[col];
+        adagrad_elem(w, a, (float)t, lr, eps);
+        wrow[col] = w;
+        grow[col] = a;
+      }
     }
     __syncthreads();
   }

@@ -58,28 +58,58 @@ def interleaved_tables(W0: torch.Tensor, G0: torch.Tensor | None = None):
     return T[:, :d], T[:, d:]
 
 
+def padded_rowwise_table(W0: torch.Tensor, A0: torch.Tensor | None = None, pad: int = 4):
+    """Copy a [num_keys, dim] value table into a [num_keys, dim + pad] tensor
+    whose column dim holds each key's row-wise AdaGrad accumulator (zero, or
+    A0); returns the (W, A) views for a row-wise Store.  pad = 4 keeps rows
+    16-byte aligned when dim is a multiple of 4."""
+    K, d = W0.shape
+    T = torch.zeros((K, d + pad), dtype=torch.float32, device=W0.device)
+    T[:, :d].copy_(W0)
+    if A0 is not None:
+        T[:, d].copy_(A0)
+    return T[:, :d], T[:, d]
+
+
 class Store:
     """A parameter store over caller-owned tables W (values) and G (AdaGrad
-    accumulators), float32 [num_keys, dim] CUDA tensors.  W and G may be
-    dense, or row-strided views with one common row stride (for example the
-    two halves of a [num_keys, 2*dim] tensor, see interleaved_tables)."""
+    accumulators), float32 CUDA tensors.  W is [num_keys, dim], dense or a
+    row-strided view.
+
+    G of shape [num_keys, dim] selects per-element AdaGrad; it may be dense
+    or share W's row stride (for example the two halves of a
+    [num_keys, 2*dim] tensor, see interleaved_tables).  G of shape
+    [num_keys] selects row-wise AdaGrad (one accumulator per key, any
+    stride: a separate vector or a column of W's row padding, see
+    padded_rowwise_table)."""
 
     def __init__(self, W: torch.Tensor, G: torch.Tensor, lr: float = 0.1, eps: float = 1e-10, stream=None):
-        for t, nm in ((W, "W"), (G, "G")):
-            if not (t.is_cuda and t.dtype == torch.float32 and t.dim() == 2 and t.stride(1) == 1):
-                raise TypeError(f"{nm} must be a float32 CUDA tensor [num_keys, dim] with unit column stride")
-        if W.shape != G.shape:
-            raise ValueError("W and G must have one shape")
-        if W.shape[0] > 1 and W.stride(0) != G.stride(0):
-            raise ValueError("W and G must share one row stride")
+        if not (W.is_cuda and W.dtype == torch.float32 and W.dim() == 2 and W.stride(1) == 1):
+            raise TypeError("W must be a float32 CUDA tensor [num_keys, dim] with unit column stride")
+        if not (G.is_cuda and G.dtype == torch.float32):
+            raise TypeError("G must be a float32 CUDA tensor")
         self.W, self.G = W, G
         self.num_keys, self.dim = W.shape
         self.row_stride = W.stride(0) if W.shape[0] > 1 else self.dim
+        self.rowwise = G.dim() == 1
         self.lr, self.eps = lr, eps
         self.ws = Workspace(W.device)
         h = C.c_void_p()
-        check(lib().ps_create_strided(C.byref(h), self.num_keys, self.dim, self.row_stride, _ptr(W), _ptr(G), lr,
-                                      eps, _stream(stream)))
+        if self.rowwise:
+            if G.shape[0] != self.num_keys:
+                raise ValueError("a row-wise accumulator vector needs one value per key")
+            astride = G.stride(0) if self.num_keys > 1 else 1
+            check(lib().ps_create_rowwise(C.byref(h), self.num_keys, self.dim, self.row_stride, _ptr(W), _ptr(G),
+                                          astride, lr, eps, _stream(stream)))
+        else:
+            if G.dim() != 2 or G.stride(1) != 1:
+                raise TypeError("G must be [num_keys, dim] with unit column stride, or [num_keys]")
+            if W.shape != G.shape:
+                raise ValueError("W and G must have one shape")
+            if W.shape[0] > 1 and W.stride(0) != G.stride(0):
+                raise ValueError("W and G must share one row stride")
+            check(lib().ps_create_strided(C.byref(h), self.num_keys, self.dim, self.row_stride, _ptr(W), _ptr(G),
+                                          lr, eps, _stream(stream)))
         self._h = h
 
     def close(self):

@@ -20,7 +20,7 @@ def declared():
 
 def test_header_declares_the_boundary():
     names = declared()
-    for n in ("ps_create", "ps_destroy", "ps_pull", "ps_push", "ps_dedup", "ps_step_mf", "ps_step_kge",
+    for n in ("ps_create", "ps_create_rowwise", "ps_destroy", "ps_pull", "ps_push", "ps_dedup", "ps_step_mf", "ps_step_kge",
               "ps_step_sgns", "ps_step_ctr", "ps_get_error", "ps_workspace_bytes"):
         assert n in names
 
@@ -77,6 +77,27 @@ def test_create_strided_rejects_overlapping_or_misaligned_rows():
     assert L.ps_create_strided(C.byref(h), K, d, d, P(0), P(d), 0.1, 0.0, None) == _lib.PS_ERR_INVALID
     assert L.ps_create_strided(C.byref(h), K, d, 2 * d + 2, P(0), P(d), 0.1, 0.0, None) == _lib.PS_ERR_INVALID
     assert L.ps_create_strided(C.byref(h), K, d, 2 * d, P(1), P(d + 1), 0.1, 0.0, None) == _lib.PS_ERR_INVALID
+    assert h.value is None
+
+
+def test_create_rowwise_rejects_overlapping_or_bad_accumulators():
+    L = _lib.lib()
+    h = C.c_void_p(1)
+    base = 0x100000
+    K, d = 1000, 100
+    P = lambda off_floats: C.c_void_p(base + 4 * off_floats)
+    cr = lambda ld, acc, ast, lr=0.1: L.ps_create_rowwise(C.byref(h), K, d, ld, P(0), acc, ast, lr, 0.0, None)
+    assert cr(d + 4, None, d + 4) == _lib.PS_ERR_INVALID                  # no accumulator
+    assert cr(d + 4, P(d), 0) == _lib.PS_ERR_INVALID                      # stride < 1
+    assert cr(d + 4, P(d - 1), d + 4) == _lib.PS_ERR_INVALID              # inside the row
+    assert cr(d, P(d), d) == _lib.PS_ERR_INVALID                          # no padding: next row's first value
+    assert cr(d + 4, P(d), d + 3) == _lib.PS_ERR_INVALID                  # drifts into later rows
+    assert cr(d + 4, P(5 * (d + 4)), 1) == _lib.PS_ERR_INVALID            # a vector inside W's extent
+    assert cr(d + 4, P(d), d + 4, lr=0.0) == _lib.PS_ERR_INVALID
+    assert cr(d + 2, P(d), d + 2) == _lib.PS_ERR_INVALID                  # stride not a multiple of 4
+    assert L.ps_create_rowwise(None, K, d, d, P(0), P(K * d), 1, 0.1, 0.0, None) == _lib.PS_ERR_INVALID
+    assert L.ps_create_rowwise(C.byref(h), K, 513, 520, P(0), P(K * 520), 1, 0.1, 0.0,
+                               None) == _lib.PS_ERR_UNSUPPORTED
     assert h.value is None
 
 

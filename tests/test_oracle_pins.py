@@ -224,13 +224,14 @@ def test_push_small_sum_uses_fp64_not_fp32():
 
 # ---------------------------------------------------------------- row-wise AdaGrad (update variant)
 def test_rowwise_first_touch_constant_magnitude_closed_form():
-    """Every |g_c| = x: the row mean of g^2 is fl(x*x) exactly (fp64 products and
-    sum of dim equal terms are exact), sqrt of it is x, so each step is exactly
-    -lr*sign(g_c) and the accumulator is fl(x*x).  A dropped 1/dim, a sum in
-    place of the mean or the old accumulator in the denominator all fail here."""
+    """Every |g_c| = x with x of at most 12 significant bits: x*x fits fp32 and
+    the fp64 partial sums k*x*x are exact, so the row mean of g^2 is x*x, its
+    square root is x, each step is exactly -lr*sign(g_c) and the accumulator
+    is x*x.  A dropped 1/dim, a sum in place of the mean or the old
+    accumulator in the denominator all fail here."""
     rng = np.random.default_rng(40)
     for dim in (1, 3, 64, 100, 129):
-        x = np.float32(rng.uniform(2.0 ** -9, 40.0))
+        x = np.float32(rng.integers(1, 4096) * 2.0 ** int(rng.integers(-16, -5)))
         g = (x * rng.choice([-1, 1], dim)).astype(np.float32)
         w0 = rng.standard_normal(dim).astype(np.float32)
         w, a = oracle.adagrad_rowwise(w0.copy(), np.float32(0), g, LR, EPS)
