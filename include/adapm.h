@@ -56,6 +56,7 @@ typedef int32_t ps_status;
 #define PS_ERR_WORKSPACE   (-3)   /* ws_bytes smaller than ps_workspace_bytes() */
 #define PS_ERR_DEVICE      (-4)   /* a HIP runtime call failed */
 #define PS_ERR_UNSUPPORTED (-5)   /* a size beyond what the kernels handle */
+#define PS_ERR_NOT_RESIDENT (-6)  /* staged store: a key with no slot was accessed */
 
 /* operation codes for ps_workspace_bytes() */
 #define PS_OP_PULL      0
@@ -231,6 +232,115 @@ const char* ps_last_error_message(void);
 #define PS_TIMING_ALL (-1)
 ps_status ps_set_timing(ps_store* s, int32_t mask);
 ps_status ps_read_timing(ps_store* s, int32_t kernel_id, double* total_ms, int64_t* launches);
+
+/* ======================================================================
+ * Staged stores: intent signalling and adaptive action timing
+ * (Section 3, "Intent signaling"; Section 4.2, Algorithm 1), for one
+ * worker, the GPU, whose full table lives in host memory.
+ *
+ * The home tables (values and AdaGrad accumulators, num_keys rows each)
+ * are caller-owned pinned host memory (hipHostMalloc; torch's
+ * pin_memory=True).  HBM holds a table of slots (caller-owned device
+ * memory, `values`/`accum` with `row_stride` as in ps_create_strided) and
+ * a device map key -> slot (`key_slot`, num_keys int32, caller-owned,
+ * filled with -1 by ps_create_staged).  The keys are split into ranges
+ * [range_begin[r], range_begin[r+1]) (the last ends at num_keys), each with
+ * range_slots[r] slots; a key offset that a step takes (col_key_offset,
+ * rel_key_offset, out_key_offset) must begin a range.
+ *
+ * The worker declares future accesses with ps_intent(keys, C_start,
+ * C_end): it will access those keys while its clock C satisfies
+ * C_start <= C < C_end (the intent is inactive before, active within,
+ * expired after).  ps_advance_clock raises C by one, typically once per
+ * batch, before the batch's step.  Rounds (ps_stage_round, or
+ * ps_stage_auto's library thread) act on intents: in a round at clock C
+ * with Delta = C minus the clock at the previous round, the estimate of
+ * clocks per round is smoothed, est <- (1-alpha) est + alpha Delta (not
+ * when Delta = 0), and every pending intent with
+ * C_start < C + Q_Poiss(2 max(est, Delta), p) is acted upon (Algorithm 1;
+ * alpha = 0.1, p = 0.9999, est_0 = 10 unless ps_set_action_timing says
+ * otherwise).  Acting makes an intent's keys resident: a key not resident
+ * gets a free slot of its range and its home rows are copied in.  A key
+ * whose every acted-upon intent has expired is written back to the home
+ * tables and its slot freed at the next round.  Intents are acted upon in
+ * C_start order; a range with no free slot stops acting until expiries free
+ * slots.  An intent still pending when the clock reaches its C_start is
+ * acted upon at once inside ps_advance_clock (a forced action, counted).
+ *
+ * Ordering: the copies of a round run on the store's staging stream after
+ * the worker stream's work enqueued before its last ps_advance_clock;
+ * ps_advance_clock makes the given worker stream wait for the rounds that
+ * staged the intents now active.  So the worker calls ps_advance_clock and
+ * the steps on one stream, and every key a step accesses must be covered by
+ * an intent that is active at the current clock; an access to a key with no
+ * slot is skipped like an invalid id and reported by ps_get_error as
+ * PS_ERR_NOT_RESIDENT.  The steps and ps_push take their workspace as for
+ * other stores (ps_workspace_bytes covers the id translation) and see the
+ * home table's keys; ps_pull reads resident rows.  The two-phase MF step is
+ * not available (PS_ERR_UNSUPPORTED).  Home rows of resident keys are stale
+ * until ps_stage_flush.  Updates are per-element AdaGrad.
+ *
+ * ps_create_staged allocates, besides the status block, a staging stream,
+ * events, and move lists of 2 x total slots (int64 keys and slots) in
+ * device memory and twice that in pinned host memory. */
+
+/* statistics reported by ps_stage_stats, in this order */
+#define PS_STAGE_CLOCK      0   /* worker clock */
+#define PS_STAGE_ROUNDS     1   /* rounds run */
+#define PS_STAGE_FORCED     2   /* forced actions in ps_advance_clock */
+#define PS_STAGE_STAGED     3   /* keys copied in, total */
+#define PS_STAGE_EVICTED    4   /* keys written back, total */
+#define PS_STAGE_RESIDENT   5   /* keys resident now */
+#define PS_STAGE_PENDING    6   /* keys of intents not yet acted upon */
+#define PS_STAGE_STALLED    7   /* times acting stopped at a full range */
+#define PS_STAGE_NUM_STATS  8
+
+ps_status ps_create_staged(ps_store** out, int64_t num_keys, int32_t dim, float* home_values,
+                           float* home_accum, int64_t home_stride, float* values, float* accum,
+                           int64_t row_stride, int32_t* key_slot, int32_t num_ranges,
+                           const int64_t* range_begin, const int64_t* range_slots, float lr, float eps,
+                           void* stream);
+
+/* Action-timing hyperparameters of Algorithm 1 (0 < alpha <= 1, 0 < p < 1,
+ * lambda0 >= 0 resets the estimate). */
+ps_status ps_set_action_timing(ps_store* s, double alpha, double p, double lambda0);
+
+/* Intent(keys, c_start, c_end): host array of n keys (duplicates and keys
+ * outside [0, num_keys) are allowed and ignored), c_start < c_end.  Cheap:
+ * the keys are queued; rounds act on them.  An intent already expired at
+ * the current clock is ignored. */
+ps_status ps_intent(ps_store* s, const int64_t* keys, int64_t n, int64_t c_start, int64_t c_end);
+
+/* advanceClock: raise the worker clock by one and order `stream` (the
+ * worker's) after the staging it now needs, acting at once on intents that
+ * became active without a round having acted on them. */
+ps_status ps_advance_clock(ps_store* s, void* stream);
+
+/* One round; with wait != 0 the call returns once its copies are done.
+ * Not while ps_stage_auto is on. */
+ps_status ps_stage_round(ps_store* s, int32_t wait);
+
+/* on != 0: run rounds back to back on a library thread (each lasts until its
+ * copies are done); on = 0: stop it and report any error it met. */
+ps_status ps_stage_auto(ps_store* s, int32_t on);
+
+/* Write the rows of every resident key back to the home tables (after the
+ * work enqueued on `stream`) and wait for it; the keys stay resident. */
+ps_status ps_stage_flush(ps_store* s, void* stream);
+
+/* counts[i] for i < n (PS_STAGE_* indices) and the current estimate of
+ * clocks per round (either may be NULL when n = 0). */
+ps_status ps_stage_stats(ps_store* s, int64_t* counts, int32_t n, double* lambda);
+
+/* The resident keys in ascending order: up to `capacity` into keys (host),
+ * their number into *count. */
+ps_status ps_stage_resident(ps_store* s, int64_t* keys, int64_t capacity, int64_t* count);
+
+/* Algorithm 1 as a pure host function: from the previous estimate, the
+ * clock at the previous round and now, return the new estimate and the
+ * horizon H (act on an intent iff C_start < H). */
+ps_status ps_action_timing(double lambda_prev, int64_t c_prev, int64_t c_now, double alpha, double p,
+                           double* lambda_new, int64_t* horizon);
 
 #ifdef __cplusplus
 }

@@ -8,11 +8,11 @@ and a missing library is an error, never a fallback.
 """
 import importlib
 
-__all__ = ["Store", "dedup", "workloads"]
+__all__ = ["Store", "StagedStore", "dedup", "action_timing", "workloads"]
 
 
 def __getattr__(name):
-    if name in ("Store", "dedup"):
+    if name in ("Store", "StagedStore", "dedup", "action_timing"):
         return getattr(importlib.import_module(__name__ + ".store"), name)
     if name == "workloads":
         return importlib.import_module(__name__ + ".workloads")

@@ -17,12 +17,15 @@ PS_ERR_KEY_RANGE = -2
 PS_ERR_WORKSPACE = -3
 PS_ERR_DEVICE = -4
 PS_ERR_UNSUPPORTED = -5
+PS_ERR_NOT_RESIDENT = -6
 
 PS_OP_PULL, PS_OP_PUSH, PS_OP_DEDUP = 0, 1, 2
 PS_OP_STEP_MF, PS_OP_STEP_KGE, PS_OP_STEP_SGNS, PS_OP_STEP_CTR = 3, 4, 5, 6
 
 PS_KERNEL_SEGREDUCE, PS_KERNEL_TASKGRAD, PS_KERNEL_SCATTER, PS_KERNEL_PULL, PS_KERNEL_MF_ROWMERGE = 0, 1, 2, 3, 4
 PS_TIMING_ALL = -1
+
+STAGE_STATS = ["clock", "rounds", "forced", "staged", "evicted", "resident", "pending", "stalled"]
 
 _p, _i64, _i32, _f32, _sz = C.c_void_p, C.c_int64, C.c_int32, C.c_float, C.c_size_t
 
@@ -47,6 +50,18 @@ SIGNATURES = {
     "ps_last_error_message": (C.c_char_p, []),
     "ps_set_timing": (_i32, [_p, _i32]),
     "ps_read_timing": (_i32, [_p, _i32, C.POINTER(C.c_double), C.POINTER(_i64)]),
+    "ps_create_staged": (_i32, [C.POINTER(_p), _i64, _i32, _p, _p, _i64, _p, _p, _i64, _p, _i32, _p, _p, _f32, _f32,
+                                _p]),
+    "ps_set_action_timing": (_i32, [_p, C.c_double, C.c_double, C.c_double]),
+    "ps_intent": (_i32, [_p, _p, _i64, _i64, _i64]),
+    "ps_advance_clock": (_i32, [_p, _p]),
+    "ps_stage_round": (_i32, [_p, _i32]),
+    "ps_stage_auto": (_i32, [_p, _i32]),
+    "ps_stage_flush": (_i32, [_p, _p]),
+    "ps_stage_stats": (_i32, [_p, _p, _i32, C.POINTER(C.c_double)]),
+    "ps_stage_resident": (_i32, [_p, _p, _i64, C.POINTER(_i64)]),
+    "ps_action_timing": (_i32, [C.c_double, _i64, _i64, C.c_double, C.c_double, C.POINTER(C.c_double),
+                                C.POINTER(_i64)]),
 }
 
 

@@ -2,17 +2,22 @@
 // the launch sequence of each call.  See include/adapm.h for the contract.
 #include "adapm.h"
 
+#include <atomic>
+#include <chrono>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
 #include <initializer_list>
+#include <mutex>
 #include <string>
+#include <thread>
 #include <utility>
 #include <vector>
 
 #include "common.hpp"
 #include "push.hpp"
 #include "sort.hpp"
+#include "staging.hpp"
 #include "tasks.hpp"
 
 using namespace adapm;
@@ -47,6 +52,35 @@ constexpr size_t MAX_TIMED_LAUNCHES = 1 << 14;
 }  // namespace
 
 // ======================================================================== store
+// Staging state of a store whose slot table caches rows of a home table in
+// pinned host memory.
+struct Staging {
+  static constexpr int RING = 256;   // round events kept
+  Planner plan;
+  std::mutex mu;                     // planner and enqueue order
+  int64_t num_keys = 0;              // keys of the home table
+  int64_t total_slots = 0;
+  const float* hW = nullptr;         // device addresses of the home tables
+  const float* hG = nullptr;
+  int64_t hld = 0;
+  int32_t* map = nullptr;            // device: key -> slot (caller-owned)
+  hipStream_t st = nullptr;          // the staging stream
+  hipEvent_t clock_ev = nullptr;     // worker stream at its last clock advance
+  hipEvent_t flush_ev = nullptr;
+  std::vector<hipEvent_t> round_ev;
+  int64_t round_id = 0;              // rounds (and forced actions) enqueued so far
+  int64_t rounds = 0;                // of which regular rounds
+  int64_t waited = -1;               // latest round the worker stream waits for
+  int64_t* d_keys = nullptr;         // device move lists [2 * total_slots]
+  int64_t* d_slots = nullptr;
+  int64_t* h_list[2] = {nullptr, nullptr};   // pinned: keys then slots, [4 * total_slots]
+  hipEvent_t list_ev[2] = {nullptr, nullptr};
+  int list_i = 0;
+  std::thread auto_thread;
+  std::atomic<bool> auto_on{false};
+  std::atomic<int32_t> auto_status{0};
+};
+
 struct ps_store {
   int64_t num_keys;
   int64_t ld;        // row stride (floats) of W
@@ -65,6 +99,7 @@ struct ps_store {
   hipEvent_t join_ev = nullptr;
   std::vector<std::pair<hipEvent_t, hipEvent_t>> events[NUM_TIMED];
   size_t used[NUM_TIMED] = {};
+  Staging* stg = nullptr;   // set for stores over a slot table (ps_create_staged)
 };
 
 namespace {
@@ -233,6 +268,7 @@ struct Plan {
   uint8_t* ok = nullptr;       // per-unit validity
   MFEntry* pe = nullptr;       // MF: entry data at the sorted position of its row occurrence
   double* loss_part = nullptr;
+  char* trans = nullptr;        // a staged store's ids in slot space (8 bytes per occurrence)
   size_t bytes = 0;
 };
 
@@ -281,6 +317,7 @@ bool plan_op(void* ws, int64_t num_keys, int dim, int op, int64_t units, int64_t
     default:
       return false;
   }
+  if (op != PS_OP_DEDUP) p->trans = c.take<char>(size_t(n) * 8);
   p->bytes = c.off + 256;
   return true;
 }
@@ -578,6 +615,171 @@ ps_status make_store(ps_store** out, int64_t num_keys, int32_t dim, int64_t row_
   return PS_OK;
 }
 
+// ------------------------------------------------------------------ staged stores
+// A staged store's step translates the batch's ids into slot ids first, into
+// the workspace region Plan::trans.
+
+// The first slot of the key range that starts at key_off (a key offset of a
+// step must start a range, so that slot ids keep the step's id split).
+ps_status slot_offset(const ps_store* s, int64_t key_off, const char* what, int64_t* out) {
+  const int r = s->stg->plan.range_starting_at(key_off);
+  if (r < 0)
+    return fail(PS_ERR_INVALID, "%s %lld does not start a key range of the staged store", what, (long long)key_off);
+  *out = s->stg->plan.range_slot0[r];
+  return PS_OK;
+}
+
+ps_status translate_ids(ps_store* s, const int32_t* in, int64_t n, int64_t key_off, int64_t slot_off, int32_t* out,
+                        hipStream_t st) {
+  if (n <= 0 || !in) return PS_OK;
+  hipLaunchKernelGGL(k_translate_ids, dim3(small_grid(n, BLOCK, 4096)), dim3(BLOCK), 0, st, in, n, s->stg->map,
+                     key_off, s->stg->num_keys - key_off, slot_off, out, s->status);
+  LAUNCHED(k_translate_ids);
+  return PS_OK;
+}
+
+ps_status translate_keys(ps_store* s, const int64_t* in, int64_t n, int64_t* out, hipStream_t st) {
+  if (n <= 0 || !in) return PS_OK;
+  hipLaunchKernelGGL(k_translate_keys, dim3(small_grid(n, BLOCK, 4096)), dim3(BLOCK), 0, st, in, n, s->stg->map,
+                     s->stg->num_keys, out, s->status);
+  LAUNCHED(k_translate_keys);
+  return PS_OK;
+}
+
+// Rows between the home tables and the slot table: `from` indexes the
+// source, `to` the destination (both device lists of n entries).
+ps_status move_rows(ps_store* s, bool to_home, const int64_t* from, const int64_t* to, int64_t n, hipStream_t st) {
+  Staging& g = *s->stg;
+  RowShape shape;
+  row_shape(s->dim, true, &shape);
+  return with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
+    const int64_t grid = small_grid(n, BLOCK / L, 16384);
+    if (to_home)
+      hipLaunchKernelGGL((k_move_rows<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->G, s->ld, from,
+                         const_cast<float*>(g.hW), const_cast<float*>(g.hG), g.hld, to, n, s->dim);
+    else
+      hipLaunchKernelGGL((k_move_rows<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, g.hW, g.hG, g.hld, from, s->W, s->G,
+                         s->ld, to, n, s->dim);
+    LAUNCHED(k_move_rows);
+    return PS_OK;
+  });
+}
+
+// Copies the planner's moves to the device and enqueues them on the staging
+// stream: write-backs (slot -> home, map entry cleared) before stage-ins
+// (home -> slot, map entry set), so a slot freed in this round can be
+// reused by it.
+ps_status enqueue_moves(ps_store* s, const std::vector<int64_t>& out_k, const std::vector<int64_t>& out_s,
+                        const std::vector<int64_t>& in_k, const std::vector<int64_t>& in_s) {
+  Staging& g = *s->stg;
+  const int64_t nout = (int64_t)out_k.size(), nin = (int64_t)in_k.size();
+  if (nout + nin == 0) return PS_OK;
+  const int b = g.list_i;
+  g.list_i ^= 1;
+  HIP_TRY(hipEventSynchronize(g.list_ev[b]));   // its previous copy has been read
+  int64_t* hk = g.h_list[b];
+  int64_t* hs = hk + 2 * g.total_slots;
+  std::copy(out_k.begin(), out_k.end(), hk);
+  std::copy(in_k.begin(), in_k.end(), hk + nout);
+  std::copy(out_s.begin(), out_s.end(), hs);
+  std::copy(in_s.begin(), in_s.end(), hs + nout);
+  HIP_TRY(hipMemcpyAsync(g.d_keys, hk, size_t(nout + nin) * 8, hipMemcpyHostToDevice, g.st));
+  HIP_TRY(hipMemcpyAsync(g.d_slots, hs, size_t(nout + nin) * 8, hipMemcpyHostToDevice, g.st));
+  HIP_TRY(hipEventRecord(g.list_ev[b], g.st));
+  if (nout) {
+    if (ps_status r = move_rows(s, true, g.d_slots, g.d_keys, nout, g.st)) return r;
+    hipLaunchKernelGGL(k_map_set, dim3(small_grid(nout, BLOCK, 4096)), dim3(BLOCK), 0, g.st, g.map, g.d_keys,
+                       (const int64_t*)nullptr, nout);
+    LAUNCHED(k_map_set);
+  }
+  if (nin) {
+    if (ps_status r = move_rows(s, false, g.d_keys + nout, g.d_slots + nout, nin, g.st)) return r;
+    hipLaunchKernelGGL(k_map_set, dim3(small_grid(nin, BLOCK, 4096)), dim3(BLOCK), 0, g.st, g.map, g.d_keys + nout,
+                       g.d_slots + nout, nin);
+    LAUNCHED(k_map_set);
+  }
+  return PS_OK;
+}
+
+// One round (forced: act only on intents already active, no rate update),
+// with the planner lock held.  The staging stream first waits for the
+// worker's steps before its last clock advance, so a write-back never races
+// a step that still uses the row.
+ps_status stage_round_locked(ps_store* s, bool forced, int64_t* rid_out, int64_t* moved) {
+  Staging& g = *s->stg;
+  Planner& P = g.plan;
+  P.clear_moves();
+  const int64_t rid = g.round_id;
+  const int64_t horizon = forced ? P.clock + 1 : P.timing.horizon(P.clock);
+  P.evict_expired();
+  P.act(horizon, rid);
+  if (forced) ++P.forced_total;
+  else ++g.rounds;
+  HIP_TRY(hipStreamWaitEvent(g.st, g.clock_ev, 0));
+  if (ps_status r = enqueue_moves(s, P.out_keys, P.out_slots, P.in_keys, P.in_slots)) return r;
+  HIP_TRY(hipEventRecord(g.round_ev[rid % Staging::RING], g.st));
+  g.round_id = rid + 1;
+  if (rid_out) *rid_out = rid;
+  if (moved) *moved = (int64_t)(P.out_keys.size() + P.in_keys.size());
+  return PS_OK;
+}
+
+// Rounds back to back on a thread of the library: each lasts until its
+// moves are done, an idle one 100 us.
+void auto_rounds(ps_store* s) {
+  Staging& g = *s->stg;
+  while (g.auto_on.load()) {
+    hipEvent_t ev = nullptr;
+    int64_t moved = 0;
+    {
+      std::lock_guard<std::mutex> lk(g.mu);
+      int64_t rid = 0;
+      ps_status r = stage_round_locked(s, false, &rid, &moved);
+      if (r != PS_OK) {
+        g.auto_status.store(r);
+        g.auto_on.store(false);
+        return;
+      }
+      ev = g.round_ev[rid % Staging::RING];
+    }
+    if (hipEventSynchronize(ev) != hipSuccess) {
+      g.auto_status.store(PS_ERR_DEVICE);
+      g.auto_on.store(false);
+      return;
+    }
+    if (moved == 0) std::this_thread::sleep_for(std::chrono::microseconds(100));
+  }
+}
+
+void stop_auto(Staging& g) {
+  g.auto_on.store(false);
+  if (g.auto_thread.joinable()) g.auto_thread.join();
+}
+
+void free_staging(Staging* g) {
+  if (!g) return;
+  stop_auto(*g);
+  if (g->st) (void)hipStreamSynchronize(g->st);
+  for (hipEvent_t e : g->round_ev)
+    if (e) (void)hipEventDestroy(e);
+  for (int i = 0; i < 2; ++i) {
+    if (g->list_ev[i]) (void)hipEventDestroy(g->list_ev[i]);
+    if (g->h_list[i]) (void)hipHostFree(g->h_list[i]);
+  }
+  if (g->clock_ev) (void)hipEventDestroy(g->clock_ev);
+  if (g->flush_ev) (void)hipEventDestroy(g->flush_ev);
+  if (g->d_keys) (void)hipFree(g->d_keys);
+  if (g->d_slots) (void)hipFree(g->d_slots);
+  if (g->st) (void)hipStreamDestroy(g->st);
+  delete g;
+}
+
+ps_status check_staged(ps_store* s) {
+  if (ps_status st = check_store(s)) return st;
+  if (!s->stg) return fail(PS_ERR_INVALID, "not a staged store (ps_create_staged)");
+  return PS_OK;
+}
+
 }  // namespace
 
 // ======================================================================== C ABI
@@ -591,6 +793,7 @@ const char* ps_status_string(ps_status st) {
     case PS_ERR_WORKSPACE: return "workspace too small";
     case PS_ERR_DEVICE: return "HIP runtime error";
     case PS_ERR_UNSUPPORTED: return "unsupported size";
+    case PS_ERR_NOT_RESIDENT: return "key not resident in the staged store";
     default: return "unknown status";
   }
 }
@@ -646,6 +849,8 @@ ps_status ps_create_rowwise(ps_store** out, int64_t num_keys, int32_t dim, int64
 
 ps_status ps_destroy(ps_store* s) {
   if (!s) return PS_OK;
+  free_staging(s->stg);
+  s->stg = nullptr;
   hipError_t e = hipDeviceSynchronize();
   for (auto& v : s->events)
     for (auto& pr : v) {
@@ -684,14 +889,14 @@ ps_status ps_pull(ps_store* s, const int64_t* keys, int64_t n, float* out, void*
     if (grid > 65536) grid = 65536;
     Timed t(s, PS_KERNEL_PULL, st);
     hipLaunchKernelGGL((k_pull<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->ld, s->num_keys, s->dim, keys, n,
-                       out, s->status);
+                       out, s->status, s->stg ? s->stg->map : nullptr, s->stg ? s->stg->num_keys : int64_t(0));
     LAUNCHED(k_pull);
     return PS_OK;
   });
 }
 
-ps_status ps_push(ps_store* s, const int64_t* keys, int64_t n, const float* grads, void* ws, size_t ws_bytes,
-                  void* stream) {
+static ps_status push_impl(ps_store* s, const int64_t* keys, int64_t n, const float* grads, void* ws, size_t ws_bytes,
+                           void* stream) {
   if (ps_status st = check_store(s)) return st;
   if (ps_status st = check_n(n, 1)) return st;
   if (n == 0) return PS_OK;
@@ -734,8 +939,8 @@ ps_status ps_dedup(int64_t num_keys, const int64_t* keys, int64_t n, int64_t* un
   return PS_OK;
 }
 
-ps_status ps_step_mf(ps_store* s, const int32_t* row, const int32_t* col, const float* val, int64_t B,
-                     int64_t col_key_offset, float lambda, double* loss, void* ws, size_t ws_bytes, void* stream) {
+static ps_status step_mf_impl(ps_store* s, const int32_t* row, const int32_t* col, const float* val, int64_t B,
+                              int64_t col_key_offset, float lambda, double* loss, void* ws, size_t ws_bytes, void* stream) {
   if (ps_status st = check_store(s)) return st;
   if (ps_status st = check_n(B, 2)) return st;
   hipStream_t st = as_stream(stream);
@@ -752,6 +957,7 @@ ps_status ps_step_mf(ps_store* s, const int32_t* row, const int32_t* col, const 
 ps_status ps_step_mf_prepare(ps_store* s, const int32_t* row, const int32_t* col, const float* val, int64_t B,
                              int64_t col_key_offset, void* ws, size_t ws_bytes, void* stream) {
   if (ps_status st = check_store(s)) return st;
+  if (s->stg) return fail(PS_ERR_UNSUPPORTED, "the two-phase MF step is not available on a staged store");
   if (ps_status st = check_n(B, 2)) return st;
   if (B == 0) return PS_OK;
   if (!row || !col || !val) return fail(PS_ERR_INVALID, "row, col or val is NULL");
@@ -765,6 +971,7 @@ ps_status ps_step_mf_prepare(ps_store* s, const int32_t* row, const int32_t* col
 ps_status ps_step_mf_apply(ps_store* s, int64_t B, float lambda, double* loss, void* ws, size_t ws_bytes,
                            void* stream, void* rows_done) {
   if (ps_status st = check_store(s)) return st;
+  if (s->stg) return fail(PS_ERR_UNSUPPORTED, "the two-phase MF step is not available on a staged store");
   if (ps_status st = check_n(B, 2)) return st;
   hipStream_t st = as_stream(stream);
   if (B == 0) return zero_loss(loss, st);
@@ -774,9 +981,9 @@ ps_status ps_step_mf_apply(ps_store* s, int64_t B, float lambda, double* loss, v
   return mf_apply(s, B, lambda, loss, p, st, static_cast<hipEvent_t>(rows_done));
 }
 
-ps_status ps_step_kge(ps_store* s, const int32_t* head, const int32_t* rel, const int32_t* tail, const int32_t* neg,
-                      int64_t B, int32_t n_neg, int32_t n_head_neg, int64_t rel_key_offset, double* loss, void* ws,
-                      size_t ws_bytes, void* stream) {
+static ps_status step_kge_impl(ps_store* s, const int32_t* head, const int32_t* rel, const int32_t* tail, const int32_t* neg,
+                               int64_t B, int32_t n_neg, int32_t n_head_neg, int64_t rel_key_offset, double* loss, void* ws,
+                               size_t ws_bytes, void* stream) {
   if (ps_status st = check_store(s)) return st;
   if (n_neg < 0 || n_head_neg < 0 || n_head_neg > n_neg)
     return fail(PS_ERR_INVALID, "need 0 <= n_head_neg <= n_neg");
@@ -829,9 +1036,9 @@ ps_status ps_step_kge(ps_store* s, const int32_t* head, const int32_t* rel, cons
   return run_reduce(s, p.sb, ks, SrcKGE{perm, p.mat, p.base, p.coef, per, n_head_neg, s->dim}, n, {PART_ALL}, st);
 }
 
-ps_status ps_step_sgns(ps_store* s, const int32_t* centre, const int32_t* ctx, const int32_t* neg, int64_t B,
-                       int32_t window, int32_t n_neg, int64_t out_key_offset, double* loss, void* ws,
-                       size_t ws_bytes, void* stream) {
+static ps_status step_sgns_impl(ps_store* s, const int32_t* centre, const int32_t* ctx, const int32_t* neg, int64_t B,
+                                int32_t window, int32_t n_neg, int64_t out_key_offset, double* loss, void* ws,
+                                size_t ws_bytes, void* stream) {
   if (ps_status st = check_store(s)) return st;
   if (window < 0 || n_neg < 0) return fail(PS_ERR_INVALID, "negative window or n_neg");
   const int slots = 2 * window;
@@ -888,8 +1095,8 @@ ps_status ps_step_sgns(ps_store* s, const int32_t* centre, const int32_t* ctx, c
   return run_reduce(s, p.sb, ks, src, n, {PART_UPPER, PART_LOWER}, st);
 }
 
-ps_status ps_step_ctr(ps_store* s, const int64_t* keys, const float* label, int64_t B, int32_t F, double* loss,
-                      void* ws, size_t ws_bytes, void* stream) {
+static ps_status step_ctr_impl(ps_store* s, const int64_t* keys, const float* label, int64_t B, int32_t F, double* loss,
+                               void* ws, size_t ws_bytes, void* stream) {
   if (ps_status st = check_store(s)) return st;
   if (F < 1) return fail(PS_ERR_INVALID, "need F >= 1");
   if (ps_status st = check_n(B, F)) return st;
@@ -934,15 +1141,342 @@ ps_status ps_step_ctr(ps_store* s, const int64_t* keys, const float* label, int6
   return run_reduce(s, p.sb, ks, SrcSorted{p.grads, s->dim}, n, {PART_ALL}, st);
 }
 
+// ---------------------------------------------------------------- public steps
+// A staged store translates the call's ids into slot ids (the plan's
+// translation region of the workspace) and runs the same step on its slot
+// table.
+ps_status ps_push(ps_store* s, const int64_t* keys, int64_t n, const float* grads, void* ws, size_t ws_bytes,
+                  void* stream) {
+  if (ps_status st = check_store(s)) return st;
+  if (!s->stg || n <= 0 || !keys) return push_impl(s, keys, n, grads, ws, ws_bytes, stream);
+  if (ps_status st = check_n(n, 1)) return st;
+  Plan p;
+  plan_op(ws, s->num_keys, s->dim, PS_OP_PUSH, n, 1, &p);
+  if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
+  char* t = p.trans;
+  int64_t* tk = reinterpret_cast<int64_t*>(t);
+  if (ps_status r = translate_keys(s, keys, n, tk, as_stream(stream))) return r;
+  return push_impl(s, tk, n, grads, ws, ws_bytes, stream);
+}
+
+ps_status ps_step_mf(ps_store* s, const int32_t* row, const int32_t* col, const float* val, int64_t B,
+                     int64_t col_key_offset, float lambda, double* loss, void* ws, size_t ws_bytes, void* stream) {
+  if (ps_status st = check_store(s)) return st;
+  if (!s->stg || B <= 0 || !row || !col || col_key_offset < 0)
+    return step_mf_impl(s, row, col, val, B, col_key_offset, lambda, loss, ws, ws_bytes, stream);
+  if (ps_status st = check_n(B, 2)) return st;
+  int64_t off;
+  if (ps_status r = slot_offset(s, col_key_offset, "col_key_offset", &off)) return r;
+  Plan p;
+  plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_MF, B, 2, &p);
+  if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
+  char* t = p.trans;
+  int32_t* tr = reinterpret_cast<int32_t*>(t);
+  int32_t* tc = tr + B;
+  hipStream_t st = as_stream(stream);
+  if (ps_status r = translate_ids(s, row, B, 0, 0, tr, st)) return r;
+  if (ps_status r = translate_ids(s, col, B, col_key_offset, off, tc, st)) return r;
+  return step_mf_impl(s, tr, tc, val, B, off, lambda, loss, ws, ws_bytes, stream);
+}
+
+ps_status ps_step_kge(ps_store* s, const int32_t* head, const int32_t* rel, const int32_t* tail, const int32_t* neg,
+                      int64_t B, int32_t n_neg, int32_t n_head_neg, int64_t rel_key_offset, double* loss, void* ws,
+                      size_t ws_bytes, void* stream) {
+  if (ps_status st = check_store(s)) return st;
+  if (!s->stg || B <= 0 || !head || !rel || !tail || (n_neg > 0 && !neg) || n_neg < 0 || rel_key_offset < 0)
+    return step_kge_impl(s, head, rel, tail, neg, B, n_neg, n_head_neg, rel_key_offset, loss, ws, ws_bytes, stream);
+  if (ps_status st = check_n(B, 3 + (int64_t)n_neg)) return st;
+  int64_t off;
+  if (ps_status r = slot_offset(s, rel_key_offset, "rel_key_offset", &off)) return r;
+  const int64_t per = 3 + (int64_t)n_neg;
+  Plan p;
+  plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_KGE, B, per, &p);
+  if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
+  char* t = p.trans;
+  int32_t* th = reinterpret_cast<int32_t*>(t);
+  int32_t* tt = th + B;
+  int32_t* trl = tt + B;
+  int32_t* tn = trl + B;
+  hipStream_t st = as_stream(stream);
+  if (ps_status r = translate_ids(s, head, B, 0, 0, th, st)) return r;
+  if (ps_status r = translate_ids(s, tail, B, 0, 0, tt, st)) return r;
+  if (ps_status r = translate_ids(s, rel, B, rel_key_offset, off, trl, st)) return r;
+  if (ps_status r = translate_ids(s, neg, B * n_neg, 0, 0, tn, st)) return r;
+  return step_kge_impl(s, th, trl, tt, n_neg > 0 ? tn : neg, B, n_neg, n_head_neg, off, loss, ws, ws_bytes, stream);
+}
+
+ps_status ps_step_sgns(ps_store* s, const int32_t* centre, const int32_t* ctx, const int32_t* neg, int64_t B,
+                       int32_t window, int32_t n_neg, int64_t out_key_offset, double* loss, void* ws,
+                       size_t ws_bytes, void* stream) {
+  if (ps_status st = check_store(s)) return st;
+  const int64_t slots = 2 * (int64_t)window;
+  if (!s->stg || B <= 0 || !centre || window < 0 || n_neg < 0 || (slots > 0 && !ctx) ||
+      (slots > 0 && n_neg > 0 && !neg))
+    return step_sgns_impl(s, centre, ctx, neg, B, window, n_neg, out_key_offset, loss, ws, ws_bytes, stream);
+  const int64_t per = 1 + slots * (1 + (int64_t)n_neg);
+  if (ps_status st = check_n(B, per)) return st;
+  int64_t off;
+  if (ps_status r = slot_offset(s, out_key_offset, "out_key_offset", &off)) return r;
+  Plan p;
+  plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_SGNS, B, per, &p);
+  if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
+  char* t = p.trans;
+  int32_t* tce = reinterpret_cast<int32_t*>(t);
+  int32_t* tcx = tce + B;
+  int32_t* tn = tcx + B * slots;
+  hipStream_t st = as_stream(stream);
+  if (ps_status r = translate_ids(s, centre, B, 0, 0, tce, st)) return r;
+  if (ps_status r = translate_ids(s, ctx, B * slots, out_key_offset, off, tcx, st)) return r;
+  if (ps_status r = translate_ids(s, neg, B * slots * n_neg, out_key_offset, off, tn, st)) return r;
+  return step_sgns_impl(s, tce, slots > 0 ? tcx : ctx, (slots > 0 && n_neg > 0) ? tn : neg, B, window, n_neg, off,
+                        loss, ws, ws_bytes, stream);
+}
+
+ps_status ps_step_ctr(ps_store* s, const int64_t* keys, const float* label, int64_t B, int32_t F, double* loss,
+                      void* ws, size_t ws_bytes, void* stream) {
+  if (ps_status st = check_store(s)) return st;
+  if (!s->stg || B <= 0 || F < 1 || !keys) return step_ctr_impl(s, keys, label, B, F, loss, ws, ws_bytes, stream);
+  if (ps_status st = check_n(B, F)) return st;
+  Plan p;
+  plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_CTR, B, F, &p);
+  if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
+  char* t = p.trans;
+  int64_t* tk = reinterpret_cast<int64_t*>(t);
+  if (ps_status r = translate_keys(s, keys, B * F, tk, as_stream(stream))) return r;
+  return step_ctr_impl(s, tk, label, B, F, loss, ws, ws_bytes, stream);
+}
+
+// ---------------------------------------------------------------- staged stores
+ps_status ps_create_staged(ps_store** out, int64_t num_keys, int32_t dim, float* home_values, float* home_accum,
+                           int64_t home_stride, float* values, float* accum, int64_t row_stride, int32_t* key_slot,
+                           int32_t num_ranges, const int64_t* range_begin, const int64_t* range_slots, float lr,
+                           float eps, void* stream) {
+  if (!out) return fail(PS_ERR_INVALID, "out is NULL");
+  *out = nullptr;
+  if (num_keys < 1 || num_keys > INT32_MAX) return fail(PS_ERR_INVALID, "num_keys %lld outside [1, 2^31-1]", (long long)num_keys);
+  if (!home_values || !home_accum || !key_slot) return fail(PS_ERR_INVALID, "home table or key_slot is NULL");
+  if (num_ranges < 1 || !range_begin || !range_slots) return fail(PS_ERR_INVALID, "need at least one key range");
+  if (range_begin[0] != 0) return fail(PS_ERR_INVALID, "the first key range must begin at key 0");
+  int64_t total = 0;
+  for (int r = 0; r < num_ranges; ++r) {
+    if (r > 0 && range_begin[r] <= range_begin[r - 1]) return fail(PS_ERR_INVALID, "key ranges must ascend");
+    if (range_begin[r] >= num_keys) return fail(PS_ERR_INVALID, "key range %d begins past num_keys", r);
+    const int64_t len = (r + 1 < num_ranges ? range_begin[r + 1] : num_keys) - range_begin[r];
+    if (range_slots[r] < 1 || range_slots[r] > len)
+      return fail(PS_ERR_INVALID, "key range %d needs between 1 and %lld slots", r, (long long)len);
+    total += range_slots[r];
+  }
+  if (total > INT32_MAX) return fail(PS_ERR_INVALID, "more than 2^31-1 slots");
+  if (home_stride < dim) return fail(PS_ERR_INVALID, "home_stride %lld < dim %d", (long long)home_stride, dim);
+  {
+    const int64_t d = (int64_t)(home_accum - home_values);
+    const int64_t ad = d < 0 ? -d : d;
+    const bool separate = ad >= num_keys * home_stride;
+    const int64_t r = ((d % home_stride) + home_stride) % home_stride;
+    const bool interleaved = home_stride >= 2 * (int64_t)dim && r >= dim && r <= home_stride - dim;
+    if (!separate && !interleaved) return fail(PS_ERR_INVALID, "home value and accumulator rows overlap");
+  }
+  if (dim % 4 == 0 && (!aligned16(home_values) || !aligned16(home_accum) || home_stride % 4 != 0))
+    return fail(PS_ERR_INVALID, "home tables must be 16-byte aligned with a stride that is a multiple of 4");
+  void* hw = nullptr;
+  void* hg = nullptr;
+  if (hipHostGetDevicePointer(&hw, home_values, 0) != hipSuccess ||
+      hipHostGetDevicePointer(&hg, home_accum, 0) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(PS_ERR_INVALID, "home tables must be pinned host memory (hipHostMalloc)");
+  }
+  ps_store* s = nullptr;
+  if (ps_status r = ps_create_strided(&s, total, dim, row_stride, values, accum, lr, eps, stream)) return r;
+  Staging* g = new Staging();
+  s->stg = g;
+  g->num_keys = num_keys;
+  g->total_slots = total;
+  g->hW = static_cast<const float*>(hw);
+  g->hG = static_cast<const float*>(hg);
+  g->hld = home_stride;
+  g->map = key_slot;
+  g->plan.init(num_keys, range_begin, range_slots, num_ranges);
+  hipError_t e = hipStreamCreateWithFlags(&g->st, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&g->clock_ev, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&g->flush_ev, hipEventDisableTiming);
+  g->round_ev.assign(Staging::RING, nullptr);
+  for (int i = 0; i < Staging::RING && e == hipSuccess; ++i)
+    e = hipEventCreateWithFlags(&g->round_ev[i], hipEventDisableTiming);
+  for (int i = 0; i < 2 && e == hipSuccess; ++i) {
+    e = hipEventCreateWithFlags(&g->list_ev[i], hipEventDisableTiming);
+    if (e == hipSuccess) e = hipHostMalloc(reinterpret_cast<void**>(&g->h_list[i]), size_t(4) * total * 8);
+  }
+  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&g->d_keys), size_t(2) * total * 8);
+  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&g->d_slots), size_t(2) * total * 8);
+  if (e == hipSuccess) {
+    hipStream_t st = as_stream(stream);
+    hipLaunchKernelGGL(k_map_fill, dim3(small_grid(num_keys, BLOCK, 4096)), dim3(BLOCK), 0, st, key_slot, num_keys);
+    e = hipGetLastError();
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+  }
+  if (e != hipSuccess) {
+    (void)ps_destroy(s);
+    return fail(PS_ERR_DEVICE, "staged store set-up: %s", hipGetErrorString(e));
+  }
+  *out = s;
+  return PS_OK;
+}
+
+ps_status ps_set_action_timing(ps_store* s, double alpha, double p, double lambda0) {
+  if (ps_status st = check_staged(s)) return st;
+  if (!(alpha > 0.0 && alpha <= 1.0) || !(p > 0.0 && p < 1.0) || !(lambda0 >= 0.0))
+    return fail(PS_ERR_INVALID, "need 0 < alpha <= 1, 0 < p < 1 and lambda0 >= 0");
+  std::lock_guard<std::mutex> lk(s->stg->mu);
+  ActionTiming& t = s->stg->plan.timing;
+  t.alpha = alpha;
+  t.p = p;
+  t.lambda = lambda0;
+  return PS_OK;
+}
+
+ps_status ps_intent(ps_store* s, const int64_t* keys, int64_t n, int64_t c_start, int64_t c_end) {
+  if (ps_status st = check_staged(s)) return st;
+  if (n < 0 || (n > 0 && !keys)) return fail(PS_ERR_INVALID, "keys is NULL or n < 0");
+  if (c_end <= c_start) return fail(PS_ERR_INVALID, "need c_start < c_end");
+  std::lock_guard<std::mutex> lk(s->stg->mu);
+  s->stg->plan.signal(keys, n, c_start, c_end);
+  return PS_OK;
+}
+
+ps_status ps_advance_clock(ps_store* s, void* stream) {
+  if (ps_status st = check_staged(s)) return st;
+  Staging& g = *s->stg;
+  std::lock_guard<std::mutex> lk(g.mu);
+  hipStream_t st = as_stream(stream);
+  g.plan.clock += 1;
+  HIP_TRY(hipEventRecord(g.clock_ev, st));
+  if (g.plan.due(g.plan.clock))
+    if (ps_status r = stage_round_locked(s, true, nullptr, nullptr)) return r;
+  const int64_t r = g.plan.take_round_for(g.plan.clock);
+  if (r > g.waited) {
+    HIP_TRY(hipStreamWaitEvent(st, g.round_ev[r % Staging::RING], 0));
+    g.waited = r;
+  }
+  return PS_OK;
+}
+
+ps_status ps_stage_round(ps_store* s, int32_t wait) {
+  if (ps_status st = check_staged(s)) return st;
+  Staging& g = *s->stg;
+  if (g.auto_on.load()) return fail(PS_ERR_INVALID, "rounds are running on the library's thread");
+  int64_t rid = 0;
+  {
+    std::lock_guard<std::mutex> lk(g.mu);
+    if (ps_status r = stage_round_locked(s, false, &rid, nullptr)) return r;
+  }
+  if (wait) HIP_TRY(hipEventSynchronize(g.round_ev[rid % Staging::RING]));
+  return PS_OK;
+}
+
+ps_status ps_stage_auto(ps_store* s, int32_t on) {
+  if (ps_status st = check_staged(s)) return st;
+  Staging& g = *s->stg;
+  if (!on) {
+    stop_auto(g);
+    const int32_t r = g.auto_status.exchange(0);
+    return r ? fail(r, "a round on the library's thread failed") : PS_OK;
+  }
+  if (g.auto_on.load()) return PS_OK;
+  if (g.auto_thread.joinable()) g.auto_thread.join();
+  g.auto_on.store(true);
+  g.auto_thread = std::thread(auto_rounds, s);
+  return PS_OK;
+}
+
+ps_status ps_stage_flush(ps_store* s, void* stream) {
+  if (ps_status st = check_staged(s)) return st;
+  Staging& g = *s->stg;
+  std::lock_guard<std::mutex> lk(g.mu);
+  HIP_TRY(hipEventRecord(g.flush_ev, as_stream(stream)));
+  HIP_TRY(hipStreamWaitEvent(g.st, g.flush_ev, 0));
+  std::vector<int64_t> keys, slots, none;
+  const Planner& P = g.plan;
+  for (int64_t k = 0; k < g.num_keys; ++k)
+    if (P.slot[k] >= 0) {
+      keys.push_back(k);
+      slots.push_back(P.slot[k]);
+    }
+  // every resident row is written back; it stays resident
+  if (!keys.empty()) {
+    const int b = g.list_i;
+    g.list_i ^= 1;
+    HIP_TRY(hipEventSynchronize(g.list_ev[b]));
+    int64_t* hk = g.h_list[b];
+    int64_t* hs = hk + 2 * g.total_slots;
+    std::copy(keys.begin(), keys.end(), hk);
+    std::copy(slots.begin(), slots.end(), hs);
+    const int64_t n = (int64_t)keys.size();
+    HIP_TRY(hipMemcpyAsync(g.d_keys, hk, size_t(n) * 8, hipMemcpyHostToDevice, g.st));
+    HIP_TRY(hipMemcpyAsync(g.d_slots, hs, size_t(n) * 8, hipMemcpyHostToDevice, g.st));
+    HIP_TRY(hipEventRecord(g.list_ev[b], g.st));
+    if (ps_status r = move_rows(s, true, g.d_slots, g.d_keys, n, g.st)) return r;
+  }
+  HIP_TRY(hipStreamSynchronize(g.st));
+  return PS_OK;
+}
+
+ps_status ps_stage_stats(ps_store* s, int64_t* counts, int32_t n, double* lambda) {
+  if (ps_status st = check_staged(s)) return st;
+  if (n < 0 || (n > 0 && !counts)) return fail(PS_ERR_INVALID, "counts is NULL");
+  Staging& g = *s->stg;
+  std::lock_guard<std::mutex> lk(g.mu);
+  const Planner& P = g.plan;
+  int64_t resident = g.total_slots;
+  for (const auto& f : P.free_slots) resident -= (int64_t)f.size();
+  int64_t pending = 0;
+  for (const auto& kv : P.pending) pending += (int64_t)(kv.second.keys.size() - kv.second.next);
+  const int64_t v[PS_STAGE_NUM_STATS] = {P.clock, g.rounds, P.forced_total, P.staged_total, P.evicted_total,
+                                         resident, pending, P.stalled_total};
+  for (int i = 0; i < n && i < PS_STAGE_NUM_STATS; ++i) counts[i] = v[i];
+  if (lambda) *lambda = P.timing.lambda;
+  return PS_OK;
+}
+
+ps_status ps_stage_resident(ps_store* s, int64_t* keys, int64_t capacity, int64_t* count) {
+  if (ps_status st = check_staged(s)) return st;
+  if (!count || capacity < 0 || (capacity > 0 && !keys)) return fail(PS_ERR_INVALID, "bad output arguments");
+  Staging& g = *s->stg;
+  std::lock_guard<std::mutex> lk(g.mu);
+  int64_t c = 0;
+  for (int64_t k = 0; k < g.num_keys; ++k)
+    if (g.plan.slot[k] >= 0) {
+      if (c < capacity) keys[c] = k;
+      ++c;
+    }
+  *count = c;
+  return PS_OK;
+}
+
+ps_status ps_action_timing(double lambda_prev, int64_t c_prev, int64_t c_now, double alpha, double p,
+                           double* lambda_new, int64_t* horizon) {
+  if (!lambda_new || !horizon) return fail(PS_ERR_INVALID, "output pointer is NULL");
+  if (!(alpha > 0.0 && alpha <= 1.0) || !(p > 0.0 && p < 1.0)) return fail(PS_ERR_INVALID, "bad alpha or p");
+  ActionTiming t;
+  t.alpha = alpha;
+  t.p = p;
+  t.lambda = lambda_prev;
+  t.round_clock = c_prev;
+  *horizon = t.horizon(c_now);
+  *lambda_new = t.lambda;
+  return PS_OK;
+}
+
 ps_status ps_get_error(ps_store* s, void* stream) {
   if (ps_status st = check_store(s)) return st;
   HIP_TRY(hipStreamSynchronize(as_stream(stream)));
-  int32_t flag = 0;
-  HIP_TRY(hipMemcpy(&flag, s->status, sizeof flag, hipMemcpyDeviceToHost));
-  if (flag) {
+  int32_t flag[2] = {0, 0};
+  HIP_TRY(hipMemcpy(flag, s->status, sizeof flag, hipMemcpyDeviceToHost));
+  if (flag[0] || flag[1]) {
     HIP_TRY(hipMemset(s->status, 0, sizeof flag));
     HIP_TRY(hipDeviceSynchronize());
-    return fail(PS_ERR_KEY_RANGE, "a key outside [0, %lld) was seen", (long long)s->num_keys);
+    if (flag[1]) return fail(PS_ERR_NOT_RESIDENT, "a key with no slot (no intent acted upon) was accessed");
+    return fail(PS_ERR_KEY_RANGE, "a key outside [0, %lld) was seen",
+                (long long)(s->stg ? s->stg->num_keys : s->num_keys));
   }
   return PS_OK;
 }

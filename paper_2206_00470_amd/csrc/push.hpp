@@ -17,17 +17,31 @@ struct RowShape {
 };
 
 // ------------------------------------------------------------------ pull
+// With a key -> slot map (a staged store), keys index the home table of
+// map_keys keys and rows are read from their slots; a key with no slot gives
+// a zero row and sets err[1].
 template <int L, int NV, int VW>
 __global__ __launch_bounds__(BLOCK) void k_pull(const float* __restrict__ W, int64_t ld, int64_t num_keys, int dim,
                                                 const int64_t* __restrict__ keys, int64_t n,
-                                                float* __restrict__ out, int32_t* __restrict__ err) {
+                                                float* __restrict__ out, int32_t* __restrict__ err,
+                                                const int32_t* __restrict__ map, int64_t map_keys) {
   constexpr int GPB = BLOCK / L;
   const int gl = threadIdx.x % L;
-  int bad = 0;
+  int bad = 0, miss = 0;
   for (int64_t i = (int64_t)blockIdx.x * GPB + threadIdx.x / L; i < n; i += (int64_t)gridDim.x * GPB) {
-    const int64_t key = keys[i];
-    const bool ok = key >= 0 && key < num_keys;
-    bad |= !ok;
+    int64_t key = keys[i];
+    bool ok;
+    if (map) {
+      ok = key >= 0 && key < map_keys;
+      bad |= !ok;
+      const int32_t m = ok ? map[key] : -1;
+      miss |= ok && m < 0;
+      ok = m >= 0;
+      key = m;
+    } else {
+      ok = key >= 0 && key < num_keys;
+      bad |= !ok;
+    }
     const float* src = W + (ok ? key : 0) * ld;
     float* dst = out + i * (int64_t)dim;
 #pragma unroll
@@ -44,6 +58,7 @@ __global__ __launch_bounds__(BLOCK) void k_pull(const float* __restrict__ W, int
     }
   }
   if (__syncthreads_or(bad) && threadIdx.x == 0) atomicOr(err, 1);
+  if (__syncthreads_or(miss) && threadIdx.x == 0) atomicOr(err + 1, 1);
 }
 
 // ------------------------------------------------------------------ gradient sources

@@ -1,0 +1,291 @@
+// Intent-driven staging of parameter rows between a home table in pinned host
+// memory and a table of slots in HBM (intent signalling, Section 3; adaptive
+// action timing, Section 4.2 and Algorithm 1), for one worker: the GPU.
+//
+// Host side: the planner keeps the worker's clock, the intents signalled and
+// not yet acted upon, the key -> slot assignment and a free list of slots per
+// key range, and decides in each round which keys to stage in and which to
+// write back.  Device side: row moves between the two tables, updates of the
+// device copy of the key -> slot map, and the translation of a batch's ids
+// into slot ids so that the step kernels run unchanged on the slot table.
+#pragma once
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <map>
+#include <utility>
+#include <vector>
+
+#include "common.hpp"
+
+namespace adapm {
+
+// ------------------------------------------------------------------ action timing
+// Q_Poiss(mu, p): the smallest k >= 0 with P(X <= k) >= p for X ~ Poisson(mu).
+// The probability mass is carried in log space by the recurrence
+// log P(k) = log P(k-1) + log mu - log k from log P(0) = -mu, so large rates
+// do not underflow; the sum stops well past the mass of the distribution.
+inline int64_t poisson_quantile(double mu, double p) {
+  if (!(mu > 0.0)) return 0;
+  const double lmu = std::log(mu);
+  double lp = -mu;
+  double cdf = std::exp(lp);
+  int64_t k = 0;
+  const int64_t kmax = (int64_t)(mu + 60.0 * std::sqrt(mu) + 200.0);
+  while (cdf < p && k < kmax) {
+    ++k;
+    lp += lmu - std::log((double)k);
+    cdf += std::exp(lp);
+  }
+  return k;
+}
+
+struct ActionTiming {
+  double alpha = 0.1;      // smoothing factor
+  double p = 0.9999;       // quantile of the soft upper bound
+  double lambda = 10.0;    // clocks per round, estimated
+  int64_t round_clock = 0; // worker clock at the previous round
+
+  // One round of Algorithm 1 at worker clock `clock`: update the estimate
+  // (not when the clock did not move) and return the horizon H; the round
+  // acts on every intent with C_start < H.
+  int64_t horizon(int64_t clock) {
+    const int64_t delta = clock - round_clock;
+    if (delta > 0) lambda = (1.0 - alpha) * lambda + alpha * (double)delta;
+    round_clock = clock;
+    const double rate = std::max(lambda, (double)delta);
+    return clock + poisson_quantile(2.0 * rate, p);
+  }
+};
+
+// ------------------------------------------------------------------ planner (host only)
+class Planner {
+ public:
+  struct Intent {
+    int64_t end;
+    std::vector<int64_t> keys;
+    size_t next = 0;   // keys before it have been acted upon
+  };
+
+  int64_t num_keys = 0;
+  std::vector<int64_t> range_begin;   // ascending, range_begin[0] == 0
+  std::vector<int64_t> range_slot0;   // first slot of each range
+  std::vector<int32_t> slot;          // key -> slot, -1 when not resident
+  std::vector<int64_t> until;         // resident key: largest C_end of intents acted upon
+  std::vector<std::vector<int32_t>> free_slots;   // per range, a stack
+  std::map<std::pair<int64_t, int64_t>, Intent> pending;   // (C_start, signal order) -> intent
+  std::map<int64_t, std::vector<int64_t>> expiring;        // C_end -> keys whose `until` was set to it
+  std::map<int64_t, int64_t> acted;   // C_start -> last round that finished acting on an intent starting there
+  ActionTiming timing;
+  int64_t clock = 0;
+  int64_t seq = 0;
+  // the last round's moves
+  std::vector<int64_t> out_keys, out_slots, in_keys, in_slots;
+  // totals
+  int64_t staged_total = 0, evicted_total = 0, forced_total = 0, stalled_total = 0;
+
+  void init(int64_t keys, const int64_t* begin, const int64_t* capacity, int nranges) {
+    num_keys = keys;
+    range_begin.assign(begin, begin + nranges);
+    range_slot0.resize(nranges);
+    free_slots.assign(nranges, {});
+    int64_t s0 = 0;
+    for (int r = 0; r < nranges; ++r) {
+      range_slot0[r] = s0;
+      auto& f = free_slots[r];
+      f.reserve(capacity[r]);
+      for (int64_t i = capacity[r] - 1; i >= 0; --i) f.push_back((int32_t)(s0 + i));   // pops ascending
+      s0 += capacity[r];
+    }
+    slot.assign(keys, -1);
+    until.assign(keys, 0);
+  }
+
+  int range_of(int64_t key) const {
+    return (int)(std::upper_bound(range_begin.begin(), range_begin.end(), key) - range_begin.begin()) - 1;
+  }
+
+  // The range that starts exactly at `key`, or -1.
+  int range_starting_at(int64_t key) const {
+    auto it = std::lower_bound(range_begin.begin(), range_begin.end(), key);
+    return (it != range_begin.end() && *it == key) ? (int)(it - range_begin.begin()) : -1;
+  }
+
+  void signal(const int64_t* keys, int64_t n, int64_t c_start, int64_t c_end) {
+    if (c_end <= clock || c_end <= c_start) return;
+    Intent it;
+    it.end = c_end;
+    it.keys.assign(keys, keys + n);
+    pending.emplace(std::make_pair(c_start, seq++), std::move(it));
+  }
+
+  bool due(int64_t c) const { return !pending.empty() && pending.begin()->first.first <= c; }
+
+  void clear_moves() {
+    out_keys.clear();
+    out_slots.clear();
+    in_keys.clear();
+    in_slots.clear();
+  }
+
+  // Keys whose every acted-upon intent has expired leave the slot table.
+  void evict_expired() {
+    while (!expiring.empty() && expiring.begin()->first <= clock) {
+      for (int64_t k : expiring.begin()->second) {
+        if (slot[k] < 0 || until[k] > clock) continue;   // already gone, or extended
+        out_keys.push_back(k);
+        out_slots.push_back(slot[k]);
+        free_slots[range_of(k)].push_back(slot[k]);
+        slot[k] = -1;
+        ++evicted_total;
+      }
+      expiring.erase(expiring.begin());
+    }
+  }
+
+  // Act on pending intents with C_start < horizon, in (C_start, signal)
+  // order; a full key range stops the acting until a later round.
+  void act(int64_t horizon, int64_t round_id) {
+    while (!pending.empty() && pending.begin()->first.first < horizon) {
+      const int64_t c_start = pending.begin()->first.first;
+      Intent& it = pending.begin()->second;
+      if (it.end <= clock) {   // expired before it could be acted upon
+        pending.erase(pending.begin());
+        continue;
+      }
+      for (; it.next < it.keys.size(); ++it.next) {
+        const int64_t k = it.keys[it.next];
+        if (k < 0 || k >= num_keys) continue;
+        if (slot[k] >= 0) {
+          if (it.end > until[k]) {
+            until[k] = it.end;
+            expiring[it.end].push_back(k);
+          }
+          continue;
+        }
+        auto& f = free_slots[range_of(k)];
+        if (f.empty()) {
+          ++stalled_total;
+          return;
+        }
+        const int32_t sl = f.back();
+        f.pop_back();
+        slot[k] = sl;
+        until[k] = it.end;
+        expiring[it.end].push_back(k);
+        in_keys.push_back(k);
+        in_slots.push_back(sl);
+        ++staged_total;
+      }
+      auto a = acted.find(c_start);
+      if (a == acted.end()) acted.emplace(c_start, round_id);
+      else a->second = std::max(a->second, round_id);
+      pending.erase(pending.begin());
+    }
+  }
+
+  // The latest round that acted on intents starting at or before `c`
+  // (forgotten afterwards), or -1.
+  int64_t take_round_for(int64_t c) {
+    int64_t r = -1;
+    while (!acted.empty() && acted.begin()->first <= c) {
+      r = std::max(r, acted.begin()->second);
+      acted.erase(acted.begin());
+    }
+    return r;
+  }
+};
+
+// ------------------------------------------------------------------ kernels
+__global__ __launch_bounds__(BLOCK) void k_map_fill(int32_t* __restrict__ map, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x; i < n; i += (int64_t)gridDim.x * BLOCK) map[i] = -1;
+}
+
+// map[keys[i]] = slots[i] (or -1 without slots).
+__global__ __launch_bounds__(BLOCK) void k_map_set(int32_t* __restrict__ map, const int64_t* __restrict__ keys,
+                                                   const int64_t* __restrict__ slots, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x; i < n; i += (int64_t)gridDim.x * BLOCK)
+    map[keys[i]] = slots ? (int32_t)slots[i] : -1;
+}
+
+// Row i of the move: the value and accumulator rows at index from[i] of the
+// source tables are copied to index to[i] of the destination tables.  One
+// group of L lanes per row; a source or destination may be host memory
+// mapped into the device's address space.
+template <int L, int NV, int VW>
+__global__ __launch_bounds__(BLOCK) void k_move_rows(const float* __restrict__ sW, const float* __restrict__ sG,
+                                                     int64_t sld, const int64_t* __restrict__ from,
+                                                     float* __restrict__ dW, float* __restrict__ dG, int64_t dld,
+                                                     const int64_t* __restrict__ to, int64_t n, int dim) {
+  constexpr int GPB = BLOCK / L;
+  const int gl = threadIdx.x % L;
+  for (int64_t i = (int64_t)blockIdx.x * GPB + threadIdx.x / L; i < n; i += (int64_t)gridDim.x * GPB) {
+    const int64_t a = from[i] * sld;
+    const int64_t b = to[i] * dld;
+    float w[NV * VW], g[NV * VW];
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int c = (gl + v * L) * VW;
+      if (c < dim) {
+        load_frag<VW>(sW + a + c, w + v * VW);
+        load_frag<VW>(sG + a + c, g + v * VW);
+      }
+    }
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int c = (gl + v * L) * VW;
+      if (c < dim) {
+        store_frag<VW>(dW + b + c, w + v * VW);
+        store_frag<VW>(dG + b + c, g + v * VW);
+      }
+    }
+  }
+}
+
+// A batch's 32-bit ids in slot space: id (a key of key_off + id) becomes
+// map[key_off + id] - slot_off.  Negative ids pass through unchanged (they
+// keep the meaning the step gives them); an id beyond the key range becomes
+// INT32_MAX (out of range for the step, which skips and flags it); a key
+// with no slot also becomes INT32_MAX and sets status[1].
+__global__ __launch_bounds__(BLOCK) void k_translate_ids(const int32_t* __restrict__ in, int64_t n,
+                                                         const int32_t* __restrict__ map, int64_t key_off,
+                                                         int64_t id_limit, int64_t slot_off,
+                                                         int32_t* __restrict__ out, int32_t* __restrict__ status) {
+  int miss = 0;
+  for (int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x; i < n; i += (int64_t)gridDim.x * BLOCK) {
+    const int32_t v = in[i];
+    int32_t r = v;
+    if (v >= 0) {
+      r = INT32_MAX;
+      if (v < id_limit) {
+        const int32_t m = map[key_off + v];
+        if (m >= 0) r = (int32_t)(m - slot_off);
+        else miss = 1;
+      }
+    }
+    out[i] = r;
+  }
+  if (__syncthreads_or(miss) && threadIdx.x == 0) atomicOr(status + 1, 1);
+}
+
+// 64-bit keys in slot space: a key in [0, num_keys) becomes its slot; a key
+// outside it, or one with no slot (which also sets status[1]), becomes -1.
+__global__ __launch_bounds__(BLOCK) void k_translate_keys(const int64_t* __restrict__ in, int64_t n,
+                                                          const int32_t* __restrict__ map, int64_t num_keys,
+                                                          int64_t* __restrict__ out, int32_t* __restrict__ status) {
+  int miss = 0;
+  for (int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x; i < n; i += (int64_t)gridDim.x * BLOCK) {
+    const int64_t v = in[i];
+    int64_t r = -1;
+    if (v >= 0 && v < num_keys) {
+      const int32_t m = map[v];
+      if (m >= 0) r = m;
+      else miss = 1;
+    }
+    out[i] = r;
+  }
+  if (__syncthreads_or(miss) && threadIdx.x == 0) atomicOr(status + 1, 1);
+}
+
+}  // namespace adapm

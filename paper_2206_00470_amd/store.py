@@ -8,6 +8,7 @@ from __future__ import annotations
 
 import ctypes as C
 
+import numpy as np
 import torch
 
 from . import _lib
@@ -226,6 +227,102 @@ class Store:
         ms, n = C.c_double(0.0), C.c_int64(0)
         check(lib().ps_read_timing(self._h, kernel_id, C.byref(ms), C.byref(n)))
         return ms.value, n.value
+
+
+class StagedStore(Store):
+    """A store whose full tables live in pinned host memory (the home store)
+    while HBM holds a table of slots for the keys of acted-upon intents:
+    intent signalling and adaptive action timing for one worker, the GPU.
+
+    W0: initial values [num_keys, dim] (numpy or CPU tensor; accumulators
+    start at zero, or from G0).  ranges: ascending first keys of the key
+    ranges (the first is 0); slots: the slot capacity of each range.  A key
+    offset that a step takes must begin a range.  The home rows are one
+    pinned [num_keys, 2*dim] tensor (values | accumulators), the slots one
+    [sum(slots), 2*dim] device tensor.
+
+    Protocol: intent(keys, c_start, c_end) ahead of use; advance_clock()
+    before each batch's step, on the step's stream; round() (or auto()) to
+    act on intents; flush() before reading home_tables()."""
+
+    def __init__(self, W0, ranges, slots, lr: float = 0.1, eps: float = 1e-10, device="cuda", stream=None,
+                 G0=None):
+        W0 = torch.as_tensor(W0, dtype=torch.float32)
+        K, d = W0.shape
+        home = torch.empty((K, 2 * d), dtype=torch.float32, pin_memory=True)
+        home[:, :d].copy_(W0)
+        if G0 is None:
+            home[:, d:].zero_()
+        else:
+            home[:, d:].copy_(torch.as_tensor(G0, dtype=torch.float32))
+        total = int(sum(slots))
+        T = torch.zeros((total, 2 * d), dtype=torch.float32, device=device)
+        self.home = home
+        self.W, self.G = T[:, :d], T[:, d:]
+        self.key_slot = torch.empty(K, dtype=torch.int32, device=device)
+        self.num_keys, self.dim = K, d
+        self.row_stride = 2 * d
+        self.rowwise = False
+        self.lr, self.eps = lr, eps
+        self.ws = Workspace(torch.device(device))
+        self.ranges, self.slots = list(ranges), list(slots)
+        rb = (C.c_int64 * len(ranges))(*ranges)
+        rs = (C.c_int64 * len(slots))(*slots)
+        h = C.c_void_p()
+        hp = home.data_ptr()
+        check(lib().ps_create_staged(C.byref(h), K, d, C.c_void_p(hp), C.c_void_p(hp + 4 * d), 2 * d, _ptr(self.W),
+                                     _ptr(self.G), 2 * d, _ptr(self.key_slot), len(ranges), rb, rs, lr, eps,
+                                     _stream(stream)))
+        self._h = h
+
+    def set_action_timing(self, alpha: float = 0.1, p: float = 0.9999, lambda0: float = 10.0):
+        check(lib().ps_set_action_timing(self._h, alpha, p, lambda0))
+
+    def intent(self, keys, c_start: int, c_end: int):
+        """Intent(keys, C_start, C_end): host keys (numpy, list or CPU tensor)."""
+        k = np.ascontiguousarray(np.asarray(keys, dtype=np.int64).ravel())
+        check(lib().ps_intent(self._h, C.c_void_p(k.ctypes.data), k.size, c_start, c_end))
+
+    def advance_clock(self, stream=None):
+        check(lib().ps_advance_clock(self._h, _stream(stream)))
+
+    def round(self, wait: bool = False):
+        check(lib().ps_stage_round(self._h, int(wait)))
+
+    def auto(self, on: bool = True):
+        check(lib().ps_stage_auto(self._h, int(on)))
+
+    def flush(self, stream=None):
+        check(lib().ps_stage_flush(self._h, _stream(stream)))
+
+    def stats(self) -> dict:
+        n = len(_lib.STAGE_STATS)
+        v = (C.c_int64 * n)()
+        lam = C.c_double(0.0)
+        check(lib().ps_stage_stats(self._h, v, n, C.byref(lam)))
+        d = dict(zip(_lib.STAGE_STATS, list(v)))
+        d["lambda"] = lam.value
+        return d
+
+    def resident(self) -> np.ndarray:
+        cnt = C.c_int64(0)
+        check(lib().ps_stage_resident(self._h, None, 0, C.byref(cnt)))
+        out = np.empty(cnt.value, np.int64)
+        check(lib().ps_stage_resident(self._h, C.c_void_p(out.ctypes.data), out.size, C.byref(cnt)))
+        return out[:cnt.value]
+
+    def home_tables(self):
+        """(values, accumulators) of the home store as numpy views (current after flush())."""
+        d = self.dim
+        a = self.home.numpy()
+        return a[:, :d], a[:, d:]
+
+
+def action_timing(lam_prev: float, c_prev: int, c_now: int, alpha: float = 0.1, p: float = 0.9999):
+    """Algorithm 1 as the library computes it: (new estimate, horizon)."""
+    lam, h = C.c_double(0.0), C.c_int64(0)
+    check(lib().ps_action_timing(lam_prev, c_prev, c_now, alpha, p, C.byref(lam), C.byref(h)))
+    return lam.value, h.value
 
 
 def dedup(num_keys: int, keys: torch.Tensor, err: torch.Tensor | None = None, stream=None):
