@@ -32,6 +32,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0   # MI355X HBM3E
+HOST_LINK_GBPS = 64.0    # PCIe 5.0 x16, one direction
 
 
 def parse():
@@ -54,6 +55,10 @@ def parse():
     ap.add_argument("--no-overlap", action="store_true",
                     help="MF: one ps_step_mf call per step instead of overlapping the next batch's key work "
                          "(sort, segments, records) on a second stream with this batch's table update")
+    ap.add_argument("--staged", action="store_true",
+                    help="home tables in pinned host memory, HBM slots for the keys of acted-upon intents; "
+                         "intents signalled --lookahead batches ahead, rounds on the library's thread")
+    ap.add_argument("--lookahead", type=int, default=2, help="staged: batches between intent and use")
     ap.add_argument("--graph", action="store_true",
                     help="capture the timed steps in one HIP graph and time its replay (for the launch-bound "
                          "small configurations); the roofline then comes from the eager breakdown steps")
@@ -228,6 +233,110 @@ class Bench:
         return self.keys_of(bt).size
 
 
+def key_ranges(wb):
+    """First keys of the key ranges a staged store needs for this task (each
+    key offset a step takes starts a range)."""
+    c = wb.cfg
+    if wb.task == "mf":
+        return [0, c.n_rows]
+    if wb.task == "kge":
+        return [0, c.n_ent]
+    if wb.task == "sgns":
+        return [0, c.vocab]
+    return [0]
+
+
+def run_staged(args, wb, dev):
+    """Steps on a staged store: each step advances the clock, runs the step
+    and signals the intent of the batch `lookahead` steps ahead (its distinct
+    keys, as a data loader would); rounds run on the library's thread.
+    Returns the fields of the JSON line that differ from the in-HBM run."""
+    import torch
+
+    from paper_2206_00470_amd import StagedStore, _lib
+    cfg, nb, L = wb.cfg, len(wb.batches), args.lookahead
+    begin = key_ranges(wb)
+    ends = begin[1:] + [cfg.num_keys]
+    ukeys = [np.unique(wb.keys_of(bt)) for bt in wb.host_batches]
+    per = [max(int(((u >= b) & (u < e)).sum()) for u in ukeys) for b, e in zip(begin, ends)]
+    # room for the batches in flight: the active one, the one expiring, L ahead
+    slots = [min(e - b, int((L + 2) * p * 1.05) + 64) for b, e, p in zip(begin, ends, per)]
+    t0 = time.time()
+    store = StagedStore(wb.W, begin, slots, cfg.opt.lr, cfg.opt.eps, device=dev)
+    print(f"# staged store: {sum(slots)} slots for {cfg.num_keys} keys, home tables pinned in "
+          f"{time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+    loss = torch.empty(1, dtype=torch.float64, device=dev)
+    for c in range(1, L + 1):
+        store.intent(ukeys[(c - 1) % nb], c, c + 1)
+    clock = [0]
+
+    def step(i):
+        store.advance_clock()
+        clock[0] += 1
+        wb.step(store, i, loss)
+        store.intent(ukeys[(i + L) % nb], clock[0] + L, clock[0] + L + 1)
+
+    store.set_timing(1 << _lib.PS_KERNEL_STAGE)
+    store.auto(True)
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    store.auto(False)
+    store.read_timing(_lib.PS_KERNEL_STAGE)   # reset
+    st0 = store.stats()
+    store.auto(True)
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t
+    store.auto(False)
+    assert store.error() == 0
+    st1 = store.stats()
+    mv_ms, mv_n = store.read_timing(_lib.PS_KERNEL_STAGE)
+    moved = (st1["staged"] - st0["staged"]) + (st1["evicted"] - st0["evicted"])
+    R = wb.R
+    link_bytes = moved * 2.0 * R          # a value row and an accumulator row cross the link per move
+    achieved = link_bytes / (mv_ms * 1e-3) / 1e9 if mv_ms > 0 else None
+    store.close()
+    staging = {"lookahead": L, "ranges": begin, "slots": slots, "home_GB": round(cfg.num_keys * 2 * R / 1e9, 2),
+               "slots_GB": round(sum(slots) * 2 * R / 1e9, 2),
+               "staged_per_step": (st1["staged"] - st0["staged"]) / args.steps,
+               "evicted_per_step": (st1["evicted"] - st0["evicted"]) / args.steps,
+               "forced_in_timed_steps": st1["forced"] - st0["forced"],
+               "rounds_in_timed_steps": st1["rounds"] - st0["rounds"],
+               "stalls_in_timed_steps": st1["stalled"] - st0["stalled"],
+               "rate_estimate": round(st1["lambda"], 4),
+               "link_GBps_over_step_time": round(link_bytes / elapsed / 1e9, 2),
+               "move_kernel_ms_per_step": round(mv_ms / args.steps, 4)}
+    roofline = {"bound": "host-link", "kernel": "k_move_rows", "achieved": round(achieved, 2) if achieved else None,
+                "peak": HOST_LINK_GBPS, "unit": "GB/s", "frac": round(achieved / HOST_LINK_GBPS, 4) if achieved else None,
+                "traffic": None, "avg_ms": round(mv_ms / max(mv_n, 1), 4),
+                "alg_bytes_per_launch": int(link_bytes / max(mv_n, 1))}
+    return elapsed, staging, roofline
+
+
+def cpu_baseline(args, wb, rowwise):
+    """The oracle on the host, single-threaded, on a bounded sample of the
+    same workload (whole steps on the full table, until --cpu-seconds)."""
+    if args.cpu_seconds <= 0:
+        return None
+    cfg = wb.cfg
+    W = wb.W
+    G = np.zeros(W.shape[0], np.float32) if rowwise else np.zeros_like(W)
+    done, rows, tc0 = 0, 0, time.perf_counter()
+    while True:
+        rows += 2 * wb.oracle_step(W, G, 1000 + done)
+        done += 1
+        if time.perf_counter() - tc0 >= args.cpu_seconds:
+            break
+    tc = time.perf_counter() - tc0
+    return {"value": rows / tc, "unit": "rows/s", "cores": 1, "kind": "oracle",
+            "sample": f"{done} step(s) of the same workload on the full {cfg.num_keys}x{cfg.dim} table, "
+                      f"single-threaded C oracle, {tc:.1f} s"}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -246,6 +355,28 @@ def main():
     rowwise = args.update == "rowwise"
     wb = Bench(args.workload, dev, nb, rowwise)
     cfg = wb.cfg
+    metric = ("param rows pulled+pushed/sec (MF 10m x 1m, rank 100)" if args.workload == "mf"
+              else f"param rows pulled+pushed/sec ({cfg.name})")
+    if args.staged:
+        if rowwise or args.graph:
+            print("--staged runs per-element AdaGrad, eagerly", file=sys.stderr)
+            sys.exit(2)
+        elapsed, staging, roofline = run_staged(args, wb, dev)
+        occ = float(np.mean([wb.occ[(args.warmup + i) % nb] for i in range(args.steps)]))
+        ms_per_step = elapsed * 1e3 / args.steps
+        line = {
+            "metric": metric + ", home table in host memory", "value": 2.0 * occ / (ms_per_step * 1e-3),
+            "unit": "rows/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+            "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+            "config": {"workload": cfg.name, "num_keys": cfg.num_keys, "dim": cfg.dim, "update": "elementwise",
+                       "launch": "eager", "key_occurrences_per_step": occ, "batches_resident": nb,
+                       "staging": staging},
+            "roofline": roofline,
+            "cpu_baseline": cpu_baseline(args, wb, False),
+        }
+        print(json.dumps(line), flush=True)
+        return
     if rowwise and args.layout == "interleaved":
         from paper_2206_00470_amd.store import padded_rowwise_table
         Wt, Gt = padded_rowwise_table(torch.from_numpy(wb.W).to(dev))
@@ -431,25 +562,10 @@ def main():
                 "GBps": round(2 * a.numel() * 4 / tcp / 1e9, 1)}
         del a, b
 
-    # ------------------------------------------------------------ CPU oracle on the host
-    cpu = None
-    if args.cpu_seconds > 0:
-        W = wb.W
-        G = np.zeros(W.shape[0], np.float32) if rowwise else np.zeros_like(W)
-        done, rows, tc0 = 0, 0, time.perf_counter()
-        while True:
-            rows += 2 * wb.oracle_step(W, G, 1000 + done)
-            done += 1
-            if time.perf_counter() - tc0 >= args.cpu_seconds:
-                break
-        tc = time.perf_counter() - tc0
-        cpu = {"value": rows / tc, "unit": "rows/s", "cores": 1, "kind": "oracle",
-               "sample": f"{done} step(s) of the same workload on the full {cfg.num_keys}x{cfg.dim} table, "
-                         f"single-threaded C oracle, {tc:.1f} s"}
+    cpu = cpu_baseline(args, wb, rowwise)
 
     line = {
-        "metric": ("param rows pulled+pushed/sec (MF 10m x 1m, rank 100)" if args.workload == "mf"
-                   else f"param rows pulled+pushed/sec ({cfg.name})") + (", row-wise AdaGrad" if rowwise else ""),
+        "metric": metric + (", row-wise AdaGrad" if rowwise else ""),
         "value": rows_per_s,
         "unit": "rows/s",
         "n_gpus": 1,

@@ -223,12 +223,15 @@ const char* ps_last_error_message(void);
  * count of one kernel since the last reset, then resets it.  kernel_id: 0 = segmented reduce + AdaGrad, 1 = task gradient
  * (MF: the per-entry record scatter), 2 = radix scatter, 3 = pull, 4 = MF
  * row-key merge that also forms the MF gradients and loss (timed under 4,
- * not 0). */
+ * not 0), 5 = row moves of a staged store between its home tables and its
+ * slots (on the staging stream; set the mask while no round runs on the
+ * library thread, read it after stopping that thread). */
 #define PS_KERNEL_SEGREDUCE 0
 #define PS_KERNEL_TASKGRAD  1
 #define PS_KERNEL_SCATTER   2
 #define PS_KERNEL_PULL      3
 #define PS_KERNEL_MF_ROWMERGE 4
+#define PS_KERNEL_STAGE     5
 #define PS_TIMING_ALL (-1)
 ps_status ps_set_timing(ps_store* s, int32_t mask);
 ps_status ps_read_timing(ps_store* s, int32_t kernel_id, double* total_ms, int64_t* launches);

@@ -23,6 +23,7 @@ PS_OP_PULL, PS_OP_PUSH, PS_OP_DEDUP = 0, 1, 2
 PS_OP_STEP_MF, PS_OP_STEP_KGE, PS_OP_STEP_SGNS, PS_OP_STEP_CTR = 3, 4, 5, 6
 
 PS_KERNEL_SEGREDUCE, PS_KERNEL_TASKGRAD, PS_KERNEL_SCATTER, PS_KERNEL_PULL, PS_KERNEL_MF_ROWMERGE = 0, 1, 2, 3, 4
+PS_KERNEL_STAGE = 5
 PS_TIMING_ALL = -1
 
 STAGE_STATS = ["clock", "rounds", "forced", "staged", "evicted", "resident", "pending", "stalled"]

@@ -46,7 +46,7 @@ ps_status fail(ps_status st, const char* fmt, ...) {
 #define LAUNCHED(name) HIP_TRY(hipGetLastError())
 
 constexpr int64_t MAX_OCC = (int64_t(1) << 31) - (int64_t(1) << 20);
-constexpr int NUM_TIMED = 5;
+constexpr int NUM_TIMED = 6;
 constexpr size_t MAX_TIMED_LAUNCHES = 1 << 14;
 
 }  // namespace
@@ -654,6 +654,7 @@ ps_status move_rows(ps_store* s, bool to_home, const int64_t* from, const int64_
   row_shape(s->dim, true, &shape);
   return with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
     const int64_t grid = small_grid(n, BLOCK / L, 16384);
+    Timed t(s, PS_KERNEL_STAGE, st);
     if (to_home)
       hipLaunchKernelGGL((k_move_rows<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->G, s->ld, from,
                          const_cast<float*>(g.hW), const_cast<float*>(g.hG), g.hld, to, n, s->dim);
@@ -1397,9 +1398,9 @@ ps_status ps_stage_flush(ps_store* s, void* stream) {
   std::vector<int64_t> keys, slots, none;
   const Planner& P = g.plan;
   for (int64_t k = 0; k < g.num_keys; ++k)
-    if (P.slot[k] >= 0) {
+    if (P.slot_of(k) >= 0) {
       keys.push_back(k);
-      slots.push_back(P.slot[k]);
+      slots.push_back(P.slot_of(k));
     }
   // every resident row is written back; it stays resident
   if (!keys.empty()) {
@@ -1444,7 +1445,7 @@ ps_status ps_stage_resident(ps_store* s, int64_t* keys, int64_t capacity, int64_
   std::lock_guard<std::mutex> lk(g.mu);
   int64_t c = 0;
   for (int64_t k = 0; k < g.num_keys; ++k)
-    if (g.plan.slot[k] >= 0) {
+    if (g.plan.slot_of(k) >= 0) {
       if (c < capacity) keys[c] = k;
       ++c;
     }

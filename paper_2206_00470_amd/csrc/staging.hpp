@@ -71,8 +71,14 @@ class Planner {
   int64_t num_keys = 0;
   std::vector<int64_t> range_begin;   // ascending, range_begin[0] == 0
   std::vector<int64_t> range_slot0;   // first slot of each range
-  std::vector<int32_t> slot;          // key -> slot, -1 when not resident
-  std::vector<int64_t> until;         // resident key: largest C_end of intents acted upon
+  // per key, one cache line access: its slot (-1 when not resident) and,
+  // while resident, the largest C_end of the intents acted upon for it
+  struct KeyState {
+    int64_t until;
+    int32_t slot;
+    int32_t pad;
+  };
+  std::vector<KeyState> ks;
   std::vector<std::vector<int32_t>> free_slots;   // per range, a stack
   std::map<std::pair<int64_t, int64_t>, Intent> pending;   // (C_start, signal order) -> intent
   std::map<int64_t, std::vector<int64_t>> expiring;        // C_end -> keys whose `until` was set to it
@@ -98,9 +104,10 @@ class Planner {
       for (int64_t i = capacity[r] - 1; i >= 0; --i) f.push_back((int32_t)(s0 + i));   // pops ascending
       s0 += capacity[r];
     }
-    slot.assign(keys, -1);
-    until.assign(keys, 0);
+    ks.assign(keys, KeyState{0, -1, 0});
   }
+
+  int32_t slot_of(int64_t key) const { return ks[key].slot; }
 
   int range_of(int64_t key) const {
     return (int)(std::upper_bound(range_begin.begin(), range_begin.end(), key) - range_begin.begin()) - 1;
@@ -129,15 +136,21 @@ class Planner {
     in_slots.clear();
   }
 
+  static constexpr size_t PREFETCH = 16;   // keys ahead whose state is fetched early
+
   // Keys whose every acted-upon intent has expired leave the slot table.
   void evict_expired() {
     while (!expiring.empty() && expiring.begin()->first <= clock) {
-      for (int64_t k : expiring.begin()->second) {
-        if (slot[k] < 0 || until[k] > clock) continue;   // already gone, or extended
+      const std::vector<int64_t>& b = expiring.begin()->second;
+      for (size_t i = 0; i < b.size(); ++i) {
+        if (i + PREFETCH < b.size()) __builtin_prefetch(&ks[b[i + PREFETCH]]);
+        const int64_t k = b[i];
+        KeyState& st = ks[k];
+        if (st.slot < 0 || st.until > clock) continue;   // already gone, or extended
         out_keys.push_back(k);
-        out_slots.push_back(slot[k]);
-        free_slots[range_of(k)].push_back(slot[k]);
-        slot[k] = -1;
+        out_slots.push_back(st.slot);
+        free_slots[range_of(k)].push_back(st.slot);
+        st.slot = -1;
         ++evicted_total;
       }
       expiring.erase(expiring.begin());
@@ -154,13 +167,20 @@ class Planner {
         pending.erase(pending.begin());
         continue;
       }
-      for (; it.next < it.keys.size(); ++it.next) {
+      std::vector<int64_t>& bucket = expiring[it.end];
+      const size_t nk = it.keys.size();
+      for (; it.next < nk; ++it.next) {
+        if (it.next + PREFETCH < nk) {
+          const int64_t kp = it.keys[it.next + PREFETCH];
+          if (kp >= 0 && kp < num_keys) __builtin_prefetch(&ks[kp]);
+        }
         const int64_t k = it.keys[it.next];
         if (k < 0 || k >= num_keys) continue;
-        if (slot[k] >= 0) {
-          if (it.end > until[k]) {
-            until[k] = it.end;
-            expiring[it.end].push_back(k);
+        KeyState& st = ks[k];
+        if (st.slot >= 0) {
+          if (it.end > st.until) {
+            st.until = it.end;
+            bucket.push_back(k);
           }
           continue;
         }
@@ -171,9 +191,9 @@ class Planner {
         }
         const int32_t sl = f.back();
         f.pop_back();
-        slot[k] = sl;
-        until[k] = it.end;
-        expiring[it.end].push_back(k);
+        st.slot = sl;
+        st.until = it.end;
+        bucket.push_back(k);
         in_keys.push_back(k);
         in_slots.push_back(sl);
         ++staged_total;
