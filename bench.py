@@ -40,7 +40,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="mf", choices=["mf", "mf_tiny", "kge", "kge2x100", "sgns", "ctr"])
+    ap.add_argument("--workload", default="mf", choices=["mf", "mf_tiny", "mf_colorder", "kge", "kge2x100", "sgns",
+                                                           "sgns_w2v", "ctr"])
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="bound on the CPU-oracle sample (0 = skip)")
     ap.add_argument("--no-ops", action="store_true", help="skip the pull-only / push-only measurements")
@@ -101,9 +102,10 @@ class Bench:
 
         self.name = name
         self.rowwise = rowwise
-        self.task = {"mf_tiny": "mf", "kge2x100": "kge"}.get(name, name)
-        cfgs = {"mf": wls.MF_10Mx1M, "mf_tiny": wls.MF_TINY, "kge": wls.KGE_COMPLEX,
-                "kge2x100": wls.KGE_COMPLEX_2x100, "sgns": wls.SGNS_1M, "ctr": wls.CTR_33M}
+        self.task = {"mf_tiny": "mf", "mf_colorder": "mf", "kge2x100": "kge", "sgns_w2v": "sgns"}.get(name, name)
+        cfgs = {"mf": wls.MF_10Mx1M, "mf_tiny": wls.MF_TINY, "mf_colorder": wls.MF_10Mx1M_COLORDER,
+                "kge": wls.KGE_COMPLEX, "kge2x100": wls.KGE_COMPLEX_2x100, "sgns": wls.SGNS_1M,
+                "sgns_w2v": wls.SGNS_1M_W2V, "ctr": wls.CTR_33M}
         self.cfg = cfg = cfgs[name]
         self.wl = wls.workload(cfg)
         self.dev = dev
@@ -399,7 +401,7 @@ def main():
     names = list(wb.alg_bytes(0))                 # kernels with algorithmic bytes for this workload
 
     # (MF tiny is launch-bound: the extra events of the overlap cost more than it hides)
-    overlap = args.workload == "mf" and not args.no_overlap and not args.graph
+    overlap = args.workload in ("mf", "mf_colorder") and not args.no_overlap and not args.graph
 
     def run_steps(first, count, mask):
         """count steps from batch `first` with the kernels in `mask` bracketed by HIP
@@ -455,7 +457,7 @@ def main():
     rows_per_s = 2.0 * occ / (ms_per_step * 1e-3)
     # launches per step of the merge kernel: SGNS merges output rows, then input rows
     # (MF's row-key merge is timed on its own, "rowmerge")
-    seg_launches_per_step = 2 if args.workload == "sgns" else 1
+    seg_launches_per_step = 2 if wb.task == "sgns" else 1
 
     def kernel_entry(name, timing, steps, bidx):
         ms, cnt = timing

@@ -146,6 +146,10 @@ class MFConfig:
     opt: AdaGradCfg = field(default_factory=AdaGradCfg)
     seed: int = 0
     fixed_dataset: bool = False   # small case: one dataset, batches in order
+    # "random": each batch draws its entries i.i.d.; "column": the paper's
+    # visiting order, the entries of one column after another, columns in a
+    # random order (Appendix C, "Matrix factorization")
+    visit: str = "random"
 
     @property
     def num_keys(self) -> int:
@@ -207,6 +211,8 @@ class SGNSConfig:
     neg_power: float = 0.75
     opt: AdaGradCfg = field(default_factory=AdaGradCfg)
     seed: int = 0
+    subsample: float = 0.0        # word2vec's frequent-word threshold t (0: keep every token)
+    dynamic_window: bool = False  # word2vec's per-centre window drawn uniformly from 1..window
 
     @property
     def num_keys(self) -> int:
@@ -267,6 +273,14 @@ CONFIGS = [MF_TINY, MF_10Mx1M, KGE_COMPLEX, SGNS_1M, CTR_33M]
 # tail-corrupted negatives per triple.
 KGE_COMPLEX_2x100 = replace(KGE_COMPLEX, name="kge_complex_4.6M_d128_2x100neg", n_neg=200, n_head_neg=100)
 
+# word2vec's common parameters as the paper uses them (Appendix C, "Word
+# vectors"): window 5 drawn per centre, frequent-word subsampling 0.01.
+SGNS_1M_W2V = replace(SGNS_1M, name="sgns_1M_d300_w2v", subsample=0.01, dynamic_window=True)
+
+# The paper's visiting order for MF: by column, columns in random order
+# (Appendix C, "Matrix factorization").
+MF_10Mx1M_COLORDER = replace(MF_10Mx1M, name="mf_10Mx1M_r100_colorder", visit="column")
+
 
 def small_variant(cfg, scale: str = "small"):
     """Reduced sizes of the same workload for oracle-speed parity tests: the
@@ -307,6 +321,20 @@ class MFWorkload:
         if cfg.fixed_dataset:
             rng = _rng(cfg.seed, self.TAG, 0)
             self._data = self._draw(rng, cfg.nnz)
+        if cfg.visit == "column":
+            # each column holds its expected share of the nnz entries (largest
+            # remainders round the shares to whole entries); columns are
+            # visited in a seeded random order
+            share = cfg.nnz * self.zipf.pmf
+            cnt = np.floor(share).astype(np.int64)
+            extra = cfg.nnz - int(cnt.sum())
+            cnt[np.argsort(-(share - cnt), kind="stable")[:extra]] += 1
+            counts = np.zeros(cfg.n_cols, np.int64)
+            counts[self.zipf.perm] = cnt                 # by column id
+            self.col_order = _rng(cfg.seed, self.TAG + 3, 0).permutation(cfg.n_cols).astype(np.int64)
+            self.col_end = np.cumsum(counts[self.col_order])
+        elif cfg.visit != "random":
+            raise ValueError(f"unknown MF visiting order {cfg.visit!r}")
 
     def _draw(self, rng, b):
         row = rng.integers(0, self.cfg.n_rows, b, dtype=np.int64).astype(np.int32)
@@ -314,8 +342,27 @@ class MFWorkload:
         val = rng.standard_normal(b, dtype=np.float32)
         return MFBatch(row, col, val)
 
+    def _column_batch(self, step: int) -> MFBatch:
+        """Entries [lo, hi) of the column-ordered epoch: the columns that
+        cover that span, each for its overlap; rows uniform, values N(0,1)."""
+        cfg = self.cfg
+        s = step % cfg.steps_per_epoch
+        lo, hi = s * cfg.batch, min(cfg.nnz, (s + 1) * cfg.batch)
+        i0 = int(np.searchsorted(self.col_end, lo, side="right"))
+        i1 = int(np.searchsorted(self.col_end, hi - 1, side="right"))
+        starts = np.concatenate([[0], self.col_end[:-1]])
+        a = np.maximum(starts[i0:i1 + 1], lo)
+        b = np.minimum(self.col_end[i0:i1 + 1], hi)
+        col = np.repeat(self.col_order[i0:i1 + 1], b - a).astype(np.int32)
+        rng = _rng(cfg.seed, self.TAG, step + 1)
+        row = rng.integers(0, cfg.n_rows, hi - lo, dtype=np.int64).astype(np.int32)
+        val = rng.standard_normal(hi - lo, dtype=np.float32)
+        return MFBatch(row, col, val)
+
     def batch(self, step: int) -> MFBatch:
         cfg = self.cfg
+        if cfg.visit == "column":
+            return self._column_batch(step)
         if self._data is not None:
             lo = (step % cfg.steps_per_epoch) * cfg.batch
             hi = min(cfg.nnz, lo + cfg.batch)
@@ -367,6 +414,10 @@ class SGNSBatch:
 
 class SGNSWorkload:
     TAG = 303
+    # counter ranges of the hash draws: tokens at the position itself, the
+    # subsampling and window draws 2^40 and 2^41 positions further on
+    _SUBSAMPLE_STREAM = np.uint64(1 << 40)
+    _WINDOW_STREAM = np.uint64(1 << 41)
 
     def __init__(self, cfg: SGNSConfig):
         self.cfg = cfg
@@ -388,8 +439,59 @@ class SGNSWorkload:
         w = self.cfg.window
         return np.array([d for d in range(-w, w + 1) if d != 0], dtype=np.int64)
 
+    def kept(self, pos: np.ndarray) -> np.ndarray:
+        """Whether the token at each stream position survives subsampling:
+        Mikolov et al.'s rule discards word w with probability
+        1 - sqrt(t / f(w)), f(w) taken as w's probability in the stream."""
+        pos = np.asarray(pos, dtype=np.int64)
+        ok = (pos >= 0) & (pos < self.cfg.n_tokens)
+        if self.cfg.subsample <= 0:
+            return ok
+        u = _hash_uniform(pos.astype(np.uint64) ^ self._key)
+        f = self.zipf.pmf[self.zipf.ranks(u)]
+        keep = np.minimum(1.0, np.sqrt(self.cfg.subsample / f))
+        v = _hash_uniform((pos.astype(np.uint64) + self._SUBSAMPLE_STREAM) ^ self._key)
+        return ok & (v < keep)
+
+    def _w2v_batch(self, step: int) -> SGNSBatch:
+        """The kept tokens of stream span [lo, lo + batch) as centres; each
+        centre's context is the nearest kept tokens on either side, up to its
+        window b (b uniform in 1..window when the window is dynamic)."""
+        cfg = self.cfg
+        w = cfg.window
+        steps = (cfg.n_tokens + cfg.batch - 1) // cfg.batch
+        lo = (step % steps) * cfg.batch
+        hi = min(cfg.n_tokens, lo + cfg.batch)
+        margin = 8 * w + 64
+        while True:
+            pos = np.arange(lo - margin, hi + margin, dtype=np.int64)
+            kp = pos[self.kept(pos)]
+            c0 = int(np.searchsorted(kp, lo))
+            c1 = int(np.searchsorted(kp, hi))
+            inside = (pos[0] < 0 or c0 >= w) and (pos[-1] >= cfg.n_tokens or len(kp) - c1 >= w)
+            if inside:
+                break
+            margin *= 2
+        B = c1 - c0
+        centre_pos = kp[c0:c1]
+        idx = np.arange(c0, c1)[:, None] + self.offsets()[None, :]
+        valid = (idx >= 0) & (idx < len(kp))
+        ctx_pos = np.where(valid, kp[np.clip(idx, 0, max(len(kp) - 1, 0))], -1)
+        if cfg.dynamic_window:
+            u = _hash_uniform((centre_pos.astype(np.uint64) + self._WINDOW_STREAM) ^ self._key)
+            b = 1 + np.minimum((u * w).astype(np.int64), w - 1)
+            valid &= np.abs(self.offsets())[None, :] <= b[:, None]
+        centre = self.tokens(centre_pos)
+        ctx = np.where(valid, self.tokens(np.where(valid, ctx_pos, -1)), -1).astype(np.int32)
+        rng = _rng(cfg.seed, self.TAG, step + 1)
+        neg = self.noise.sample(rng, (B, 2 * w, cfg.n_neg)).astype(np.int32)
+        neg = np.where(ctx[:, :, None] < 0, -1, neg).astype(np.int32)
+        return SGNSBatch(centre, ctx, neg)
+
     def batch(self, step: int) -> SGNSBatch:
         cfg = self.cfg
+        if cfg.subsample > 0 or cfg.dynamic_window:
+            return self._w2v_batch(step)
         steps = (cfg.n_tokens + cfg.batch - 1) // cfg.batch
         s = step % steps
         lo = s * cfg.batch

@@ -5,7 +5,7 @@ import torch
 
 import oracle
 from paper_2206_00470_amd import Store
-from paper_2206_00470_amd.workloads import MF_10Mx1M, MF_TINY, MFWorkload, small_variant
+from paper_2206_00470_amd.workloads import MF_10Mx1M, MF_10Mx1M_COLORDER, MF_TINY, MFWorkload, small_variant
 from tests.helpers import assert_bitwise, assert_close_tables, mismatch_fraction, say
 
 pytestmark = pytest.mark.gpu
@@ -131,16 +131,29 @@ def test_mf_deterministic():
     assert out[0][2:] == out[1][2:]
 
 
-def test_mf_paper_scale_one_step():
-    """10M x 1M, rank 100, 1,048,576 entries: the full table, the bench's launch."""
-    cfg = MF_10Mx1M
+def test_mf_column_order_small():
+    """The paper's visiting order: a column's entries together, so a batch
+    holds long segments of a few column keys (up to the whole batch)."""
+    cfg = small_variant(MF_10Mx1M_COLORDER)
+    wl = MFWorkload(cfg)
+    biggest = max(np.bincount(wl.batch(s).col).max() for s in range(cfg.steps_per_epoch))
+    assert biggest > cfg.batch // 2
+    check_step_from_same_state(cfg, range(cfg.steps_per_epoch))
+
+
+@pytest.mark.parametrize("cfg,step", [(MF_10Mx1M, 0), (MF_10Mx1M_COLORDER, 0), (MF_10Mx1M_COLORDER, 346)],
+                         ids=["random", "column_order", "column_order_one_column"])
+def test_mf_paper_scale_one_step(cfg, step):
+    """10M x 1M, rank 100, 1,048,576 entries: the full table, the bench's
+    launch.  In column order, step 346 lies inside the hottest column's 124M
+    entries: one column key with 1,048,576 occurrences."""
     wl = MFWorkload(cfg)
     say("generating the 11M x 100 table")
     W = wl.init_table()
     G = np.zeros_like(W)
     Wt, Gt = dev(W), dev(G)
     s = Store(Wt, Gt, cfg.opt.lr, cfg.opt.eps)
-    bt = wl.batch(0)
+    bt = wl.batch(step)
     say("gpu step")
     loss = gpu_step(s, cfg, bt)
     assert s.error() == 0

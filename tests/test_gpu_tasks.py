@@ -5,8 +5,8 @@ import torch
 
 import oracle
 from paper_2206_00470_amd import Store
-from paper_2206_00470_amd.workloads import (CTR_33M, KGE_COMPLEX, KGE_COMPLEX_2x100, SGNS_1M, CTRWorkload, KGEWorkload,
-                                            SGNSWorkload, small_variant)
+from paper_2206_00470_amd.workloads import (CTR_33M, KGE_COMPLEX, KGE_COMPLEX_2x100, SGNS_1M, SGNS_1M_W2V, CTRWorkload,
+                                            KGEWorkload, SGNSWorkload, small_variant)
 from tests.helpers import assert_bitwise, assert_close_tables, mismatch_fraction, say
 
 pytestmark = pytest.mark.gpu
@@ -183,6 +183,14 @@ def test_deterministic(task):
     assert res[0][2:] == res[1][2:]
 
 
+def test_sgns_word2vec_subsampling_and_dynamic_window_small():
+    """Subsampling 0.01 and per-centre windows of 1..5: centres per batch
+    vary and many context slots are absent."""
+    cfg = small_variant(SGNS_1M_W2V)
+    assert (SGNSWorkload(cfg).batch(1).ctx == -1).mean() > 0.2
+    run_steps("sgns", cfg, range(3))
+
+
 def test_kge_two_times_100_negatives_small():
     """100 head- and 100 tail-corrupted negatives per triple (four id tiles of 64)."""
     run_steps("kge", small_variant(KGE_COMPLEX_2x100), range(3))
@@ -190,7 +198,8 @@ def test_kge_two_times_100_negatives_small():
 
 # ------------------------------------------------------------------ full sizes, one step each
 @pytest.mark.parametrize("task,cfg", [("kge", KGE_COMPLEX), ("ctr", CTR_33M), ("sgns", SGNS_1M),
-                                      ("kge", KGE_COMPLEX_2x100)])
+                                      ("kge", KGE_COMPLEX_2x100), ("sgns", SGNS_1M_W2V)],
+                         ids=["kge", "ctr", "sgns", "kge_2x100", "sgns_w2v"])
 def test_paper_scale_one_step(task, cfg):
     _, WL, gpu, ref = TASKS[task]
     wl = WL(cfg)
