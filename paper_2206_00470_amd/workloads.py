@@ -239,10 +239,24 @@ class CTRConfig:
     init_std: float = 0.1
     opt: AdaGradCfg = field(default_factory=AdaGradCfg)
     seed: int = 0
+    # Wide & Deep (empty deep: the embedding model with pairwise interaction):
+    # rows hold [embedding (emb_dim) | wide weight | zero padding to dim],
+    # the deep part is an MLP with these hidden widths over the F embeddings
+    deep: tuple = ()
+    emb_dim: int = 0
 
     @property
     def num_keys(self) -> int:
         return self.table_rows
+
+    @property
+    def dense_size(self) -> int:
+        """Floats of the Wide & Deep dense buffer (hidden layers, output)."""
+        n, fan = 0, self.n_fields * self.emb_dim
+        for h in self.deep:
+            n += fan * h + h
+            fan = h
+        return n + fan + 1
 
     def occurrences(self, b: int) -> int:
         return b * self.n_fields
@@ -265,6 +279,12 @@ KGE_COMPLEX = KGEConfig("kge_complex_4.6M_d128", n_ent=4_600_000, n_rel=822,
 SGNS_1M = SGNSConfig("sgns_1M_d300", vocab=1_000_000, n_tokens=1_000_000_000, dim=300,
                      window=5, n_neg=25, batch=65_536)
 CTR_33M = CTRConfig("ctr_26f_2^25_d64", n_fields=26, table_rows=1 << 25, dim=64, batch=8192)
+
+# The paper's CTR model is Wide & Deep (Appendix C, "Click-through-rate
+# prediction", learning rate 1e-4): embeddings of 64 plus a wide weight per
+# key (rows of 68 floats with padding), three hidden layers of 1024.
+CTR_33M_WD = replace(CTR_33M, name="ctr_26f_2^25_d64_widedeep", dim=68, emb_dim=64, deep=(1024, 1024, 1024),
+                     opt=AdaGradCfg(lr=1e-4))
 
 CONFIGS = [MF_TINY, MF_10Mx1M, KGE_COMPLEX, SGNS_1M, CTR_33M]
 
@@ -542,7 +562,25 @@ class CTRWorkload:
         return CTRBatch(keys, label)
 
     def init_table(self) -> np.ndarray:
-        return normal_table(self.cfg.num_keys, self.cfg.dim, self.cfg.init_std, self.cfg.seed, self.TAG + 2)
+        W = normal_table(self.cfg.num_keys, self.cfg.dim, self.cfg.init_std, self.cfg.seed, self.TAG + 2)
+        if self.cfg.deep:
+            W[:, self.cfg.emb_dim:] = 0.0      # wide weights start at zero; padding stays zero
+        return W
+
+    def init_dense(self) -> np.ndarray:
+        """Wide & Deep dense buffer: each weight matrix (and the output
+        vector) uniform in +-1/sqrt(fan_in), biases zero, in the layout
+        [W_1, b_1, ..., W_L, b_L, w, c]."""
+        cfg = self.cfg
+        out = np.zeros(cfg.dense_size, np.float32)
+        rng = _rng(cfg.seed, self.TAG + 5, 0)
+        off, fan = 0, cfg.n_fields * cfg.emb_dim
+        for h in cfg.deep:
+            out[off:off + fan * h] = rng.uniform(-1, 1, fan * h) / np.sqrt(fan)
+            off += fan * h + h
+            fan = h
+        out[off:off + fan] = rng.uniform(-1, 1, fan) / np.sqrt(fan)
+        return out
 
 
 def workload(cfg):
