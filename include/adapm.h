@@ -225,16 +225,49 @@ const char* ps_last_error_message(void);
  * row-key merge that also forms the MF gradients and loss (timed under 4,
  * not 0), 5 = row moves of a staged store between its home tables and its
  * slots (on the staging stream; set the mask while no round runs on the
- * library thread, read it after stopping that thread). */
+ * library thread, read it after stopping that thread), 6 = the fp64
+ * matrix-core products of the Wide & Deep step. */
 #define PS_KERNEL_SEGREDUCE 0
 #define PS_KERNEL_TASKGRAD  1
 #define PS_KERNEL_SCATTER   2
 #define PS_KERNEL_PULL      3
 #define PS_KERNEL_MF_ROWMERGE 4
 #define PS_KERNEL_STAGE     5
+#define PS_KERNEL_MLP       6
 #define PS_TIMING_ALL (-1)
 ps_status ps_set_timing(ps_store* s, int32_t mask);
 ps_status ps_read_timing(ps_store* s, int32_t kernel_id, double* total_ms, int64_t* launches);
+
+/* ======================================================================
+ * Wide & Deep click-through-rate step (Appendix C, "Click-through-rate
+ * prediction": the Wide & Deep model, AdaGrad).
+ *
+ * Table rows hold [embedding (emb_dim) | wide weight | anything]; only the
+ * first emb_dim + 1 values of a row enter the model, the rest get a zero
+ * gradient (so AdaGrad leaves them as they are).  For sample b with keys
+ * k_f = keys[b*F + f]:
+ *   x = concat_f W[k_f][0 .. emb_dim)                    (F*emb_dim values)
+ *   h_0 = x;  h_l = relu(h_{l-1} W_l + b_l),  l = 1 .. n_hidden
+ *   logit = h_L . w + c + sum_f W[k_f][emb_dim]
+ *   loss += softplus(logit) - label[b] * logit
+ * The dense parameters are one caller-owned device buffer of fp32 `dense`
+ * (and `dense_accum`, their AdaGrad accumulators, same size): for each
+ * hidden layer W_l (fan_in x fan_out, row-major, fan_in of the first layer
+ * F*emb_dim) then b_l, then w (h_L values) and c (one value).
+ * Arithmetic: the MLP forward and backward in fp64 (on the matrix cores);
+ * each key occurrence's gradient row [dx_f | dlogit | 0 ...] is rounded to
+ * fp32 and merged like every push; the dense gradients are sums over the
+ * batch in fp64, rounded once to fp32, then one per-element AdaGrad step
+ * with the store's lr and eps.  All gradients come from the pre-step
+ * parameters.  A sample with a key outside the table is skipped and
+ * flagged (as ps_step_ctr).  hidden: host array of n_hidden (<= 8) widths.
+ * The workspace size comes from ps_ctr_wd_workspace_bytes (0 = invalid
+ * arguments). */
+size_t ps_ctr_wd_workspace_bytes(int64_t num_keys, int32_t dim, int64_t B, int32_t F, int32_t emb_dim,
+                                 int32_t n_hidden, const int32_t* hidden);
+ps_status ps_step_ctr_wd(ps_store* s, const int64_t* keys, const float* label, int64_t B, int32_t F,
+                         int32_t emb_dim, int32_t n_hidden, const int32_t* hidden, float* dense,
+                         float* dense_accum, double* loss, void* ws, size_t ws_bytes, void* stream);
 
 /* ======================================================================
  * Staged stores: intent signalling and adaptive action timing

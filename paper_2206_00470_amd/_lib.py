@@ -24,6 +24,7 @@ PS_OP_STEP_MF, PS_OP_STEP_KGE, PS_OP_STEP_SGNS, PS_OP_STEP_CTR = 3, 4, 5, 6
 
 PS_KERNEL_SEGREDUCE, PS_KERNEL_TASKGRAD, PS_KERNEL_SCATTER, PS_KERNEL_PULL, PS_KERNEL_MF_ROWMERGE = 0, 1, 2, 3, 4
 PS_KERNEL_STAGE = 5
+PS_KERNEL_MLP = 6
 PS_TIMING_ALL = -1
 
 STAGE_STATS = ["clock", "rounds", "forced", "staged", "evicted", "resident", "pending", "stalled"]
@@ -51,6 +52,8 @@ SIGNATURES = {
     "ps_last_error_message": (C.c_char_p, []),
     "ps_set_timing": (_i32, [_p, _i32]),
     "ps_read_timing": (_i32, [_p, _i32, C.POINTER(C.c_double), C.POINTER(_i64)]),
+    "ps_ctr_wd_workspace_bytes": (_sz, [_i64, _i32, _i64, _i32, _i32, _i32, _p]),
+    "ps_step_ctr_wd": (_i32, [_p, _p, _p, _i64, _i32, _i32, _i32, _p, _p, _p, _p, _p, _sz, _p]),
     "ps_create_staged": (_i32, [C.POINTER(_p), _i64, _i32, _p, _p, _i64, _p, _p, _i64, _p, _i32, _p, _p, _f32, _f32,
                                 _p]),
     "ps_set_action_timing": (_i32, [_p, C.c_double, C.c_double, C.c_double]),

@@ -15,6 +15,7 @@
 #include <vector>
 
 #include "common.hpp"
+#include "mlp.hpp"
 #include "push.hpp"
 #include "sort.hpp"
 #include "staging.hpp"
@@ -46,7 +47,7 @@ ps_status fail(ps_status st, const char* fmt, ...) {
 #define LAUNCHED(name) HIP_TRY(hipGetLastError())
 
 constexpr int64_t MAX_OCC = (int64_t(1) << 31) - (int64_t(1) << 20);
-constexpr int NUM_TIMED = 6;
+constexpr int NUM_TIMED = 7;
 constexpr size_t MAX_TIMED_LAUNCHES = 1 << 14;
 
 }  // namespace
@@ -612,6 +613,86 @@ ps_status make_store(ps_store** out, int64_t num_keys, int32_t dim, int64_t row_
     return fail(PS_ERR_DEVICE, "store set-up: %s", hipGetErrorString(e));
   }
   *out = s;
+  return PS_OK;
+}
+
+// ------------------------------------------------------------------ Wide & Deep
+constexpr int WD_MAX_HIDDEN = 8;
+
+// Offsets of the dense buffer: per hidden layer W (fan_in x fan_out) then b,
+// then the output vector w and bias c.
+struct DenseLayout {
+  int64_t offW[WD_MAX_HIDDEN], offb[WD_MAX_HIDDEN], offw, offc, total, widest;
+};
+
+DenseLayout dense_layout(int64_t K0, int L, const int32_t* hidden) {
+  DenseLayout d{};
+  int64_t off = 0, fan = K0;
+  d.widest = K0;
+  for (int l = 0; l < L; ++l) {
+    d.offW[l] = off;
+    off += fan * hidden[l];
+    d.offb[l] = off;
+    off += hidden[l];
+    fan = hidden[l];
+    d.widest = std::max<int64_t>(d.widest, fan);
+  }
+  d.offw = off;
+  off += fan;
+  d.offc = off;
+  d.total = off + 1;
+  return d;
+}
+
+struct PlanWD {
+  Plan base;                 // the CTR step's sort, segments, gradient rows, loss, validity, translation
+  double* X = nullptr;       // [B][F*E] inputs of the first layer
+  double* H[WD_MAX_HIDDEN] = {};   // [B][h_l] activations
+  double* dA = nullptr;      // [B][widest] gradients, ping-pong
+  double* dB = nullptr;
+  double* dlogit = nullptr;  // [B]
+  double* dg = nullptr;      // dense gradient, fp64, in the dense layout
+  double* part = nullptr;    // column-sum partials
+};
+
+void plan_wd(void* ws, int dim, int64_t B, int F, int E, int L, const int32_t* hidden, PlanWD* p) {
+  const int64_t n = B * F;
+  const DenseLayout d = dense_layout((int64_t)F * E, L, hidden);
+  Carver c(ws);
+  carve_sort(c, n, dim, true, true, &p->base.sb);
+  p->base.grads = c.take<float>(size_t(n) * dim);
+  p->base.loss_part = c.take<double>(LOSS_GRID);
+  p->base.ok = c.take<uint8_t>(B);
+  p->base.trans = c.take<char>(size_t(n) * 8);
+  p->X = c.take<double>(size_t(B) * F * E);
+  for (int l = 0; l < L; ++l) p->H[l] = c.take<double>(size_t(B) * hidden[l]);
+  p->dA = c.take<double>(size_t(B) * d.widest);
+  p->dB = c.take<double>(size_t(B) * d.widest);
+  p->dlogit = c.take<double>(B);
+  p->dg = c.take<double>(d.total);
+  p->part = c.take<double>(size_t(ceil_div(B, COLSUM_ROWS)) * d.widest);
+  p->base.bytes = c.off + 256;
+}
+
+template <bool TA, bool TB, typename BT, int EPI>
+ps_status gemm(ps_store* s, int64_t M, int64_t N, int64_t K, const double* A, int64_t lda, const BT* B, int64_t ldb,
+               double* C, int64_t ldc, const float* bias, const double* mask, int64_t ldm, hipStream_t st) {
+  const int64_t gy = ceil_div(M, GEMM_BM), gx = ceil_div(N, GEMM_BN);
+  if (gy > 65535) return fail(PS_ERR_UNSUPPORTED, "%lld rows exceed the product kernel's grid", (long long)M);
+  Timed t(s, PS_KERNEL_MLP, st);
+  hipLaunchKernelGGL((k_gemm_f64<TA, TB, BT, EPI>), dim3(gx, gy), dim3(BLOCK), 0, st, M, N, K, A, lda, B, ldb, C, ldc,
+                     bias, mask, ldm);
+  LAUNCHED(k_gemm_f64);
+  return PS_OK;
+}
+
+ps_status colsum(const double* A, int64_t rows, int64_t cols, const double* scale, double* part, double* out,
+                 hipStream_t st) {
+  const int64_t ny = ceil_div(rows, COLSUM_ROWS);
+  hipLaunchKernelGGL(k_colsum_part, dim3(ceil_div(cols, BLOCK), ny), dim3(BLOCK), 0, st, A, rows, cols, scale, part);
+  LAUNCHED(k_colsum_part);
+  hipLaunchKernelGGL(k_colsum_final, dim3(ceil_div(cols, BLOCK)), dim3(BLOCK), 0, st, part, ny, cols, out);
+  LAUNCHED(k_colsum_final);
   return PS_OK;
 }
 
@@ -1245,6 +1326,119 @@ ps_status ps_step_ctr(ps_store* s, const int64_t* keys, const float* label, int6
   int64_t* tk = reinterpret_cast<int64_t*>(t);
   if (ps_status r = translate_keys(s, keys, B * F, tk, as_stream(stream))) return r;
   return step_ctr_impl(s, tk, label, B, F, loss, ws, ws_bytes, stream);
+}
+
+// ---------------------------------------------------------------- Wide & Deep CTR
+size_t ps_ctr_wd_workspace_bytes(int64_t num_keys, int32_t dim, int64_t B, int32_t F, int32_t emb_dim,
+                                 int32_t n_hidden, const int32_t* hidden) {
+  if (num_keys < 1 || dim < 1 || B < 0 || F < 1 || emb_dim < 1 || emb_dim >= dim || n_hidden < 0 ||
+      n_hidden > WD_MAX_HIDDEN || (n_hidden > 0 && !hidden))
+    return 0;
+  for (int l = 0; l < n_hidden; ++l)
+    if (hidden[l] < 1) return 0;
+  if (B > MAX_OCC / F) return 0;
+  PlanWD p;
+  plan_wd(nullptr, dim, B, F, emb_dim, n_hidden, hidden, &p);
+  return p.base.bytes;
+}
+
+ps_status ps_step_ctr_wd(ps_store* s, const int64_t* keys, const float* label, int64_t B, int32_t F, int32_t emb_dim,
+                         int32_t n_hidden, const int32_t* hidden, float* dense, float* dense_accum, double* loss,
+                         void* ws, size_t ws_bytes, void* stream) {
+  if (ps_status st = check_store(s)) return st;
+  if (F < 1) return fail(PS_ERR_INVALID, "need F >= 1");
+  if (emb_dim < 1 || emb_dim >= s->dim) return fail(PS_ERR_INVALID, "need 1 <= emb_dim < dim (the row holds the wide weight)");
+  if (n_hidden < 0 || n_hidden > WD_MAX_HIDDEN || (n_hidden > 0 && !hidden))
+    return fail(PS_ERR_INVALID, "need 0 <= n_hidden <= %d hidden widths", WD_MAX_HIDDEN);
+  for (int l = 0; l < n_hidden; ++l)
+    if (hidden[l] < 1) return fail(PS_ERR_INVALID, "hidden width %d < 1", hidden[l]);
+  if (ps_status st = check_n(B, F)) return st;
+  hipStream_t st = as_stream(stream);
+  if (B == 0) return zero_loss(loss, st);
+  if (!keys || !label || !dense || !dense_accum) return fail(PS_ERR_INVALID, "keys, label or a dense buffer is NULL");
+  const int L = n_hidden;
+  const int E = emb_dim;
+  const int64_t K0 = (int64_t)F * E;
+  const int64_t n = B * F;
+  PlanWD p;
+  plan_wd(ws, s->dim, B, F, E, L, hidden, &p);
+  if (ps_status r = check_ws(p.base, ws, ws_bytes)) return r;
+  const DenseLayout d = dense_layout(K0, L, hidden);
+  if (s->stg) {
+    int64_t* tk = reinterpret_cast<int64_t*>(p.base.trans);
+    if (ps_status r = translate_keys(s, keys, n, tk, st)) return r;
+    keys = tk;
+  }
+  hipLaunchKernelGGL(k_unit_valid<ValidCTR>, dim3(small_grid(B, WAVES_PER_BLOCK, 4096)), dim3(BLOCK), 0, st,
+                     ValidCTR{keys, F, s->num_keys}, B, p.base.ok, s->status);
+  LAUNCHED(k_unit_valid);
+  // the key sort and segments run beside the MLP on the store's second stream
+  if (ps_status r = fork_aux(s, st)) return r;
+  uint32_t *ks, *perm;
+  if (ps_status r = run_sort(s, KeysCTR{keys, F, p.base.ok}, n, s->num_keys, p.base.sb, s->status, nullptr, true,
+                             s->aux, &ks, &perm))
+    return r;
+  if (ps_status r = run_segments(p.base.sb, ks, n, s->num_keys, p.base.sb.seg_off, nullptr, s->aux)) return r;
+  // inputs
+  RowShape shape;
+  row_shape(E, E % 4 == 0 && s->ld % 4 == 0, &shape);
+  if (ps_status r = with_shape(shape, [&]<int Lw, int NV, int VW>() -> ps_status {
+        hipLaunchKernelGGL((k_wd_gather<Lw, NV, VW>), dim3(small_grid(n, BLOCK / Lw, 16384)), dim3(BLOCK), 0, st, s->W,
+                           s->ld, keys, B, F, E, p.base.ok, p.X);
+        LAUNCHED(k_wd_gather);
+        return PS_OK;
+      }))
+    return r;
+  // forward
+  const double* h = p.X;
+  int64_t fan = K0;
+  for (int l = 0; l < L; ++l) {
+    if (ps_status r = gemm<false, false, float, EPI_BIAS_RELU>(s, B, hidden[l], fan, h, fan, dense + d.offW[l],
+                                                               hidden[l], p.H[l], hidden[l], dense + d.offb[l],
+                                                               nullptr, 0, st))
+      return r;
+    h = p.H[l];
+    fan = hidden[l];
+  }
+  const int64_t head_grid = small_grid(B, WAVES_PER_BLOCK, LOSS_GRID);
+  hipLaunchKernelGGL(k_wd_head, dim3(head_grid), dim3(BLOCK), 0, st, h, fan, dense + d.offw, dense + d.offc, s->W,
+                     s->ld, E, keys, F, label, p.base.ok, B, L > 0 ? 1 : 0, p.dlogit, p.dA, p.base.loss_part);
+  LAUNCHED(k_wd_head);
+  if (loss) {
+    hipLaunchKernelGGL(k_sum_loss, dim3(1), dim3(BLOCK), 0, st, p.base.loss_part, head_grid, loss);
+    LAUNCHED(k_sum_loss);
+  }
+  // output layer gradients
+  if (ps_status r = colsum(h, B, fan, p.dlogit, p.part, p.dg + d.offw, st)) return r;
+  if (ps_status r = colsum(p.dlogit, B, 1, nullptr, p.part, p.dg + d.offc, st)) return r;
+  // backward through the hidden layers
+  double* cur = p.dA;
+  for (int l = L - 1; l >= 0; --l) {
+    const double* hp = l > 0 ? p.H[l - 1] : p.X;
+    const int64_t fin = l > 0 ? hidden[l - 1] : K0;
+    const int64_t fout = hidden[l];
+    if (ps_status r = gemm<true, false, double, EPI_STORE>(s, fin, fout, B, hp, fin, cur, fout, p.dg + d.offW[l],
+                                                           fout, nullptr, nullptr, 0, st))
+      return r;
+    if (ps_status r = colsum(cur, B, fout, nullptr, p.part, p.dg + d.offb[l], st)) return r;
+    double* next = cur == p.dA ? p.dB : p.dA;
+    ps_status r = l > 0 ? gemm<false, true, float, EPI_MASK>(s, B, fin, fout, cur, fout, dense + d.offW[l], fout,
+                                                            next, fin, nullptr, hp, fin, st)
+                        : gemm<false, true, float, EPI_STORE>(s, B, fin, fout, cur, fout, dense + d.offW[l], fout,
+                                                             next, fin, nullptr, nullptr, 0, st);
+    if (r) return r;
+    cur = next;
+  }
+  // per-occurrence embedding gradient rows, at their sorted positions
+  if (ps_status r = join_aux(s, st)) return r;
+  hipLaunchKernelGGL(k_wd_rows, dim3(small_grid(n, WAVES_PER_BLOCK, 16384)), dim3(BLOCK), 0, st, cur, p.dlogit, B, F,
+                     E, s->dim, p.base.sb.rank, p.base.grads);
+  LAUNCHED(k_wd_rows);
+  if (ps_status r = run_reduce(s, p.base.sb, ks, SrcSorted{p.base.grads, s->dim}, n, {PART_ALL}, st)) return r;
+  hipLaunchKernelGGL(k_dense_adagrad, dim3(small_grid(d.total, BLOCK, 4096)), dim3(BLOCK), 0, st, dense, dense_accum,
+                     p.dg, d.total, s->lr, s->eps);
+  LAUNCHED(k_dense_adagrad);
+  return PS_OK;
 }
 
 // ---------------------------------------------------------------- staged stores

@@ -213,6 +213,22 @@ class Store:
         check(lib().ps_step_ctr(self._h, _ptr(keys), _ptr(label), B, F, _ptr(loss), ws, wsb, _stream(stream)))
         return loss
 
+    def step_ctr_wd(self, keys, label, dense, dense_acc, emb_dim: int, hidden, loss=None, stream=None):
+        """Wide & Deep CTR step: rows [embedding (emb_dim) | wide weight | ...],
+        an MLP of the given hidden widths over the F embeddings; `dense` and
+        `dense_acc` are the flat fp32 dense parameters and accumulators."""
+        _dev(keys, torch.int64, "keys"), _dev(label, torch.float32, "label")
+        _dev(dense, torch.float32, "dense"), _dev(dense_acc, torch.float32, "dense_acc")
+        B = label.numel()
+        F = keys.numel() // B if B else 1
+        hid = (C.c_int32 * max(len(hidden), 1))(*hidden)
+        loss = self._loss(loss)
+        nbytes = int(lib().ps_ctr_wd_workspace_bytes(self.num_keys, self.dim, B, F, emb_dim, len(hidden), hid))
+        ws, wsb = self.ws.get(nbytes)
+        check(lib().ps_step_ctr_wd(self._h, _ptr(keys), _ptr(label), B, F, emb_dim, len(hidden), hid, _ptr(dense),
+                                   _ptr(dense_acc), _ptr(loss), ws, wsb, _stream(stream)))
+        return loss
+
     # ---------------------------------------------------------------- status and timing
     def error(self, stream=None) -> int:
         """Synchronize, then return and clear the sticky device status."""
