@@ -33,6 +33,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0   # MI355X HBM3E
 HOST_LINK_GBPS = 64.0    # PCIe 5.0 x16, one direction
+MFMA_F64_TFLOPS = 78.6   # MI355X dense fp64 matrix peak
 
 
 def parse():
@@ -41,7 +42,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="mf", choices=["mf", "mf_tiny", "mf_colorder", "kge", "kge2x100", "sgns",
-                                                           "sgns_w2v", "ctr"])
+                                                           "sgns_w2v", "ctr", "ctr_wd"])
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="bound on the CPU-oracle sample (0 = skip)")
     ap.add_argument("--no-ops", action="store_true", help="skip the pull-only / push-only measurements")
@@ -105,13 +106,17 @@ class Bench:
         self.task = {"mf_tiny": "mf", "mf_colorder": "mf", "kge2x100": "kge", "sgns_w2v": "sgns"}.get(name, name)
         cfgs = {"mf": wls.MF_10Mx1M, "mf_tiny": wls.MF_TINY, "mf_colorder": wls.MF_10Mx1M_COLORDER,
                 "kge": wls.KGE_COMPLEX, "kge2x100": wls.KGE_COMPLEX_2x100, "sgns": wls.SGNS_1M,
-                "sgns_w2v": wls.SGNS_1M_W2V, "ctr": wls.CTR_33M}
+                "sgns_w2v": wls.SGNS_1M_W2V, "ctr": wls.CTR_33M, "ctr_wd": wls.CTR_33M_WD}
         self.cfg = cfg = cfgs[name]
         self.wl = wls.workload(cfg)
         self.dev = dev
         self.dim = cfg.dim
         self.R = 4 * cfg.dim
         self.W = self.wl.init_table()
+        if self.task == "ctr_wd":
+            self.dense0 = self.wl.init_dense()
+            self.D = torch.from_numpy(self.dense0).to(dev)
+            self.A = torch.zeros_like(self.D)
         T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
         self.T = T
         self.batches, self.host_batches, self.occ, self.uniq = [], [], [], []
@@ -145,8 +150,21 @@ class Bench:
             store.step_kge(b["head"], b["rel"], b["tail"], b["neg"], c.n_head_neg, c.n_ent, loss=loss)
         elif self.task == "sgns":
             store.step_sgns(b["centre"], b["ctx"], b["neg"], c.window, c.vocab, loss=loss)
+        elif self.task == "ctr_wd":
+            store.step_ctr_wd(b["keys"], b["label"], self.D, self.A, c.emb_dim, c.deep, loss=loss)
         else:
             store.step_ctr(b["keys"], b["label"], loss=loss)
+
+    def mlp_flops(self, B):
+        """fp64 products of one Wide & Deep step: per hidden layer the
+        forward, the weight gradient and the input gradient, 2 B fan_in
+        fan_out flops each."""
+        c = self.cfg
+        fan, fl = c.n_fields * c.emb_dim, 0.0
+        for h in c.deep:
+            fl += 3 * 2.0 * B * fan * h
+            fan = h
+        return fl
 
     def run_overlapped(self, store, first, count, loss):
         """MF steps first .. first+count-1 with the two-phase step: the key work
@@ -203,6 +221,9 @@ class Bench:
             B, F = bt.keys.shape
             return {"segreduce": n * R + table,
                     "taskgrad": B * (4.0 + F * (8.0 + R + R + 4.0))}
+        if self.task == "ctr_wd":
+            # "mlp" counts flops of the fp64 products, not bytes
+            return {"segreduce": n * R + table, "mlp": self.mlp_flops(bt.keys.shape[0])}
         if self.task == "kge":
             B, nn = bt.neg.shape
             return {"segreduce": n * 4.0 + 3 * B * R + B * nn * 8.0 + 2 * B * 2 * R + table,
@@ -218,6 +239,13 @@ class Bench:
         import oracle
         c, bt = self.cfg, self.wl.batch(i)
         lr, eps = c.opt.lr, c.opt.eps
+        if self.task == "ctr_wd":
+            from oracle.widedeep import step_ctr_wd
+            if not hasattr(self, "_dense_host"):
+                self._dense_host = self.dense0.copy()
+                self._acc_host = np.zeros_like(self._dense_host)
+            step_ctr_wd(W, G, self._dense_host, self._acc_host, bt.keys, bt.label, c.emb_dim, c.deep, lr, eps)
+            return self.keys_of(bt).size
         if self.rowwise:
             args = {"mf": (bt.row, bt.col, bt.val, c.n_rows, c.lam),
                     "kge": (bt.head, bt.rel, bt.tail, bt.neg, c.n_head_neg, c.n_ent),
@@ -327,12 +355,14 @@ def cpu_baseline(args, wb, rowwise):
     cfg = wb.cfg
     W = wb.W
     G = np.zeros(W.shape[0], np.float32) if rowwise else np.zeros_like(W)
+    from threadpoolctl import threadpool_limits
     done, rows, tc0 = 0, 0, time.perf_counter()
-    while True:
-        rows += 2 * wb.oracle_step(W, G, 1000 + done)
-        done += 1
-        if time.perf_counter() - tc0 >= args.cpu_seconds:
-            break
+    with threadpool_limits(1):               # numpy's matrix products single-threaded, like the C oracle
+        while True:
+            rows += 2 * wb.oracle_step(W, G, 1000 + done)
+            done += 1
+            if time.perf_counter() - tc0 >= args.cpu_seconds:
+                break
     tc = time.perf_counter() - tc0
     return {"value": rows / tc, "unit": "rows/s", "cores": 1, "kind": "oracle",
             "sample": f"{done} step(s) of the same workload on the full {cfg.num_keys}x{cfg.dim} table, "
@@ -397,7 +427,7 @@ def main():
           file=sys.stderr, flush=True)
 
     KID = {"segreduce": _lib.PS_KERNEL_SEGREDUCE, "taskgrad": _lib.PS_KERNEL_TASKGRAD,
-           "rowmerge": _lib.PS_KERNEL_MF_ROWMERGE, "scatter": _lib.PS_KERNEL_SCATTER}
+           "rowmerge": _lib.PS_KERNEL_MF_ROWMERGE, "scatter": _lib.PS_KERNEL_SCATTER, "mlp": _lib.PS_KERNEL_MLP}
     names = list(wb.alg_bytes(0))                 # kernels with algorithmic bytes for this workload
 
     # (MF tiny is launch-bound: the extra events of the overlap cost more than it hides)
@@ -466,17 +496,18 @@ def main():
         return {"avg_ms": ms / max(cnt, 1), "ms_per_step": per_step_ms, "launches": cnt,
                 "alg_bytes_per_step": nbytes,
                 "alg_GBps": nbytes / (per_step_ms * 1e-3) / 1e9 if cnt else None,
-                "launches_per_step": seg_launches_per_step if name == "segreduce" else 1}
+                "launches_per_step": seg_launches_per_step if name == "segreduce" else
+                (3 * len(wb.cfg.deep) if name == "mlp" else 1)}
 
     kernels = {name: kernel_entry(name, kt_all[name], nprof, idx_prof) for name in names}
     # from the timed steps (graph mode: from the eager breakdown steps)
     dk = kernels[dom] if args.graph else kernel_entry(dom, kt[dom], args.steps, idx)
     kernels["scatter"] = {"ms_per_step": kt_all["scatter"][0] / nprof, "launches": kt_all["scatter"][1]}
     symbol = {"segreduce": "k_segreduce<%s>" % {"mf": "SrcSorted", "kge": "SrcKGE", "sgns": "SrcSGNS",
-                                                 "ctr": "SrcSorted"}[wb.task],
-              "rowmerge": "k_segreduce<SrcMFRow>",
+                                                 "ctr": "SrcSorted", "ctr_wd": "SrcSorted"}[wb.task],
+              "rowmerge": "k_segreduce<SrcMFRow>", "mlp": "k_gemm_f64",
               "taskgrad": {"mf": "k_mf_pack", "kge": "k_kge_grad", "sgns": "k_sgns_grad",
-                           "ctr": "k_ctr_grad"}[wb.task]}[dom]
+                           "ctr": "k_ctr_grad", "ctr_wd": "k_wd_head"}[wb.task]}[dom]
     traffic = counter_traffic(args.workload + ("_rowwise" if rowwise else ""), symbol)
     roofline = {
         "bound": "hbm",
@@ -489,6 +520,12 @@ def main():
         "avg_ms": round(dk["avg_ms"], 4),
         "alg_bytes_per_launch": int(dk["alg_bytes_per_step"] / dk["launches_per_step"]),
     }
+    if dom == "mlp":
+        tf = dk["alg_GBps"] / 1e3            # "bytes" of the mlp entry are flops
+        roofline = {"bound": "mfma", "kernel": symbol, "dtype": "f64", "achieved": round(tf, 2),
+                    "peak": MFMA_F64_TFLOPS, "unit": "TFLOP/s", "frac": round(tf / MFMA_F64_TFLOPS, 4),
+                    "traffic": None, "avg_ms": round(dk["avg_ms"], 4),
+                    "alg_flops_per_launch": int(dk["alg_bytes_per_step"] / dk["launches_per_step"])}
 
     # ------------------------------------------------------------ push-only / pull-only (MF)
     ops = {}
@@ -577,7 +614,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "f64" if wb.task == "ctr_wd" else "f32",   # the Wide & Deep MLP runs in fp64
         "data": "synthetic",
         "config": {"workload": cfg.name, "num_keys": cfg.num_keys, "dim": cfg.dim, "layout": args.layout,
                    "update": args.update,
