@@ -653,7 +653,17 @@ struct PlanWD {
   double* dlogit = nullptr;  // [B]
   double* dg = nullptr;      // dense gradient, fp64, in the dense layout
   double* part = nullptr;    // column-sum partials
+  double* slices = nullptr;  // split-K partial products of the weight gradients
 };
+
+// K slices of a weight-gradient product (K = the batch): enough workgroups
+// to fill the chip (about 1024), slices of at least 256 rows.
+int64_t wgrad_slices(int64_t M, int64_t N, int64_t K) {
+  const int64_t blocks = ceil_div(M, GEMM_BM) * ceil_div(N, GEMM_BN);
+  int64_t S = ceil_div(1024, blocks);
+  S = std::min<int64_t>(S, std::max<int64_t>(1, K / 256));
+  return std::max<int64_t>(1, std::min<int64_t>(S, 32));
+}
 
 void plan_wd(void* ws, int dim, int64_t B, int F, int E, int L, const int32_t* hidden, PlanWD* p) {
   const int64_t n = B * F;
@@ -671,18 +681,36 @@ void plan_wd(void* ws, int dim, int64_t B, int F, int E, int L, const int32_t* h
   p->dlogit = c.take<double>(B);
   p->dg = c.take<double>(d.total);
   p->part = c.take<double>(size_t(ceil_div(B, COLSUM_ROWS)) * d.widest);
+  int64_t sl = 0, fan = (int64_t)F * E;
+  for (int l = 0; l < L; ++l) {
+    const int64_t S = wgrad_slices(fan, hidden[l], B);
+    if (S > 1) sl = std::max<int64_t>(sl, S * fan * hidden[l]);
+    fan = hidden[l];
+  }
+  p->slices = c.take<double>(size_t(sl));
   p->base.bytes = c.off + 256;
 }
 
-template <bool TA, bool TB, typename BT, int EPI>
+// One product; with S > 1 K is split into S slices whose partial products go
+// to `slices` (S * M * N doubles) and are then added in order into C (which
+// must then be dense: ldc = N, plain store).
+template <bool TA, bool TB, typename BT>
 ps_status gemm(ps_store* s, int64_t M, int64_t N, int64_t K, const double* A, int64_t lda, const BT* B, int64_t ldb,
-               double* C, int64_t ldc, const float* bias, const double* mask, int64_t ldm, hipStream_t st) {
+               double* C, int64_t ldc, hipStream_t st, int64_t S = 1, double* slices = nullptr) {
   const int64_t gy = ceil_div(M, GEMM_BM), gx = ceil_div(N, GEMM_BN);
   if (gy > 65535) return fail(PS_ERR_UNSUPPORTED, "%lld rows exceed the product kernel's grid", (long long)M);
-  Timed t(s, PS_KERNEL_MLP, st);
-  hipLaunchKernelGGL((k_gemm_f64<TA, TB, BT, EPI>), dim3(gx, gy), dim3(BLOCK), 0, st, M, N, K, A, lda, B, ldb, C, ldc,
-                     bias, mask, ldm);
-  LAUNCHED(k_gemm_f64);
+  const int64_t kslice = S > 1 ? ceil_div(ceil_div(K, S), GEMM_BK) * GEMM_BK : K;
+  S = S > 1 ? ceil_div(K, kslice) : 1;
+  {
+    Timed t(s, PS_KERNEL_MLP, st);
+    hipLaunchKernelGGL((k_gemm_f64<TA, TB, BT>), dim3(gx, gy, S), dim3(BLOCK), 0, st, M, N, K, A, lda, B, ldb,
+                       S > 1 ? slices : C, S > 1 ? N : ldc, kslice);
+    LAUNCHED(k_gemm_f64);
+    if (S > 1) {
+      hipLaunchKernelGGL(k_sum_slices, dim3(small_grid(M * N, BLOCK, 4096)), dim3(BLOCK), 0, st, slices, S, M * N, C);
+      LAUNCHED(k_sum_slices);
+    }
+  }
   return PS_OK;
 }
 
@@ -1393,10 +1421,12 @@ ps_status ps_step_ctr_wd(ps_store* s, const int64_t* keys, const float* label, i
   const double* h = p.X;
   int64_t fan = K0;
   for (int l = 0; l < L; ++l) {
-    if (ps_status r = gemm<false, false, float, EPI_BIAS_RELU>(s, B, hidden[l], fan, h, fan, dense + d.offW[l],
-                                                               hidden[l], p.H[l], hidden[l], dense + d.offb[l],
-                                                               nullptr, 0, st))
+    if (ps_status r = gemm<false, false, float>(s, B, hidden[l], fan, h, fan, dense + d.offW[l], hidden[l], p.H[l],
+                                                hidden[l], st))
       return r;
+    hipLaunchKernelGGL(k_bias_relu, dim3(small_grid(B * hidden[l], BLOCK, 8192)), dim3(BLOCK), 0, st, p.H[l], B,
+                       (int64_t)hidden[l], dense + d.offb[l]);
+    LAUNCHED(k_bias_relu);
     h = p.H[l];
     fan = hidden[l];
   }
@@ -1417,16 +1447,17 @@ ps_status ps_step_ctr_wd(ps_store* s, const int64_t* keys, const float* label, i
     const double* hp = l > 0 ? p.H[l - 1] : p.X;
     const int64_t fin = l > 0 ? hidden[l - 1] : K0;
     const int64_t fout = hidden[l];
-    if (ps_status r = gemm<true, false, double, EPI_STORE>(s, fin, fout, B, hp, fin, cur, fout, p.dg + d.offW[l],
-                                                           fout, nullptr, nullptr, 0, st))
+    if (ps_status r = gemm<true, false, double>(s, fin, fout, B, hp, fin, cur, fout, p.dg + d.offW[l], fout, st,
+                                                wgrad_slices(fin, fout, B), p.slices))
       return r;
     if (ps_status r = colsum(cur, B, fout, nullptr, p.part, p.dg + d.offb[l], st)) return r;
     double* next = cur == p.dA ? p.dB : p.dA;
-    ps_status r = l > 0 ? gemm<false, true, float, EPI_MASK>(s, B, fin, fout, cur, fout, dense + d.offW[l], fout,
-                                                            next, fin, nullptr, hp, fin, st)
-                        : gemm<false, true, float, EPI_STORE>(s, B, fin, fout, cur, fout, dense + d.offW[l], fout,
-                                                             next, fin, nullptr, nullptr, 0, st);
-    if (r) return r;
+    if (ps_status r = gemm<false, true, float>(s, B, fin, fout, cur, fout, dense + d.offW[l], fout, next, fin, st))
+      return r;
+    if (l > 0) {
+      hipLaunchKernelGGL(k_relu_mask, dim3(small_grid(B * fin, BLOCK, 8192)), dim3(BLOCK), 0, st, next, hp, B * fin);
+      LAUNCHED(k_relu_mask);
+    }
     cur = next;
   }
   // per-occurrence embedding gradient rows, at their sorted positions

@@ -15,22 +15,27 @@ namespace adapm {
 typedef double f64x4 __attribute__((ext_vector_type(4)));
 
 // ------------------------------------------------------------------ GEMM
-// C[M][N] = op(A)[M][K] op(B)[K][N] with an epilogue, all sums in fp64.
+// C[M][N] = op(A)[M][K] op(B)[K][N], all sums in fp64.
 // op(A)[m][k] = TA ? A[k * lda + m] : A[m * lda + k]; op(B) likewise with
-// TB.  B's elements are fp32 (the dense parameters) or fp64.
-// Epilogues: store; add bias[n] (fp32) then ReLU; keep only where
-// mask[m * ldm + n] > 0 (the ReLU derivative of the layer below).
-enum { EPI_STORE = 0, EPI_BIAS_RELU = 1, EPI_MASK = 2 };
-
-constexpr int GEMM_BM = 64, GEMM_BN = 64, GEMM_BK = 16;
+// TB.  B's elements are fp32 (the dense parameters) or fp64.  The bias and
+// ReLU of a forward layer and the ReLU mask of a backward one are applied
+// by k_bias_relu / k_relu_mask afterwards: an epilogue with arithmetic would
+// copy the 128 accumulator registers into ordinary ones and halve the
+// workgroups a compute unit holds.
+//
+// A workgroup computes a 128 x 128 tile of C, each of its four wavefronts a
+// 64 x 64 quarter as 4 x 4 products of 16 x 16.  K advances 16 at a time
+// through LDS; the next step's operands are loaded into registers while the
+// matrix cores work on the current one.  With gridDim.z = S > 1 the K range
+// is split into S slices and slice z writes its partial product to
+// C + z * M * N (plain store only); k_sum_slices adds them in slice order.
+constexpr int GEMM_BM = 128, GEMM_BN = 128, GEMM_BK = 16;
 constexpr int GEMM_PAD = 2;   // doubles of padding per LDS row
 
-template <bool TA, bool TB, typename BT, int EPI>
+template <bool TA, bool TB, typename BT>
 __global__ __launch_bounds__(BLOCK) void k_gemm_f64(int64_t M, int64_t N, int64_t K, const double* __restrict__ A,
                                                     int64_t lda, const BT* __restrict__ B, int64_t ldb,
-                                                    double* __restrict__ C, int64_t ldc,
-                                                    const float* __restrict__ bias, const double* __restrict__ mask,
-                                                    int64_t ldm) {
+                                                    double* __restrict__ C, int64_t ldc, int64_t kslice) {
   __shared__ double As[GEMM_BK][GEMM_BM + GEMM_PAD];   // [k][m]
   __shared__ double Bs[GEMM_BK][GEMM_BN + GEMM_PAD];   // [k][n]
   const int t = threadIdx.x;
@@ -38,86 +43,111 @@ __global__ __launch_bounds__(BLOCK) void k_gemm_f64(int64_t M, int64_t N, int64_
   const int wave = t / WAVE;
   const int64_t m0 = (int64_t)blockIdx.y * GEMM_BM;
   const int64_t n0 = (int64_t)blockIdx.x * GEMM_BN;
-  const int wm = (wave / 2) * 32;   // the wave's 32 x 32 quarter of the tile
-  const int wn = (wave % 2) * 32;
-  f64x4 acc[2][2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
+  const int64_t kbeg = (int64_t)blockIdx.z * kslice;
+  const int64_t kend = kbeg + kslice < K ? kbeg + kslice : K;
+  if (gridDim.z > 1) C += (int64_t)blockIdx.z * M * N;
+  const int wm = (wave / 2) * 64;   // the wave's 64 x 64 quarter of the tile
+  const int wn = (wave % 2) * 64;
 
-  for (int64_t k0 = 0; k0 < K; k0 += GEMM_BK) {
-    // A tile: 64 x 16 elements, 4 per thread, read along A's contiguous axis
-    if constexpr (!TA) {
-      const int r = t / 4, kq = (t % 4) * 4;
-      const int64_t m = m0 + r;
+  // the thread's 8 elements of each operand tile: A (TA = false) rows t/2,
+  // k (t%2)*8..+8; A (TA) k t/16, m (t%16)*8..+8; B likewise
+  const int ar = TA ? t / 16 : t / 2;            // TA: k row; else m row
+  const int aq = TA ? (t % 16) * 8 : (t % 2) * 8;
+  const int br = TB ? t / 2 : t / 16;            // TB: n row; else k row
+  const int bq = TB ? (t % 2) * 8 : (t % 16) * 8;
+  double ra[8], rb[8];
+  auto load = [&](int64_t k0) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int64_t k = k0 + kq + e;
-        As[kq + e][r] = (m < M && k < K) ? A[m * lda + k] : 0.0;
+    for (int e = 0; e < 8; ++e) {
+      if constexpr (!TA) {
+        const int64_t m = m0 + ar, k = k0 + aq + e;
+        ra[e] = (m < M && k < kend) ? A[m * lda + k] : 0.0;
+      } else {
+        const int64_t k = k0 + ar, m = m0 + aq + e;
+        ra[e] = (m < M && k < kend) ? A[k * lda + m] : 0.0;
       }
-    } else {
-      const int kk = t / 16, mq = (t % 16) * 4;
-      const int64_t k = k0 + kk;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int64_t m = m0 + mq + e;
-        As[kk][mq + e] = (m < M && k < K) ? A[k * lda + m] : 0.0;
-      }
-    }
-    // B tile: 16 x 64
-    if constexpr (!TB) {
-      const int kk = t / 16, nq = (t % 16) * 4;
-      const int64_t k = k0 + kk;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int64_t n = n0 + nq + e;
-        Bs[kk][nq + e] = (n < N && k < K) ? (double)B[k * ldb + n] : 0.0;
-      }
-    } else {
-      const int c = t / 4, kq = (t % 4) * 4;
-      const int64_t n = n0 + c;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int64_t k = k0 + kq + e;
-        Bs[kq + e][c] = (n < N && k < K) ? (double)B[n * ldb + k] : 0.0;
+      if constexpr (!TB) {
+        const int64_t k = k0 + br, n = n0 + bq + e;
+        rb[e] = (n < N && k < kend) ? (double)B[k * ldb + n] : 0.0;
+      } else {
+        const int64_t n = n0 + br, k = k0 + bq + e;
+        rb[e] = (n < N && k < kend) ? (double)B[n * ldb + k] : 0.0;
       }
     }
+  };
+  auto stash = [&]() {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      if constexpr (!TA) As[aq + e][ar] = ra[e];
+      else As[ar][aq + e] = ra[e];
+      if constexpr (!TB) Bs[br][bq + e] = rb[e];
+      else Bs[bq + e][br] = rb[e];
+    }
+  };
+
+  f64x4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
+
+  if (kbeg < kend) load(kbeg);
+  for (int64_t k0 = kbeg; k0 < kend; k0 += GEMM_BK) {
+    stash();
     __syncthreads();
+    if (k0 + GEMM_BK < kend) load(k0 + GEMM_BK);   // in flight during the products below
 #pragma unroll
     for (int ks = 0; ks < GEMM_BK; ks += 4) {
       const int kr = ks + lane / 16;
-      double a[2], b[2];
+      double a[4], b[4];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) a[i] = As[kr][wm + i * 16 + lane % 16];
+      for (int i = 0; i < 4; ++i) a[i] = As[kr][wm + i * 16 + lane % 16];
 #pragma unroll
-      for (int j = 0; j < 2; ++j) b[j] = Bs[kr][wn + j * 16 + lane % 16];
+      for (int j = 0; j < 4; ++j) b[j] = Bs[kr][wn + j * 16 + lane % 16];
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[i], b[j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[i], b[j], acc[i][j], 0, 0, 0);
     }
     __syncthreads();
   }
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int64_t m = m0 + wm + i * 16 + lane / 16 + 4 * v;
         const int64_t n = n0 + wn + j * 16 + lane % 16;
-        if (m < M && n < N) {
-          double x = acc[i][j][v];
-          if constexpr (EPI == EPI_BIAS_RELU) {
-            x += (double)bias[n];
-            x = x > 0.0 ? x : 0.0;
-          } else if constexpr (EPI == EPI_MASK) {
-            x = mask[m * ldm + n] > 0.0 ? x : 0.0;
-          }
-          C[m * ldc + n] = x;
-        }
+        if (m < M && n < N) C[m * ldc + n] = acc[i][j][v];
       }
+}
+
+// H[m][n] = max(H[m][n] + bias[n], 0): a forward layer's bias and ReLU.
+__global__ __launch_bounds__(BLOCK) void k_bias_relu(double* __restrict__ H, int64_t M, int64_t N,
+                                                     const float* __restrict__ bias) {
+  const int64_t n_all = M * N;
+  for (int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x; i < n_all; i += (int64_t)gridDim.x * BLOCK) {
+    const double x = H[i] + (double)bias[i % N];
+    H[i] = x > 0.0 ? x : 0.0;
+  }
+}
+
+// D[m][n] = 0 where H[m][n] <= 0: the ReLU derivative of the layer below.
+__global__ __launch_bounds__(BLOCK) void k_relu_mask(double* __restrict__ D, const double* __restrict__ H,
+                                                     int64_t count) {
+  for (int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x; i < count; i += (int64_t)gridDim.x * BLOCK)
+    if (!(H[i] > 0.0)) D[i] = 0.0;
+}
+
+// out[i] = sum over z of part[z * count + i], z = 0 .. S-1 in order.
+__global__ __launch_bounds__(BLOCK) void k_sum_slices(const double* __restrict__ part, int64_t S, int64_t count,
+                                                      double* __restrict__ out) {
+  for (int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x; i < count; i += (int64_t)gridDim.x * BLOCK) {
+    double t = 0.0;
+    for (int64_t z = 0; z < S; ++z) t += part[z * count + i];
+    out[i] = t;
+  }
 }
 
 // ------------------------------------------------------------------ inputs and head
