@@ -123,3 +123,53 @@ def test_wd_paper_scale_one_step():
     assert_close_tables(Gt.cpu().numpy(), G, "G")
     assert_close_tables(Dt.cpu().numpy(), dense, "dense parameters")
     assert_close_tables(At.cpu().numpy(), A, "dense accumulators")
+
+
+def test_wd_on_a_staged_store():
+    """Home table in pinned host memory, slots for the batch's keys: the
+    same step as on an in-HBM store (the keys are translated to slots)."""
+    from paper_2206_00470_amd import StagedStore
+    cfg = ODD
+    wl = CTRWorkload(cfg)
+    W, dense = wl.init_table(), wl.init_dense()
+    s = StagedStore(W, [0], [400], cfg.opt.lr, cfg.opt.eps)
+    Dt, At = dev(dense), torch.zeros(dense.shape, dtype=torch.float32, device="cuda")
+    Dr, Ar = dense.copy(), np.zeros_like(dense)
+    Wr, Gr = W.copy(), np.zeros_like(W)
+    for step in range(3):
+        bt = wl.batch(step)
+        s.intent(bt.keys.ravel(), step + 1, step + 2)
+        s.round()
+        s.advance_clock()
+        loss = s.step_ctr_wd(dev(bt.keys), dev(bt.label), Dt, At, cfg.emb_dim, cfg.deep)
+        assert s.error() == 0
+        rloss, _ = step_ctr_wd(Wr, Gr, Dr, Ar, bt.keys, bt.label, cfg.emb_dim, cfg.deep, cfg.opt.lr, cfg.opt.eps)
+        assert float(loss.item()) == pytest.approx(rloss, rel=1e-9)
+    s.flush()
+    Wh, Gh = s.home_tables()
+    assert_close_tables(Wh, Wr, "home W after three staged steps")
+    assert_close_tables(Gh, Gr, "home G after three staged steps")
+    assert_close_tables(Dt.cpu().numpy(), Dr, "dense parameters")
+
+
+def test_wd_on_a_rowwise_store():
+    """Row-wise AdaGrad for the table rows (one accumulator per key), per
+    element for the dense buffer."""
+    import oracle
+    from oracle.widedeep import grad_ctr_wd
+    cfg = ODD
+    wl = CTRWorkload(cfg)
+    W, dense = wl.init_table(), wl.init_dense()
+    Wt, At_rows = dev(W), torch.zeros(W.shape[0], dtype=torch.float32, device="cuda")
+    Dt, At = dev(dense), torch.zeros(dense.shape, dtype=torch.float32, device="cuda")
+    s = Store(Wt, At_rows, cfg.opt.lr, cfg.opt.eps)
+    bt = wl.batch(0)
+    s.step_ctr_wd(dev(bt.keys), dev(bt.label), Dt, At, cfg.emb_dim, cfg.deep)
+    assert s.error() == 0
+    okeys, grads, dflat, _, _ = grad_ctr_wd(W, dense, bt.keys, bt.label, cfg.emb_dim, cfg.deep)
+    Wr, Ar = W.copy(), np.zeros(W.shape[0], np.float32)
+    oracle.push_rowwise(Wr, Ar, okeys, grads, cfg.opt.lr, cfg.opt.eps)
+    Dr, _ = oracle.adagrad_row(dense.copy(), np.zeros_like(dense), dflat.astype(np.float32), cfg.opt.lr, cfg.opt.eps)
+    assert_close_tables(Wt.cpu().numpy(), Wr, "W")
+    assert_close_tables(At_rows.cpu().numpy(), Ar, "row accumulators")
+    assert_close_tables(Dt.cpu().numpy(), Dr, "dense parameters")
