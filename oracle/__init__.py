@@ -49,6 +49,9 @@ def lib():
             "orc_push": (i64, [p, p, i64, i32, f32, f32, p, i64, p]),
             "orc_adagrad_rowwise": (None, [p, p, p, i32, f32, f32]),
             "orc_push_rowwise": (i64, [p, p, i64, i32, f32, f32, p, i64, p]),
+            "orc_bf16_to_f32": (f32, [C.c_uint16]),
+            "orc_f32_to_bf16": (C.c_uint16, [f32]),
+            "orc_push_bf16": (i64, [p, p, i64, i32, f32, f32, p, i64, p]),
             "orc_complex_score": (f64, [p, p, p, i32]),
             "orc_grad_mf": (f64, [p, i64, i32, p, p, p, i64, i64, f32, p, p, p]),
             "orc_grad_kge": (f64, [p, i64, i32, p, p, p, p, i64, i32, i32, i64, p, p, p]),
@@ -139,6 +142,39 @@ def step_rowwise(task, W, Gr, batch, lr, eps, **kw):
     grad = {"mf": grad_mf, "kge": grad_kge, "sgns": grad_sgns, "ctr": grad_ctr}[task]
     keys, grads, loss, bad = grad(W, *batch, **kw)
     push_rowwise(W, Gr, keys, grads, lr, eps)
+    return loss, bad
+
+
+def bf16_to_f32(b):
+    """Widen bf16 words (uint16) to fp32: exact, the word is the upper half."""
+    b = np.asarray(b, np.uint16)
+    return (b.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def f32_to_bf16(x):
+    """Round fp32 values to bf16 words (nearest, ties to even), element by element."""
+    x = np.asarray(x, np.float32)
+    f = lib().orc_f32_to_bf16
+    return np.fromiter((f(float(v)) for v in x.ravel()), np.uint16, x.size).reshape(x.shape)
+
+
+def push_bf16(Wb, G, keys, grads, lr, eps):
+    """The merged push on a table of bf16 values (uint16 words) with fp32
+    accumulators: per key the fp64 sum rounded to fp32, one per-element
+    AdaGrad step on the widened values, the result narrowed to bf16."""
+    assert Wb.dtype == np.uint16 and Wb.flags.c_contiguous and G.shape == Wb.shape
+    G = _table(G)
+    keys = _c(keys, np.int64)
+    grads = _c(grads, np.float32).reshape(keys.size, Wb.shape[1])
+    return int(lib().orc_push_bf16(_p(Wb), _p(G), Wb.shape[0], Wb.shape[1], lr, eps, _p(keys), keys.size,
+                                   _p(grads)))
+
+
+def step_mf_bf16(Wb, G, row, col, val, col_off, lam, lr, eps):
+    """An MF step on bf16 values: gradients from the widened pre-step table,
+    then push_bf16.  Returns (loss, bad)."""
+    keys, grads, loss, bad = grad_mf(bf16_to_f32(Wb), row, col, val, col_off, lam)
+    push_bf16(Wb, G, keys, grads, lr, eps)
     return loss, bad
 
 

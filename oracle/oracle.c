@@ -235,6 +235,61 @@ ORC_API int64_t orc_push_rowwise(float* W, float* Gr, int64_t num_keys, int32_t 
 }
 
 /* ------------------------------------------------------------------------ */
+/* bf16 value storage, an update variant that halves the bytes of a value:  */
+/* a bf16 word is the upper half of an fp32 word, so widening is exact;     */
+/* narrowing rounds to the nearest bf16, ties to the even one (NaN stays a  */
+/* quiet NaN).  Accumulators stay fp32; the updated value is narrowed once. */
+/* ------------------------------------------------------------------------ */
+ORC_API float orc_bf16_to_f32(uint16_t b)
+{
+    uint32_t u = (uint32_t)b << 16;
+    float f;
+    memcpy(&f, &u, 4);
+    return f;
+}
+
+ORC_API uint16_t orc_f32_to_bf16(float f)
+{
+    uint32_t u;
+    memcpy(&u, &f, 4);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+    uint32_t lower = u & 0xffffu;          /* the bits that are dropped */
+    uint32_t upper = u >> 16;
+    if (lower > 0x8000u || (lower == 0x8000u && (upper & 1u))) upper += 1u;   /* carries into the exponent */
+    return (uint16_t)upper;
+}
+
+ORC_API int64_t orc_push_bf16(uint16_t* W, float* G, int64_t num_keys, int32_t dim, float lr, float eps,
+                              const int64_t* keys, int64_t n, const float* grads)
+{
+    occ_t* occ = (occ_t*)malloc(sizeof(occ_t) * (size_t)(n > 0 ? n : 1));
+    double* sum = (double*)malloc(sizeof(double) * (size_t)dim);
+    float* g32 = (float*)malloc(sizeof(float) * (size_t)dim);
+    float* w32 = (float*)malloc(sizeof(float) * (size_t)dim);
+    int64_t bad = sort_occurrences(num_keys, keys, n, occ);
+    int64_t j = 0;
+    while (j < n && occ[j].key < num_keys) {
+        int64_t key = occ[j].key;
+        for (int32_t c = 0; c < dim; ++c) sum[c] = 0.0;
+        for (; j < n && occ[j].key == key; ++j) {
+            const float* row = grads + occ[j].idx * dim;
+            for (int32_t c = 0; c < dim; ++c) sum[c] += (double)row[c];
+        }
+        for (int32_t c = 0; c < dim; ++c) {
+            g32[c] = (float)sum[c];
+            w32[c] = orc_bf16_to_f32(W[key * dim + c]);
+        }
+        orc_adagrad_row(w32, G + key * dim, g32, dim, lr, eps);
+        for (int32_t c = 0; c < dim; ++c) W[key * dim + c] = orc_f32_to_bf16(w32[c]);
+    }
+    free(w32);
+    free(g32);
+    free(sum);
+    free(occ);
+    return bad;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Matrix factorization (Appendix C, "Matrix factorization"; Table 3).       */
 /* Entry (i, j, v): u = W[i], m = W[col_off + j].                            */
 /*   e = v - <u, m>                                                          */

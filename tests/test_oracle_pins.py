@@ -596,3 +596,63 @@ def test_table3_bytes_per_value_fits_fp32_value_plus_fp32_accumulator():
     for task in ("kge", "wv"):
         _, values, gb = rows[task]
         assert gb * 2 ** 30 / values == pytest.approx(8.0, rel=0.02)
+
+
+# ---------------------------------------------------------------- bf16 values (update variant)
+def bf16_nearest_brute(x):
+    """The nearest bf16 value by comparing the two candidates around x in
+    fp64; ties go to the word with an even last bit."""
+    u = np.float32(x).view(np.uint32)
+    lo = np.uint16(u >> np.uint32(16))
+    hi = np.uint16(lo + 1)
+    vlo = float(oracle.bf16_to_f32(np.array([lo]))[0])
+    vhi = float(oracle.bf16_to_f32(np.array([hi]))[0])
+    dlo, dhi = abs(float(x) - vlo), abs(vhi - float(x))
+    if dlo < dhi or (dlo == dhi and lo % 2 == 0):
+        return lo
+    return hi
+
+
+def test_bf16_rounding_is_nearest_ties_to_even_and_matches_torch():
+    rng = np.random.default_rng(70)
+    x = np.concatenate([rng.standard_normal(20000).astype(np.float32) * 10.0 ** rng.integers(-30, 30, 20000),
+                        np.array([0.0, -0.0, 1.0, 1 + 2 ** -8, 1 + 3 * 2 ** -9, -2.5, 3e38, 1e-40, -1e-41],
+                                 np.float32)]).astype(np.float32)
+    got = oracle.f32_to_bf16(x)
+    want_torch = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(got, want_torch)
+    for v in x[:3000]:
+        if np.isfinite(v) and abs(v) < 3.3e38:
+            assert oracle.f32_to_bf16(np.array([v]))[0] == bf16_nearest_brute(v), v
+
+
+def test_bf16_widening_is_exact_and_rounds_back_to_itself():
+    words = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    f = oracle.bf16_to_f32(words)
+    finite = np.isfinite(f)
+    assert np.array_equal(oracle.f32_to_bf16(f[finite]), words[finite])
+    assert np.isnan(f[~finite & (words & 0x7f != 0) & ((words & 0x7f80) == 0x7f80)]).all()
+
+
+def test_push_bf16_is_the_fp32_push_on_widened_values_then_one_rounding():
+    rng = np.random.default_rng(71)
+    K, d, n = 40, 12, 600
+    Wb = oracle.f32_to_bf16(rng.standard_normal((K, d)).astype(np.float32) * 0.1)
+    G0 = rng.uniform(0, 1, (K, d)).astype(np.float32)
+    keys = rng.integers(-1, K + 1, n)
+    grads = rng.standard_normal((n, d)).astype(np.float32)
+    W1, G1 = Wb.copy(), G0.copy()
+    bad = oracle.push_bf16(W1, G1, keys, grads, LR, EPS)
+    W2, G2 = oracle.bf16_to_f32(Wb), G0.copy()
+    assert oracle.push(W2, G2, keys, grads, LR, EPS) == bad
+    assert np.array_equal(W1, oracle.f32_to_bf16(W2))
+    assert np.array_equal(G1, G2)
+
+
+def test_push_bf16_zero_gradients_keep_every_bit():
+    rng = np.random.default_rng(72)
+    Wb = oracle.f32_to_bf16(rng.standard_normal((30, 8)).astype(np.float32))
+    G0 = rng.uniform(0, 1, (30, 8)).astype(np.float32)
+    W1, G1 = Wb.copy(), G0.copy()
+    oracle.push_bf16(W1, G1, rng.integers(0, 30, 90), np.zeros((90, 8), np.float32), LR, EPS)
+    assert np.array_equal(W1, Wb) and np.array_equal(G1.view(np.uint32), G0.view(np.uint32))
