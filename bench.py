@@ -57,6 +57,8 @@ def parse():
     ap.add_argument("--no-overlap", action="store_true",
                     help="MF: one ps_step_mf call per step instead of overlapping the next batch's key work "
                          "(sort, segments, records) on a second stream with this batch's table update")
+    ap.add_argument("--values", default="f32", choices=["f32", "bf16"],
+                    help="fp32 values, or bf16 values with fp32 accumulators (an update variant; MF workloads)")
     ap.add_argument("--staged", action="store_true",
                     help="home tables in pinned host memory, HBM slots for the keys of acted-upon intents; "
                          "intents signalled --lookahead batches ahead, rounds on the library's thread")
@@ -102,12 +104,13 @@ class Bench:
     """One workload: its table, resident step batches, the step call, the
     algorithmic bytes of its two big kernels and the oracle step."""
 
-    def __init__(self, name, dev, nbatches, rowwise=False):
+    def __init__(self, name, dev, nbatches, rowwise=False, values="f32"):
         import torch
         from paper_2206_00470_amd import workloads as wls
 
         self.name = name
         self.rowwise = rowwise
+        self.values = values
         self.task = {"mf_tiny": "mf", "mf_colorder": "mf", "kge2x100": "kge", "sgns_w2v": "sgns"}.get(name, name)
         cfgs = {"mf": wls.MF_10Mx1M, "mf_tiny": wls.MF_TINY, "mf_colorder": wls.MF_10Mx1M_COLORDER,
                 "kge": wls.KGE_COMPLEX, "kge2x100": wls.KGE_COMPLEX_2x100, "sgns": wls.SGNS_1M,
@@ -116,7 +119,8 @@ class Bench:
         self.wl = wls.workload(cfg)
         self.dev = dev
         self.dim = cfg.dim
-        self.R = 4 * cfg.dim
+        self.R = 4 * cfg.dim                              # an fp32 row (gradients, accumulators)
+        self.RV = (2 if values == "bf16" else 4) * cfg.dim   # a value row
         self.W = self.wl.init_table()
         if self.task == "ctr_wd":
             self.dense0 = self.wl.init_dense()
@@ -209,7 +213,8 @@ class Bench:
         c, bt = self.cfg, self.host_batches[i % len(self.host_batches)]
         n, U, R = self.occ[i % len(self.occ)], self.uniq[i % len(self.uniq)], self.R
         # per distinct key: W read and written, and G (a row, or one value when row-wise)
-        tab = 2.0 * R + 8.0 if self.rowwise else 4.0 * R
+        RV = self.RV
+        tab = 2.0 * RV + 8.0 if self.rowwise else 2.0 * RV + 2.0 * R
         table = tab * U
         if self.task == "mf":
             B = bt.row.size
@@ -219,7 +224,7 @@ class Bench:
             # distinct column key), the column-occurrence gradient row out, and the row keys'
             # W and G; column-key merge: the stored gradient rows and the column keys' W and G;
             # record scatter: col, val, two ranks in, one record out
-            return {"rowmerge": B * (16.0 + R) + Ucol * R + tab * Urow,
+            return {"rowmerge": B * (16.0 + R) + Ucol * RV + tab * Urow,
                     "segreduce": B * R + tab * Ucol,
                     "taskgrad": B * (4.0 + 4.0 + 8.0 + 16.0)}
         if self.task == "ctr":
@@ -244,6 +249,9 @@ class Bench:
         import oracle
         c, bt = self.cfg, self.wl.batch(i)
         lr, eps = c.opt.lr, c.opt.eps
+        if self.values == "bf16":
+            oracle.step_mf_bf16(W, G, bt.row, bt.col, bt.val, c.n_rows, c.lam, lr, eps)
+            return self.keys_of(bt).size
         if self.task == "ctr_wd":
             from oracle.widedeep import step_ctr_wd
             if not hasattr(self, "_dense_host"):
@@ -360,6 +368,9 @@ def cpu_baseline(args, wb, rowwise):
     cfg = wb.cfg
     W = wb.W
     G = np.zeros(W.shape[0], np.float32) if rowwise else np.zeros_like(W)
+    if wb.values == "bf16":
+        import oracle
+        W = oracle.f32_to_bf16(W)
     from threadpoolctl import threadpool_limits
     done, rows, tc0 = 0, 0, time.perf_counter()
     with threadpool_limits(1):               # numpy's matrix products single-threaded, like the C oracle
@@ -390,7 +401,11 @@ def main():
     t0 = time.time()
     nb = max(1, min(args.steps + args.warmup, 8))
     rowwise = args.update == "rowwise"
-    wb = Bench(args.workload, dev, nb, rowwise)
+    bf16 = args.values == "bf16"
+    if bf16 and (rowwise or args.staged or not args.workload.startswith("mf")):
+        print("--values bf16 runs the MF workloads with per-element AdaGrad, in HBM", file=sys.stderr)
+        sys.exit(2)
+    wb = Bench(args.workload, dev, nb, rowwise, args.values)
     cfg = wb.cfg
     metric = ("param rows pulled+pushed/sec (MF 10m x 1m, rank 100)" if args.workload == "mf"
               else f"param rows pulled+pushed/sec ({cfg.name})")
@@ -414,7 +429,13 @@ def main():
         }
         print(json.dumps(line), flush=True)
         return
-    if rowwise and args.layout == "interleaved":
+    if bf16 and args.layout == "interleaved":
+        from paper_2206_00470_amd.store import interleaved_bf16_tables
+        Wt, Gt = interleaved_bf16_tables(torch.from_numpy(wb.W).to(dev))
+    elif bf16:
+        Wt = torch.from_numpy(wb.W).to(dev).to(torch.bfloat16)   # nearest, ties to even
+        Gt = torch.zeros(wb.W.shape, dtype=torch.float32, device=dev)
+    elif rowwise and args.layout == "interleaved":
         from paper_2206_00470_amd.store import padded_rowwise_table
         Wt, Gt = padded_rowwise_table(torch.from_numpy(wb.W).to(dev))
     elif rowwise:
@@ -513,7 +534,7 @@ def main():
               "rowmerge": "k_segreduce<SrcMFRow>", "mlp": "k_gemm_f64",
               "taskgrad": {"mf": "k_mf_pack", "kge": "k_kge_grad", "sgns": "k_sgns_grad",
                            "ctr": "k_ctr_grad", "ctr_wd": "k_wd_head"}[wb.task]}[dom]
-    traffic = counter_traffic(args.workload + ("_rowwise" if rowwise else ""), symbol)
+    traffic = counter_traffic(args.workload + ("_rowwise" if rowwise else "") + ("_bf16" if bf16 else ""), symbol)
     roofline = {
         "bound": "hbm",
         "kernel": symbol,
@@ -562,9 +583,10 @@ def main():
         tl = (time.perf_counter() - t1) / reps
         assert store.error() == 0
         R = wb.R
-        tab = 2.0 * R + 8.0 if rowwise else 4.0 * R
+        RV = wb.RV
+        tab = 2.0 * RV + 8.0 if rowwise else 2.0 * RV + 2.0 * R
         push_alg = 8.0 * n + n * R + tab * U
-        pull_alg = 8.0 * n + U * R + n * R
+        pull_alg = 8.0 * n + U * RV + n * R
         # the bare read-modify-write pattern through the merge kernel: U distinct
         # random keys, one contiguous gradient row each (no duplicates to merge)
         ukeys = torch.from_numpy(np.sort(np.random.default_rng(11).choice(cfg.num_keys, int(U), replace=False))).to(dev)
@@ -609,7 +631,7 @@ def main():
     cpu = cpu_baseline(args, wb, rowwise)
 
     line = {
-        "metric": metric + (", row-wise AdaGrad" if rowwise else ""),
+        "metric": metric + (", row-wise AdaGrad" if rowwise else "") + (", bf16 values" if bf16 else ""),
         "value": rows_per_s,
         "unit": "rows/s",
         "n_gpus": 1,
@@ -622,7 +644,7 @@ def main():
         "dtype": "f64" if wb.task == "ctr_wd" else "f32",   # the Wide & Deep MLP runs in fp64
         "data": "synthetic",
         "config": {"workload": cfg.name, "num_keys": cfg.num_keys, "dim": cfg.dim, "layout": args.layout,
-                   "update": args.update,
+                   "update": args.update, "values": args.values,
                    "launch": "hip graph replay" if args.graph else "eager",
                    "mf_key_work_overlapped": overlap,
                    "key_occurrences_per_step": occ, "avg_unique_keys_per_step": U_avg,

@@ -100,6 +100,21 @@ ps_status ps_create_strided(ps_store** out, int64_t num_keys, int32_t dim, int64
  * dim <= c < row_stride and accum_stride = row_stride), so that a key's
  * update touches one region of HBM.  An accumulator inside a value row is
  * PS_ERR_INVALID. */
+/* As ps_create, with bf16 values: row k of the values is values +
+ * k*value_stride (uint16 words, each the upper half of an fp32 word), row k
+ * of the fp32 AdaGrad accumulators accum + k*accum_stride: two separate
+ * allocations, or rows interleaved in one (equal byte strides, each key's
+ * accumulator row after its value row), so that an update touches one
+ * span of HBM.  An update variant that halves the bytes of a value: reads
+ * widen exactly to fp32, arithmetic and accumulators are unchanged, and the
+ * updated value is narrowed once to the nearest bf16 (ties to even).
+ * ps_pull returns fp32 rows; ps_push and the MF steps run on such a store;
+ * the other steps return PS_ERR_UNSUPPORTED.  When dim % 4 == 0 the values
+ * must be 8-byte aligned, the accumulators 16-byte aligned and both strides
+ * multiples of 4. */
+ps_status ps_create_bf16(ps_store** out, int64_t num_keys, int32_t dim, uint16_t* values, int64_t value_stride,
+                         float* accum, int64_t accum_stride, float lr, float eps, void* stream);
+
 ps_status ps_create_rowwise(ps_store** out, int64_t num_keys, int32_t dim, int64_t row_stride,
                             float* values, float* accum, int64_t accum_stride, float lr, float eps,
                             void* stream);

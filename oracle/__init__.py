@@ -52,6 +52,7 @@ def lib():
             "orc_bf16_to_f32": (f32, [C.c_uint16]),
             "orc_f32_to_bf16": (C.c_uint16, [f32]),
             "orc_push_bf16": (i64, [p, p, i64, i32, f32, f32, p, i64, p]),
+            "orc_f32_to_bf16_array": (None, [p, p, i64]),
             "orc_complex_score": (f64, [p, p, p, i32]),
             "orc_grad_mf": (f64, [p, i64, i32, p, p, p, i64, i64, f32, p, p, p]),
             "orc_grad_kge": (f64, [p, i64, i32, p, p, p, p, i64, i32, i32, i64, p, p, p]),
@@ -153,9 +154,10 @@ def bf16_to_f32(b):
 
 def f32_to_bf16(x):
     """Round fp32 values to bf16 words (nearest, ties to even), element by element."""
-    x = np.asarray(x, np.float32)
-    f = lib().orc_f32_to_bf16
-    return np.fromiter((f(float(v)) for v in x.ravel()), np.uint16, x.size).reshape(x.shape)
+    x = np.ascontiguousarray(x, np.float32)
+    out = np.empty(x.shape, np.uint16)
+    lib().orc_f32_to_bf16_array(_p(x), _p(out), x.size)
+    return out
 
 
 def push_bf16(Wb, G, keys, grads, lr, eps):

@@ -259,6 +259,11 @@ ORC_API uint16_t orc_f32_to_bf16(float f)
     return (uint16_t)upper;
 }
 
+ORC_API void orc_f32_to_bf16_array(const float* x, uint16_t* out, int64_t n)
+{
+    for (int64_t i = 0; i < n; ++i) out[i] = orc_f32_to_bf16(x[i]);
+}
+
 ORC_API int64_t orc_push_bf16(uint16_t* W, float* G, int64_t num_keys, int32_t dim, float lr, float eps,
                               const int64_t* keys, int64_t n, const float* grads)
 {

@@ -36,6 +36,7 @@ SIGNATURES = {
     "ps_create": (_i32, [C.POINTER(_p), _i64, _i32, _p, _p, _f32, _f32, _p]),
     "ps_create_strided": (_i32, [C.POINTER(_p), _i64, _i32, _i64, _p, _p, _f32, _f32, _p]),
     "ps_create_rowwise": (_i32, [C.POINTER(_p), _i64, _i32, _i64, _p, _p, _i64, _f32, _f32, _p]),
+    "ps_create_bf16": (_i32, [C.POINTER(_p), _i64, _i32, _p, _i64, _p, _i64, _f32, _f32, _p]),
     "ps_destroy": (_i32, [_p]),
     "ps_workspace_bytes": (_sz, [_i64, _i32, _i32, _i64, _i64]),
     "ps_pull": (_i32, [_p, _p, _i64, _p, _p]),

@@ -88,6 +88,7 @@ struct ps_store {
   int64_t gld;       // stride (floats) between consecutive keys' accumulator rows or values
   int32_t dim;
   bool rowwise = false;   // one AdaGrad accumulator per key instead of per element
+  bool bf16 = false;      // values stored as bf16 words (W then points at bf16_t)
   float* W;
   float* G;
   float lr;
@@ -413,6 +414,19 @@ int64_t reduce_grid(int64_t n, int L, int64_t cap = MERGE_GRID_MAX) {
 // given to run_segments: PART_UPPER = keys >= split, PART_LOWER = keys below.
 enum { PART_ALL = 0, PART_UPPER = 1, PART_LOWER = 2 };
 
+// Value types a gradient source can run on: the MF row source reads rows of
+// its own value type; the sources of stored gradient rows read no table row.
+template <class Src> struct SrcValue { using type = void; };
+template <class VT> struct SrcValue<SrcMFRow<VT>> { using type = VT; };
+template <class Src, class VT>
+constexpr bool src_runs_on() {
+  using T = typename SrcValue<Src>::type;
+  if constexpr (std::is_same_v<VT, bf16_t>)   // bf16 stores: pull, push and the MF step
+    return std::is_same_v<Src, SrcIndirect> || std::is_same_v<Src, SrcSorted> || std::is_same_v<T, bf16_t>;
+  else
+    return std::is_same_v<T, void> || std::is_same_v<T, VT>;
+}
+
 template <class Src>
 ps_status launch_segreduce(ps_store* s, const SortBufs& b, const uint32_t* ks, Src src, int64_t n, int part,
                            hipStream_t st, int timing_id = PS_KERNEL_SEGREDUCE, int64_t grid_cap = MERGE_GRID_MAX) {
@@ -422,12 +436,23 @@ ps_status launch_segreduce(ps_store* s, const SortBufs& b, const uint32_t* ks, S
   return with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
     const int64_t grid = reduce_grid(n, L, grid_cap);
     Timed t(s, timing_id, st);
-    if (s->rowwise)
-      hipLaunchKernelGGL((k_segreduce<L, NV, VW, Src, true>), dim3(grid), dim3(BLOCK), 0, st, sv, src, n, s->W, s->G,
-                         s->ld, s->gld, s->dim, s->lr, s->eps, b.partial, b.split_list, b.hdr, part);
-    else
-      hipLaunchKernelGGL((k_segreduce<L, NV, VW, Src, false>), dim3(grid), dim3(BLOCK), 0, st, sv, src, n, s->W, s->G,
-                         s->ld, s->gld, s->dim, s->lr, s->eps, b.partial, b.split_list, b.hdr, part);
+    if (s->bf16) {
+      if constexpr (src_runs_on<Src, bf16_t>())
+        hipLaunchKernelGGL((k_segreduce<L, NV, VW, Src, false, bf16_t>), dim3(grid), dim3(BLOCK), 0, st, sv, src, n,
+                           reinterpret_cast<bf16_t*>(s->W), s->G, s->ld, s->gld, s->dim, s->lr, s->eps, b.partial,
+                           b.split_list, b.hdr, part);
+      else
+        return fail(PS_ERR_UNSUPPORTED, "this step does not run on bf16 values");
+    } else if constexpr (src_runs_on<Src, float>()) {
+      if (s->rowwise)
+        hipLaunchKernelGGL((k_segreduce<L, NV, VW, Src, true, float>), dim3(grid), dim3(BLOCK), 0, st, sv, src, n,
+                           s->W, s->G, s->ld, s->gld, s->dim, s->lr, s->eps, b.partial, b.split_list, b.hdr, part);
+      else
+        hipLaunchKernelGGL((k_segreduce<L, NV, VW, Src, false, float>), dim3(grid), dim3(BLOCK), 0, st, sv, src, n,
+                           s->W, s->G, s->ld, s->gld, s->dim, s->lr, s->eps, b.partial, b.split_list, b.hdr, part);
+    } else {
+      return fail(PS_ERR_UNSUPPORTED, "this step does not run on fp32 values");
+    }
     LAUNCHED(k_segreduce);
     return PS_OK;
   });
@@ -448,12 +473,16 @@ ps_status launch_finalize(ps_store* s, const SortBufs& b, const uint32_t* ks, in
     // at most n / CHUNK + 1 split segments; blocks beyond their count exit at once
     int64_t fgrid = n / CHUNK + 1;
     if (fgrid > 16384) fgrid = 16384;
-    if (s->rowwise)
-      hipLaunchKernelGGL((k_seg_finalize<L, NV, VW, true>), dim3(fgrid), dim3(BLOCK), lds, st, sv, s->W, s->G, s->ld,
-                         s->gld, s->dim, s->lr, s->eps, b.partial, b.fold, b.split_list);
+    if (s->bf16)
+      hipLaunchKernelGGL((k_seg_finalize<L, NV, VW, false, bf16_t>), dim3(fgrid), dim3(BLOCK), lds, st, sv,
+                         reinterpret_cast<bf16_t*>(s->W), s->G, s->ld, s->gld, s->dim, s->lr, s->eps, b.partial,
+                         b.fold, b.split_list);
+    else if (s->rowwise)
+      hipLaunchKernelGGL((k_seg_finalize<L, NV, VW, true, float>), dim3(fgrid), dim3(BLOCK), lds, st, sv, s->W, s->G,
+                         s->ld, s->gld, s->dim, s->lr, s->eps, b.partial, b.fold, b.split_list);
     else
-      hipLaunchKernelGGL((k_seg_finalize<L, NV, VW, false>), dim3(fgrid), dim3(BLOCK), lds, st, sv, s->W, s->G, s->ld,
-                         s->gld, s->dim, s->lr, s->eps, b.partial, b.fold, b.split_list);
+      hipLaunchKernelGGL((k_seg_finalize<L, NV, VW, false, float>), dim3(fgrid), dim3(BLOCK), lds, st, sv, s->W, s->G,
+                         s->ld, s->gld, s->dim, s->lr, s->eps, b.partial, b.fold, b.split_list);
     LAUNCHED(k_seg_finalize);
     return PS_OK;
   });
@@ -537,12 +566,18 @@ ps_status mf_apply(ps_store* s, int64_t B, float lambda, double* loss, Plan& p, 
   // Row keys first: their source reads the column rows before any column
   // update, forms e, the loss and the column-occurrence gradients; then the
   // column keys merge those stored rows.
-  SrcMFRow src{p.pe, s->W, s->ld, p.grads, p.loss_part, (double)lambda, s->dim};
   // (about one key per chunk here: a smaller grid gives each group a longer
   // run of chunks whose metadata it prefetches together)
   constexpr int64_t kRowMergeGrid = 2048;
-  if (ps_status r = launch_segreduce(s, p.sb, ks, src, n, PART_LOWER, st, PS_KERNEL_MF_ROWMERGE, kRowMergeGrid))
-    return r;
+  ps_status r = s->bf16
+      ? launch_segreduce(s, p.sb, ks,
+                         SrcMFRow<bf16_t>{p.pe, reinterpret_cast<const bf16_t*>(s->W), s->ld, p.grads, p.loss_part,
+                                          (double)lambda, s->dim},
+                         n, PART_LOWER, st, PS_KERNEL_MF_ROWMERGE, kRowMergeGrid)
+      : launch_segreduce(s, p.sb, ks,
+                         SrcMFRow<float>{p.pe, s->W, s->ld, p.grads, p.loss_part, (double)lambda, s->dim}, n,
+                         PART_LOWER, st, PS_KERNEL_MF_ROWMERGE, kRowMergeGrid);
+  if (r) return r;
   if (rows_done) HIP_TRY(hipEventRecord(rows_done, st));
   if (loss) {
     RowShape shape;
@@ -935,6 +970,36 @@ ps_status ps_create_strided(ps_store** out, int64_t num_keys, int32_t dim, int64
   return make_store(out, num_keys, dim, row_stride, values, accum, row_stride, false, lr, eps, stream);
 }
 
+ps_status ps_create_bf16(ps_store** out, int64_t num_keys, int32_t dim, uint16_t* values, int64_t value_stride,
+                         float* accum, int64_t accum_stride, float lr, float eps, void* stream) {
+  if (!out) return fail(PS_ERR_INVALID, "out is NULL");
+  *out = nullptr;
+  if (num_keys < 1 || num_keys > INT32_MAX) return fail(PS_ERR_INVALID, "num_keys %lld outside [1, 2^31-1]", (long long)num_keys);
+  RowShape shape;
+  if (dim < 1 || !row_shape(dim, true, &shape)) return fail(PS_ERR_UNSUPPORTED, "dim %d unsupported (at most 512)", dim);
+  if (!values || !accum) return fail(PS_ERR_INVALID, "table pointer is NULL");
+  if (value_stride < dim || accum_stride < dim) return fail(PS_ERR_INVALID, "a row stride is smaller than dim");
+  if (dim % 4 == 0 && ((reinterpret_cast<uintptr_t>(values) & 7u) != 0 || value_stride % 4 != 0 || !aligned16(accum) ||
+                       accum_stride % 4 != 0))
+    return fail(PS_ERR_INVALID, "values must be 8-byte and accumulators 16-byte aligned, strides multiples of 4");
+  if (!(lr > 0.0f) || !(eps >= 0.0f)) return fail(PS_ERR_INVALID, "need lr > 0 and eps >= 0");
+  {
+    // two separate allocations, or rows interleaved in one: the same byte
+    // stride, each key's accumulator row between its value row and the next
+    const int64_t vs = value_stride * 2, as = accum_stride * 4;
+    const int64_t d = (int64_t)(reinterpret_cast<uintptr_t>(accum) - reinterpret_cast<uintptr_t>(values));
+    const bool separate = d >= num_keys * vs || -d >= num_keys * as;
+    const int64_t r = vs > 0 ? ((d % vs) + vs) % vs : 0;
+    const bool interleaved = vs == as && r >= 2 * (int64_t)dim && r <= vs - 4 * (int64_t)dim;
+    if (!separate && !interleaved) return fail(PS_ERR_INVALID, "values and accumulators overlap");
+  }
+  if (ps_status r = make_store(out, num_keys, dim, value_stride, reinterpret_cast<float*>(values), accum, accum_stride,
+                               false, lr, eps, stream))
+    return r;
+  (*out)->bf16 = true;
+  return PS_OK;
+}
+
 ps_status ps_create_rowwise(ps_store** out, int64_t num_keys, int32_t dim, int64_t row_stride, float* values,
                             float* accum, int64_t accum_stride, float lr, float eps, void* stream) {
   if (!out) return fail(PS_ERR_INVALID, "out is NULL");
@@ -998,8 +1063,14 @@ ps_status ps_pull(ps_store* s, const int64_t* keys, int64_t n, float* out, void*
     int64_t grid = ceil_div(n, BLOCK / L);
     if (grid > 65536) grid = 65536;
     Timed t(s, PS_KERNEL_PULL, st);
-    hipLaunchKernelGGL((k_pull<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->ld, s->num_keys, s->dim, keys, n,
-                       out, s->status, s->stg ? s->stg->map : nullptr, s->stg ? s->stg->num_keys : int64_t(0));
+    if (s->bf16)
+      hipLaunchKernelGGL((k_pull<L, NV, VW, bf16_t>), dim3(grid), dim3(BLOCK), 0, st,
+                         reinterpret_cast<const bf16_t*>(s->W), s->ld, s->num_keys, s->dim, keys, n, out, s->status,
+                         (const int32_t*)nullptr, int64_t(0));
+    else
+      hipLaunchKernelGGL((k_pull<L, NV, VW, float>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->ld, s->num_keys, s->dim,
+                         keys, n, out, s->status, s->stg ? s->stg->map : nullptr,
+                         s->stg ? s->stg->num_keys : int64_t(0));
     LAUNCHED(k_pull);
     return PS_OK;
   });
@@ -1095,6 +1166,7 @@ static ps_status step_kge_impl(ps_store* s, const int32_t* head, const int32_t* 
                                int64_t B, int32_t n_neg, int32_t n_head_neg, int64_t rel_key_offset, double* loss, void* ws,
                                size_t ws_bytes, void* stream) {
   if (ps_status st = check_store(s)) return st;
+  if (s->bf16) return fail(PS_ERR_UNSUPPORTED, "this step runs on fp32 values only (bf16 stores: pull, push, MF)");
   if (n_neg < 0 || n_head_neg < 0 || n_head_neg > n_neg)
     return fail(PS_ERR_INVALID, "need 0 <= n_head_neg <= n_neg");
   if (ps_status st = check_n(B, 3 + (int64_t)n_neg)) return st;
@@ -1150,6 +1222,7 @@ static ps_status step_sgns_impl(ps_store* s, const int32_t* centre, const int32_
                                 int32_t window, int32_t n_neg, int64_t out_key_offset, double* loss, void* ws,
                                 size_t ws_bytes, void* stream) {
   if (ps_status st = check_store(s)) return st;
+  if (s->bf16) return fail(PS_ERR_UNSUPPORTED, "this step runs on fp32 values only (bf16 stores: pull, push, MF)");
   if (window < 0 || n_neg < 0) return fail(PS_ERR_INVALID, "negative window or n_neg");
   const int slots = 2 * window;
   const int64_t per = 1 + (int64_t)slots * (1 + n_neg);
@@ -1208,6 +1281,7 @@ static ps_status step_sgns_impl(ps_store* s, const int32_t* centre, const int32_
 static ps_status step_ctr_impl(ps_store* s, const int64_t* keys, const float* label, int64_t B, int32_t F, double* loss,
                                void* ws, size_t ws_bytes, void* stream) {
   if (ps_status st = check_store(s)) return st;
+  if (s->bf16) return fail(PS_ERR_UNSUPPORTED, "this step runs on fp32 values only (bf16 stores: pull, push, MF)");
   if (F < 1) return fail(PS_ERR_INVALID, "need F >= 1");
   if (ps_status st = check_n(B, F)) return st;
   hipStream_t st = as_stream(stream);
@@ -1374,6 +1448,7 @@ ps_status ps_step_ctr_wd(ps_store* s, const int64_t* keys, const float* label, i
                          int32_t n_hidden, const int32_t* hidden, float* dense, float* dense_accum, double* loss,
                          void* ws, size_t ws_bytes, void* stream) {
   if (ps_status st = check_store(s)) return st;
+  if (s->bf16) return fail(PS_ERR_UNSUPPORTED, "this step runs on fp32 values only (bf16 stores: pull, push, MF)");
   if (F < 1) return fail(PS_ERR_INVALID, "need F >= 1");
   if (emb_dim < 1 || emb_dim >= s->dim) return fail(PS_ERR_INVALID, "need 1 <= emb_dim < dim (the row holds the wide weight)");
   if (n_hidden < 0 || n_hidden > WD_MAX_HIDDEN || (n_hidden > 0 && !hidden))

@@ -3,6 +3,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include <cstddef>
 #include <cstdint>
 
@@ -185,6 +187,63 @@ __device__ __forceinline__ void store_frag(float* p, const float* in) {
     *p = in[0];
   }
 }
+
+// ------------------------------------------------------------------ bf16 values
+// A store may keep its values as bf16 words (the upper half of an fp32
+// word): widening is exact, narrowing rounds to the nearest bf16 with ties
+// to the even word (a NaN stays a quiet NaN).  Arithmetic is unchanged.
+struct bf16_t {
+  uint16_t bits;
+};
+
+__device__ __forceinline__ float bf16_widen(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
+
+__device__ __forceinline__ uint32_t bf16_narrow(float f) {
+  const uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;   // a carry moves into the exponent, as it should
+}
+
+// VW values of type VT at p <-> VW floats (VT = float or bf16_t).
+template <int VW, class VT>
+__device__ __forceinline__ void load_vals(const VT* p, float* out) {
+  if constexpr (std::is_same_v<VT, float>) {
+    load_frag<VW>(p, out);
+  } else if constexpr (VW == 4) {
+    const uint2 x = *reinterpret_cast<const uint2*>(p);
+    out[0] = bf16_widen(x.x & 0xffffu);
+    out[1] = bf16_widen(x.x >> 16);
+    out[2] = bf16_widen(x.y & 0xffffu);
+    out[3] = bf16_widen(x.y >> 16);
+  } else if constexpr (VW == 2) {
+    const uint32_t x = *reinterpret_cast<const uint32_t*>(p);
+    out[0] = bf16_widen(x & 0xffffu);
+    out[1] = bf16_widen(x >> 16);
+  } else {
+    out[0] = bf16_widen(p->bits);
+  }
+}
+
+template <int VW, class VT>
+__device__ __forceinline__ void store_vals(VT* p, const float* in) {
+  if constexpr (std::is_same_v<VT, float>) {
+    store_frag<VW>(p, in);
+  } else if constexpr (VW == 4) {
+    uint2 x;
+    x.x = bf16_narrow(in[0]) | (bf16_narrow(in[1]) << 16);
+    x.y = bf16_narrow(in[2]) | (bf16_narrow(in[3]) << 16);
+    *reinterpret_cast<uint2*>(p) = x;
+  } else if constexpr (VW == 2) {
+    *reinterpret_cast<uint32_t*>(p) = bf16_narrow(in[0]) | (bf16_narrow(in[1]) << 16);
+  } else {
+    p->bits = (uint16_t)bf16_narrow(in[0]);
+  }
+}
+
+__device__ __forceinline__ float val_load(const float* p) { return *p; }
+__device__ __forceinline__ float val_load(const bf16_t* p) { return bf16_widen(p->bits); }
+__device__ __forceinline__ void val_store(float* p, float x) { *p = x; }
+__device__ __forceinline__ void val_store(bf16_t* p, float x) { p->bits = (uint16_t)bf16_narrow(x); }
 
 // Non-temporal fragment store for streams that are read back only once.
 template <int VW>

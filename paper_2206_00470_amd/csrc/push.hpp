@@ -19,9 +19,10 @@ struct RowShape {
 // ------------------------------------------------------------------ pull
 // With a key -> slot map (a staged store), keys index the home table of
 // map_keys keys and rows are read from their slots; a key with no slot gives
-// a zero row and sets err[1].
-template <int L, int NV, int VW>
-__global__ __launch_bounds__(BLOCK) void k_pull(const float* __restrict__ W, int64_t ld, int64_t num_keys, int dim,
+// a zero row and sets err[1].  VT: the table's value type (float or bf16_t);
+// the pulled rows are fp32 either way.
+template <int L, int NV, int VW, class VT>
+__global__ __launch_bounds__(BLOCK) void k_pull(const VT* __restrict__ W, int64_t ld, int64_t num_keys, int dim,
                                                 const int64_t* __restrict__ keys, int64_t n,
                                                 float* __restrict__ out, int32_t* __restrict__ err,
                                                 const int32_t* __restrict__ map, int64_t map_keys) {
@@ -42,14 +43,14 @@ __global__ __launch_bounds__(BLOCK) void k_pull(const float* __restrict__ W, int
       ok = key >= 0 && key < num_keys;
       bad |= !ok;
     }
-    const float* src = W + (ok ? key : 0) * ld;
+    const VT* src = W + (ok ? key : 0) * ld;
     float* dst = out + i * (int64_t)dim;
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
       const int c = (gl + v * L) * VW;
       if (c < dim) {
         float x[VW];
-        if (ok) load_frag<VW>(src + c, x);
+        if (ok) load_vals<VW>(src + c, x);
         else
 #pragma unroll
           for (int e = 0; e < VW; ++e) x[e] = 0.0f;
@@ -167,8 +168,8 @@ __device__ __forceinline__ int64_t xcd_slot(int64_t block, int64_t nblocks) {
 // of such a segment also appends the segment to split_list.
 // RW selects row-wise AdaGrad: G then holds one accumulator per key, at
 // G[key * gld]; otherwise G is a table of rows at G + key * gld.
-template <int L, int NV, int VW, class Src, bool RW>
-__global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, int64_t n, float* __restrict__ W,
+template <int L, int NV, int VW, class Src, bool RW, class VT>
+__global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, int64_t n, VT* __restrict__ W,
                                                      float* __restrict__ G, int64_t ld, int64_t gld, int dim,
                                                      float lr, float eps,
                                                      double* __restrict__ partial,
@@ -213,7 +214,7 @@ __global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, int64_
     const bool head = flags & 1u;
     const bool whole = flags & 2u;
     const Meta first = shfl_pod(my_first, ci, L);
-    float* wrow = W + (int64_t)key * ld;
+    VT* wrow = W + (int64_t)key * ld;
     float* grow = G + (int64_t)key * gld;
     float wv[NE], gv[NE];
     float gacc = 0.0f;   // RW: the key's accumulator
@@ -222,7 +223,7 @@ __global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, int64_
       for (int v = 0; v < NV; ++v) {
         const int col = (gl + v * L) * VW;
         if (col < dim) {
-          load_frag<VW>(wrow + col, wv + v * VW);
+          load_vals<VW>(wrow + col, wv + v * VW);
           if (!RW && whole) load_frag<VW>(grow + col, gv + v * VW);
         }
       }
@@ -273,7 +274,7 @@ __global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, int64_
         if (col < dim) {
 #pragma unroll
           for (int e = 0; e < VW; ++e) rowwise_elem(wv[v * VW + e], g[v * VW + e], den, lr);
-          store_frag<VW>(wrow + col, wv + v * VW);
+          store_vals<VW>(wrow + col, wv + v * VW);
         }
       }
       if (gl == 0) *grow = gacc;
@@ -285,7 +286,7 @@ __global__ __launch_bounds__(BLOCK) void k_segreduce(SegView sv, Src src, int64_
 #pragma unroll
           for (int e = 0; e < VW; ++e)
             adagrad_elem(wv[v * VW + e], gv[v * VW + e], (float)acc[v * VW + e], lr, eps);
-          store_frag<VW>(wrow + col, wv + v * VW);
+          store_vals<VW>(wrow + col, wv + v * VW);
           store_frag<VW>(grow + col, gv + v * VW);
         }
       }
@@ -403,8 +404,8 @@ __global__ __launch_bounds__(BLOCK) void k_seg_fold(SegView sv, int64_t nsb, uin
 // results in group order, rounded once and applied with AdaGrad (row-wise
 // when RW, with the accumulator at G[key * gld]).  The order is fixed, so
 // the result is deterministic.
-template <int L, int NV, int VW, bool RW>
-__global__ __launch_bounds__(BLOCK) void k_seg_finalize(SegView sv, float* __restrict__ W, float* __restrict__ G,
+template <int L, int NV, int VW, bool RW, class VT>
+__global__ __launch_bounds__(BLOCK) void k_seg_finalize(SegView sv, VT* __restrict__ W, float* __restrict__ G,
                                                         int64_t ld, int64_t gld, int dim, float lr, float eps,
                                                         const double* __restrict__ partial,
                                                         const double* __restrict__ fold,
@@ -435,7 +436,7 @@ __global__ __launch_bounds__(BLOCK) void k_seg_finalize(SegView sv, float* __res
     };
     group_sum_rows<L, NV, VW>(row, 1 + n1 + nf + n3, dim, lds);
     __syncthreads();
-    float* wrow = W + (int64_t)key * ld;
+    VT* wrow = W + (int64_t)key * ld;
     float* grow = G + (int64_t)key * gld;
     if constexpr (RW) {
       // each thread keeps the fp32 sums of its own columns in lds[col]
@@ -456,17 +457,17 @@ __global__ __launch_bounds__(BLOCK) void k_seg_finalize(SegView sv, float* __res
       __syncthreads();
       const float den = den_sh;
       for (int col = threadIdx.x; col < dim; col += BLOCK) {
-        float w = wrow[col];
+        float w = val_load(wrow + col);
         rowwise_elem(w, (float)lds[col], den, lr);
-        wrow[col] = w;
+        val_store(wrow + col, w);
       }
     } else {
       for (int col = threadIdx.x; col < dim; col += BLOCK) {
         double t = 0.0;
         for (int gg = 0; gg < GPB; ++gg) t += lds[gg * dim + col];
-        float w = wrow[col], a = grow[col];
+        float w = val_load(wrow + col), a = grow[col];
         adagrad_elem(w, a, (float)t, lr, eps);
-        wrow[col] = w;
+        val_store(wrow + col, w);
         grow[col] = a;
       }
     }

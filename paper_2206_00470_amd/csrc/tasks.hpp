@@ -78,18 +78,20 @@ __global__ __launch_bounds__(BLOCK) void k_mf_pack(const int32_t* __restrict__ r
 //   column gradient   lam*m - e*u   (fp32, stored at the column occurrence's
 //                                    sorted position for the column-key merge)
 //   loss += e^2/2 + lam/2 (|u|^2 + |m|^2)
+template <class VT>
 struct SrcMFRow {
   static constexpr bool kNeedsOwn = true;
   static constexpr bool kLoss = true;
+  using Value = VT;   // the table's value type
   const MFEntry* pe;
-  const float* W;
+  const VT* W;
   int64_t ld;
   float* grads;
   double* loss_part;
   double lam;
   int dim;
   struct Meta {
-    const float* partner;
+    const VT* partner;
     float y;
     uint32_t col_pos;
   };
@@ -105,7 +107,7 @@ struct SrcMFRow {
     for (int v = 0; v < NV; ++v) {
       const int c = (gl + v * L) * VW;
       if (c < dim) {
-        load_frag<VW>(m.partner + c, p + v * VW);
+        load_vals<VW>(m.partner + c, p + v * VW);
 #pragma unroll
         for (int q = 0; q < VW; ++q) {
           // a product of two floats is exact in fp64, so a fused multiply-add

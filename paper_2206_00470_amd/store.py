@@ -72,6 +72,22 @@ def padded_rowwise_table(W0: torch.Tensor, A0: torch.Tensor | None = None, pad: 
     return T[:, :d], T[:, d]
 
 
+def interleaved_bf16_tables(W0: torch.Tensor, G0: torch.Tensor | None = None):
+    """One allocation holding, per key, the bf16 values (rounded to nearest,
+    ties to even) padded to 16 bytes, then the fp32 accumulators; returns
+    the (W bf16, G fp32) row-strided views for a bf16 Store."""
+    K, d = W0.shape
+    vbytes = (2 * d + 15) // 16 * 16
+    row = vbytes + 4 * d
+    T = torch.zeros((K, row), dtype=torch.uint8, device=W0.device)
+    W = T[:, :2 * d].view(torch.bfloat16)
+    G = T[:, vbytes:].view(torch.float32)
+    W.copy_(W0.to(torch.bfloat16))
+    if G0 is not None:
+        G.copy_(G0)
+    return W, G
+
+
 class Store:
     """A parameter store over caller-owned tables W (values) and G (AdaGrad
     accumulators), float32 CUDA tensors.  W is [num_keys, dim], dense or a
@@ -85,6 +101,9 @@ class Store:
     padded_rowwise_table)."""
 
     def __init__(self, W: torch.Tensor, G: torch.Tensor, lr: float = 0.1, eps: float = 1e-10, stream=None):
+        if W.is_cuda and W.dtype == torch.bfloat16:
+            self._init_bf16(W, G, lr, eps, stream)
+            return
         if not (W.is_cuda and W.dtype == torch.float32 and W.dim() == 2 and W.stride(1) == 1):
             raise TypeError("W must be a float32 CUDA tensor [num_keys, dim] with unit column stride")
         if not (G.is_cuda and G.dtype == torch.float32):
@@ -111,6 +130,24 @@ class Store:
                 raise ValueError("W and G must share one row stride")
             check(lib().ps_create_strided(C.byref(h), self.num_keys, self.dim, self.row_stride, _ptr(W), _ptr(G),
                                           lr, eps, _stream(stream)))
+        self._h = h
+
+    def _init_bf16(self, W, G, lr, eps, stream):
+        """bf16 values W [num_keys, dim] with fp32 accumulators G of the same
+        shape, in separate allocations (rows may be strided)."""
+        if not (W.dim() == 2 and W.stride(1) == 1 and G.is_cuda and G.dtype == torch.float32 and
+                G.shape == W.shape and G.stride(1) == 1):
+            raise TypeError("bf16 values need fp32 accumulators of the same shape, unit column strides")
+        self.W, self.G = W, G
+        self.num_keys, self.dim = W.shape
+        self.row_stride = W.stride(0) if W.shape[0] > 1 else self.dim
+        self.rowwise, self.bf16 = False, True
+        self.lr, self.eps = lr, eps
+        self.ws = Workspace(W.device)
+        h = C.c_void_p()
+        gs = G.stride(0) if G.shape[0] > 1 else self.dim
+        check(lib().ps_create_bf16(C.byref(h), self.num_keys, self.dim, _ptr(W), self.row_stride, _ptr(G), gs, lr,
+                                   eps, _stream(stream)))
         self._h = h
 
     def close(self):

@@ -15,7 +15,7 @@ HEADER = os.path.join(ROOT, "include", "adapm.h")
 def declared():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(ps_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(ps_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_header_declares_the_boundary():
@@ -98,6 +98,24 @@ def test_create_rowwise_rejects_overlapping_or_bad_accumulators():
     assert L.ps_create_rowwise(None, K, d, d, P(0), P(K * d), 1, 0.1, 0.0, None) == _lib.PS_ERR_INVALID
     assert L.ps_create_rowwise(C.byref(h), K, 513, 520, P(0), P(K * 520), 1, 0.1, 0.0,
                                None) == _lib.PS_ERR_UNSUPPORTED
+    assert h.value is None
+
+
+def test_create_bf16_rejects_overlap_and_misalignment():
+    L = _lib.lib()
+    h = C.c_void_p(1)
+    base = 0x100000
+    K, d = 1000, 100
+    V = lambda off_bytes: C.c_void_p(base + off_bytes)
+    cr = lambda va, vs, aa, as_: L.ps_create_bf16(C.byref(h), K, d, V(va), vs, V(aa), as_, 0.1, 0.0, None)
+    assert cr(0, 100, 100, 100) == _lib.PS_ERR_INVALID                 # accumulators inside the value table
+    assert cr(0, 304, 200, 152) == _lib.PS_ERR_INVALID                 # 8-byte aligned only
+    assert cr(0, 304, 192, 152) == _lib.PS_ERR_INVALID                 # interleaved but overlapping the values
+    assert cr(0, 300, 208, 152) == _lib.PS_ERR_INVALID                 # byte strides differ
+    assert cr(4, 304, 208 + 4, 152) == _lib.PS_ERR_INVALID             # values not 8-byte aligned
+    assert cr(0, 99, 10 ** 6, 100) == _lib.PS_ERR_INVALID              # stride below dim
+    assert L.ps_create_bf16(C.byref(h), K, 513, V(0), 600, V(10 ** 7), 600, 0.1, 0.0, None) == \
+        _lib.PS_ERR_UNSUPPORTED
     assert h.value is None
 
 
