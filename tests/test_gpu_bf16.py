@@ -148,3 +148,16 @@ def test_push_bf16_interleaved_rows(d):
     oracle.push_bf16(Wr, Gr, keys, grads, LR, EPS)
     assert_close_tables(oracle.bf16_to_f32(bf16_host(Wt.contiguous())), oracle.bf16_to_f32(Wr), "widened W")
     assert_close_tables(Gt.cpu().numpy(), Gr, "G")
+
+
+def test_bf16_empty_push_and_step_are_no_ops():
+    cfg = small_variant(MF_10Mx1M)
+    Wb = bf16_table(cfg.num_keys, cfg.dim, 87)
+    Wt, Gt = bf16_dev(Wb), torch.zeros(Wb.shape, dtype=torch.float32, device="cuda")
+    s = Store(Wt, Gt, LR, EPS)
+    s.push(torch.zeros(0, dtype=torch.int64, device="cuda"), torch.zeros((0, cfg.dim), dtype=torch.float32,
+                                                                          device="cuda"))
+    e = torch.zeros(0, dtype=torch.int32, device="cuda")
+    loss = s.step_mf(e, e, torch.zeros(0, dtype=torch.float32, device="cuda"), cfg.n_rows, cfg.lam)
+    assert s.error() == 0 and float(loss.item()) == 0.0
+    assert_bitwise(bf16_host(Wt), Wb, "W")

@@ -259,3 +259,37 @@ def test_push_workspace_too_small_is_rejected():
     st = _lib.lib().ps_push(s._h, C.c_void_p(keys.data_ptr()), 50, C.c_void_p(grads.data_ptr()),
                             C.c_void_p(ws.data_ptr()), need - 1, C.c_void_p(0))
     assert st == _lib.PS_ERR_WORKSPACE
+
+
+def test_push_at_the_largest_key_count():
+    """num_keys = 2^31 - 1 (dim 1: 8.6 GB each for W and G in HBM): keys at
+    both ends, heavy duplicates.  The oracle runs on the touched rows only
+    (a push never reads other rows); a sample of untouched rows is checked
+    unchanged."""
+    K, d, n = (1 << 31) - 1, 1, 1 << 20
+    say("allocating 2 x 8.6 GB")
+    idx = torch.arange(K, dtype=torch.int64, device="cuda")
+    Wt = ((idx % 1000).to(torch.float32) * 1e-3).reshape(K, d)
+    del idx
+    Gt = torch.zeros((K, d), dtype=torch.float32, device="cuda")
+    rng = np.random.default_rng(90)
+    keys = np.concatenate([rng.integers(0, K, n - 3000), np.full(1000, K - 1), np.full(1000, 0),
+                           rng.integers(K - 500, K, 1000)]).astype(np.int64)
+    rng.shuffle(keys)
+    grads = rng.standard_normal((n, d)).astype(np.float32)
+    s = Store(Wt, Gt, LR, EPS)
+    say("push")
+    s.push(dev(keys), dev(grads))
+    assert s.error() == 0
+    u, inv = np.unique(keys, return_inverse=True)
+    Ws = ((u % 1000).astype(np.float32) * np.float32(1e-3)).reshape(-1, d)
+    Gs = np.zeros_like(Ws)
+    oracle.push(Ws, Gs, inv.astype(np.int64), grads, LR, EPS)
+    out = s.pull(dev(u)).cpu().numpy()
+    assert_close_tables(out, Ws, "touched rows")
+    assert_close_tables(Gt[torch.from_numpy(u).cuda()].cpu().numpy(), Gs, "touched accumulators")
+    probe = np.setdiff1d(rng.integers(0, K, 5000), u)
+    assert_bitwise(s.pull(dev(probe)).cpu().numpy(), ((probe % 1000).astype(np.float32) * np.float32(1e-3)).reshape(-1, 1),
+                   "untouched rows")
+    del Wt, Gt
+    torch.cuda.empty_cache()

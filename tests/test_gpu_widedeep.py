@@ -173,3 +173,17 @@ def test_wd_on_a_rowwise_store():
     assert_close_tables(Wt.cpu().numpy(), Wr, "W")
     assert_close_tables(At_rows.cpu().numpy(), Ar, "row accumulators")
     assert_close_tables(Dt.cpu().numpy(), Dr, "dense parameters")
+
+
+def test_wd_empty_batch_is_a_no_op():
+    cfg = ODD
+    wl = CTRWorkload(cfg)
+    W, dense = wl.init_table(), wl.init_dense()
+    Wt, Gt = dev(W), torch.zeros(W.shape, dtype=torch.float32, device="cuda")
+    Dt, At = dev(dense), torch.zeros(dense.shape, dtype=torch.float32, device="cuda")
+    s = Store(Wt, Gt, cfg.opt.lr, cfg.opt.eps)
+    loss = s.step_ctr_wd(torch.zeros((0, cfg.n_fields), dtype=torch.int64, device="cuda"),
+                         torch.zeros(0, dtype=torch.float32, device="cuda"), Dt, At, cfg.emb_dim, cfg.deep)
+    assert s.error() == 0 and float(loss.item()) == 0.0
+    assert_bitwise(Wt.cpu().numpy(), W, "W")
+    assert_bitwise(Dt.cpu().numpy(), dense, "dense")
