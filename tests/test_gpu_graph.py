@@ -89,3 +89,78 @@ def test_step_graph_replays_match_eager(name):
         assert_bitwise(WB.cpu().numpy(), WA.cpu().numpy(), f"W after replay {step}")
         assert_bitwise(GB.cpu().numpy(), GA.cpu().numpy(), f"G after replay {step}")
         assert lossB.item() == lossA.item()
+
+
+def graph_vs_eager(make_store, call, batch, snapshot, name):
+    """Capture call(store_B, static batch) once; before each replay copy the
+    next batch in, run the same step eagerly on store_A, and compare."""
+    A, B = make_store(), make_store()
+    lossA = torch.zeros(1, dtype=torch.float64, device="cuda")
+    lossB = torch.zeros(1, dtype=torch.float64, device="cuda")
+    warm = batch(0)
+    call(A, warm, lossA)
+    call(B, warm, lossB)
+    static = batch(1)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        call(B, static, lossB)
+    torch.cuda.synchronize()
+    for step in range(1, 5):
+        say(f"{name}: replay for step {step}")
+        b = batch(step)
+        for k in b:
+            static[k].copy_(b[k])
+        call(A, b, lossA)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert A[0].error() == 0 and B[0].error() == 0
+        for i, (x, y) in enumerate(zip(snapshot(A), snapshot(B))):
+            assert_bitwise(y, x, f"{name} state {i} after replay {step}")
+        assert lossB.item() == lossA.item()
+
+
+def test_widedeep_graph_replays_match_eager():
+    from dataclasses import replace
+    from paper_2206_00470_amd.workloads import CTR_33M_WD
+    cfg = replace(small_variant(CTR_33M_WD), deep=(96, 40), emb_dim=12, dim=16, n_fields=7)
+    wl = CTRWorkload(cfg)
+    W0, D0 = wl.init_table(), wl.init_dense()
+
+    def make():
+        s = Store(dev(W0), torch.zeros(W0.shape, dtype=torch.float32, device="cuda"), cfg.opt.lr, cfg.opt.eps)
+        return (s, dev(D0), torch.zeros(D0.shape, dtype=torch.float32, device="cuda"))
+
+    def call(st, b, loss):
+        s, D, Acc = st
+        s.step_ctr_wd(b["keys"], b["label"], D, Acc, cfg.emb_dim, cfg.deep, loss=loss)
+
+    graph_vs_eager(make, call, lambda i: {k: dev(v) for k, v in wl.batch(i).__dict__.items()},
+                   lambda st: (st[0].W.cpu().numpy(), st[0].G.cpu().numpy(), st[1].cpu().numpy(), st[2].cpu().numpy()),
+                   "wide & deep")
+
+
+@pytest.mark.parametrize("kind", ["rowwise", "bf16"])
+def test_mf_variant_graph_replays_match_eager(kind):
+    from paper_2206_00470_amd.store import interleaved_bf16_tables, padded_rowwise_table
+    cfg = small_variant(MF_10Mx1M)
+    wl = MFWorkload(cfg)
+    W0 = torch.from_numpy(wl.init_table()).cuda()
+
+    def make():
+        if kind == "rowwise":
+            W, A = padded_rowwise_table(W0)
+        else:
+            W, A = interleaved_bf16_tables(W0)
+        return (Store(W, A, cfg.opt.lr, cfg.opt.eps),)
+
+    def call(st, b, loss):
+        st[0].step_mf(b["row"], b["col"], b["val"], cfg.n_rows, cfg.lam, loss=loss)
+
+    def snap(st):
+        W = st[0].W
+        w = W.float().cpu().numpy() if W.dtype == torch.bfloat16 else W.cpu().numpy()
+        return (w, st[0].G.cpu().numpy())
+
+    graph_vs_eager(make, call, lambda i: {k: dev(v) for k, v in wl.batch(i).__dict__.items()}, snap, f"mf {kind}")

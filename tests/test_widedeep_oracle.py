@@ -51,6 +51,10 @@ def test_gradients_match_torch_autograd_float64(hidden):
     d = unpack(dflat, F * E, hidden)
     for k in tp:
         np.testing.assert_allclose(d[k], tp[k], rtol=1e-11, atol=1e-13, err_msg=k)
+    # the packed per-occurrence rows: [dx_f | dlogit | padding], rounded once to fp32
+    okeys, grads, _, _, _ = grad_ctr_wd(W, dense, keys, label, E, hidden)
+    assert np.array_equal(okeys, keys.ravel())
+    np.testing.assert_allclose(grads, trow.reshape(-1, WIDTH).astype(np.float32), rtol=3e-7, atol=1e-12)
 
 
 def test_gradients_match_central_finite_differences():
