@@ -428,7 +428,7 @@ __global__ __launch_bounds__(BLOCK) void k_seg_finalize(SegView sv, VT* __restri
     const int64_t nf = sb > sa ? sb - sa : 0;
     const int64_t n1 = nf ? sa * FOLD_SB - f : bl - f + 1;   // cut partials before the folds
     const int64_t n3 = nf ? bl - sb * FOLD_SB + 1 : 0;       // cut partials after them
-    auto row = [&](int64_t i) -> const double* {
+    auto row = [=](int64_t i) -> const double* {
       if (i == 0) return partial + (2 * b0 + ((s0 % CHUNK) != 0)) * dim;
       if (i <= n1) return partial + 2 * (f + (i - 1)) * dim;
       if (i <= n1 + nf) return fold + (sa + (i - 1 - n1)) * dim;
