@@ -49,6 +49,8 @@ def lib():
             "orc_push": (i64, [p, p, i64, i32, f32, f32, p, i64, p]),
             "orc_adagrad_rowwise": (None, [p, p, p, i32, f32, f32]),
             "orc_push_rowwise": (i64, [p, p, i64, i32, f32, f32, p, i64, p]),
+            "orc_push_sequential": (i64, [p, p, i64, i32, f32, f32, p, i64, p, p]),
+            "orc_push_sequential_rowwise": (i64, [p, p, i64, i32, f32, f32, p, i64, p, p]),
             "orc_bf16_to_f32": (f32, [C.c_uint16]),
             "orc_f32_to_bf16": (C.c_uint16, [f32]),
             "orc_push_bf16": (i64, [p, p, i64, i32, f32, f32, p, i64, p]),
@@ -135,6 +137,72 @@ def push_rowwise(W, Gr, keys, grads, lr, eps):
     grads = _c(grads, np.float32).reshape(keys.size, W.shape[1])
     return int(lib().orc_push_rowwise(_p(W), _p(Gr), W.shape[0], W.shape[1], lr, eps, _p(keys), keys.size,
                                       _p(grads)))
+
+
+def push_sequential(W, G, keys, grads, lr, eps, order=None, rowwise=False):
+    """Write access without merging (the asynchronous update semantics):
+    each occurrence's gradient row is its own AdaGrad step, the occurrences
+    applied one after another in `order` (occurrence indices; None: index
+    order).  rowwise: G holds one accumulator per key (row-wise AdaGrad).
+    Returns the number of invalid keys."""
+    W = _table(W)
+    if rowwise:
+        assert G.dtype == np.float32 and G.flags.c_contiguous and G.shape == (W.shape[0],)
+    else:
+        G = _table(G)
+    keys = _c(keys, np.int64)
+    grads = _c(grads, np.float32).reshape(keys.size, W.shape[1])
+    o = None
+    if order is not None:
+        o = _c(order, np.int64)
+        assert o.size == keys.size
+    fn = lib().orc_push_sequential_rowwise if rowwise else lib().orc_push_sequential
+    return int(fn(_p(W), _p(G), W.shape[0], W.shape[1], lr, eps, _p(keys), keys.size, _p(grads),
+                  None if o is None else _p(o)))
+
+
+def async_bounds(W0, G0, keys, grads, lr, eps, rowwise=False):
+    """Per element of W, the interval [lo, hi] (fp64, exact arithmetic) that
+    holds W after the unmerged push in ANY order of the occurrences.
+
+    Occurrence j of key k takes the step lr * g_j / (sqrt(a_j) + eps), where
+    a_j is k's accumulator just after j's own square was added:
+    G0[k] + g_j^2 <= a_j <= G0[k] + (sum of all of k's squares).  Each step
+    therefore lies between its values at those two ends, and the sum of the
+    steps between the sums of their smaller and larger ends."""
+    K, d = W0.shape
+    keys = np.asarray(keys, np.int64)
+    g = np.asarray(grads, np.float64).reshape(keys.size, d)
+    ok = (keys >= 0) & (keys < K)
+    keys, g = keys[ok], g[ok]
+    if rowwise:
+        t = (g * g).sum(axis=1) / d                   # one square per occurrence (the row mean)
+        total = np.asarray(G0, np.float64).copy()
+        np.add.at(total, keys, t)
+        a_lo = (np.asarray(G0, np.float64)[keys] + t)[:, None]
+        a_hi = total[keys][:, None]
+    else:
+        t = g * g
+        total = np.asarray(G0, np.float64).copy()
+        np.add.at(total, keys, t)
+        a_lo = np.asarray(G0, np.float64)[keys] + t
+        a_hi = total[keys]
+    s1 = lr * g / (np.sqrt(a_lo) + eps)
+    s2 = lr * g / (np.sqrt(a_hi) + eps)
+    smin, smax = np.zeros((K, d)), np.zeros((K, d))
+    np.add.at(smin, keys, np.minimum(s1, s2))
+    np.add.at(smax, keys, np.maximum(s1, s2))
+    W = np.asarray(W0, np.float64)
+    return W - smax, W - smin
+
+
+def step_mf_sequential(W, G, row, col, val, col_off, lam, lr, eps, order=None, rowwise=False):
+    """An MF step with the asynchronous update semantics: every entry's two
+    gradient rows from the pre-step table (occurrences 2b: row key, 2b+1:
+    column key), then push_sequential in `order`.  Returns (loss, bad)."""
+    keys, grads, loss, bad = grad_mf(W, row, col, val, col_off, lam)
+    push_sequential(W, G, keys, grads, lr, eps, order, rowwise)
+    return loss, bad
 
 
 def step_rowwise(task, W, Gr, batch, lr, eps, **kw):

@@ -209,6 +209,50 @@ ORC_API int64_t orc_push(float* W, float* G, int64_t num_keys, int32_t dim, floa
     return bad;
 }
 
+/* ------------------------------------------------------------------------ */
+/* Write access without merging: the asynchronous update semantics of the    */
+/* paper's experiments (Section 5.1: asynchronous SGD; each worker's update   */
+/* reaches the store on its own, with no merging of concurrent updates).    */
+/* Reading: every occurrence's gradient row is its own AdaGrad step on its   */
+/* key's row, the occurrences applied one after another in the order        */
+/* order[0..n) (occurrence indices; NULL: index order).  A store that       */
+/* applies them concurrently, each element atomically, ends, element by     */
+/* element, where some such order ends.  Invalid keys are ignored, counted. */
+/* ------------------------------------------------------------------------ */
+ORC_API int64_t orc_push_sequential(float* W, float* G, int64_t num_keys, int32_t dim, float lr, float eps,
+                                    const int64_t* keys, int64_t n, const float* grads, const int64_t* order)
+{
+    int64_t bad = 0;
+    for (int64_t t = 0; t < n; ++t) {
+        int64_t i = order ? order[t] : t;
+        int64_t key = keys[i];
+        if (!key_ok(key, num_keys)) {
+            ++bad;
+            continue;
+        }
+        orc_adagrad_row(W + key * dim, G + key * dim, grads + i * dim, dim, lr, eps);
+    }
+    return bad;
+}
+
+/* The same with row-wise AdaGrad: Gr holds one accumulator per key.         */
+ORC_API int64_t orc_push_sequential_rowwise(float* W, float* Gr, int64_t num_keys, int32_t dim, float lr,
+                                            float eps, const int64_t* keys, int64_t n, const float* grads,
+                                            const int64_t* order)
+{
+    int64_t bad = 0;
+    for (int64_t t = 0; t < n; ++t) {
+        int64_t i = order ? order[t] : t;
+        int64_t key = keys[i];
+        if (!key_ok(key, num_keys)) {
+            ++bad;
+            continue;
+        }
+        orc_adagrad_rowwise(W + key * dim, Gr + key, grads + i * dim, dim, lr, eps);
+    }
+    return bad;
+}
+
 /* The same merge with row-wise AdaGrad: Gr holds one accumulator per key.   */
 ORC_API int64_t orc_push_rowwise(float* W, float* Gr, int64_t num_keys, int32_t dim, float lr, float eps,
                                  const int64_t* keys, int64_t n, const float* grads)
