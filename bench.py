@@ -49,9 +49,10 @@ def parse():
     ap.add_argument("--layout", default="interleaved", choices=["interleaved", "dense"],
                     help="W and G rows of a key side by side in one allocation, or two dense tables "
                          "(row-wise update: the accumulator in each W row's padding, or a separate vector)")
-    ap.add_argument("--update", default="elementwise", choices=["elementwise", "rowwise"],
+    ap.add_argument("--update", default="elementwise", choices=["elementwise", "rowwise", "async"],
                     help="AdaGrad with one accumulator per element (the paper's), or per key (an update "
-                         "variant with half the table traffic)")
+                         "variant with half the table traffic), or per element applied without merging "
+                         "(async: every occurrence its own step, atomic adds in no fixed order; MF only)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a 4 GiB device-to-device copy (reference for HBM counters)")
     ap.add_argument("--no-overlap", action="store_true",
@@ -104,13 +105,14 @@ class Bench:
     """One workload: its table, resident step batches, the step call, the
     algorithmic bytes of its two big kernels and the oracle step."""
 
-    def __init__(self, name, dev, nbatches, rowwise=False, values="f32"):
+    def __init__(self, name, dev, nbatches, rowwise=False, values="f32", unmerged=False):
         import torch
         from paper_2206_00470_amd import workloads as wls
 
         self.name = name
         self.rowwise = rowwise
         self.values = values
+        self.unmerged = unmerged
         self.task = {"mf_tiny": "mf", "mf_colorder": "mf", "kge2x100": "kge", "sgns_w2v": "sgns"}.get(name, name)
         cfgs = {"mf": wls.MF_10Mx1M, "mf_tiny": wls.MF_TINY, "mf_colorder": wls.MF_10Mx1M_COLORDER,
                 "kge": wls.KGE_COMPLEX, "kge2x100": wls.KGE_COMPLEX_2x100, "sgns": wls.SGNS_1M,
@@ -153,7 +155,9 @@ class Bench:
 
     def step(self, store, i, loss):
         c, b = self.cfg, self.batches[i % len(self.batches)]
-        if self.task == "mf":
+        if self.task == "mf" and self.unmerged:
+            store.step_mf_async(b["row"], b["col"], b["val"], c.n_rows, c.lam, loss=loss)
+        elif self.task == "mf":
             store.step_mf(b["row"], b["col"], b["val"], c.n_rows, c.lam, loss=loss)
         elif self.task == "kge":
             store.step_kge(b["head"], b["rel"], b["tail"], b["neg"], c.n_head_neg, c.n_ent, loss=loss)
@@ -216,6 +220,12 @@ class Bench:
         RV = self.RV
         tab = 2.0 * RV + 8.0 if self.rowwise else 2.0 * RV + 2.0 * R
         table = tab * U
+        if self.task == "mf" and self.unmerged:
+            # gradient rows: row, col, val in, each distinct key's row read once, two
+            # gradient rows out per entry; unmerged update: every gradient row read and
+            # each distinct key's W and G read and written once
+            B = bt.row.size
+            return {"async": n * R + tab * U, "taskgrad": B * 12.0 + U * RV + 2.0 * B * R}
         if self.task == "mf":
             B = bt.row.size
             Ucol = np.unique(bt.col).size
@@ -265,6 +275,8 @@ class Bench:
                     "sgns": (bt.centre, bt.ctx, bt.neg, c.window, c.vocab),
                     "ctr": (bt.keys, bt.label)}[self.task]
             oracle.step_rowwise(self.task, W, G, args, lr, eps)
+        elif self.task == "mf" and self.unmerged:
+            oracle.step_mf_sequential(W, G, bt.row, bt.col, bt.val, c.n_rows, c.lam, lr, eps)
         elif self.task == "mf":
             oracle.step_mf(W, G, bt.row, bt.col, bt.val, c.n_rows, c.lam, lr, eps)
         elif self.task == "kge":
@@ -401,11 +413,15 @@ def main():
     t0 = time.time()
     nb = max(1, min(args.steps + args.warmup, 8))
     rowwise = args.update == "rowwise"
+    unmerged = args.update == "async"
     bf16 = args.values == "bf16"
+    if unmerged and (bf16 or args.staged or not args.workload.startswith("mf")):
+        print("--update async runs the MF workloads on fp32 values, in HBM", file=sys.stderr)
+        sys.exit(2)
     if bf16 and (rowwise or args.staged or not args.workload.startswith("mf")):
         print("--values bf16 runs the MF workloads with per-element AdaGrad, in HBM", file=sys.stderr)
         sys.exit(2)
-    wb = Bench(args.workload, dev, nb, rowwise, args.values)
+    wb = Bench(args.workload, dev, nb, rowwise, args.values, unmerged)
     cfg = wb.cfg
     metric = ("param rows pulled+pushed/sec (MF 10m x 1m, rank 100)" if args.workload == "mf"
               else f"param rows pulled+pushed/sec ({cfg.name})")
@@ -453,11 +469,12 @@ def main():
           file=sys.stderr, flush=True)
 
     KID = {"segreduce": _lib.PS_KERNEL_SEGREDUCE, "taskgrad": _lib.PS_KERNEL_TASKGRAD,
-           "rowmerge": _lib.PS_KERNEL_MF_ROWMERGE, "scatter": _lib.PS_KERNEL_SCATTER, "mlp": _lib.PS_KERNEL_MLP}
+           "rowmerge": _lib.PS_KERNEL_MF_ROWMERGE, "scatter": _lib.PS_KERNEL_SCATTER, "mlp": _lib.PS_KERNEL_MLP,
+           "async": _lib.PS_KERNEL_ASYNC}
     names = list(wb.alg_bytes(0))                 # kernels with algorithmic bytes for this workload
 
     # (MF tiny is launch-bound: the extra events of the overlap cost more than it hides)
-    overlap = args.workload in ("mf", "mf_colorder") and not args.no_overlap and not args.graph
+    overlap = args.workload in ("mf", "mf_colorder") and not args.no_overlap and not args.graph and not unmerged
 
     def run_steps(first, count, mask):
         """count steps from batch `first` with the kernels in `mask` bracketed by HIP
@@ -531,10 +548,11 @@ def main():
     kernels["scatter"] = {"ms_per_step": kt_all["scatter"][0] / nprof, "launches": kt_all["scatter"][1]}
     symbol = {"segreduce": "k_segreduce<%s>" % {"mf": "SrcSorted", "kge": "SrcKGE", "sgns": "SrcSGNS",
                                                  "ctr": "SrcSorted", "ctr_wd": "SrcSorted"}[wb.task],
-              "rowmerge": "k_segreduce<SrcMFRow>", "mlp": "k_gemm_f64",
-              "taskgrad": {"mf": "k_mf_pack", "kge": "k_kge_grad", "sgns": "k_sgns_grad",
+              "rowmerge": "k_segreduce<SrcMFRow>", "mlp": "k_gemm_f64", "async": "k_push_async",
+              "taskgrad": {"mf": "k_mf_grad_rows" if unmerged else "k_mf_pack", "kge": "k_kge_grad", "sgns": "k_sgns_grad",
                            "ctr": "k_ctr_grad", "ctr_wd": "k_wd_head"}[wb.task]}[dom]
-    traffic = counter_traffic(args.workload + ("_rowwise" if rowwise else "") + ("_bf16" if bf16 else ""), symbol)
+    traffic = counter_traffic(args.workload + ("_rowwise" if rowwise else "") + ("_bf16" if bf16 else "")
+                              + ("_async" if unmerged else ""), symbol)
     roofline = {
         "bound": "hbm",
         "kernel": symbol,
@@ -581,6 +599,15 @@ def main():
             store.pull(keys, out=out)
         torch.cuda.synchronize()
         tl = (time.perf_counter() - t1) / reps
+        ta = None
+        if unmerged:
+            store.push_async(keys, grads)
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            for _ in range(reps):
+                store.push_async(keys, grads)
+            torch.cuda.synchronize()
+            ta = (time.perf_counter() - t1) / reps
         assert store.error() == 0
         R = wb.R
         RV = wb.RV
@@ -604,6 +631,8 @@ def main():
             "push": {"ms": round(tp * 1e3, 4), "rows_per_s": n / tp, "alg_GBps": round(push_alg / tp / 1e9, 1),
                      "frac_of_peak": round(push_alg / tp / 1e9 / HBM_PEAK_GBPS, 4), "unique_keys": int(U)},
             "pull": {"ms": round(tl * 1e3, 4), "rows_per_s": n / tl, "alg_GBps": round(pull_alg / tl / 1e9, 1)},
+            **({"push_async": {"ms": round(ta * 1e3, 4), "rows_per_s": n / ta,
+                               "alg_GBps": round((n * R + tab * U) / ta / 1e9, 1)}} if ta else {}),
             "merge_distinct_keys": {"keys": int(U), "merge_ms": round(merge_ms, 4),
                                     "alg_GBps": round(rmw_alg / (merge_ms * 1e-3) / 1e9, 1),
                                     "what": "merge kernel alone on a push of distinct random keys: W and G "
@@ -631,7 +660,8 @@ def main():
     cpu = cpu_baseline(args, wb, rowwise)
 
     line = {
-        "metric": metric + (", row-wise AdaGrad" if rowwise else "") + (", bf16 values" if bf16 else ""),
+        "metric": metric + (", row-wise AdaGrad" if rowwise else "") + (", bf16 values" if bf16 else "")
+                  + (", unmerged (asynchronous) updates" if unmerged else ""),
         "value": rows_per_s,
         "unit": "rows/s",
         "n_gpus": 1,

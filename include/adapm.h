@@ -66,6 +66,7 @@ typedef int32_t ps_status;
 #define PS_OP_STEP_KGE  4
 #define PS_OP_STEP_SGNS 5
 #define PS_OP_STEP_CTR  6
+#define PS_OP_STEP_MF_ASYNC 7
 
 /* Limits: num_keys in [1, 2^31-1]; dim in [1, 512]; key occurrences per
  * call n < 2^31 - 2^20. */
@@ -127,7 +128,8 @@ ps_status ps_destroy(ps_store* s);
  * (keys for PULL/PUSH/DEDUP; entries, triples, centres or samples for the
  * steps) and `per_unit` the key occurrences each unit creates: 1 for
  * PULL/PUSH/DEDUP, 2 for MF, 3+n_neg for KGE, 1+2*window*(1+n_neg) for
- * SGNS, F for CTR.  Returns 0 for an invalid combination. */
+ * SGNS, F for CTR (2 for MF_ASYNC).  Returns 0 for an invalid
+ * combination. */
 size_t ps_workspace_bytes(int64_t num_keys, int32_t dim, int32_t op, int64_t units, int64_t per_unit);
 
 /* Read access (Section 1: global read access to parameters by key).
@@ -187,6 +189,29 @@ ps_status ps_step_mf_prepare(ps_store* s, const int32_t* row, const int32_t* col
 ps_status ps_step_mf_apply(ps_store* s, int64_t B, float lambda, double* loss, void* ws,
                            size_t ws_bytes, void* stream, void* rows_done);
 
+/* Unmerged write access: the asynchronous update semantics of the paper's
+ * experiments (Section 5.1, asynchronous SGD), as an opt-in alternative to
+ * ps_push.  Every occurrence's gradient row is applied as its own AdaGrad
+ * step (per element, or row-wise on a row-wise store), each element update
+ * a device-scope atomic add: an occurrence's step uses the accumulator just
+ * after its own square was added.  Occurrences of one key are applied in
+ * no fixed order, so results are not reproducible bit for bit; element by
+ * element they equal those of applying the occurrences one after another
+ * in some order.  Needs no sort and no workspace.  keys: device int64[n];
+ * grads: device float[n*dim] (16-byte aligned when dim % 4 == 0).  A key
+ * outside [0, num_keys) is skipped and reported by ps_get_error.  Staged
+ * stores and bf16 values: PS_ERR_UNSUPPORTED. */
+ps_status ps_push_async(ps_store* s, const int64_t* keys, int64_t n, const float* grads, void* stream);
+
+/* The MF step of ps_step_mf with the unmerged update: both gradient rows of
+ * every entry from the pre-step table (as in ps_step_mf), then applied as
+ * by ps_push_async (occurrence 2b: the row key, 2b+1: the column key).  ws
+ * holds the 2*B gradient rows: ps_workspace_bytes(num_keys, dim,
+ * PS_OP_STEP_MF_ASYNC, B, 2).  loss as for ps_step_mf. */
+ps_status ps_step_mf_async(ps_store* s, const int32_t* row, const int32_t* col, const float* val,
+                           int64_t B, int64_t col_key_offset, float lambda, double* loss,
+                           void* ws, size_t ws_bytes, void* stream);
+
 /* One ComplEx knowledge-graph-embedding step with negative sampling
  * (Appendix C, "Knowledge graph embeddings").  Rows hold [Re | Im] of a
  * complex vector of dim/2 components (dim must be even).  Triple t uses
@@ -241,7 +266,8 @@ const char* ps_last_error_message(void);
  * not 0), 5 = row moves of a staged store between its home tables and its
  * slots (on the staging stream; set the mask while no round runs on the
  * library thread, read it after stopping that thread), 6 = the fp64
- * matrix-core products of the Wide & Deep step. */
+ * matrix-core products of the Wide & Deep step, 7 = the unmerged (atomic)
+ * update of ps_push_async and ps_step_mf_async. */
 #define PS_KERNEL_SEGREDUCE 0
 #define PS_KERNEL_TASKGRAD  1
 #define PS_KERNEL_SCATTER   2
@@ -249,6 +275,7 @@ const char* ps_last_error_message(void);
 #define PS_KERNEL_MF_ROWMERGE 4
 #define PS_KERNEL_STAGE     5
 #define PS_KERNEL_MLP       6
+#define PS_KERNEL_ASYNC     7
 #define PS_TIMING_ALL (-1)
 ps_status ps_set_timing(ps_store* s, int32_t mask);
 ps_status ps_read_timing(ps_store* s, int32_t kernel_id, double* total_ms, int64_t* launches);

@@ -21,10 +21,12 @@ PS_ERR_NOT_RESIDENT = -6
 
 PS_OP_PULL, PS_OP_PUSH, PS_OP_DEDUP = 0, 1, 2
 PS_OP_STEP_MF, PS_OP_STEP_KGE, PS_OP_STEP_SGNS, PS_OP_STEP_CTR = 3, 4, 5, 6
+PS_OP_STEP_MF_ASYNC = 7
 
 PS_KERNEL_SEGREDUCE, PS_KERNEL_TASKGRAD, PS_KERNEL_SCATTER, PS_KERNEL_PULL, PS_KERNEL_MF_ROWMERGE = 0, 1, 2, 3, 4
 PS_KERNEL_STAGE = 5
 PS_KERNEL_MLP = 6
+PS_KERNEL_ASYNC = 7
 PS_TIMING_ALL = -1
 
 STAGE_STATS = ["clock", "rounds", "forced", "staged", "evicted", "resident", "pending", "stalled"]
@@ -45,6 +47,8 @@ SIGNATURES = {
     "ps_step_mf": (_i32, [_p, _p, _p, _p, _i64, _i64, _f32, _p, _p, _sz, _p]),
     "ps_step_mf_prepare": (_i32, [_p, _p, _p, _p, _i64, _i64, _p, _sz, _p]),
     "ps_step_mf_apply": (_i32, [_p, _i64, _f32, _p, _p, _sz, _p, _p]),
+    "ps_push_async": (_i32, [_p, _p, _i64, _p, _p]),
+    "ps_step_mf_async": (_i32, [_p, _p, _p, _p, _i64, _i64, _f32, _p, _p, _sz, _p]),
     "ps_step_kge": (_i32, [_p, _p, _p, _p, _p, _i64, _i32, _i32, _i64, _p, _p, _sz, _p]),
     "ps_step_sgns": (_i32, [_p, _p, _p, _p, _i64, _i32, _i32, _i64, _p, _p, _sz, _p]),
     "ps_step_ctr": (_i32, [_p, _p, _p, _i64, _i32, _p, _p, _sz, _p]),

@@ -14,6 +14,7 @@
 #include <utility>
 #include <vector>
 
+#include "async.hpp"
 #include "common.hpp"
 #include "mlp.hpp"
 #include "push.hpp"
@@ -47,7 +48,7 @@ ps_status fail(ps_status st, const char* fmt, ...) {
 #define LAUNCHED(name) HIP_TRY(hipGetLastError())
 
 constexpr int64_t MAX_OCC = (int64_t(1) << 31) - (int64_t(1) << 20);
-constexpr int NUM_TIMED = 7;
+constexpr int NUM_TIMED = 8;
 constexpr size_t MAX_TIMED_LAUNCHES = 1 << 14;
 
 }  // namespace
@@ -309,6 +310,10 @@ bool plan_op(void* ws, int64_t num_keys, int dim, int op, int64_t units, int64_t
       p->loss_part = c.take<double>(LOSS_GRID);
       p->ok = c.take<uint8_t>(units);
       break;
+    case PS_OP_STEP_MF_ASYNC:
+      p->grads = c.take<float>(size_t(n) * dim);   // both gradient rows of each entry, entry order
+      p->loss_part = c.take<double>(LOSS_GRID);
+      break;
     case PS_OP_STEP_SGNS:
       carve_sort(c, n, dim, false, true, &p->sb);
       p->mat = c.take<float>(size_t(units) * dim);
@@ -319,7 +324,7 @@ bool plan_op(void* ws, int64_t num_keys, int dim, int op, int64_t units, int64_t
     default:
       return false;
   }
-  if (op != PS_OP_DEDUP) p->trans = c.take<char>(size_t(n) * 8);
+  if (op != PS_OP_DEDUP && op != PS_OP_STEP_MF_ASYNC) p->trans = c.take<char>(size_t(n) * 8);
   p->bytes = c.off + 256;
   return true;
 }
@@ -925,6 +930,34 @@ ps_status check_staged(ps_store* s) {
   return PS_OK;
 }
 
+// ------------------------------------------------------------------ unmerged (asynchronous) updates
+ps_status check_async(const ps_store* s) {
+  if (s->stg) return fail(PS_ERR_UNSUPPORTED, "unmerged updates are not available on a staged store");
+  if (s->bf16) return fail(PS_ERR_UNSUPPORTED, "unmerged updates run on fp32 values only");
+  return PS_OK;
+}
+
+template <class Keys>
+ps_status launch_push_async(ps_store* s, Keys keys, const float* grads, int64_t n, hipStream_t st) {
+  // one float per lane and atomic instruction, consecutive lanes on
+  // consecutive floats: a wave's atomic touches whole cache lines (four
+  // times faster than four consecutive floats per lane)
+  RowShape shape;
+  if (!row_shape(s->dim, false, &shape)) return fail(PS_ERR_UNSUPPORTED, "dim %d not supported", s->dim);
+  return with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
+    const int64_t grid = small_grid(n, BLOCK / L, int64_t(1) << 16);
+    Timed t(s, PS_KERNEL_ASYNC, st);
+    if (s->rowwise)
+      hipLaunchKernelGGL((k_push_async<L, NV, VW, true, Keys>), dim3(grid), dim3(BLOCK), 0, st, keys, grads, n, s->W,
+                         s->G, s->ld, s->gld, s->dim, s->num_keys, s->lr, s->eps, s->status);
+    else
+      hipLaunchKernelGGL((k_push_async<L, NV, VW, false, Keys>), dim3(grid), dim3(BLOCK), 0, st, keys, grads, n, s->W,
+                         s->G, s->ld, s->gld, s->dim, s->num_keys, s->lr, s->eps, s->status);
+    LAUNCHED(k_push_async);
+    return PS_OK;
+  });
+}
+
 }  // namespace
 
 // ======================================================================== C ABI
@@ -1341,6 +1374,48 @@ ps_status ps_push(ps_store* s, const int64_t* keys, int64_t n, const float* grad
   int64_t* tk = reinterpret_cast<int64_t*>(t);
   if (ps_status r = translate_keys(s, keys, n, tk, as_stream(stream))) return r;
   return push_impl(s, tk, n, grads, ws, ws_bytes, stream);
+}
+
+// ------------------------------------------------------------------ unmerged (asynchronous) updates
+ps_status ps_push_async(ps_store* s, const int64_t* keys, int64_t n, const float* grads, void* stream) {
+  if (ps_status st = check_store(s)) return st;
+  if (ps_status st = check_async(s)) return st;
+  if (ps_status st = check_n(n, 1)) return st;
+  if (n == 0) return PS_OK;
+  if (!keys || !grads) return fail(PS_ERR_INVALID, "keys or grads is NULL");
+  if (s->dim % 4 == 0 && !aligned16(grads)) return fail(PS_ERR_INVALID, "grads must be 16-byte aligned");
+  return launch_push_async(s, KeysList{keys}, grads, n, as_stream(stream));
+}
+
+ps_status ps_step_mf_async(ps_store* s, const int32_t* row, const int32_t* col, const float* val, int64_t B,
+                           int64_t col_key_offset, float lambda, double* loss, void* ws, size_t ws_bytes,
+                           void* stream) {
+  if (ps_status st = check_store(s)) return st;
+  if (ps_status st = check_async(s)) return st;
+  if (ps_status st = check_n(B, 2)) return st;
+  hipStream_t st = as_stream(stream);
+  if (B == 0) return zero_loss(loss, st);
+  if (!row || !col || !val) return fail(PS_ERR_INVALID, "row, col or val is NULL");
+  if (col_key_offset < 0) return fail(PS_ERR_INVALID, "negative col_key_offset");
+  Plan p;
+  plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_MF_ASYNC, B, 2, &p);
+  if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
+  RowShape shape;
+  if (!row_shape(s->dim, true, &shape)) return fail(PS_ERR_UNSUPPORTED, "dim %d not supported", s->dim);
+  const int64_t grid = small_grid(B, BLOCK / shape.L, LOSS_GRID);
+  ps_status r = with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
+    Timed t(s, PS_KERNEL_TASKGRAD, st);
+    hipLaunchKernelGGL((k_mf_grad_rows<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->ld, s->dim, row, col,
+                       val, B, col_key_offset, s->num_keys, (double)lambda, p.grads, p.loss_part);
+    LAUNCHED(k_mf_grad_rows);
+    return PS_OK;
+  });
+  if (r) return r;
+  if (loss) {
+    hipLaunchKernelGGL(k_sum_loss, dim3(1), dim3(BLOCK), 0, st, p.loss_part, grid, loss);
+    LAUNCHED(k_sum_loss);
+  }
+  return launch_push_async(s, KeysMF{row, col, col_key_offset, s->num_keys}, p.grads, 2 * B, st);
 }
 
 ps_status ps_step_mf(ps_store* s, const int32_t* row, const int32_t* col, const float* val, int64_t B,

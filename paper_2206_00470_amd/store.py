@@ -187,6 +187,16 @@ class Store:
         ws, wsb = self._ws(_lib.PS_OP_PUSH, n, 1)
         check(lib().ps_push(self._h, _ptr(keys), n, _ptr(grads), ws, wsb, _stream(stream)))
 
+    def push_async(self, keys: torch.Tensor, grads: torch.Tensor, stream=None):
+        """Unmerged push: every occurrence its own AdaGrad step, applied with
+        atomic adds in no fixed order (the asynchronous update semantics)."""
+        _dev(keys, torch.int64, "keys")
+        _dev(grads, torch.float32, "grads")
+        n = keys.numel()
+        if grads.numel() != n * self.dim:
+            raise ValueError("grads must hold n*dim floats")
+        check(lib().ps_push_async(self._h, _ptr(keys), n, _ptr(grads), _stream(stream)))
+
     # ---------------------------------------------------------------- task steps
     def _loss(self, loss):
         if loss is None:
@@ -200,6 +210,16 @@ class Store:
         ws, wsb = self._ws(_lib.PS_OP_STEP_MF, B, 2)
         check(lib().ps_step_mf(self._h, _ptr(row), _ptr(col), _ptr(val), B, col_key_offset, lam, _ptr(loss),
                                ws, wsb, _stream(stream)))
+        return loss
+
+    def step_mf_async(self, row, col, val, col_key_offset: int, lam: float, loss=None, stream=None):
+        """The MF step with the unmerged update (see push_async)."""
+        _dev(row, torch.int32, "row"), _dev(col, torch.int32, "col"), _dev(val, torch.float32, "val")
+        B = row.numel()
+        loss = self._loss(loss)
+        ws, wsb = self._ws(_lib.PS_OP_STEP_MF_ASYNC, B, 2)
+        check(lib().ps_step_mf_async(self._h, _ptr(row), _ptr(col), _ptr(val), B, col_key_offset, lam,
+                                     _ptr(loss), ws, wsb, _stream(stream)))
         return loss
 
     def mf_workspace(self, B: int) -> torch.Tensor:
