@@ -617,26 +617,48 @@ __global__ __launch_bounds__(BLOCK) void k_sgns_grad(const float* __restrict__ W
     }
 #pragma unroll
     for (int e = 0; e < NE; ++e) gv[e * BLOCK] = 0.0;
-    // all output rows of the centre in occurrence order: row r is slot r / (K+1),
-    // position r % (K+1) (0 = the context word, then the negatives).  Lane i
-    // holds the table id of row t*L + i of the current tile t of L rows (-1:
-    // absent slot or past the end); the next tile's ids are loaded one tile
+    // the output rows of the centre's present slots in occurrence order: row
+    // r is slot r / (K+1), position r % (K+1) (0 = the context word, then the
+    // negatives).  The loop runs over "live" rows rp, the rows of present
+    // slots only (a slot whose context is -1 has no rows), mapped to r
+    // through a bit mask of the present slots (up to 64 slots; with more,
+    // every slot is visited and absent ones are skipped row by row).  Lane i
+    // holds the table id of live row t*L + i of the current tile t of L rows
+    // (-1: absent or past the end); the next tile's ids are loaded one tile
     // ahead, so the row loads never wait for an id load.
-    const int rows = slots * (K + 1);
-    auto row_id = [&](int r) -> int64_t {
-      if (r >= rows) return -1;
+    uint64_t present = 0;
+    bool compact = false;   // some slot absent, and at most 64 slots
+    if (slots <= 64) {
+      for (int q = 0; q < slots; ++q) present |= (uint64_t)(ctx[b * slots + q] != -1) << q;
+      compact = __popcll(present) < slots;
+    }
+    const int rows = (compact ? __popcll(present) : slots) * (K + 1);
+    auto map_row = [&](int rp) -> int {   // live row -> row of the centre
+      if (!compact) return rp;
+      const int nth = rp / (K + 1);
+      uint64_t m = present;
+      for (int i = 0; i < nth; ++i) m &= m - 1;   // drop the nth lowest present slots
+      return __builtin_ctzll(m) * (K + 1) + (rp - nth * (K + 1));
+    };
+    // table id of live row rp (-1: absent or past the end) and its row r
+    auto row_id = [&](int rp, int& r) -> int64_t {
+      r = 0;
+      if (rp >= rows) return -1;
+      r = map_row(rp);
       const int q = r / (K + 1);
       const int k = r - q * (K + 1);
       const int64_t cx = ctx[b * slots + q];
       const int64_t ng = k == 0 ? 0 : (int64_t)neg[(b * slots + q) * K + (k - 1)];
       return cx == -1 ? -1 : (k == 0 ? cx : ng);
     };
-    int64_t id_cur = row_id(gl);
-    int64_t id_nxt = row_id(L + gl);
+    int r_cur, r_nxt;
+    int64_t id_cur = row_id(gl, r_cur);
+    int64_t id_nxt = row_id(L + gl, r_nxt);
     for (int r0 = 0; r0 < rows; r0 += JB) {
       if (r0 > 0 && r0 % L == 0) {
         id_cur = id_nxt;
-        id_nxt = row_id(r0 + L + gl);
+        r_cur = r_nxt;
+        id_nxt = row_id(r0 + L + gl, r_nxt);
       }
       float u[JB][NE];
       bool live[JB];
@@ -670,14 +692,14 @@ __global__ __launch_bounds__(BLOCK) void k_sgns_grad(const float* __restrict__ W
       for (int jj = 0; jj < JB; ++jj)
 #pragma unroll
         for (int e = 0; e < NE; ++e) ustash[jj * NE + e][threadIdx.x] = u[jj][e];
-      // lane finishes the score of row r0 + gl / (L / JB) and its coefficient
+      // lane finishes the score of live row r0 + gl / (L / JB) and its coefficient
       const double x_my = group_multi_sum<L, JB>(x, gl);
-      const int r_my = r0 + gl / (L / JB);
-      const int q_my = r_my / (K + 1);
-      const int k_my = r_my - q_my * (K + 1);
       const bool live_my = __shfl(id_cur, r0 % L + gl / (L / JB), L) != -1;   // also false past the end
+      const int r_my = __shfl(r_cur, r0 % L + gl / (L / JB), L);
       double a_my = 0.0;
       if (live_my) {
+        const int q_my = r_my / (K + 1);
+        const int k_my = r_my - q_my * (K + 1);
         // context word: a = -sigmoid(-x), loss softplus(-x); negative: a = sigmoid(x), loss softplus(x)
         const double sgn = k_my == 0 ? -1.0 : 1.0;
         double sig, sp;

@@ -258,6 +258,26 @@ def test_mf_async_paper_scale_sampled():
     check_accumulators(Gg, G0s, local, grads[sel])
 
 
+def test_mf_async_rowwise_store():
+    """Row-wise AdaGrad under the unmerged MF step (accumulators in the
+    padding of each value row)."""
+    from paper_2206_00470_amd.store import padded_rowwise_table
+    cfg = small_variant(MF_10Mx1M)
+    wl = MFWorkload(cfg)
+    W = wl.init_table()
+    Wt, At = padded_rowwise_table(torch.from_numpy(W).cuda())
+    s = Store(Wt, At, cfg.opt.lr, cfg.opt.eps)
+    for step in range(2):
+        bt = wl.batch(step)
+        W0, A0 = np.ascontiguousarray(Wt.cpu().numpy()), np.ascontiguousarray(At.cpu().numpy())
+        loss = s.step_mf_async(dev(bt.row), dev(bt.col), dev(bt.val), cfg.n_rows, cfg.lam)
+        assert s.error() == 0
+        keys, grads, rloss, _ = oracle.grad_mf(W0, bt.row, bt.col, bt.val, cfg.n_rows, cfg.lam)
+        assert float(loss.item()) == pytest.approx(rloss, rel=1e-9)
+        check_bounds(np.ascontiguousarray(Wt.cpu().numpy()), W0, A0, keys, grads, rowwise=True)
+        check_accumulators(np.ascontiguousarray(At.cpu().numpy()), A0, keys, grads, rowwise=True)
+
+
 def test_async_rejects_bf16_and_staged_stores():
     from paper_2206_00470_amd import StagedStore
     K, d = 100, 8

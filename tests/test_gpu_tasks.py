@@ -1,4 +1,6 @@
 """GPU parity of the ComplEx-KGE, skip-gram and CTR steps against the CPU oracle."""
+from dataclasses import replace
+
 import numpy as np
 import pytest
 import torch
@@ -189,6 +191,16 @@ def test_sgns_word2vec_subsampling_and_dynamic_window_small():
     cfg = small_variant(SGNS_1M_W2V)
     assert (SGNSWorkload(cfg).batch(1).ctx == -1).mean() > 0.2
     run_steps("sgns", cfg, range(3))
+
+
+def test_sgns_window_beyond_64_slots():
+    """A window of 33 (66 context slots per centre, drawn per centre): the
+    gradient kernel visits the present slots through a 64-bit mask up to 64
+    slots, and every slot beyond that."""
+    cfg = replace(small_variant(SGNS_1M_W2V), window=33, n_neg=3, batch=200)
+    assert (SGNSWorkload(cfg).batch(0).ctx == -1).any()
+    run_steps("sgns", cfg, range(2))
+    run_steps("sgns", replace(cfg, window=32), range(2))
 
 
 def test_kge_two_times_100_negatives_small():
