@@ -25,19 +25,20 @@ typedef double f64x4 __attribute__((ext_vector_type(4)));
 //
 // A workgroup computes a 128 x 128 tile of C, each of its four wavefronts a
 // 64 x 64 quarter as 4 x 4 products of 16 x 16.  K advances 16 at a time
-// through LDS; the next step's operands are loaded into registers while the
-// matrix cores work on the current one.  With gridDim.z = S > 1 the K range
+// through two LDS buffers: the next step's operands are loaded into
+// registers while the matrix cores work on the current buffer, then stored
+// to the other one, with one barrier per step.  With gridDim.z = S > 1 the K range
 // is split into S slices and slice z writes its partial product to
 // C + z * M * N (plain store only); k_sum_slices adds them in slice order.
 constexpr int GEMM_BM = 128, GEMM_BN = 128, GEMM_BK = 16;
-constexpr int GEMM_PAD = 2;   // doubles of padding per LDS row
+constexpr int GEMM_PAD = 0;   // doubles of padding per LDS row (padding measured no faster)
 
 template <bool TA, bool TB, typename BT>
 __global__ __launch_bounds__(BLOCK) void k_gemm_f64(int64_t M, int64_t N, int64_t K, const double* __restrict__ A,
                                                     int64_t lda, const BT* __restrict__ B, int64_t ldb,
                                                     double* __restrict__ C, int64_t ldc, int64_t kslice) {
-  __shared__ double As[GEMM_BK][GEMM_BM + GEMM_PAD];   // [k][m]
-  __shared__ double Bs[GEMM_BK][GEMM_BN + GEMM_PAD];   // [k][n]
+  __shared__ double As[2][GEMM_BK][GEMM_BM + GEMM_PAD];   // [buffer][k][m]
+  __shared__ double Bs[2][GEMM_BK][GEMM_BN + GEMM_PAD];   // [buffer][k][n]
   const int t = threadIdx.x;
   const int lane = t % WAVE;
   const int wave = t / WAVE;
@@ -75,13 +76,13 @@ __global__ __launch_bounds__(BLOCK) void k_gemm_f64(int64_t M, int64_t N, int64_
       }
     }
   };
-  auto stash = [&]() {
+  auto stash = [&](int buf) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      if constexpr (!TA) As[aq + e][ar] = ra[e];
-      else As[ar][aq + e] = ra[e];
-      if constexpr (!TB) Bs[br][bq + e] = rb[e];
-      else Bs[bq + e][br] = rb[e];
+      if constexpr (!TA) As[buf][aq + e][ar] = ra[e];
+      else As[buf][ar][aq + e] = ra[e];
+      if constexpr (!TB) Bs[buf][br][bq + e] = rb[e];
+      else Bs[buf][bq + e][br] = rb[e];
     }
   };
 
@@ -91,25 +92,33 @@ __global__ __launch_bounds__(BLOCK) void k_gemm_f64(int64_t M, int64_t N, int64_
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
 
-  if (kbeg < kend) load(kbeg);
+  if (kbeg < kend) {
+    load(kbeg);
+    stash(0);
+  }
+  __syncthreads();
+  int buf = 0;
   for (int64_t k0 = kbeg; k0 < kend; k0 += GEMM_BK) {
-    stash();
-    __syncthreads();
-    if (k0 + GEMM_BK < kend) load(k0 + GEMM_BK);   // in flight during the products below
+    const bool more = k0 + GEMM_BK < kend;
+    if (more) load(k0 + GEMM_BK);   // in flight during the products below
 #pragma unroll
     for (int ks = 0; ks < GEMM_BK; ks += 4) {
       const int kr = ks + lane / 16;
       double a[4], b[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = As[kr][wm + i * 16 + lane % 16];
+      for (int i = 0; i < 4; ++i) a[i] = As[buf][kr][wm + i * 16 + lane % 16];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) b[j] = Bs[kr][wn + j * 16 + lane % 16];
+      for (int j = 0; j < 4; ++j) b[j] = Bs[buf][kr][wn + j * 16 + lane % 16];
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[i], b[j], acc[i][j], 0, 0, 0);
     }
+    // the other buffer was last read in the previous step, which every wave
+    // finished before that step's barrier
+    if (more) stash(buf ^ 1);
     __syncthreads();
+    buf ^= 1;
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i)
