@@ -25,16 +25,17 @@ typedef double f64x4 __attribute__((ext_vector_type(4)));
 //
 // A workgroup computes a 128 x 128 tile of C, each of its four wavefronts a
 // 64 x 64 quarter as 4 x 4 products of 16 x 16.  K advances 16 at a time
-// through two LDS buffers: the next step's operands are loaded into
-// registers while the matrix cores work on the current buffer, then stored
-// to the other one, with one barrier per step.  With gridDim.z = S > 1 the K range
+// through two LDS buffers, one barrier per step; the operands of the step
+// after next are loaded into registers while the matrix cores work on the
+// current buffer (two register sets, so each load has two steps to land),
+// and the next step's registers are stored to the other buffer.  With gridDim.z = S > 1 the K range
 // is split into S slices and slice z writes its partial product to
 // C + z * M * N (plain store only); k_sum_slices adds them in slice order.
 constexpr int GEMM_BM = 128, GEMM_BN = 128, GEMM_BK = 16;
 constexpr int GEMM_PAD = 0;   // doubles of padding per LDS row (padding measured no faster)
 
 template <bool TA, bool TB, typename BT>
-__global__ __launch_bounds__(BLOCK) void k_gemm_f64(int64_t M, int64_t N, int64_t K, const double* __restrict__ A,
+__global__ __launch_bounds__(BLOCK, 2) void k_gemm_f64(int64_t M, int64_t N, int64_t K, const double* __restrict__ A,
                                                     int64_t lda, const BT* __restrict__ B, int64_t ldb,
                                                     double* __restrict__ C, int64_t ldc, int64_t kslice) {
   __shared__ double As[2][GEMM_BK][GEMM_BM + GEMM_PAD];   // [buffer][k][m]
@@ -56,8 +57,10 @@ __global__ __launch_bounds__(BLOCK) void k_gemm_f64(int64_t M, int64_t N, int64_
   const int aq = TA ? (t % 16) * 8 : (t % 2) * 8;
   const int br = TB ? t / 2 : t / 16;            // TB: n row; else k row
   const int bq = TB ? (t % 2) * 8 : (t % 16) * 8;
-  double ra[8], rb[8];
-  auto load = [&](int64_t k0) {
+  double ra_[2][8], rb_[2][8];
+  auto load = [&]<int R>(int64_t k0) {
+    double* ra = ra_[R];
+    double* rb = rb_[R];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       if constexpr (!TA) {
@@ -76,7 +79,9 @@ __global__ __launch_bounds__(BLOCK) void k_gemm_f64(int64_t M, int64_t N, int64_
       }
     }
   };
-  auto stash = [&](int buf) {
+  auto stash = [&]<int R>(int buf) {
+    const double* ra = ra_[R];
+    const double* rb = rb_[R];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       if constexpr (!TA) As[buf][aq + e][ar] = ra[e];
@@ -92,15 +97,7 @@ __global__ __launch_bounds__(BLOCK) void k_gemm_f64(int64_t M, int64_t N, int64_
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
 
-  if (kbeg < kend) {
-    load(kbeg);
-    stash(0);
-  }
-  __syncthreads();
-  int buf = 0;
-  for (int64_t k0 = kbeg; k0 < kend; k0 += GEMM_BK) {
-    const bool more = k0 + GEMM_BK < kend;
-    if (more) load(k0 + GEMM_BK);   // in flight during the products below
+  auto products = [&](int buf) {
 #pragma unroll
     for (int ks = 0; ks < GEMM_BK; ks += 4) {
       const int kr = ks + lane / 16;
@@ -114,11 +111,27 @@ __global__ __launch_bounds__(BLOCK) void k_gemm_f64(int64_t M, int64_t N, int64_
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[i], b[j], acc[i][j], 0, 0, 0);
     }
-    // the other buffer was last read in the previous step, which every wave
-    // finished before that step's barrier
-    if (more) stash(buf ^ 1);
+  };
+  // step s: LDS buffer s % 2 holds its operands, register set (s + 1) % 2
+  // those of step s + 1; set s % 2 is free (stored at the end of step s - 1)
+  // and receives step s + 2.  The other buffer was last read in step s - 1,
+  // which every wave finished before that step's barrier.
+  const int64_t nsteps = kbeg < kend ? (kend - kbeg + GEMM_BK - 1) / GEMM_BK : 0;
+  auto step = [&]<int P>(int64_t s) {
+    if (s + 2 < nsteps) load.template operator()<P>(kbeg + (s + 2) * GEMM_BK);
+    products(P);
+    if (s + 1 < nsteps) stash.template operator()<1 - P>(1 - P);
     __syncthreads();
-    buf ^= 1;
+  };
+  if (nsteps > 0) {
+    load.template operator()<0>(kbeg);
+    stash.template operator()<0>(0);
+    if (nsteps > 1) load.template operator()<1>(kbeg + GEMM_BK);
+  }
+  __syncthreads();
+  for (int64_t s = 0; s < nsteps; s += 2) {
+    step.template operator()<0>(s);
+    if (s + 1 < nsteps) step.template operator()<1>(s + 1);
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i)
