@@ -118,6 +118,25 @@ def test_push_async_some_order(K, d):
     assert_bitwise(Wg[untouched], W0[untouched], "untouched rows")
 
 
+def test_push_async_interleaved_rows():
+    """W and G rows of a key side by side in one allocation (the benchmark's
+    layout)."""
+    from paper_2206_00470_amd.store import interleaved_tables
+    K, d = 3000, 100
+    rng = np.random.default_rng(31)
+    W0 = (rng.standard_normal((K, d)) * 0.1).astype(np.float32)
+    G0 = rng.uniform(0, 1, (K, d)).astype(np.float32)
+    keys = keys_with_at_most_three(K, 2000, 32)
+    grads = rng.standard_normal((keys.size, d)).astype(np.float32)
+    Wt, Gt = interleaved_tables(dev(W0), dev(G0))
+    s = Store(Wt, Gt, LR, EPS)
+    s.push_async(dev(keys), dev(grads))
+    assert s.error() == 0
+    Wg, Gg = np.ascontiguousarray(Wt.cpu().numpy()), np.ascontiguousarray(Gt.cpu().numpy())
+    check_some_order(Wg, W0, G0, keys, grads)
+    check_accumulators(Gg, G0, keys, grads)
+
+
 def test_push_async_distinct_keys_equal_the_merged_push():
     K, d, n = 20_000, 100, 15_000
     rng = np.random.default_rng(22)
