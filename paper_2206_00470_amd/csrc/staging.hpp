@@ -136,7 +136,7 @@ class Planner {
     in_slots.clear();
   }
 
-  static constexpr size_t PREFETCH = 16;   // keys ahead whose state is fetched early
+  static constexpr size_t PREFETCH = 48;   // keys ahead whose state is fetched early (host DRAM latency)
 
   // Keys whose every acted-upon intent has expired leave the slot table.
   void evict_expired() {
