@@ -10,10 +10,14 @@
 // into slot ids so that the step kernels run unchanged on the slot table.
 #pragma once
 
+#include <sys/mman.h>
+
 #include <algorithm>
 #include <cmath>
 #include <cstdint>
+#include <cstdlib>
 #include <map>
+#include <new>
 #include <utility>
 #include <vector>
 
@@ -60,6 +64,31 @@ struct ActionTiming {
 };
 
 // ------------------------------------------------------------------ planner (host only)
+// Allocator for the planner's per-key table (16 bytes per key, hundreds of
+// MB, read at random keys): 2 MB-aligned and advised for transparent huge
+// pages, so that a lookup does not also miss the TLB.  The advice is a hint
+// the kernel may ignore.
+template <class T>
+struct HugePageAlloc {
+  using value_type = T;
+  HugePageAlloc() = default;
+  template <class U>
+  HugePageAlloc(const HugePageAlloc<U>&) {}
+  T* allocate(size_t n) {
+    constexpr size_t align = size_t(2) << 20;
+    const size_t bytes = (n * sizeof(T) + align - 1) / align * align;
+    void* p = nullptr;
+    if (posix_memalign(&p, align, bytes) != 0) throw std::bad_alloc();
+    (void)madvise(p, bytes, MADV_HUGEPAGE);
+    return static_cast<T*>(p);
+  }
+  void deallocate(T* p, size_t) { std::free(p); }
+  template <class U>
+  bool operator==(const HugePageAlloc<U>&) const { return true; }
+  template <class U>
+  bool operator!=(const HugePageAlloc<U>&) const { return false; }
+};
+
 class Planner {
  public:
   struct Intent {
@@ -78,7 +107,7 @@ class Planner {
     int32_t slot;
     int32_t pad;
   };
-  std::vector<KeyState> ks;
+  std::vector<KeyState, HugePageAlloc<KeyState>> ks;
   std::vector<std::vector<int32_t>> free_slots;   // per range, a stack
   std::map<std::pair<int64_t, int64_t>, Intent> pending;   // (C_start, signal order) -> intent
   std::map<int64_t, std::vector<int64_t>> expiring;        // C_end -> keys whose `until` was set to it
@@ -90,6 +119,20 @@ class Planner {
   std::vector<int64_t> out_keys, out_slots, in_keys, in_slots;
   // totals
   int64_t staged_total = 0, evicted_total = 0, forced_total = 0, stalled_total = 0;
+  // emptied key lists of finished intents and expiry buckets, kept with their
+  // capacity: a round reuses them instead of faulting in new pages
+  std::vector<std::vector<int64_t>> spare;
+
+  std::vector<int64_t> take_list() {
+    if (spare.empty()) return {};
+    std::vector<int64_t> v = std::move(spare.back());
+    spare.pop_back();
+    v.clear();
+    return v;
+  }
+  void give_list(std::vector<int64_t>&& v) {
+    if (spare.size() < 16) spare.push_back(std::move(v));
+  }
 
   void init(int64_t keys, const int64_t* begin, const int64_t* capacity, int nranges) {
     num_keys = keys;
@@ -123,6 +166,7 @@ class Planner {
     if (c_end <= clock || c_end <= c_start) return;
     Intent it;
     it.end = c_end;
+    it.keys = take_list();
     it.keys.assign(keys, keys + n);
     pending.emplace(std::make_pair(c_start, seq++), std::move(it));
   }
@@ -153,6 +197,7 @@ class Planner {
         st.slot = -1;
         ++evicted_total;
       }
+      give_list(std::move(expiring.begin()->second));
       expiring.erase(expiring.begin());
     }
   }
@@ -164,10 +209,13 @@ class Planner {
       const int64_t c_start = pending.begin()->first.first;
       Intent& it = pending.begin()->second;
       if (it.end <= clock) {   // expired before it could be acted upon
+        give_list(std::move(it.keys));
         pending.erase(pending.begin());
         continue;
       }
-      std::vector<int64_t>& bucket = expiring[it.end];
+      auto [bpos, fresh] = expiring.try_emplace(it.end);
+      if (fresh) bpos->second = take_list();
+      std::vector<int64_t>& bucket = bpos->second;
       const size_t nk = it.keys.size();
       for (; it.next < nk; ++it.next) {
         if (it.next + PREFETCH < nk) {
@@ -201,6 +249,7 @@ class Planner {
       auto a = acted.find(c_start);
       if (a == acted.end()) acted.emplace(c_start, round_id);
       else a->second = std::max(a->second, round_id);
+      give_list(std::move(it.keys));
       pending.erase(pending.begin());
     }
   }
