@@ -198,7 +198,7 @@ ps_status ps_step_mf_apply(ps_store* s, int64_t B, float lambda, double* loss, v
  * no fixed order, so results are not reproducible bit for bit; element by
  * element they equal those of applying the occurrences one after another
  * in some order.  Needs no sort and no workspace.  keys: device int64[n];
- * grads: device float[n*dim] (16-byte aligned when dim % 4 == 0).  A key
+ * grads: device float[n*dim], row-major.  A key
  * outside [0, num_keys) is skipped and reported by ps_get_error.  Staged
  * stores and bf16 values: PS_ERR_UNSUPPORTED. */
 ps_status ps_push_async(ps_store* s, const int64_t* keys, int64_t n, const float* grads, void* stream);

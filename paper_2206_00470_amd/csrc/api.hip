@@ -1383,7 +1383,6 @@ ps_status ps_push_async(ps_store* s, const int64_t* keys, int64_t n, const float
   if (ps_status st = check_n(n, 1)) return st;
   if (n == 0) return PS_OK;
   if (!keys || !grads) return fail(PS_ERR_INVALID, "keys or grads is NULL");
-  if (s->dim % 4 == 0 && !aligned16(grads)) return fail(PS_ERR_INVALID, "grads must be 16-byte aligned");
   return launch_push_async(s, KeysList{keys}, grads, n, as_stream(stream));
 }
 

@@ -137,6 +137,25 @@ def test_push_async_interleaved_rows():
     check_accumulators(Gg, G0, keys, grads)
 
 
+def test_push_async_unaligned_gradient_rows():
+    """Gradient rows starting 4 bytes past a 16-byte boundary are accepted
+    (the unmerged push loads one float per lane)."""
+    K, d, n = 1000, 100, 700
+    rng = np.random.default_rng(33)
+    W0 = (rng.standard_normal((K, d)) * 0.1).astype(np.float32)
+    keys = rng.permutation(K)[:n].astype(np.int64)
+    grads = rng.standard_normal((n, d)).astype(np.float32)
+    buf = torch.zeros(n * d + 1, dtype=torch.float32, device="cuda")
+    buf[1:].copy_(dev(grads).reshape(-1))
+    Wt, Gt = dev(W0), torch.zeros((K, d), dtype=torch.float32, device="cuda")
+    s = Store(Wt, Gt, LR, EPS)
+    s.push_async(dev(keys), buf[1:])
+    assert s.error() == 0
+    Wr, Gr = W0.copy(), np.zeros((K, d), np.float32)
+    oracle.push(Wr, Gr, keys, grads, LR, EPS)
+    assert_close_tables(Wt.cpu().numpy(), Wr, "W")
+
+
 def test_push_async_distinct_keys_equal_the_merged_push():
     K, d, n = 20_000, 100, 15_000
     rng = np.random.default_rng(22)
