@@ -363,6 +363,9 @@ def run_staged(args, wb, dev):
                "rounds_in_timed_steps": st1["rounds"] - st0["rounds"],
                "stalls_in_timed_steps": st1["stalled"] - st0["stalled"],
                "rate_estimate": round(st1["lambda"], 4),
+               "host_planning_ms_per_round": round((st1["plan_us"] - st0["plan_us"]) / 1e3
+                                                   / max(1, (st1["rounds"] - st0["rounds"]) + (st1["forced"] - st0["forced"])), 4),
+               "host_planning_ms_per_step": round((st1["plan_us"] - st0["plan_us"]) / 1e3 / args.steps, 4),
                "link_GBps_over_step_time": round(link_bytes / elapsed / 1e9, 2),
                "move_kernel_ms_per_step": round(mv_ms / args.steps, 4)}
     roofline = {"bound": "host-link", "kernel": "k_move_rows", "achieved": round(achieved, 2) if achieved else None,

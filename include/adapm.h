@@ -371,7 +371,8 @@ ps_status ps_step_ctr_wd(ps_store* s, const int64_t* keys, const float* label, i
 #define PS_STAGE_RESIDENT   5   /* keys resident now */
 #define PS_STAGE_PENDING    6   /* keys of intents not yet acted upon */
 #define PS_STAGE_STALLED    7   /* times acting stopped at a full range */
-#define PS_STAGE_NUM_STATS  8
+#define PS_STAGE_PLAN_US    8   /* host time of all rounds' planning and enqueueing, microseconds */
+#define PS_STAGE_NUM_STATS  9
 
 ps_status ps_create_staged(ps_store** out, int64_t num_keys, int32_t dim, float* home_values,
                            float* home_accum, int64_t home_stride, float* values, float* accum,

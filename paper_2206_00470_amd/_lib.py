@@ -29,7 +29,7 @@ PS_KERNEL_MLP = 6
 PS_KERNEL_ASYNC = 7
 PS_TIMING_ALL = -1
 
-STAGE_STATS = ["clock", "rounds", "forced", "staged", "evicted", "resident", "pending", "stalled"]
+STAGE_STATS = ["clock", "rounds", "forced", "staged", "evicted", "resident", "pending", "stalled", "plan_us"]
 
 _p, _i64, _i32, _f32, _sz = C.c_void_p, C.c_int64, C.c_int32, C.c_float, C.c_size_t
 

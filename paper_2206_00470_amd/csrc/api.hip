@@ -81,6 +81,7 @@ struct Staging {
   std::thread auto_thread;
   std::atomic<bool> auto_on{false};
   std::atomic<int32_t> auto_status{0};
+  int64_t plan_us = 0;               // host time spent in rounds (planning and enqueueing the moves)
 };
 
 struct ps_store {
@@ -858,6 +859,7 @@ ps_status enqueue_moves(ps_store* s, const std::vector<int64_t>& out_k, const st
 ps_status stage_round_locked(ps_store* s, bool forced, int64_t* rid_out, int64_t* moved) {
   Staging& g = *s->stg;
   Planner& P = g.plan;
+  const auto t0 = std::chrono::steady_clock::now();
   P.clear_moves();
   const int64_t rid = g.round_id;
   const int64_t horizon = forced ? P.clock + 1 : P.timing.horizon(P.clock);
@@ -868,6 +870,7 @@ ps_status stage_round_locked(ps_store* s, bool forced, int64_t* rid_out, int64_t
   HIP_TRY(hipStreamWaitEvent(g.st, g.clock_ev, 0));
   if (ps_status r = enqueue_moves(s, P.out_keys, P.out_slots, P.in_keys, P.in_slots)) return r;
   HIP_TRY(hipEventRecord(g.round_ev[rid % Staging::RING], g.st));
+  g.plan_us += std::chrono::duration_cast<std::chrono::microseconds>(std::chrono::steady_clock::now() - t0).count();
   g.round_id = rid + 1;
   if (rid_out) *rid_out = rid;
   if (moved) *moved = (int64_t)(P.out_keys.size() + P.in_keys.size());
@@ -1806,7 +1809,7 @@ ps_status ps_stage_stats(ps_store* s, int64_t* counts, int32_t n, double* lambda
   int64_t pending = 0;
   for (const auto& kv : P.pending) pending += (int64_t)(kv.second.keys.size() - kv.second.next);
   const int64_t v[PS_STAGE_NUM_STATS] = {P.clock, g.rounds, P.forced_total, P.staged_total, P.evicted_total,
-                                         resident, pending, P.stalled_total};
+                                         resident, pending, P.stalled_total, g.plan_us};
   for (int i = 0; i < n && i < PS_STAGE_NUM_STATS; ++i) counts[i] = v[i];
   if (lambda) *lambda = P.timing.lambda;
   return PS_OK;
