@@ -816,24 +816,17 @@ ps_status move_rows(ps_store* s, bool to_home, const int64_t* from, const int64_
   });
 }
 
-// Copies the planner's moves to the device and enqueues them on the staging
-// stream: write-backs (slot -> home, map entry cleared) before stage-ins
-// (home -> slot, map entry set), so a slot freed in this round can be
-// reused by it.
-ps_status enqueue_moves(ps_store* s, const std::vector<int64_t>& out_k, const std::vector<int64_t>& out_s,
-                        const std::vector<int64_t>& in_k, const std::vector<int64_t>& in_s) {
+// Uploads a round's moves (written by the planner into pinned list b: keys
+// at h_list[b], slots 2 * total_slots further) and enqueues them on the
+// staging stream: write-backs (slot -> home, map entry cleared) before
+// stage-ins (home -> slot, map entry set), so a slot freed in this round
+// can be reused by it.
+ps_status enqueue_moves(ps_store* s, int b, int64_t nout, int64_t nin) {
   Staging& g = *s->stg;
-  const int64_t nout = (int64_t)out_k.size(), nin = (int64_t)in_k.size();
   if (nout + nin == 0) return PS_OK;
-  const int b = g.list_i;
-  g.list_i ^= 1;
-  HIP_TRY(hipEventSynchronize(g.list_ev[b]));   // its previous copy has been read
+  g.list_i = b ^ 1;
   int64_t* hk = g.h_list[b];
   int64_t* hs = hk + 2 * g.total_slots;
-  std::copy(out_k.begin(), out_k.end(), hk);
-  std::copy(in_k.begin(), in_k.end(), hk + nout);
-  std::copy(out_s.begin(), out_s.end(), hs);
-  std::copy(in_s.begin(), in_s.end(), hs + nout);
   HIP_TRY(hipMemcpyAsync(g.d_keys, hk, size_t(nout + nin) * 8, hipMemcpyHostToDevice, g.st));
   HIP_TRY(hipMemcpyAsync(g.d_slots, hs, size_t(nout + nin) * 8, hipMemcpyHostToDevice, g.st));
   HIP_TRY(hipEventRecord(g.list_ev[b], g.st));
@@ -860,7 +853,9 @@ ps_status stage_round_locked(ps_store* s, bool forced, int64_t* rid_out, int64_t
   Staging& g = *s->stg;
   Planner& P = g.plan;
   const auto t0 = std::chrono::steady_clock::now();
-  P.clear_moves();
+  const int b = g.list_i;   // the pinned list this round's moves are written into
+  HIP_TRY(hipEventSynchronize(g.list_ev[b]));   // its previous upload has been read
+  P.clear_moves(g.h_list[b], g.h_list[b] + 2 * g.total_slots);
   const int64_t rid = g.round_id;
   const int64_t horizon = forced ? P.clock + 1 : P.timing.horizon(P.clock);
   P.evict_expired();
@@ -868,12 +863,12 @@ ps_status stage_round_locked(ps_store* s, bool forced, int64_t* rid_out, int64_t
   if (forced) ++P.forced_total;
   else ++g.rounds;
   HIP_TRY(hipStreamWaitEvent(g.st, g.clock_ev, 0));
-  if (ps_status r = enqueue_moves(s, P.out_keys, P.out_slots, P.in_keys, P.in_slots)) return r;
+  if (ps_status r = enqueue_moves(s, b, P.nout, P.nin)) return r;
   HIP_TRY(hipEventRecord(g.round_ev[rid % Staging::RING], g.st));
   g.plan_us += std::chrono::duration_cast<std::chrono::microseconds>(std::chrono::steady_clock::now() - t0).count();
   g.round_id = rid + 1;
   if (rid_out) *rid_out = rid;
-  if (moved) *moved = (int64_t)(P.out_keys.size() + P.in_keys.size());
+  if (moved) *moved = P.nout + P.nin;
   return PS_OK;
 }
 

@@ -115,8 +115,14 @@ class Planner {
   ActionTiming timing;
   int64_t clock = 0;
   int64_t seq = 0;
-  // the last round's moves
-  std::vector<int64_t> out_keys, out_slots, in_keys, in_slots;
+  // The current round's moves, written straight into the caller's buffers
+  // (the pinned upload lists): nout write-backs at [0, nout), then nin
+  // stage-ins at [nout, nout + nin).  A round evicts before it acts, so the
+  // write-backs are complete when the first stage-in is written; the buffers
+  // hold 2 x the slot count (at most every slot written back and refilled).
+  int64_t* mkeys = nullptr;
+  int64_t* mslots = nullptr;
+  int64_t nout = 0, nin = 0;
   // totals
   int64_t staged_total = 0, evicted_total = 0, forced_total = 0, stalled_total = 0;
   // emptied key lists of finished intents and expiry buckets, kept with their
@@ -173,11 +179,10 @@ class Planner {
 
   bool due(int64_t c) const { return !pending.empty() && pending.begin()->first.first <= c; }
 
-  void clear_moves() {
-    out_keys.clear();
-    out_slots.clear();
-    in_keys.clear();
-    in_slots.clear();
+  void clear_moves(int64_t* keys, int64_t* slots) {
+    mkeys = keys;
+    mslots = slots;
+    nout = nin = 0;
   }
 
   static constexpr size_t PREFETCH = 48;   // keys ahead whose state is fetched early (host DRAM latency)
@@ -191,8 +196,9 @@ class Planner {
         const int64_t k = b[i];
         KeyState& st = ks[k];
         if (st.slot < 0 || st.until > clock) continue;   // already gone, or extended
-        out_keys.push_back(k);
-        out_slots.push_back(st.slot);
+        mkeys[nout] = k;
+        mslots[nout] = st.slot;
+        ++nout;
         free_slots[range_of(k)].push_back(st.slot);
         st.slot = -1;
         ++evicted_total;
@@ -242,8 +248,9 @@ class Planner {
         st.slot = sl;
         st.until = it.end;
         bucket.push_back(k);
-        in_keys.push_back(k);
-        in_slots.push_back(sl);
+        mkeys[nout + nin] = k;
+        mslots[nout + nin] = sl;
+        ++nin;
         ++staged_total;
       }
       auto a = acted.find(c_start);
