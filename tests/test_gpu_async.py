@@ -63,13 +63,13 @@ def counts_per_key(K, keys, shape):
     return n[:, None] if len(shape) == 2 else n
 
 
-def check_bounds(Wg, W0, G0, keys, grads, rowwise=False):
+def check_bounds(Wg, W0, G0, keys, grads, rowwise=False, lr=LR, eps=EPS):
     """Wg within the any-order interval; the slack for fp32 rounding grows
     with the number n_k of the key's occurrences: each of its n_k updates
     rounds once in W and its step a few times (|W| along the way is at most
     |W0| plus the sum of the steps' largest magnitudes)."""
-    lo, hi = oracle.async_bounds(W0, G0, keys, grads, LR, EPS, rowwise=rowwise)
-    lo_abs, _ = oracle.async_bounds(W0, G0, keys, np.abs(grads), LR, EPS, rowwise=rowwise)
+    lo, hi = oracle.async_bounds(W0, G0, keys, grads, lr, eps, rowwise=rowwise)
+    lo_abs, _ = oracle.async_bounds(W0, G0, keys, np.abs(grads), lr, eps, rowwise=rowwise)
     reach = np.abs(W0) + (W0 - lo_abs)
     n = counts_per_key(W0.shape[0], keys, W0.shape)
     tol = ATOL + RTOL * np.abs(Wg) + 4.0 * n * U32 * reach
@@ -256,7 +256,7 @@ def run_mf_async(cfg, steps):
         assert bad == 0
         assert float(loss.item()) == pytest.approx(rloss, rel=1e-9)
         Wg, Gg = Wt.cpu().numpy(), Gt.cpu().numpy()
-        check_bounds(Wg, W0, G0, keys, grads)
+        check_bounds(Wg, W0, G0, keys, grads, lr=cfg.opt.lr, eps=cfg.opt.eps)
         check_accumulators(Gg, G0, keys, grads)
     return s
 
@@ -292,7 +292,7 @@ def test_mf_async_paper_scale_sampled():
     Wg, Gg = Wt[idx].cpu().numpy(), Gt[idx].cpu().numpy()
     W0s, G0s = W[sample], np.zeros((sample.size, cfg.dim), np.float32)
     say(f"checking {sample.size} keys with {int(sel.sum())} occurrences")
-    check_bounds(Wg, W0s, G0s, local, grads[sel])
+    check_bounds(Wg, W0s, G0s, local, grads[sel], lr=cfg.opt.lr, eps=cfg.opt.eps)
     check_accumulators(Gg, G0s, local, grads[sel])
 
 
@@ -312,7 +312,8 @@ def test_mf_async_rowwise_store():
         assert s.error() == 0
         keys, grads, rloss, _ = oracle.grad_mf(W0, bt.row, bt.col, bt.val, cfg.n_rows, cfg.lam)
         assert float(loss.item()) == pytest.approx(rloss, rel=1e-9)
-        check_bounds(np.ascontiguousarray(Wt.cpu().numpy()), W0, A0, keys, grads, rowwise=True)
+        check_bounds(np.ascontiguousarray(Wt.cpu().numpy()), W0, A0, keys, grads, rowwise=True, lr=cfg.opt.lr,
+                     eps=cfg.opt.eps)
         check_accumulators(np.ascontiguousarray(At.cpu().numpy()), A0, keys, grads, rowwise=True)
 
 

@@ -164,3 +164,38 @@ def test_mf_variant_graph_replays_match_eager(kind):
         return (w, st[0].G.cpu().numpy())
 
     graph_vs_eager(make, call, lambda i: {k: dev(v) for k, v in wl.batch(i).__dict__.items()}, snap, f"mf {kind}")
+
+
+def test_mf_async_graph_replays_within_bounds():
+    """The unmerged MF step captured once and replayed on new batches: each
+    replay's result equals some order's result, so it is checked against the
+    any-order bounds and the sum of squares from the state before it."""
+    from tests.test_gpu_async import check_accumulators, check_bounds
+    import oracle
+    cfg = small_variant(MF_10Mx1M)
+    wl = MFWorkload(cfg)
+    W0 = wl.init_table()
+    s = Store(dev(W0), torch.zeros(W0.shape, dtype=torch.float32, device="cuda"), cfg.opt.lr, cfg.opt.eps)
+    loss = torch.zeros(1, dtype=torch.float64, device="cuda")
+    b0 = {k: dev(v) for k, v in wl.batch(0).__dict__.items()}
+    s.step_mf_async(b0["row"], b0["col"], b0["val"], cfg.n_rows, cfg.lam, loss=loss)
+    static = {k: dev(v) for k, v in wl.batch(1).__dict__.items()}
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        s.step_mf_async(static["row"], static["col"], static["val"], cfg.n_rows, cfg.lam, loss=loss)
+    torch.cuda.synchronize()
+    for step in range(1, 5):
+        say(f"unmerged mf: replay for step {step}")
+        bt = wl.batch(step)
+        for k, v in bt.__dict__.items():
+            static[k].copy_(dev(v))
+        Wb, Gb = s.W.cpu().numpy(), s.G.cpu().numpy()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert s.error() == 0
+        keys, grads, rloss, _ = oracle.grad_mf(Wb, bt.row, bt.col, bt.val, cfg.n_rows, cfg.lam)
+        assert float(loss.item()) == pytest.approx(rloss, rel=1e-9)
+        check_bounds(s.W.cpu().numpy(), Wb, Gb, keys, grads, lr=cfg.opt.lr, eps=cfg.opt.eps)
+        check_accumulators(s.G.cpu().numpy(), Gb, keys, grads)
