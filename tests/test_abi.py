@@ -158,3 +158,19 @@ def test_workspace_sizes(op, per):
 
 def test_pull_needs_no_workspace():
     assert _lib.lib().ps_workspace_bytes(1000, 100, _lib.PS_OP_PULL, 10, 1) == 0
+
+
+def test_binding_constants_match_the_header():
+    """The binding's operation codes, kernel ids and staging statistics
+    follow the header's numbering."""
+    import re
+    text = open(HEADER).read()
+    defs = {m.group(1): int(m.group(2)) for m in re.finditer(r"#define (PS_[A-Z0-9_]+)\s+\(?(-?\d+)\)?", text)}
+    for name in ("PS_OP_PUSH", "PS_OP_STEP_MF", "PS_OP_STEP_CTR", "PS_OP_STEP_MF_ASYNC", "PS_KERNEL_SEGREDUCE",
+                 "PS_KERNEL_MF_ROWMERGE", "PS_KERNEL_STAGE", "PS_KERNEL_MLP", "PS_KERNEL_ASYNC",
+                 "PS_ERR_KEY_RANGE", "PS_ERR_UNSUPPORTED", "PS_ERR_NOT_RESIDENT"):
+        assert getattr(_lib, name) == defs[name], name
+    stats = [n for n in defs if n.startswith("PS_STAGE_") and n != "PS_STAGE_NUM_STATS"]
+    assert len(_lib.STAGE_STATS) == defs["PS_STAGE_NUM_STATS"] == len(stats)
+    for n in stats:
+        assert _lib.STAGE_STATS[defs[n]] == n[len("PS_STAGE_"):].lower(), n

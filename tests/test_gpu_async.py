@@ -98,7 +98,7 @@ def keys_with_at_most_three(K, n_distinct, seed):
     return rng.permutation(keys).astype(np.int64)
 
 
-@pytest.mark.parametrize("K,d", [(5000, 100), (3000, 16), (2000, 3), (800, 300)])
+@pytest.mark.parametrize("K,d", [(5000, 100), (3000, 16), (2000, 3), (800, 300), (600, 512)])
 def test_push_async_some_order(K, d):
     say(f"unmerged push K={K} d={d}")
     rng = np.random.default_rng(20)
