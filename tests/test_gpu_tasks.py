@@ -97,7 +97,7 @@ def test_kge_all_head_or_all_tail_negatives():
     run_steps("kge", replace(base, n_neg=0, n_head_neg=0), range(1))
 
 
-@pytest.mark.parametrize("dim", [3, 16, 64, 300])
+@pytest.mark.parametrize("dim", [3, 16, 64, 258, 300, 384, 386])
 def test_sgns_other_dims(dim):
     from dataclasses import replace
     run_steps("sgns", replace(small_variant(SGNS_1M), dim=dim, batch=130), range(2))
