@@ -226,21 +226,35 @@ __global__ __launch_bounds__(BLOCK) void k_ctr_grad(const float* __restrict__ W,
 #pragma unroll
     for (int e = 0; e < NE; ++e) S[e] = 0.0;
     double sq = 0.0;
-    for (int f = 0; f < F; ++f) {
-      const float* row = W + keys[b * F + f] * ld;
-      float x[NE];
+    // the sample's keys are loaded L at a time, one per lane, and FU rows are
+    // in flight at once; the sums still take the fields in order
+    constexpr int FU = 4;
+    for (int f0 = 0; f0 < F; f0 += L) {
+      const int nf = F - f0 < L ? F - f0 : L;
+      const int64_t my_key = gl < nf ? keys[b * F + f0 + gl] : 0;
+      for (int f = 0; f < nf; f += FU) {
+        float x[FU][NE];
 #pragma unroll
-      for (int v = 0; v < NV; ++v) {
-        const int c = (gl + v * L) * VW;
-        if (c < dim) load_frag<VW>(row + c, x + v * VW);
-        else
+        for (int u = 0; u < FU; ++u) {
+          const int64_t key = __shfl(my_key, (f + u) % L, L);
+          const float* row = W + key * ld;
 #pragma unroll
-          for (int e = 0; e < VW; ++e) x[v * VW + e] = 0.0f;
-      }
+          for (int v = 0; v < NV; ++v) {
+            const int c = (gl + v * L) * VW;
+            if (f + u < nf && c < dim) load_frag<VW>(row + c, x[u] + v * VW);
+            else
 #pragma unroll
-      for (int e = 0; e < NE; ++e) {
-        S[e] += (double)x[e];
-        sq = __builtin_fma((double)x[e], (double)x[e], sq);   // exact product: same rounding as mul + add
+              for (int e = 0; e < VW; ++e) x[u][v * VW + e] = 0.0f;
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < FU; ++u)
+          if (f + u < nf)
+#pragma unroll
+            for (int e = 0; e < NE; ++e) {
+              S[e] += (double)x[u][e];
+              sq = __builtin_fma((double)x[u][e], (double)x[u][e], sq);   // exact product: same rounding as mul + add
+            }
       }
     }
     double ss = 0.0;
@@ -252,18 +266,34 @@ __global__ __launch_bounds__(BLOCK) void k_ctr_grad(const float* __restrict__ W,
     const double y = (double)label[b];
     const double a = sigmoid_d(z) - y;
     if (gl == 0) lsum += softplus_d(z) - y * z;
-    for (int f = 0; f < F; ++f) {
-      const float* row = W + keys[b * F + f] * ld;
-      float* dst = grads + (int64_t)rank[b * F + f] * dim;
+    for (int f0 = 0; f0 < F; f0 += L) {
+      const int nf = F - f0 < L ? F - f0 : L;
+      const int64_t my_key = gl < nf ? keys[b * F + f0 + gl] : 0;
+      const uint32_t my_rank = gl < nf ? rank[b * F + f0 + gl] : 0u;
+      for (int f = 0; f < nf; f += FU) {
+        float x[FU][NE];
 #pragma unroll
-      for (int v = 0; v < NV; ++v) {
-        const int c = (gl + v * L) * VW;
-        if (c < dim) {
-          float x[VW], g[VW];
-          load_frag<VW>(row + c, x);
+        for (int u = 0; u < FU; ++u) {
+          const float* row = W + __shfl(my_key, (f + u) % L, L) * ld;
 #pragma unroll
-          for (int e = 0; e < VW; ++e) g[e] = (float)(a * (S[v * VW + e] - (double)x[e]));
-          store_frag<VW>(dst + c, g);
+          for (int v = 0; v < NV; ++v) {
+            const int c = (gl + v * L) * VW;
+            if (f + u < nf && c < dim) load_frag<VW>(row + c, x[u] + v * VW);
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < FU; ++u) {
+          float* dst = grads + (int64_t)__shfl(my_rank, (f + u) % L, L) * dim;
+#pragma unroll
+          for (int v = 0; v < NV; ++v) {
+            const int c = (gl + v * L) * VW;
+            if (f + u < nf && c < dim) {
+              float g[VW];
+#pragma unroll
+              for (int e = 0; e < VW; ++e) g[e] = (float)(a * (S[v * VW + e] - (double)x[u][v * VW + e]));
+              store_frag<VW>(dst + c, g);
+            }
+          }
         }
       }
     }
