@@ -422,20 +422,14 @@ __global__ __launch_bounds__(BLOCK) void k_kge_grad(const float* __restrict__ W,
     const int32_t* nt = neg + t * n_neg;
     int32_t id_cur = lane < n_neg ? nt[lane] : 0;
     int32_t id_nxt = WAVE + lane < n_neg ? nt[WAVE + lane] : 0;
-    for (int j0 = 0; j0 < n_neg; j0 += JB) {
-      // convert s, r, o per batch instead of holding fp64 copies across the loop
-#pragma unroll
-      for (int i = 0; i < KPL; ++i)
-        asm volatile("" : "+v"(sRf[i]), "+v"(sIf[i]), "+v"(rRf[i]), "+v"(rIf[i]), "+v"(oRf[i]), "+v"(oIf[i]));
-      if (j0 > 0 && j0 % WAVE == 0) {
-        id_cur = id_nxt;
-        id_nxt = j0 + WAVE + lane < n_neg ? nt[j0 + WAVE + lane] : 0;
-      }
-      float xR[JB][KPL], xI[JB][KPL];
+    // the rows of the batch of negatives starting at jb (a multiple of JB,
+    // inside the id tile held in id_cur)
+    float xR[JB][KPL], xI[JB][KPL];
+    auto load_batch = [&](int jb) {
 #pragma unroll
       for (int jj = 0; jj < JB; ++jj) {
-        const int j = j0 + jj;
-        const int32_t id = __shfl(id_cur, j0 % WAVE + jj, WAVE);
+        const int j = jb + jj;
+        const int32_t id = __shfl(id_cur, jb % WAVE + jj, WAVE);
         const float* xp = W + (int64_t)(j < n_neg ? id : 0) * ld;
 #pragma unroll
         for (int i = 0; i < KPL; ++i) {
@@ -445,6 +439,13 @@ __global__ __launch_bounds__(BLOCK) void k_kge_grad(const float* __restrict__ W,
           xI[jj][i] = in ? xp[cdim + k] : 0.0f;
         }
       }
+    };
+    if (n_neg > 0) load_batch(0);
+    for (int j0 = 0; j0 < n_neg; j0 += JB) {
+      // convert s, r, o per batch instead of holding fp64 copies across the loop
+#pragma unroll
+      for (int i = 0; i < KPL; ++i)
+        asm volatile("" : "+v"(sRf[i]), "+v"(sIf[i]), "+v"(rRf[i]), "+v"(rIf[i]), "+v"(oRf[i]), "+v"(oIf[i]));
       double ph[JB];
 #pragma unroll
       for (int jj = 0; jj < JB; ++jj) {
@@ -464,6 +465,14 @@ __global__ __launch_bounds__(BLOCK) void k_kge_grad(const float* __restrict__ W,
           xstash[(jj * KPL + i) * 2 + 1][threadIdx.x] = xI[jj][i];
         }
       asm volatile("" ::: "memory");   // read them back from LDS, not from registers
+      // the next batch's rows load while this batch's coefficients are formed
+      if (j0 + JB < n_neg) {
+        if ((j0 + JB) % WAVE == 0) {
+          id_cur = id_nxt;
+          id_nxt = j0 + JB + WAVE + lane < n_neg ? nt[j0 + JB + WAVE + lane] : 0;
+        }
+        load_batch(j0 + JB);
+      }
       // lane finishes the score of negative j0 + lane / (WAVE / JB) and its coefficient
       const double phi_my = group_multi_sum<WAVE, JB>(ph, lane);
       const int j_my = j0 + lane / (WAVE / JB);
