@@ -693,17 +693,14 @@ __global__ __launch_bounds__(BLOCK) void k_sgns_grad(const float* __restrict__ W
     int r_cur, r_nxt;
     int64_t id_cur = row_id(gl, r_cur);
     int64_t id_nxt = row_id(L + gl, r_nxt);
-    for (int r0 = 0; r0 < rows; r0 += JB) {
-      if (r0 > 0 && r0 % L == 0) {
-        id_cur = id_nxt;
-        r_cur = r_nxt;
-        id_nxt = row_id(r0 + L + gl, r_nxt);
-      }
-      float u[JB][NE];
-      bool live[JB];
+    // the rows of live rows rb .. rb + JB - 1 (rb a multiple of JB, inside
+    // the id tile held in id_cur)
+    float u[JB][NE];
+    bool live[JB];
+    auto load_batch = [&](int rb) {
 #pragma unroll
       for (int jj = 0; jj < JB; ++jj) {
-        const int64_t id = __shfl(id_cur, r0 % L + jj, L);
+        const int64_t id = __shfl(id_cur, rb % L + jj, L);
         live[jj] = id != -1;
         const float* up = W + (out_off + (live[jj] ? id : 0)) * ld;
 #pragma unroll
@@ -715,6 +712,9 @@ __global__ __launch_bounds__(BLOCK) void k_sgns_grad(const float* __restrict__ W
             for (int e = 0; e < VW; ++e) u[jj][q2 * VW + e] = 0.0f;
         }
       }
+    };
+    if (rows > 0) load_batch(0);
+    for (int r0 = 0; r0 < rows; r0 += JB) {
       double x[JB];
 #pragma unroll
       for (int e = 0; e < NE; ++e) asm volatile("" : "+v"(v[e]));   // convert v per batch, not once for the loop
@@ -735,6 +735,18 @@ __global__ __launch_bounds__(BLOCK) void k_sgns_grad(const float* __restrict__ W
       const double x_my = group_multi_sum<L, JB>(x, gl);
       const bool live_my = __shfl(id_cur, r0 % L + gl / (L / JB), L) != -1;   // also false past the end
       const int r_my = __shfl(r_cur, r0 % L + gl / (L / JB), L);
+      bool used[JB];
+#pragma unroll
+      for (int jj = 0; jj < JB; ++jj) used[jj] = live[jj];
+      // the next batch's rows load while this batch's coefficients are formed
+      if (r0 + JB < rows) {
+        if ((r0 + JB) % L == 0) {
+          id_cur = id_nxt;
+          r_cur = r_nxt;
+          id_nxt = row_id(r0 + JB + L + gl, r_nxt);
+        }
+        load_batch(r0 + JB);
+      }
       double a_my = 0.0;
       if (live_my) {
         const int q_my = r_my / (K + 1);
@@ -752,7 +764,7 @@ __global__ __launch_bounds__(BLOCK) void k_sgns_grad(const float* __restrict__ W
 #pragma unroll
       for (int jj = 0; jj < JB; ++jj) {
         const double aj = __shfl(a_my, jj * (L / JB), L);
-        if (live[jj])
+        if (used[jj])
 #pragma unroll
           for (int e = 0; e < NE; ++e) gv[e * BLOCK] += aj * (double)ustash[jj * NE + e][threadIdx.x];
       }
