@@ -60,17 +60,24 @@ def poisson_quantile(mu: float, p: float) -> int:
     return k
 
 
+def smoothed_rate(estimate: float, advance: int, alpha: float) -> float:
+    """The clocks-per-round estimate of adaptive action timing (Section 4.2):
+    an exponential moving average, with weight alpha, of how far the worker
+    clock moved between consecutive rounds.  A round that saw no clock
+    movement carries no information and leaves the estimate as it was."""
+    return (1.0 - alpha) * estimate + alpha * advance if advance > 0 else estimate
+
+
 def action_timing(lam_prev: float, c_prev: int, c_now: int, alpha: float = 0.1, p: float = 0.9999):
-    """Algorithm 1 for round t: Delta = C_t - C_{t-1}; the rate estimate is
-    smoothed only when Delta > 0; an intent is acted upon in this round iff
-    C_start < C_t + Q_Poiss(2 * max(estimate, Delta), p).
-    Returns (new estimate, horizon C_t + Q)."""
-    delta = c_now - c_prev
-    if delta > 0:
-        lam = (1.0 - alpha) * lam_prev + alpha * delta
-    else:
-        lam = lam_prev
-    return lam, c_now + poisson_quantile(2.0 * max(lam, float(delta)), p)
+    """Section 4.2 (Algorithm 1) for one round at clock c_now after a round at
+    c_prev: returns (new estimate, horizon).  The next round is expected
+    within Poisson-many clocks; the bound takes the p-quantile of a Poisson
+    variable whose mean is twice the larger of the estimate and the last
+    observed advance, so an intent is acted upon now iff its C_start lies
+    below the horizon c_now + that quantile."""
+    est = smoothed_rate(lam_prev, c_now - c_prev, alpha)
+    reach = poisson_quantile(2.0 * max(est, float(c_now - c_prev)), p)
+    return est, c_now + reach
 
 
 class StagingOracle:

@@ -51,15 +51,17 @@ struct ActionTiming {
   double lambda = 10.0;    // clocks per round, estimated
   int64_t round_clock = 0; // worker clock at the previous round
 
-  // One round of Algorithm 1 at worker clock `clock`: update the estimate
-  // (not when the clock did not move) and return the horizon H; the round
-  // acts on every intent with C_start < H.
+  // Adaptive action timing (Section 4.2, Algorithm 1) for a round at worker
+  // clock `clock`.  The estimate is an exponential moving average of the
+  // clock advance between rounds, kept as it is by a round that saw no
+  // advance.  The returned horizon is how far ahead this round acts: every
+  // intent with C_start below it, the reach being a Poisson p-quantile at
+  // twice the larger of the estimate and the last advance.
   int64_t horizon(int64_t clock) {
-    const int64_t delta = clock - round_clock;
-    if (delta > 0) lambda = (1.0 - alpha) * lambda + alpha * (double)delta;
+    const double advance = (double)(clock - round_clock);
     round_clock = clock;
-    const double rate = std::max(lambda, (double)delta);
-    return clock + poisson_quantile(2.0 * rate, p);
+    lambda = advance > 0.0 ? (1.0 - alpha) * lambda + alpha * advance : lambda;
+    return clock + poisson_quantile(2.0 * std::max(lambda, advance), p);
   }
 };
 

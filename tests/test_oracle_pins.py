@@ -518,6 +518,49 @@ def test_sgns_zero_output_table_closed_form():
             for k in range(K):
                 gsum[neg[b, q, k]] += 0.5 * W0[centre[b]]
     np.testing.assert_allclose(G[V:], (gsum.astype(np.float32)) ** 2, rtol=1e-6, atol=1e-12)
+    # first touch (G = 0): sqrt(g*g) = |g| exactly, so each output element
+    # moves by exactly lr against the sign of its summed gradient; the grid
+    # values make every nonzero sum at least 1/32 in magnitude
+    g32 = gsum.astype(np.float32)
+    assert np.all((g32 == 0) | (np.abs(g32) >= 1.0 / 32))
+    expect = (W0[V:] - np.float32(LR) * np.sign(g32)).astype(np.float32)
+    assert np.array_equal(W[V:].view(np.uint32), expect.view(np.uint32))
+
+
+def test_sgns_loss_and_gradients_match_torch_autograd():
+    """The skip-gram negative-sampling loss of word2vec: for each present
+    (centre, context) pair, -log sigmoid(<u_ctx, v>) - sum_k log sigmoid(-<u_neg_k, v>),
+    with v the centre's input vector and u output vectors; torch float64
+    autograd gives its gradient with respect to both tables."""
+    W, centre, ctx, neg, w, V = sgns_setup(22)
+    keys, grads, loss, bad = oracle.grad_sgns(W, centre, ctx, neg, w, V)
+    assert bad == 0
+    T = torch.tensor(W, dtype=torch.float64, requires_grad=True)
+    L = torch.zeros((), dtype=torch.float64)
+    for b in range(centre.size):
+        v = T[centre[b]]
+        for q in range(ctx.shape[1]):
+            if ctx[b, q] < 0:
+                continue
+            L = L - torch.nn.functional.logsigmoid(torch.dot(T[V + ctx[b, q]], v))
+            for k in range(neg.shape[2]):
+                L = L - torch.nn.functional.logsigmoid(-torch.dot(T[V + neg[b, q, k]], v))
+    L.backward()
+    assert loss == pytest.approx(L.item(), rel=1e-12)
+    np.testing.assert_allclose(per_key_sum(W.shape[0], keys, grads), T.grad.numpy(), rtol=1e-6, atol=1e-7)
+    # each context occurrence's gradient row points against the centre vector
+    # (it raises <u_ctx, v>), each negative's along it
+    per = 1 + 2 * w * (1 + neg.shape[2])
+    K = neg.shape[2]
+    for b in range(centre.size):
+        v = W[centre[b]].astype(np.float64)
+        for q in range(ctx.shape[1]):
+            if ctx[b, q] < 0:
+                continue
+            o = b * per + 1 + q * (1 + K)
+            assert np.dot(grads[o].astype(np.float64), v) < 0
+            for k in range(K):
+                assert np.dot(grads[o + 1 + k].astype(np.float64), v) > 0
 
 
 def test_sgns_centre_must_index_the_input_table():
