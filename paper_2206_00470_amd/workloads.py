@@ -150,6 +150,9 @@ class MFConfig:
     # visiting order, the entries of one column after another, columns in a
     # random order (Appendix C, "Matrix factorization")
     visit: str = "random"
+    # rows uniform (None, the configurations above) or Zipf with this
+    # exponent over a seeded permutation (users of very unequal activity)
+    row_zipf_s: float | None = None
 
     @property
     def num_keys(self) -> int:
@@ -337,6 +340,7 @@ class MFWorkload:
     def __init__(self, cfg: MFConfig):
         self.cfg = cfg
         self.zipf = Zipf(cfg.n_cols, cfg.zipf_s, cfg.seed, self.TAG + 1)
+        self.row_zipf = None if cfg.row_zipf_s is None else Zipf(cfg.n_rows, cfg.row_zipf_s, cfg.seed, self.TAG + 4)
         self._data = None
         if cfg.fixed_dataset:
             rng = _rng(cfg.seed, self.TAG, 0)
@@ -357,7 +361,10 @@ class MFWorkload:
             raise ValueError(f"unknown MF visiting order {cfg.visit!r}")
 
     def _draw(self, rng, b):
-        row = rng.integers(0, self.cfg.n_rows, b, dtype=np.int64).astype(np.int32)
+        if self.row_zipf is None:
+            row = rng.integers(0, self.cfg.n_rows, b, dtype=np.int64).astype(np.int32)
+        else:
+            row = self.row_zipf.sample(rng, b).astype(np.int32)
         col = self.zipf.sample(rng, b).astype(np.int32)
         val = rng.standard_normal(b, dtype=np.float32)
         return MFBatch(row, col, val)
@@ -393,6 +400,25 @@ class MFWorkload:
     def init_table(self) -> np.ndarray:
         return normal_table(self.cfg.num_keys, self.cfg.dim, self.cfg.init_std, self.cfg.seed, self.TAG + 2)
 
+    def hot_row_batch(self, counts, n_plain: int, step: int = 0) -> MFBatch:
+        """A batch whose row keys include len(counts) distinct rows repeated
+        counts[i] times each, mixed in random order with n_plain entries of
+        the configuration's own distribution; columns and values as usual."""
+        cfg = self.cfg
+        rng = _rng(cfg.seed, self.TAG + 5, step)
+        hot = rng.choice(cfg.n_rows, len(counts), replace=False)
+        plain = self._draw(rng, n_plain)
+        clash = np.isin(plain.row, hot)
+        while clash.any():   # the hot rows keep exactly their counts
+            plain.row[clash] = rng.integers(0, cfg.n_rows, int(clash.sum()), dtype=np.int64)
+            clash = np.isin(plain.row, hot)
+        n_hot = int(np.sum(counts))
+        row = np.concatenate([np.repeat(hot, counts), plain.row]).astype(np.int32)
+        col = np.concatenate([self.zipf.sample(rng, n_hot).astype(np.int32), plain.col])
+        val = np.concatenate([rng.standard_normal(n_hot, dtype=np.float32), plain.val])
+        order = rng.permutation(row.size)
+        return MFBatch(row[order], col[order], val[order])
+
 
 @dataclass
 class KGEBatch:
@@ -423,6 +449,25 @@ class KGEWorkload:
 
     def init_table(self) -> np.ndarray:
         return normal_table(self.cfg.num_keys, self.cfg.dim, self.cfg.init_std, self.cfg.seed, self.TAG + 2)
+
+    def hot_row_batch(self, counts, n_plain: int, step: int = 0) -> MFBatch:
+        """A batch whose row keys include len(counts) distinct rows repeated
+        counts[i] times each, mixed in random order with n_plain entries of
+        the configuration's own distribution; columns and values as usual."""
+        cfg = self.cfg
+        rng = _rng(cfg.seed, self.TAG + 5, step)
+        hot = rng.choice(cfg.n_rows, len(counts), replace=False)
+        plain = self._draw(rng, n_plain)
+        clash = np.isin(plain.row, hot)
+        while clash.any():   # the hot rows keep exactly their counts
+            plain.row[clash] = rng.integers(0, cfg.n_rows, int(clash.sum()), dtype=np.int64)
+            clash = np.isin(plain.row, hot)
+        n_hot = int(np.sum(counts))
+        row = np.concatenate([np.repeat(hot, counts), plain.row]).astype(np.int32)
+        col = np.concatenate([self.zipf.sample(rng, n_hot).astype(np.int32), plain.col])
+        val = np.concatenate([rng.standard_normal(n_hot, dtype=np.float32), plain.val])
+        order = rng.permutation(row.size)
+        return MFBatch(row[order], col[order], val[order])
 
 
 @dataclass
