@@ -145,6 +145,23 @@ ps_status ps_pull(ps_store* s, const int64_t* keys, int64_t n, float* out, void*
 ps_status ps_push(ps_store* s, const int64_t* keys, int64_t n, const float* grads,
                   void* ws, size_t ws_bytes, void* stream);
 
+/* ps_push for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same merge and update, with the workspace taken from a static device array
+ * of PS_NOALLOC_SCRATCH_BYTES that the library holds, one per device, from
+ * the first store created on that device until the process ends.  The call
+ * allocates nothing and sets no memory with hipMemset.  A push whose
+ * workspace (ps_workspace_bytes(num_keys, dim, PS_OP_PUSH, n, 1)) exceeds
+ * the array returns PS_ERR_UNSUPPORTED before anything is enqueued (the
+ * limit is about 1,500,000 keys at dim 16, 770,000 at dim 100 and 227,000
+ * at dim 512).  Every call on one device
+ * shares that device's array and leaves its contents behind, so calls that
+ * overlap on one device (other streams, other stores, other threads) race
+ * and must be ordered by the caller.  Kernel timing (ps_set_timing) creates
+ * events and should be off. */
+#define PS_NOALLOC_SCRATCH_BYTES (64u << 20)
+ps_status ps_push_noalloc(ps_store* s, const int64_t* keys, int64_t n, const float* grads, void* stream);
+
 /* The merge order used by ps_push, exposed for bit-exact checking: a stable
  * sort of the occurrences by key.  Keys outside [0, num_keys) sort after all
  * valid keys in their original order and belong to no segment.

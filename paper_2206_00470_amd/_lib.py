@@ -23,6 +23,8 @@ PS_OP_PULL, PS_OP_PUSH, PS_OP_DEDUP = 0, 1, 2
 PS_OP_STEP_MF, PS_OP_STEP_KGE, PS_OP_STEP_SGNS, PS_OP_STEP_CTR = 3, 4, 5, 6
 PS_OP_STEP_MF_ASYNC = 7
 
+PS_NOALLOC_SCRATCH_BYTES = 64 << 20
+
 PS_KERNEL_SEGREDUCE, PS_KERNEL_TASKGRAD, PS_KERNEL_SCATTER, PS_KERNEL_PULL, PS_KERNEL_MF_ROWMERGE = 0, 1, 2, 3, 4
 PS_KERNEL_STAGE = 5
 PS_KERNEL_MLP = 6
@@ -43,6 +45,7 @@ SIGNATURES = {
     "ps_workspace_bytes": (_sz, [_i64, _i32, _i32, _i64, _i64]),
     "ps_pull": (_i32, [_p, _p, _i64, _p, _p]),
     "ps_push": (_i32, [_p, _p, _i64, _p, _p, _sz, _p]),
+    "ps_push_noalloc": (_i32, [_p, _p, _i64, _p, _p]),
     "ps_dedup": (_i32, [_i64, _p, _i64, _p, _p, _p, _p, _p, _p, _sz, _p]),
     "ps_step_mf": (_i32, [_p, _p, _p, _p, _i64, _i64, _f32, _p, _p, _sz, _p]),
     "ps_step_mf_prepare": (_i32, [_p, _p, _p, _p, _i64, _i64, _p, _sz, _p]),

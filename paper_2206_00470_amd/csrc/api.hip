@@ -53,6 +53,40 @@ constexpr size_t MAX_TIMED_LAUNCHES = 1 << 14;
 
 }  // namespace
 
+// ======================================================================== static scratch
+// Workspace of the allocation-free push (ps_push_noalloc): one array per
+// device, held from the first store created on that device until the
+// process ends.  In host code the array's name is not a device address;
+// host code reaches it only through the address hipGetSymbolAddress gives
+// for the current device (scratch_address below).
+static_assert(PS_NOALLOC_SCRATCH_BYTES % 256 == 0, "scratch size must keep the workspace alignment");
+static __device__ __align__(256) unsigned char scratch[PS_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[MAX_DEVICES] = {};
+
+// The device address of `scratch` on the current device, looked up once per
+// device and kept.
+ps_status scratch_address(int* device, void** out) {
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= MAX_DEVICES) return fail(PS_ERR_UNSUPPORTED, "device %d beyond the scratch table", dev);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    g_scratch[dev] = p;
+  }
+  *device = dev;
+  *out = g_scratch[dev];
+  return PS_OK;
+}
+
+}  // namespace
+
 // ======================================================================== store
 // Staging state of a store whose slot table caches rows of a home table in
 // pinned host memory.
@@ -96,6 +130,8 @@ struct ps_store {
   float lr;
   float eps;
   int32_t* status;   // device: [0] sticky key-range flag
+  int device = 0;           // the device current at creation
+  void* scratch = nullptr;  // that device's address of the static scratch array
   uint32_t timing = 0;   // bit k: bracket launches of kernel id k
   // a second stream for key work that runs beside a step's task kernel
   hipStream_t aux = nullptr;
@@ -651,6 +687,11 @@ ps_status make_store(ps_store** out, int64_t num_keys, int32_t dim, int64_t row_
   if (e != hipSuccess) {
     delete s;
     return fail(PS_ERR_DEVICE, "hipMalloc(status): %s", hipGetErrorString(e));
+  }
+  if (ps_status r = scratch_address(&s->device, &s->scratch)) {
+    (void)hipFree(s->status);
+    delete s;
+    return r;
   }
   hipStream_t st = as_stream(stream);
   hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(BLOCK), 0, st, reinterpret_cast<uint32_t*>(s->status), int64_t(64));
@@ -1384,6 +1425,18 @@ ps_status ps_push(ps_store* s, const int64_t* keys, int64_t n, const float* grad
   int64_t* tk = reinterpret_cast<int64_t*>(t);
   if (ps_status r = translate_keys(s, keys, n, tk, as_stream(stream))) return r;
   return push_impl(s, tk, n, grads, ws, ws_bytes, stream);
+}
+
+ps_status ps_push_noalloc(ps_store* s, const int64_t* keys, int64_t n, const float* grads, void* stream) {
+  if (ps_status st = check_store(s)) return st;
+  if (ps_status st = check_n(n, 1)) return st;
+  if (n == 0) return PS_OK;
+  const size_t need = ps_workspace_bytes(s->num_keys, s->dim, PS_OP_PUSH, n, 1);
+  if (need == 0 || need > PS_NOALLOC_SCRATCH_BYTES)
+    return fail(PS_ERR_UNSUPPORTED, "a push of %lld keys of dim %d needs %zu bytes of scratch, the static scratch holds %zu",
+                (long long)n, s->dim, need, (size_t)PS_NOALLOC_SCRATCH_BYTES);
+  if (!s->scratch) return fail(PS_ERR_DEVICE, "no scratch address for the store's device");
+  return ps_push(s, keys, n, grads, s->scratch, PS_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 // ------------------------------------------------------------------ unmerged (asynchronous) updates

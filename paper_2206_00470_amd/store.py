@@ -187,6 +187,16 @@ class Store:
         ws, wsb = self._ws(_lib.PS_OP_PUSH, n, 1)
         check(lib().ps_push(self._h, _ptr(keys), n, _ptr(grads), ws, wsb, _stream(stream)))
 
+    def push_noalloc(self, keys: torch.Tensor, grads: torch.Tensor, stream=None):
+        """push() with the library's static device scratch as workspace: no
+        device memory is allocated, here or in the library."""
+        _dev(keys, torch.int64, "keys")
+        _dev(grads, torch.float32, "grads")
+        n = keys.numel()
+        if grads.numel() != n * self.dim:
+            raise ValueError("grads must hold n*dim floats")
+        check(lib().ps_push_noalloc(self._h, _ptr(keys), n, _ptr(grads), _stream(stream)))
+
     def push_async(self, keys: torch.Tensor, grads: torch.Tensor, stream=None):
         """Unmerged push: every occurrence its own AdaGrad step, applied with
         atomic adds in no fixed order (the asynchronous update semantics)."""
