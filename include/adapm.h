@@ -35,7 +35,8 @@
  *   - Output buffers must not alias the tables or each other.
  *   - Workspace: calls that need scratch memory take (ws, ws_bytes) from
  *     the caller, sized by ps_workspace_bytes(); the library allocates no
- *     device memory except a small status block in ps_create().
+ *     device memory except a small status block in ps_create() (and, once
+ *     per device, the static scratch array of ps_push_noalloc).
  */
 #ifndef ADAPM_H
 #define ADAPM_H
@@ -73,8 +74,11 @@ typedef int32_t ps_status;
 
 /* Create a store over caller-owned device tables W (values) and G
  * (AdaGrad accumulators), each num_keys*dim floats, with AdaGrad learning
- * rate lr > 0 and eps >= 0.  Allocates one small device status block and
- * clears it on `stream`.  *out receives the handle (NULL on error). */
+ * rate lr > 0 and eps >= 0.  The store is the node-local parameter store
+ * that the workers of a node share (Section 4, Figure 3); every task of
+ * Appendix C trains its parameters with AdaGrad.  Allocates one small
+ * device status block and clears it on `stream`.  *out receives the handle
+ * (NULL on error). */
 ps_status ps_create(ps_store** out, int64_t num_keys, int32_t dim, float* values, float* accum,
                     float lr, float eps, void* stream);
 
@@ -162,8 +166,10 @@ ps_status ps_push(ps_store* s, const int64_t* keys, int64_t n, const float* grad
 #define PS_NOALLOC_SCRATCH_BYTES (64u << 20)
 ps_status ps_push_noalloc(ps_store* s, const int64_t* keys, int64_t n, const float* grads, void* stream);
 
-/* The merge order used by ps_push, exposed for bit-exact checking: a stable
- * sort of the occurrences by key.  Keys outside [0, num_keys) sort after all
+/* The merge order used by ps_push (the updates of one parameter are merged
+ * before they reach the store, Appendix B.1.2), exposed for bit-exact
+ * checking: a stable sort of the occurrences by key.  There is no store,
+ * so a device flag `err` takes the place of the store's sticky error.  Keys outside [0, num_keys) sort after all
  * valid keys in their original order and belong to no segment.
  *   uniq      device int64[n]  : distinct valid keys ascending (first U used)
  *   perm      device int32[n]  : occurrence index at each sorted position
