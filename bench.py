@@ -11,11 +11,20 @@ the pulled rows, fp64 per-key merge and the AdaGrad row update.
 --workload selects one of the other task shapes (mf_tiny, kge, sgns, ctr).
 
 Prints one JSON line: rows pulled + pushed per second (2 row accesses per
-key occurrence), the roofline of the dominant kernel measured with HIP
-events during the timed steps (only that kernel is bracketed there: every
-event costs the GPU a few microseconds; the warm-up steps pick it, and a few
-extra steps with every big kernel bracketed give the per-kernel breakdown),
-push-only / pull-only rates (MF), and the CPU oracle timed on the host.
+key occurrence) over exactly --steps timed steps, each on its own
+pre-generated batch resident in HBM, and their median from HIP events; the
+roofline of the dominant kernel measured with HIP events during the timed
+steps (only that kernel is bracketed there: every event costs the GPU a few
+microseconds; the warm-up steps pick it, and a few extra steps with every
+big kernel bracketed give the per-kernel breakdown); push-only and
+pull-only rates; kernel launches per step; and the CPU oracle timed on the
+host, on one core and on all of them.
+
+Algorithmic bytes: the fused step reads the batch's inputs once and, per
+distinct key, its value and accumulator rows once and writes them once
+(inputs + 4 U R); a kernel's share is the inputs it reads plus the keys it
+updates.  The bytes the kernels actually move for gradient rows, records
+and row gathers are reported beside them as kernel bytes.
 """
 from __future__ import annotations
 
@@ -46,6 +55,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="bound on the CPU-oracle sample (0 = skip)")
     ap.add_argument("--no-ops", action="store_true", help="skip the pull-only / push-only measurements")
+    ap.add_argument("--ops-only", action="store_true",
+                    help="only the pull-only / push-only measurements (for counter runs of those calls)")
     ap.add_argument("--layout", default="interleaved", choices=["interleaved", "dense"],
                     help="W and G rows of a key side by side in one allocation, or two dense tables "
                          "(row-wise update: the accumulator in each W row's padding, or a separate vector)")
@@ -131,13 +142,19 @@ class Bench:
         T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
         self.T = T
         self.batches, self.host_batches, self.occ, self.uniq = [], [], [], []
-        for i in range(nbatches):
+
+        def gen(i):
             bt = self.wl.batch(i)
-            self.host_batches.append(bt)
-            self.batches.append({k: T(v) for k, v in bt.__dict__.items()})
             keys = self.keys_of(bt)
-            self.occ.append(keys.size)
-            self.uniq.append(np.unique(keys).size)
+            return bt, keys.size, np.unique(keys).size
+
+        from concurrent.futures import ThreadPoolExecutor
+        with ThreadPoolExecutor(min(host_threads(), max(1, nbatches))) as ex:
+            for bt, n, u in ex.map(gen, range(nbatches)):
+                self.host_batches.append(bt)
+                self.batches.append({k: T(v) for k, v in bt.__dict__.items()})
+                self.occ.append(n)
+                self.uniq.append(u)
 
     def keys_of(self, bt):
         c = self.cfg
@@ -179,7 +196,7 @@ class Bench:
             fan = h
         return fl
 
-    def run_overlapped(self, store, first, count, loss):
+    def run_overlapped(self, store, first, count, loss, after_step=None):
         """MF steps first .. first+count-1 with the two-phase step: the key work
         of batch i+1 (sort, segments, records) runs on a second stream while
         batch i updates the table on the current one; two workspaces, events
@@ -203,6 +220,8 @@ class Bench:
             main.wait_event(prepared[k % 2])
             store.step_mf_apply(bt["row"].numel(), c.lam, ws[k % 2], loss=loss, stream=main, rows_done=rows_done)
             applied[k % 2].record(main)
+            if after_step is not None:
+                after_step(k)
             if k + 1 < count:
                 nx = b(first + k + 1)
                 if k >= 1:
@@ -255,10 +274,56 @@ class Bench:
                 "taskgrad": B * (4.0 + 4 * bt.ctx.shape[1] * (1 + c.n_neg)) + (B + out_occ) * R + B * R
                             + out_occ * 8.0}
 
-    def oracle_step(self, W, G, i):
+    def input_bytes(self, i):
+        """Bytes of the step's batch as the caller hands it over (ids, values,
+        labels)."""
+        bt = self.host_batches[i % len(self.host_batches)]
+        return float(sum(v.nbytes for v in bt.__dict__.values()))
+
+    def sec8_bytes(self, i):
+        """Algorithmic bytes of the fused step (the batch's inputs read once,
+        then per distinct key its value and accumulator rows read and
+        written once: inputs + 4 U R for per-element AdaGrad) and each
+        kernel's share of them: the inputs it reads plus the keys it
+        updates.  Gradient rows, records, gathers of rows for the task
+        arithmetic and sort traffic are the implementation's, not in these
+        bytes (they are in alg_bytes)."""
+        c, bt = self.cfg, self.host_batches[i % len(self.host_batches)]
+        U, R, RV = self.uniq[i % len(self.uniq)], self.R, self.RV
+        tab = 2.0 * RV + 8.0 if self.rowwise else 2.0 * RV + 2.0 * R
+        inp = self.input_bytes(i)
+        out = {"step": inp + tab * U, "inputs": inp, "per_key": tab, "U": U}
+        if self.task == "mf" and self.unmerged:
+            out.update({"async": tab * U, "taskgrad": inp})
+        elif self.task == "mf":
+            Ucol = np.unique(bt.col).size
+            out.update({"rowmerge": inp + tab * (U - Ucol), "segreduce": tab * Ucol, "taskgrad": inp})
+        elif self.task == "ctr_wd":
+            out.update({"segreduce": tab * U, "mlp": self.mlp_flops(bt.keys.shape[0])})
+        else:
+            out.update({"segreduce": tab * U, "taskgrad": inp})
+        return out
+
+    def oracle_args(self, bt):
+        c = self.cfg
+        return {"mf": lambda: (bt.row, bt.col, bt.val, c.n_rows, c.lam),
+                "kge": lambda: (bt.head, bt.rel, bt.tail, bt.neg, c.n_head_neg, c.n_ent),
+                "sgns": lambda: (bt.centre, bt.ctx, bt.neg, c.window, c.vocab),
+                "ctr": lambda: (bt.keys, bt.label)}[self.task]()
+
+    def threadable(self):
+        """Whether the oracle step has a threaded form (step_threads): the
+        per-element fp32 steps of the four tasks, merged."""
+        return self.task in ("mf", "kge", "sgns", "ctr") and not (self.rowwise or self.unmerged
+                                                                  or self.values == "bf16")
+
+    def oracle_step(self, W, G, i, threads=1):
         import oracle
         c, bt = self.cfg, self.wl.batch(i)
         lr, eps = c.opt.lr, c.opt.eps
+        if threads > 1 and self.threadable():
+            oracle.step_threads(self.task, W, G, self.oracle_args(bt), lr, eps, threads)
+            return self.keys_of(bt).size
         if self.values == "bf16":
             oracle.step_mf_bf16(W, G, bt.row, bt.col, bt.val, c.n_rows, c.lam, lr, eps)
             return self.keys_of(bt).size
@@ -270,11 +335,7 @@ class Bench:
             step_ctr_wd(W, G, self._dense_host, self._acc_host, bt.keys, bt.label, c.emb_dim, c.deep, lr, eps)
             return self.keys_of(bt).size
         if self.rowwise:
-            args = {"mf": (bt.row, bt.col, bt.val, c.n_rows, c.lam),
-                    "kge": (bt.head, bt.rel, bt.tail, bt.neg, c.n_head_neg, c.n_ent),
-                    "sgns": (bt.centre, bt.ctx, bt.neg, c.window, c.vocab),
-                    "ctr": (bt.keys, bt.label)}[self.task]
-            oracle.step_rowwise(self.task, W, G, args, lr, eps)
+            oracle.step_rowwise(self.task, W, G, self.oracle_args(bt), lr, eps)
         elif self.task == "mf" and self.unmerged:
             oracle.step_mf_sequential(W, G, bt.row, bt.col, bt.val, c.n_rows, c.lam, lr, eps)
         elif self.task == "mf":
@@ -375,29 +436,66 @@ def run_staged(args, wb, dev):
     return elapsed, staging, roofline
 
 
+def host_threads():
+    """Threads for the all-core oracle: the cores this process may run on,
+    capped by OMP_NUM_THREADS when that is set (the host share of one GPU)."""
+    n = len(os.sched_getaffinity(0))
+    cap = os.environ.get("OMP_NUM_THREADS")
+    if cap and cap.isdigit() and int(cap) > 0:
+        n = min(n, int(cap))
+    return max(1, n)
+
+
 def cpu_baseline(args, wb, rowwise):
-    """The oracle on the host, single-threaded, on a bounded sample of the
-    same workload (whole steps on the full table, until --cpu-seconds)."""
+    """The oracle on the host on a bounded sample of the same workload (whole
+    steps on the full table): single-threaded, and on all the host's cores
+    (step_threads: gradients of unit ranges, then the merge of key ranges,
+    one range per thread), each for about half of --cpu-seconds.  Also the
+    host's memcpy bandwidth, for context."""
     if args.cpu_seconds <= 0:
         return None
     cfg = wb.cfg
-    W = wb.W
+    W = wb.W.copy()
     G = np.zeros(W.shape[0], np.float32) if rowwise else np.zeros_like(W)
     if wb.values == "bf16":
         import oracle
         W = oracle.f32_to_bf16(W)
     from threadpoolctl import threadpool_limits
-    done, rows, tc0 = 0, 0, time.perf_counter()
-    with threadpool_limits(1):               # numpy's matrix products single-threaded, like the C oracle
-        while True:
-            rows += 2 * wb.oracle_step(W, G, 1000 + done)
-            done += 1
-            if time.perf_counter() - tc0 >= args.cpu_seconds:
-                break
-    tc = time.perf_counter() - tc0
-    return {"value": rows / tc, "unit": "rows/s", "cores": 1, "kind": "oracle",
-            "sample": f"{done} step(s) of the same workload on the full {cfg.num_keys}x{cfg.dim} table, "
-                      f"single-threaded C oracle, {tc:.1f} s"}
+
+    def run(threads, budget, first):
+        done, rows, t0 = 0, 0, time.perf_counter()
+        with threadpool_limits(threads):      # numpy's products (Wide & Deep) on as many threads
+            while True:
+                rows += 2 * wb.oracle_step(W, G, first + done, threads)
+                done += 1
+                if time.perf_counter() - t0 >= budget:
+                    break
+        t = time.perf_counter() - t0
+        return rows / t, done, t
+
+    T = host_threads()
+    v1, n1, t1 = run(1, args.cpu_seconds / 2, 1000)
+    res = {"value": v1, "unit": "rows/s", "cores": 1, "kind": "oracle",
+           "sample": f"{n1} step(s) of the same workload on the full {cfg.num_keys}x{cfg.dim} table, "
+                     f"single-threaded C oracle, {t1:.1f} s"}
+    if T > 1 and (wb.threadable() or wb.task == "ctr_wd"):
+        vT, nT, tT = run(T, args.cpu_seconds / 2, 2000)
+        multi = {"value": vT, "unit": "rows/s", "cores": T, "kind": "oracle",
+                 "sample": f"{nT} step(s) of the same workload on the full {cfg.num_keys}x{cfg.dim} table, the C "
+                           f"oracle on {T} threads (unit ranges, then key ranges), {tT:.1f} s"}
+        # the faster of the two is the baseline (small batches run faster on one thread)
+        if vT >= v1:
+            res = dict(multi, single_core=res)
+        else:
+            res = dict(res, all_cores=multi)
+    a = np.ones(1 << 28, np.float32)
+    b = np.empty_like(a)
+    np.copyto(b, a)
+    t0 = time.perf_counter()
+    for _ in range(3):
+        np.copyto(b, a)
+    res["host_memcpy_GBps"] = round(3 * 2 * a.nbytes / (time.perf_counter() - t0) / 1e9, 1)
+    return res
 
 
 def main():
@@ -414,7 +512,7 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     t0 = time.time()
-    nb = max(1, min(args.steps + args.warmup, 8))
+    nb = max(1, args.steps + args.warmup)        # a distinct batch for every warm-up and timed step
     rowwise = args.update == "rowwise"
     unmerged = args.update == "async"
     bf16 = args.values == "bf16"
@@ -471,6 +569,13 @@ def main():
     print(f"# setup {time.time() - t0:.1f}s: {cfg.name}, table {cfg.num_keys}x{cfg.dim}, {nb} batches resident",
           file=sys.stderr, flush=True)
 
+    ops = {}
+    if args.ops_only:
+        ops = measure_ops(args, wb, store, dev, rowwise, unmerged)
+        print(json.dumps({"metric": "push / pull alone (" + cfg.name + ")", "ops": ops}), flush=True)
+        store.close()
+        return
+
     KID = {"segreduce": _lib.PS_KERNEL_SEGREDUCE, "taskgrad": _lib.PS_KERNEL_TASKGRAD,
            "rowmerge": _lib.PS_KERNEL_MF_ROWMERGE, "scatter": _lib.PS_KERNEL_SCATTER, "mlp": _lib.PS_KERNEL_MLP,
            "async": _lib.PS_KERNEL_ASYNC}
@@ -479,19 +584,25 @@ def main():
     # (MF tiny is launch-bound: the extra events of the overlap cost more than it hides)
     overlap = args.workload in ("mf", "mf_colorder") and not args.no_overlap and not args.graph and not unmerged
 
-    def run_steps(first, count, mask):
+    def run_steps(first, count, mask, marks=None):
         """count steps from batch `first` with the kernels in `mask` bracketed by HIP
-        events; returns host seconds and {name: (total ms, launches)}."""
+        events (and, with marks, an event on the current stream after each step);
+        returns host seconds and {name: (total ms, launches)}."""
         for k in KID.values():
             store.read_timing(k)                  # reset
         store.set_timing(mask)
         torch.cuda.synchronize()
+        if marks is not None:
+            marks[0].record()
         t = time.perf_counter()
         if overlap:
-            wb.run_overlapped(store, first, count, loss)
+            wb.run_overlapped(store, first, count, loss,
+                              after_step=(lambda k: marks[k + 1].record()) if marks is not None else None)
         else:
             for i in range(count):
                 wb.step(store, first + i, loss)
+                if marks is not None:
+                    marks[i + 1].record()
         torch.cuda.synchronize()
         secs = time.perf_counter() - t
         store.set_timing(False)
@@ -504,7 +615,9 @@ def main():
 
     # ------------------------------------------------------------ timed steps
     # Each HIP event costs the GPU a few microseconds, so only the dominant
-    # kernel is bracketed while the step time is measured.
+    # kernel is bracketed while the step time is measured (plus one event per
+    # step on the stream, for the median).
+    step_ms = []
     if args.graph:
         # the same steps, captured once (the workspace is already sized) and replayed
         g = torch.cuda.CUDAGraph()
@@ -518,12 +631,24 @@ def main():
         torch.cuda.synchronize()
         elapsed = time.perf_counter() - t
         assert store.error() == 0
+        # four more replays, each timed with events: the median replay per step
+        for _ in range(4):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            g.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            step_ms.append(e0.elapsed_time(e1) / args.steps)
+        step_ms.append(elapsed * 1e3 / args.steps)
     else:
-        elapsed, kt = run_steps(args.warmup, args.steps, 1 << KID[dom])
+        marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+        elapsed, kt = run_steps(args.warmup, args.steps, 1 << KID[dom], marks)
+        step_ms = [marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)]
     # per-kernel breakdown from a few more steps with every big kernel timed
     # (instrumentation only, not part of the timed figure)
     nprof = max(1, min(args.steps, 5))
     _, kt_all = run_steps(args.warmup + args.steps, nprof, _lib.PS_TIMING_ALL)
+    launches = launches_per_step(wb, store, args.warmup, loss)
 
     idx = [args.warmup + i for i in range(args.steps)]
     idx_prof = [args.warmup + args.steps + i for i in range(nprof)]
@@ -537,11 +662,14 @@ def main():
 
     def kernel_entry(name, timing, steps, bidx):
         ms, cnt = timing
-        nbytes = float(np.mean([wb.alg_bytes(i)[name] for i in bidx]))
+        kbytes = float(np.mean([wb.alg_bytes(i)[name] for i in bidx]))
+        sbytes = float(np.mean([wb.sec8_bytes(i)[name] for i in bidx]))
         per_step_ms = ms / max(steps, 1)
         return {"avg_ms": ms / max(cnt, 1), "ms_per_step": per_step_ms, "launches": cnt,
-                "alg_bytes_per_step": nbytes,
-                "alg_GBps": nbytes / (per_step_ms * 1e-3) / 1e9 if cnt else None,
+                "alg_bytes_per_step": sbytes,
+                "alg_GBps": sbytes / (per_step_ms * 1e-3) / 1e9 if cnt else None,
+                "kernel_bytes_per_step": kbytes,
+                "kernel_GBps": kbytes / (per_step_ms * 1e-3) / 1e9 if cnt else None,
                 "launches_per_step": seg_launches_per_step if name == "segreduce" else
                 (3 * len(wb.cfg.deep) if name == "mlp" else 1)}
 
@@ -556,6 +684,9 @@ def main():
                            "ctr": "k_ctr_grad", "ctr_wd": "k_wd_head"}[wb.task]}[dom]
     traffic = counter_traffic(args.workload + ("_rowwise" if rowwise else "") + ("_bf16" if bf16 else "")
                               + ("_async" if unmerged else ""), symbol)
+    lpl = dk["launches_per_step"]
+    alg_launch = dk["alg_bytes_per_step"] / lpl
+    step_alg = float(np.mean([wb.sec8_bytes(i)["step"] for i in idx]))
     roofline = {
         "bound": "hbm",
         "kernel": symbol,
@@ -563,85 +694,28 @@ def main():
         "peak": HBM_PEAK_GBPS,
         "unit": "GB/s",
         "frac": round(dk["alg_GBps"] / HBM_PEAK_GBPS, 4),
-        "traffic": traffic,
+        "traffic": int(traffic) if traffic else None,
+        "traffic_over_alg": round(traffic / alg_launch, 3) if traffic else None,
         "avg_ms": round(dk["avg_ms"], 4),
-        "alg_bytes_per_launch": int(dk["alg_bytes_per_step"] / dk["launches_per_step"]),
+        "alg_bytes_per_launch": int(alg_launch),
+        "alg_bytes": "the fused step's bytes (inputs read once, each distinct key's value and accumulator "
+                     "rows read and written once) that this kernel accounts for: the inputs it reads and "
+                     "the keys it updates",
+        "kernel_bytes_per_launch": int(dk["kernel_bytes_per_step"] / lpl),
+        "kernel_GBps": round(dk["kernel_GBps"], 1),
+        "step": {"alg_bytes": int(step_alg), "GBps": round(step_alg / (ms_per_step * 1e-3) / 1e9, 1),
+                 "frac": round(step_alg / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)},
     }
     if dom == "mlp":
         tf = dk["alg_GBps"] / 1e3            # "bytes" of the mlp entry are flops
         roofline = {"bound": "mfma", "kernel": symbol, "dtype": "f64", "achieved": round(tf, 2),
                     "peak": MFMA_F64_TFLOPS, "unit": "TFLOP/s", "frac": round(tf / MFMA_F64_TFLOPS, 4),
                     "traffic": None, "avg_ms": round(dk["avg_ms"], 4),
-                    "alg_flops_per_launch": int(dk["alg_bytes_per_step"] / dk["launches_per_step"])}
+                    "alg_flops_per_launch": int(dk["alg_bytes_per_step"] / dk["launches_per_step"]),
+                    "step": roofline["step"]}
 
-    # ------------------------------------------------------------ push-only / pull-only (MF)
-    ops = {}
-    if not args.no_ops and args.workload == "mf":
-        from paper_2206_00470_amd.workloads import random_push
-        n = int(wb.occ[0])
-        bt = wb.wl.batch(100)
-        keys_np = wb.keys_of(bt)
-        U = np.unique(keys_np).size
-        _, grads_np = random_push(cfg.num_keys, n, cfg.dim, 7)
-        keys = torch.from_numpy(keys_np).to(dev)
-        grads = torch.from_numpy(grads_np).to(dev)
-        del grads_np
-        out = torch.empty((n, cfg.dim), dtype=torch.float32, device=dev)
-        reps = 10
-        for _ in range(2):
-            store.push(keys, grads)
-            store.pull(keys, out=out)
-        torch.cuda.synchronize()
-        t1 = time.perf_counter()
-        for _ in range(reps):
-            store.push(keys, grads)
-        torch.cuda.synchronize()
-        tp = (time.perf_counter() - t1) / reps
-        t1 = time.perf_counter()
-        for _ in range(reps):
-            store.pull(keys, out=out)
-        torch.cuda.synchronize()
-        tl = (time.perf_counter() - t1) / reps
-        ta = None
-        if unmerged:
-            store.push_async(keys, grads)
-            torch.cuda.synchronize()
-            t1 = time.perf_counter()
-            for _ in range(reps):
-                store.push_async(keys, grads)
-            torch.cuda.synchronize()
-            ta = (time.perf_counter() - t1) / reps
-        assert store.error() == 0
-        R = wb.R
-        RV = wb.RV
-        tab = 2.0 * RV + 8.0 if rowwise else 2.0 * RV + 2.0 * R
-        push_alg = 8.0 * n + n * R + tab * U
-        pull_alg = 8.0 * n + U * RV + n * R
-        # the bare read-modify-write pattern through the merge kernel: U distinct
-        # random keys, one contiguous gradient row each (no duplicates to merge)
-        ukeys = torch.from_numpy(np.sort(np.random.default_rng(11).choice(cfg.num_keys, int(U), replace=False))).to(dev)
-        ugrads = grads[:int(U)]
-        store.push(ukeys, ugrads)
-        store.read_timing(_lib.PS_KERNEL_SEGREDUCE)
-        store.set_timing(1 << _lib.PS_KERNEL_SEGREDUCE)
-        for _ in range(reps):
-            store.push(ukeys, ugrads)
-        store.set_timing(False)
-        mms, mcnt = store.read_timing(_lib.PS_KERNEL_SEGREDUCE)
-        merge_ms = mms / max(mcnt, 1)
-        rmw_alg = U * R + tab * U
-        ops = {
-            "push": {"ms": round(tp * 1e3, 4), "rows_per_s": n / tp, "alg_GBps": round(push_alg / tp / 1e9, 1),
-                     "frac_of_peak": round(push_alg / tp / 1e9 / HBM_PEAK_GBPS, 4), "unique_keys": int(U)},
-            "pull": {"ms": round(tl * 1e3, 4), "rows_per_s": n / tl, "alg_GBps": round(pull_alg / tl / 1e9, 1)},
-            **({"push_async": {"ms": round(ta * 1e3, 4), "rows_per_s": n / ta,
-                               "alg_GBps": round((n * R + tab * U) / ta / 1e9, 1)}} if ta else {}),
-            "merge_distinct_keys": {"keys": int(U), "merge_ms": round(merge_ms, 4),
-                                    "alg_GBps": round(rmw_alg / (merge_ms * 1e-3) / 1e9, 1),
-                                    "what": "merge kernel alone on a push of distinct random keys: W and G "
-                                            "read-modify-write plus one gradient row per key"},
-        }
-        del keys, grads, out, ukeys, ugrads
+    if not args.no_ops:
+        ops = measure_ops(args, wb, store, dev, rowwise, unmerged)
 
     copy = None
     if args.calibrate_copy:
@@ -671,6 +745,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4),
+        "median_ms_per_step": round(float(np.median(step_ms)), 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -681,19 +756,134 @@ def main():
                    "launch": "hip graph replay" if args.graph else "eager",
                    "mf_key_work_overlapped": overlap,
                    "key_occurrences_per_step": occ, "avg_unique_keys_per_step": U_avg,
-                   "batches_resident": nb},
+                   "batches_resident": nb, "distinct_batch_per_timed_step": nb >= args.warmup + args.steps,
+                   "kernel_launches_per_step": launches},
         "roofline": roofline,
         "kernels": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv) for kk, vv in v.items()}
                     for k, v in kernels.items()},
         "kernels_from": f"{nprof} extra steps with every big kernel timed (the timed steps time only {dom})"
                         if not args.graph else f"{nprof} eager steps with every big kernel timed; the timed steps "
                                                f"are one HIP-graph replay",
+        "median_from": "HIP events on the stream after each timed step" if not args.graph else
+                       "the timed replay and four more, each over all steps",
         "ops": ops,
         "copy_calibration": copy,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
     store.close()
+
+
+def launches_per_step(wb, store, i, loss):
+    """Kernel launches of one step: the step captured into a HIP graph (not
+    replayed) and its kernel nodes counted."""
+    import ctypes as C
+
+    import torch
+    try:
+        hip = C.CDLL("libamdhip64.so")
+        wb.step(store, i, loss)           # eager first: the step's workspace exists before the capture
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph(keep_graph=True)
+        with torch.cuda.graph(g):
+            wb.step(store, i, loss)
+        graph = C.c_void_p(g.raw_cuda_graph())
+        n = C.c_size_t(0)
+        if hip.hipGraphGetNodes(graph, None, C.byref(n)) != 0:
+            return None
+        nodes = (C.c_void_p * n.value)()
+        if hip.hipGraphGetNodes(graph, nodes, C.byref(n)) != 0:
+            return None
+        kinds = C.c_int(0)
+        count = 0
+        for nd in nodes:
+            if hip.hipGraphNodeGetType(C.c_void_p(nd), C.byref(kinds)) == 0 and kinds.value == 0:
+                count += 1            # hipGraphNodeTypeKernel
+        g.reset()
+        torch.cuda.synchronize()
+        return count
+    except (OSError, RuntimeError, AttributeError):
+        return None
+
+
+def measure_ops(args, wb, store, dev, rowwise, unmerged):
+    """ps_push and ps_pull alone on one batch's key occurrences (random
+    gradient rows), each rep timed with HIP events; reported as medians.
+    MF also: the merge kernel alone on distinct random keys (the bare
+    read-modify-write pattern), and the unmerged push."""
+    import torch
+
+    from paper_2206_00470_amd import _lib
+    cfg = wb.cfg
+    bt = wb.wl.batch(100)
+    keys_np = wb.keys_of(bt)
+    n = int(keys_np.size)
+    U = int(np.unique(keys_np).size)
+    keys = torch.from_numpy(keys_np).to(dev)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(7)
+    grads = torch.randn((n, cfg.dim), generator=gen, dtype=torch.float32, device=dev)
+    out = torch.empty((n, cfg.dim), dtype=torch.float32, device=dev)
+    reps = 10
+
+    def timed(fn):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+        ev[0].record()
+        for r in range(reps):
+            fn()
+            ev[r + 1].record()
+        torch.cuda.synchronize()
+        assert store.error() == 0
+        return float(np.median([ev[r].elapsed_time(ev[r + 1]) for r in range(reps)])) * 1e-3
+
+    tp = timed(lambda: store.push(keys, grads))
+    tl = timed(lambda: store.pull(keys, out=out))
+    R, RV = wb.R, wb.RV
+    tab = 2.0 * RV + 8.0 if rowwise else 2.0 * RV + 2.0 * R
+    push_alg = 8.0 * n + n * R + tab * U
+    pull_alg = 8.0 * n + U * RV + n * R
+    ops = {
+        "push": {"ms": round(tp * 1e3, 4), "rows_per_s": n / tp, "alg_GBps": round(push_alg / tp / 1e9, 1),
+                 "frac_of_peak": round(push_alg / tp / 1e9 / HBM_PEAK_GBPS, 4), "occurrences": n, "unique_keys": U,
+                 "roofline": {"bound": "hbm", "achieved": round(push_alg / tp / 1e9, 1), "peak": HBM_PEAK_GBPS,
+                              "unit": "GB/s", "frac": round(push_alg / tp / 1e9 / HBM_PEAK_GBPS, 4),
+                              "alg_bytes": int(push_alg),
+                              "what": "8 n (keys) + n R (gradient rows) + per distinct key its value and "
+                                      "accumulator rows read and written, over the whole ps_push (sort, "
+                                      "segments, merge, finalize)"}},
+        "pull": {"ms": round(tl * 1e3, 4), "rows_per_s": n / tl, "alg_GBps": round(pull_alg / tl / 1e9, 1),
+                 "frac_of_peak": round(pull_alg / tl / 1e9 / HBM_PEAK_GBPS, 4)},
+        "median_of": reps,
+    }
+    if unmerged:
+        ta = timed(lambda: store.push_async(keys, grads))
+        ops["push_async"] = {"ms": round(ta * 1e3, 4), "rows_per_s": n / ta,
+                             "alg_GBps": round((n * R + tab * U) / ta / 1e9, 1)}
+    if wb.task == "mf" and not args.ops_only:
+        # the bare read-modify-write pattern through the merge kernel: U distinct
+        # random keys, one contiguous gradient row each (no duplicates to merge)
+        ukeys = torch.from_numpy(np.sort(np.random.default_rng(11).choice(cfg.num_keys, U, replace=False))).to(dev)
+        ugrads = grads[:U]
+        store.push(ukeys, ugrads)
+        store.read_timing(_lib.PS_KERNEL_SEGREDUCE)
+        store.set_timing(1 << _lib.PS_KERNEL_SEGREDUCE)
+        for _ in range(reps):
+            store.push(ukeys, ugrads)
+        store.set_timing(False)
+        mms, mcnt = store.read_timing(_lib.PS_KERNEL_SEGREDUCE)
+        merge_ms = mms / max(mcnt, 1)
+        rmw_alg = U * R + tab * U
+        ops["merge_distinct_keys"] = {"keys": U, "merge_ms": round(merge_ms, 4),
+                                      "alg_GBps": round(rmw_alg / (merge_ms * 1e-3) / 1e9, 1),
+                                      "what": "merge kernel alone on a push of distinct random keys: W and G "
+                                              "read-modify-write plus one gradient row per key"}
+        del ukeys, ugrads
+    del keys, grads, out
+    torch.cuda.empty_cache()
+    return ops
 
 
 if __name__ == "__main__":

@@ -349,3 +349,102 @@ def step_ctr(W, G, keys, label, lr, eps):
     loss = lib().orc_step_ctr(_p(W), _p(G), W.shape[0], W.shape[1], lr, eps, _p(keys), _p(label),
                               B, F, C.byref(bad))
     return float(loss), int(bad.value)
+
+
+# ---------------------------------------------------------------------------
+# The same steps spread over host threads (for timing the oracle on all of a
+# host's cores).  The work of a step splits into independent pieces: each
+# unit's gradients depend only on the pre-step table, and each key's merge
+# and AdaGrad update only on that key's occurrences (Appendix B.1.2: the
+# updates of a parameter are merged into its store).  Threads take
+# contiguous unit ranges for the first phase and disjoint key ranges for the
+# second; every key's occurrences keep their order, so W and G come out bit
+# for bit as from the one-thread step.  The loss is the sum of the ranges'
+# losses, a different order of additions.
+_GRAD = {"mf": "orc_grad_mf", "kge": "orc_grad_kge", "sgns": "orc_grad_sgns", "ctr": "orc_grad_ctr"}
+
+
+def _grad_call(task, W, a, lo, hi, keys, grads, per):
+    """Gradients of units [lo, hi) of the batch `a` into keys/grads at unit lo."""
+    L = lib()
+    bad = C.c_int64(0)
+    K, d = W.shape
+    ko, go = _p(keys[lo * per:]), _p(grads[lo * per:])
+    if task == "mf":
+        loss = L.orc_grad_mf(_p(W), K, d, _p(a["row"][lo:]), _p(a["col"][lo:]), _p(a["val"][lo:]), hi - lo,
+                             a["col_off"], a["lam"], ko, go, C.byref(bad))
+    elif task == "kge":
+        loss = L.orc_grad_kge(_p(W), K, d, _p(a["head"][lo:]), _p(a["rel"][lo:]), _p(a["tail"][lo:]),
+                              _p(a["neg"][lo:]), hi - lo, a["n_neg"], a["n_head_neg"], a["rel_off"], ko, go,
+                              C.byref(bad))
+    elif task == "sgns":
+        loss = L.orc_grad_sgns(_p(W), K, d, _p(a["centre"][lo:]), _p(a["ctx"][lo:]), _p(a["neg"][lo:]), hi - lo,
+                               a["window"], a["n_neg"], a["out_off"], ko, go, C.byref(bad))
+    else:
+        loss = L.orc_grad_ctr(_p(W), K, d, _p(a["keys"][lo:]), _p(a["label"][lo:]), hi - lo, a["F"], ko, go,
+                              C.byref(bad))
+    return float(loss), int(bad.value)
+
+
+def _batch_args(task, batch):
+    """Contiguous C-typed inputs of a task step, the unit count and the key
+    occurrences per unit."""
+    if task == "mf":
+        row, col, val, col_off, lam = batch
+        a = {"row": _c(row, np.int32), "col": _c(col, np.int32), "val": _c(val, np.float32), "col_off": col_off,
+             "lam": lam}
+        return a, a["row"].size, 2
+    if task == "kge":
+        head, rel, tail, neg, n_head_neg, rel_off = batch
+        a = {"head": _c(head, np.int32), "rel": _c(rel, np.int32), "tail": _c(tail, np.int32),
+             "neg": _c(neg, np.int32), "n_head_neg": n_head_neg, "rel_off": rel_off}
+        B = a["head"].size
+        a["n_neg"] = a["neg"].size // max(B, 1) if B else 0
+        return a, B, 3 + a["n_neg"]
+    if task == "sgns":
+        centre, ctx, neg, window, out_off = batch
+        a = {"centre": _c(centre, np.int32), "ctx": _c(ctx, np.int32), "neg": _c(neg, np.int32), "window": window,
+             "out_off": out_off}
+        B = a["centre"].size
+        a["n_neg"] = a["neg"].size // max(B * 2 * window, 1) if B else 0
+        return a, B, 1 + 2 * window * (1 + a["n_neg"])
+    keys, label = batch
+    a = {"keys": _c(keys, np.int64), "label": _c(label, np.float32)}
+    B = a["label"].size
+    a["F"] = a["keys"].size // max(B, 1) if B else 0
+    return a, B, a["F"]
+
+
+def step_threads(task, W, G, batch, lr, eps, threads):
+    """One step of `task` ("mf", "kge", "sgns", "ctr"; batch = the arguments
+    of grad_<task> after the table) on `threads` host threads: gradients of
+    contiguous unit ranges, then the merged per-element AdaGrad push of
+    disjoint key ranges.  W and G equal those of step_<task> bit for bit.
+    Returns (loss, bad)."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    W, G = _table(W), _table(G)
+    a, B, per = _batch_args(task, batch)
+    K, d = W.shape
+    keys = np.empty(B * per, np.int64)
+    grads = np.empty((B * per, d), np.float32)
+    T = max(1, int(threads))
+    cuts = [B * t // T for t in range(T + 1)]
+    with ThreadPoolExecutor(T) as ex:
+        parts = list(ex.map(lambda t: _grad_call(task, W, a, cuts[t], cuts[t + 1], keys, grads, per), range(T)))
+        loss = sum(p[0] for p in parts)
+        bad = sum(p[1] for p in parts)
+        # disjoint key ranges, each range's occurrences in their original order
+        part = np.where(keys >= 0, keys * T // K, 0).astype(np.uint8)
+        order = np.argsort(part, kind="stable")
+        ks, gs = keys[order], grads[order]
+        del grads
+        bounds = np.searchsorted(part[order], np.arange(T + 1))
+        L = lib()
+
+        def push_range(t):
+            lo, hi = int(bounds[t]), int(bounds[t + 1])
+            return int(L.orc_push(_p(W), _p(G), K, d, lr, eps, _p(ks[lo:]), hi - lo, _p(gs[lo:])))
+
+        list(ex.map(push_range, range(T)))
+    return loss, bad
