@@ -806,6 +806,42 @@ def launches_per_step(wb, store, i, loss):
         return None
 
 
+def pipelined_push(store, keys, grads, n, reps):
+    """Seconds per push of `reps` pushes back to back, the key work of push
+    i+1 (ps_push_prepare, second stream, two workspaces) beside the merge
+    of push i (ps_push_apply)."""
+    import torch
+    main, side = torch.cuda.current_stream(), torch.cuda.Stream()
+    ws = [store.push_workspace(n), store.push_workspace(n)]
+    prepared = [torch.cuda.Event(), torch.cuda.Event()]
+    applied = [torch.cuda.Event(), torch.cuda.Event()]
+
+    def run(count):
+        side.wait_stream(main)
+        store.push_prepare(keys, ws[0], stream=side)
+        prepared[0].record(side)
+        for k in range(count):
+            main.wait_event(prepared[k % 2])
+            store.push_apply(n, grads, ws[k % 2], stream=main)
+            applied[k % 2].record(main)
+            if k + 1 < count:
+                if k >= 1:
+                    side.wait_event(applied[(k + 1) % 2])
+                store.push_prepare(keys, ws[(k + 1) % 2], stream=side)
+                prepared[(k + 1) % 2].record(side)
+
+    run(2)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(main)
+    run(reps)
+    e1.record(main)
+    torch.cuda.synchronize()
+    assert store.error() == 0
+    del ws
+    return e0.elapsed_time(e1) * 1e-3 / reps
+
+
 def measure_ops(args, wb, store, dev, rowwise, unmerged):
     """ps_push and ps_pull alone on one batch's key occurrences (random
     gradient rows), each rep timed with HIP events; reported as medians.
@@ -841,6 +877,7 @@ def measure_ops(args, wb, store, dev, rowwise, unmerged):
 
     tp = timed(lambda: store.push(keys, grads))
     tl = timed(lambda: store.pull(keys, out=out))
+    tpp = pipelined_push(store, keys, grads, n, reps)
     R, RV = wb.R, wb.RV
     tab = 2.0 * RV + 8.0 if rowwise else 2.0 * RV + 2.0 * R
     push_alg = 8.0 * n + n * R + tab * U
@@ -854,6 +891,15 @@ def measure_ops(args, wb, store, dev, rowwise, unmerged):
                               "what": "8 n (keys) + n R (gradient rows) + per distinct key its value and "
                                       "accumulator rows read and written, over the whole ps_push (sort, "
                                       "segments, merge, finalize)"}},
+        "push_pipelined": {"ms": round(tpp * 1e3, 4), "rows_per_s": n / tpp,
+                           "alg_GBps": round(push_alg / tpp / 1e9, 1),
+                           "frac_of_peak": round(push_alg / tpp / 1e9 / HBM_PEAK_GBPS, 4),
+                           "roofline": {"bound": "hbm", "achieved": round(push_alg / tpp / 1e9, 1),
+                                        "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                                        "frac": round(push_alg / tpp / 1e9 / HBM_PEAK_GBPS, 4),
+                                        "alg_bytes": int(push_alg)},
+                           "what": f"{reps} pushes back to back, each push's key work (ps_push_prepare) on a "
+                                   "second stream beside the previous push's merge (ps_push_apply); time per push"},
         "pull": {"ms": round(tl * 1e3, 4), "rows_per_s": n / tl, "alg_GBps": round(pull_alg / tl / 1e9, 1),
                  "frac_of_peak": round(pull_alg / tl / 1e9 / HBM_PEAK_GBPS, 4)},
         "median_of": reps,

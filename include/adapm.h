@@ -149,6 +149,24 @@ ps_status ps_pull(ps_store* s, const int64_t* keys, int64_t n, float* out, void*
 ps_status ps_push(ps_store* s, const int64_t* keys, int64_t n, const float* grads,
                   void* ws, size_t ws_bytes, void* stream);
 
+/* ps_push in two phases, for callers that overlap the key work of the next
+ * push with the merge of this one (two workspaces, two streams), as
+ * ps_step_mf_prepare / ps_step_mf_apply do for the MF step.
+ * ps_push_prepare reads only the keys and writes the workspace (key
+ * intake, sort, segments; a key outside [0, num_keys) raises the store's
+ * sticky error here); it reads and writes no table row, so it may run
+ * while another workspace's apply updates W and G.  ps_push_apply then
+ * merges grads (device float[n*dim], as for ps_push) into W and G in the
+ * order that workspace holds; it no longer reads the keys.  ws must hold
+ * the result of ps_push_prepare for this store and the same n, unmodified;
+ * the order of prepare before apply, and of an apply before the next
+ * prepare into the same workspace, is the caller's (e.g. events).
+ * Prepare then apply on one stream is exactly ps_push.  Workspace size:
+ * ps_workspace_bytes(num_keys, dim, PS_OP_PUSH, n, 1).  Staged stores:
+ * PS_ERR_UNSUPPORTED. */
+ps_status ps_push_prepare(ps_store* s, const int64_t* keys, int64_t n, void* ws, size_t ws_bytes, void* stream);
+ps_status ps_push_apply(ps_store* s, int64_t n, const float* grads, void* ws, size_t ws_bytes, void* stream);
+
 /* ps_push for callers that cannot allocate device memory (code under HIP
  * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
  * same merge and update, with the workspace taken from a static device array

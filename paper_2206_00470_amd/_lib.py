@@ -45,6 +45,8 @@ SIGNATURES = {
     "ps_workspace_bytes": (_sz, [_i64, _i32, _i32, _i64, _i64]),
     "ps_pull": (_i32, [_p, _p, _i64, _p, _p]),
     "ps_push": (_i32, [_p, _p, _i64, _p, _p, _sz, _p]),
+    "ps_push_prepare": (_i32, [_p, _p, _i64, _p, _sz, _p]),
+    "ps_push_apply": (_i32, [_p, _i64, _p, _p, _sz, _p]),
     "ps_push_noalloc": (_i32, [_p, _p, _i64, _p, _p]),
     "ps_dedup": (_i32, [_i64, _p, _i64, _p, _p, _p, _p, _p, _p, _sz, _p]),
     "ps_step_mf": (_i32, [_p, _p, _p, _p, _i64, _i64, _f32, _p, _p, _sz, _p]),

@@ -1162,22 +1162,65 @@ ps_status ps_pull(ps_store* s, const int64_t* keys, int64_t n, float* out, void*
   });
 }
 
+// The push in two phases: the key work (intake, sort, segments; workspace
+// only) and the merge of the gradient rows into the table.
+static ps_status push_prepare(ps_store* s, const int64_t* keys, int64_t n, Plan& p, hipStream_t st) {
+  uint32_t *ks, *perm;
+  if (ps_status r = run_sort(s, KeysInt64{keys}, n, s->num_keys, p.sb, s->status, nullptr, false, st, &ks, &perm))
+    return r;
+  return run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st);
+}
+
+static ps_status push_apply(ps_store* s, int64_t n, const float* grads, Plan& p, hipStream_t st) {
+  const int passes = radix_plan(s->num_keys).passes;   // where the sort left keys and permutation
+  const uint32_t* ks = p.sb.k[passes % 2];
+  const uint32_t* perm = p.sb.v[passes % 2];
+  return run_reduce(s, p.sb, ks, SrcIndirect{grads, perm, s->dim}, n, {PART_ALL}, st);
+}
+
+static ps_status check_grads(const ps_store* s, const float* grads) {
+  if (!grads) return fail(PS_ERR_INVALID, "grads is NULL");
+  if (s->dim % 4 == 0 && !aligned16(grads)) return fail(PS_ERR_INVALID, "grads must be 16-byte aligned");
+  return PS_OK;
+}
+
 static ps_status push_impl(ps_store* s, const int64_t* keys, int64_t n, const float* grads, void* ws, size_t ws_bytes,
                            void* stream) {
   if (ps_status st = check_store(s)) return st;
   if (ps_status st = check_n(n, 1)) return st;
   if (n == 0) return PS_OK;
-  if (!keys || !grads) return fail(PS_ERR_INVALID, "keys or grads is NULL");
-  if (s->dim % 4 == 0 && !aligned16(grads)) return fail(PS_ERR_INVALID, "grads must be 16-byte aligned");
+  if (!keys) return fail(PS_ERR_INVALID, "keys is NULL");
+  if (ps_status st = check_grads(s, grads)) return st;
   Plan p;
   plan_op(ws, s->num_keys, s->dim, PS_OP_PUSH, n, 1, &p);
   if (ps_status st = check_ws(p, ws, ws_bytes)) return st;
   hipStream_t st = as_stream(stream);
-  uint32_t *ks, *perm;
-  if (ps_status r = run_sort(s, KeysInt64{keys}, n, s->num_keys, p.sb, s->status, nullptr, false, st, &ks, &perm))
-    return r;
-  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st)) return r;
-  return run_reduce(s, p.sb, ks, SrcIndirect{grads, perm, s->dim}, n, {PART_ALL}, st);
+  if (ps_status r = push_prepare(s, keys, n, p, st)) return r;
+  return push_apply(s, n, grads, p, st);
+}
+
+ps_status ps_push_prepare(ps_store* s, const int64_t* keys, int64_t n, void* ws, size_t ws_bytes, void* stream) {
+  if (ps_status st = check_store(s)) return st;
+  if (s->stg) return fail(PS_ERR_UNSUPPORTED, "the two-phase push is not available on a staged store");
+  if (ps_status st = check_n(n, 1)) return st;
+  if (n == 0) return PS_OK;
+  if (!keys) return fail(PS_ERR_INVALID, "keys is NULL");
+  Plan p;
+  plan_op(ws, s->num_keys, s->dim, PS_OP_PUSH, n, 1, &p);
+  if (ps_status st = check_ws(p, ws, ws_bytes)) return st;
+  return push_prepare(s, keys, n, p, as_stream(stream));
+}
+
+ps_status ps_push_apply(ps_store* s, int64_t n, const float* grads, void* ws, size_t ws_bytes, void* stream) {
+  if (ps_status st = check_store(s)) return st;
+  if (s->stg) return fail(PS_ERR_UNSUPPORTED, "the two-phase push is not available on a staged store");
+  if (ps_status st = check_n(n, 1)) return st;
+  if (n == 0) return PS_OK;
+  if (ps_status st = check_grads(s, grads)) return st;
+  Plan p;
+  plan_op(ws, s->num_keys, s->dim, PS_OP_PUSH, n, 1, &p);
+  if (ps_status st = check_ws(p, ws, ws_bytes)) return st;
+  return push_apply(s, n, grads, p, as_stream(stream));
 }
 
 ps_status ps_dedup(int64_t num_keys, const int64_t* keys, int64_t n, int64_t* uniq, int32_t* perm,

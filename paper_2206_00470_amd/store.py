@@ -187,6 +187,23 @@ class Store:
         ws, wsb = self._ws(_lib.PS_OP_PUSH, n, 1)
         check(lib().ps_push(self._h, _ptr(keys), n, _ptr(grads), ws, wsb, _stream(stream)))
 
+    def push_workspace(self, n: int) -> torch.Tensor:
+        """A workspace of its own for push_prepare / push_apply of n keys."""
+        return torch.empty(max(self.workspace_bytes(_lib.PS_OP_PUSH, n, 1), 1), dtype=torch.uint8,
+                           device=self.W.device)
+
+    def push_prepare(self, keys: torch.Tensor, ws: torch.Tensor, stream=None):
+        """Key work of a push (sort, segments) into ws; reads no table row."""
+        _dev(keys, torch.int64, "keys")
+        check(lib().ps_push_prepare(self._h, _ptr(keys), keys.numel(), _ptr(ws), ws.numel(), _stream(stream)))
+
+    def push_apply(self, n: int, grads: torch.Tensor, ws: torch.Tensor, stream=None):
+        """Merge of a prepared push of n keys: grads into W and G."""
+        _dev(grads, torch.float32, "grads")
+        if grads.numel() != n * self.dim:
+            raise ValueError("grads must hold n*dim floats")
+        check(lib().ps_push_apply(self._h, n, _ptr(grads), _ptr(ws), ws.numel(), _stream(stream)))
+
     def push_noalloc(self, keys: torch.Tensor, grads: torch.Tensor, stream=None):
         """push() with the library's static device scratch as workspace: no
         device memory is allocated, here or in the library."""
