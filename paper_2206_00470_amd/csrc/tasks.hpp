@@ -4,6 +4,7 @@
 #pragma once
 
 #include "common.hpp"
+#include "fp64math.hpp"
 
 namespace adapm {
 
@@ -143,24 +144,7 @@ struct SrcMFRow {
 };
 
 // ------------------------------------------------------------------ shared pieces
-__device__ __forceinline__ double sigmoid_d(double x) {
-  if (x >= 0.0) return 1.0 / (1.0 + exp(-x));
-  const double e = exp(x);
-  return e / (1.0 + e);
-}
-
-__device__ __forceinline__ double softplus_d(double x) {
-  return x > 0.0 ? x + log1p(exp(-x)) : log1p(exp(x));
-}
-
-// sigmoid(x) and softplus(x) from one exp(-|x|), without divergent branches;
-// each result rounds exactly as the two-branch forms above.
-__device__ __forceinline__ void sigmoid_softplus(double x, double* sig, double* sp) {
-  const double e = exp(-fabs(x));
-  *sig = (x >= 0.0 ? 1.0 : e) / (1.0 + e);
-  const double l = log1p(e);
-  *sp = x > 0.0 ? x + l : l;
-}
+// sigmoid and softplus of the logistic losses: fp64math.hpp.
 
 // Per-unit validity: a unit (sample, triple, centre) with any id outside its
 // table is skipped entirely and raises the sticky error flag.
@@ -264,8 +248,10 @@ __global__ __launch_bounds__(BLOCK) void k_ctr_grad(const float* __restrict__ W,
     sq = group_sum<L>(sq);
     const double z = 0.5 * (ss - sq);
     const double y = (double)label[b];
-    const double a = sigmoid_d(z) - y;
-    if (gl == 0) lsum += softplus_d(z) - y * z;
+    double sig, sp;
+    sigmoid_softplus(z, &sig, &sp);
+    const double a = sig - y;
+    if (gl == 0) lsum += sp - y * z;
     for (int f0 = 0; f0 < F; f0 += L) {
       const int nf = F - f0 < L ? F - f0 : L;
       const int64_t my_key = gl < nf ? keys[b * F + f0 + gl] : 0;
@@ -398,8 +384,10 @@ __global__ __launch_bounds__(BLOCK) void k_kge_grad(const float* __restrict__ W,
       part -= (double)sIf[i] * (double)rIf[i] * (double)oRf[i];
     }
     const double phi = group_sum<WAVE>(part);
-    double c = -sigmoid_d(-phi);
-    if (lane == 0) lsum += softplus_d(-phi);
+    double c, sp0;
+    sigmoid_softplus(-phi, &c, &sp0);
+    c = -c;
+    if (lane == 0) lsum += sp0;
 #pragma unroll
     for (int i = 0; i < KPL; ++i) {
       gsR[i * BLOCK] = c * fR[i];
