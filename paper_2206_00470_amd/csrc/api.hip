@@ -238,7 +238,7 @@ RadixPlan radix_plan(int64_t num_keys) {
   int bits = 0;
   while (bits < 32 && (uint64_t(1) << bits) <= uint64_t(num_keys)) ++bits;
   RadixPlan p{};
-  p.passes = (bits + 7) / 8;
+  p.passes = (bits + 8) / 9;   // digits of at most 9 bits
   if (p.passes < 1) p.passes = 1;
   const int per = (bits + p.passes - 1) / p.passes;
   for (int i = 0; i < p.passes; ++i) {
@@ -514,7 +514,8 @@ ps_status launch_segreduce(ps_store* s, const SortBufs& b, const uint32_t* ks, S
   });
 }
 
-ps_status launch_finalize(ps_store* s, const SortBufs& b, const uint32_t* ks, int64_t n, hipStream_t st) {
+ps_status launch_finalize(ps_store* s, const SortBufs& b, const uint32_t* ks, int64_t n, hipStream_t st,
+                          LossTotal lt = LossTotal{nullptr, 0, nullptr}) {
   RowShape shape;
   if (!row_shape(s->dim, true, &shape)) return fail(PS_ERR_UNSUPPORTED, "dim %d not supported", s->dim);
   SegView sv{ks, b.seg_off, b.chunk_start, b.chunk_seg, b.hdr};
@@ -532,13 +533,13 @@ ps_status launch_finalize(ps_store* s, const SortBufs& b, const uint32_t* ks, in
     if (s->bf16)
       hipLaunchKernelGGL((k_seg_finalize<L, NV, VW, false, bf16_t>), dim3(fgrid), dim3(BLOCK), lds, st, sv,
                          reinterpret_cast<bf16_t*>(s->W), s->G, s->ld, s->gld, s->dim, s->lr, s->eps, b.partial,
-                         b.fold, b.split_list);
+                         b.fold, b.split_list, lt);
     else if (s->rowwise)
       hipLaunchKernelGGL((k_seg_finalize<L, NV, VW, true, float>), dim3(fgrid), dim3(BLOCK), lds, st, sv, s->W, s->G,
-                         s->ld, s->gld, s->dim, s->lr, s->eps, b.partial, b.fold, b.split_list);
+                         s->ld, s->gld, s->dim, s->lr, s->eps, b.partial, b.fold, b.split_list, lt);
     else
       hipLaunchKernelGGL((k_seg_finalize<L, NV, VW, false, float>), dim3(fgrid), dim3(BLOCK), lds, st, sv, s->W, s->G,
-                         s->ld, s->gld, s->dim, s->lr, s->eps, b.partial, b.fold, b.split_list);
+                         s->ld, s->gld, s->dim, s->lr, s->eps, b.partial, b.fold, b.split_list, lt);
     LAUNCHED(k_seg_finalize);
     return PS_OK;
   });
@@ -546,10 +547,11 @@ ps_status launch_finalize(ps_store* s, const SortBufs& b, const uint32_t* ks, in
 
 template <class Src>
 ps_status run_reduce(ps_store* s, const SortBufs& b, const uint32_t* ks, Src src, int64_t n,
-                     std::initializer_list<int> parts, hipStream_t st) {
+                     std::initializer_list<int> parts, hipStream_t st,
+                     LossTotal lt = LossTotal{nullptr, 0, nullptr}) {
   for (int part : parts)
     if (ps_status r = launch_segreduce(s, b, ks, src, n, part, st)) return r;
-  return launch_finalize(s, b, ks, n, st);
+  return launch_finalize(s, b, ks, n, st, lt);
 }
 
 
@@ -635,15 +637,11 @@ ps_status mf_apply(ps_store* s, int64_t B, float lambda, double* loss, Plan& p, 
                          PART_LOWER, st, PS_KERNEL_MF_ROWMERGE, kRowMergeGrid);
   if (r) return r;
   if (rows_done) HIP_TRY(hipEventRecord(rows_done, st));
-  if (loss) {
-    RowShape shape;
-    row_shape(s->dim, true, &shape);
-    hipLaunchKernelGGL(k_sum_loss, dim3(1), dim3(BLOCK), 0, st, p.loss_part, reduce_grid(n, shape.L, kRowMergeGrid),
-                       loss);
-    LAUNCHED(k_sum_loss);
-  }
   if (ps_status r = launch_segreduce(s, p.sb, ks, SrcSorted{p.grads, s->dim}, n, PART_UPPER, st)) return r;
-  return launch_finalize(s, p.sb, ks, n, st);
+  // the finalize pass also totals the row-key merge's loss partials
+  RowShape shape;
+  row_shape(s->dim, true, &shape);
+  return launch_finalize(s, p.sb, ks, n, st, LossTotal{p.loss_part, reduce_grid(n, shape.L, kRowMergeGrid), loss});
 }
 
 ps_status zero_loss(double* loss, hipStream_t st) {
@@ -1339,12 +1337,9 @@ static ps_status step_kge_impl(ps_store* s, const int32_t* head, const int32_t* 
   else if (cdim <= 128) r = launch(k_kge_grad<2>);
   else r = launch(k_kge_grad<4>);   // cdim <= 256: the store holds rows of at most 512 floats
   if (r) return r;
-  if (loss) {
-    hipLaunchKernelGGL(k_sum_loss, dim3(1), dim3(BLOCK), 0, st, p.loss_part, grid, loss);
-    LAUNCHED(k_sum_loss);
-  }
   if (ps_status r = join_aux(s, st)) return r;
-  return run_reduce(s, p.sb, ks, SrcKGE{perm, p.mat, p.base, p.coef, per, n_head_neg, s->dim}, n, {PART_ALL}, st);
+  return run_reduce(s, p.sb, ks, SrcKGE{perm, p.mat, p.base, p.coef, per, n_head_neg, s->dim}, n, {PART_ALL}, st,
+                    LossTotal{p.loss_part, grid, loss});
 }
 
 static ps_status step_sgns_impl(ps_store* s, const int32_t* centre, const int32_t* ctx, const int32_t* neg, int64_t B,
@@ -1384,25 +1379,22 @@ static ps_status step_sgns_impl(ps_store* s, const int32_t* centre, const int32_
   if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, s->aux,
                                  (uint32_t)out_key_offset))
     return r;
+  int64_t grid = 0;   // loss partials of the gradient kernel
   ps_status r = with_sgns_shape(s->dim, s->ld, [&]<int L, int NV, int VW>() -> ps_status {
-    const int64_t grid = small_grid(B, BLOCK / L, LOSS_GRID);
+    grid = small_grid(B, BLOCK / L, LOSS_GRID);
     {
       Timed t(s, PS_KERNEL_TASKGRAD, st);
       hipLaunchKernelGGL((k_sgns_grad<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->ld, s->dim, centre, ctx, neg,
                          B, slots, n_neg, out_key_offset, p.ok, p.mat, p.coef, p.loss_part);
     }
     LAUNCHED(k_sgns_grad);
-    if (loss) {
-      hipLaunchKernelGGL(k_sum_loss, dim3(1), dim3(BLOCK), 0, st, p.loss_part, grid, loss);
-      LAUNCHED(k_sum_loss);
-    }
     return PS_OK;
   });
   if (r) return r;
   if (ps_status r = join_aux(s, st)) return r;
   // output rows first: their gradients read the input rows, which are updated second
   SrcSGNS src{perm, p.mat, p.coef, centre, s->W, s->ld, (int)per, s->dim};
-  return run_reduce(s, p.sb, ks, src, n, {PART_UPPER, PART_LOWER}, st);
+  return run_reduce(s, p.sb, ks, src, n, {PART_UPPER, PART_LOWER}, st, LossTotal{p.loss_part, grid, loss});
 }
 
 static ps_status step_ctr_impl(ps_store* s, const int64_t* keys, const float* label, int64_t B, int32_t F, double* loss,
@@ -1434,22 +1426,19 @@ static ps_status step_ctr_impl(ps_store* s, const int64_t* keys, const float* la
   if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st)) return r;
   RowShape shape;
   row_shape(s->dim, true, &shape);
+  int64_t grid = 0;   // loss partials of the gradient kernel
   ps_status r = with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
-    const int64_t grid = small_grid(B, BLOCK / L, LOSS_GRID);
+    grid = small_grid(B, BLOCK / L, LOSS_GRID);
     {
       Timed t(s, PS_KERNEL_TASKGRAD, st);
       hipLaunchKernelGGL((k_ctr_grad<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->ld, s->dim, keys, label, B, F,
                          p.ok, p.sb.rank, p.grads, p.loss_part);
     }
     LAUNCHED(k_ctr_grad);
-    if (loss) {
-      hipLaunchKernelGGL(k_sum_loss, dim3(1), dim3(BLOCK), 0, st, p.loss_part, grid, loss);
-      LAUNCHED(k_sum_loss);
-    }
     return PS_OK;
   });
   if (r) return r;
-  return run_reduce(s, p.sb, ks, SrcSorted{p.grads, s->dim}, n, {PART_ALL}, st);
+  return run_reduce(s, p.sb, ks, SrcSorted{p.grads, s->dim}, n, {PART_ALL}, st, LossTotal{p.loss_part, grid, loss});
 }
 
 // ---------------------------------------------------------------- public steps
@@ -1517,7 +1506,7 @@ ps_status ps_step_mf_async(ps_store* s, const int32_t* row, const int32_t* col, 
   });
   if (r) return r;
   if (loss) {
-    hipLaunchKernelGGL(k_sum_loss, dim3(1), dim3(BLOCK), 0, st, p.loss_part, grid, loss);
+    hipLaunchKernelGGL(k_sum_loss, dim3(1), dim3(BLOCK), 0, st, LossTotal{p.loss_part, grid, loss});
     LAUNCHED(k_sum_loss);
   }
   return launch_push_async(s, KeysMF{row, col, col_key_offset, s->num_keys}, p.grads, 2 * B, st);
@@ -1690,7 +1679,7 @@ ps_status ps_step_ctr_wd(ps_store* s, const int64_t* keys, const float* label, i
                      s->ld, E, keys, F, label, p.base.ok, B, L > 0 ? 1 : 0, p.dlogit, p.dA, p.base.loss_part);
   LAUNCHED(k_wd_head);
   if (loss) {
-    hipLaunchKernelGGL(k_sum_loss, dim3(1), dim3(BLOCK), 0, st, p.base.loss_part, head_grid, loss);
+    hipLaunchKernelGGL(k_sum_loss, dim3(1), dim3(BLOCK), 0, st, LossTotal{p.base.loss_part, head_grid, loss});
     LAUNCHED(k_sum_loss);
   }
   // output layer gradients

@@ -13,8 +13,9 @@ namespace adapm {
 constexpr int WAVE = 64;                 // CDNA wavefront width
 constexpr int BLOCK = 256;               // threads per workgroup for every kernel here
 constexpr int WAVES_PER_BLOCK = BLOCK / WAVE;
-constexpr int MAX_PASSES = 4;            // 32-bit keys, at most 8 bits per pass
-constexpr int MAX_BINS = 256;
+constexpr int MAX_PASSES = 4;            // 32-bit keys, at most 9 bits per pass
+constexpr int MAX_BINS = 512;            // digits of up to 9 bits
+constexpr int DIG_PER_THREAD = MAX_BINS / 256;   // digits per thread in the per-digit loops of a 256-thread block
 constexpr int GH_COPIES = 32;             // copies of the whole-array histograms (spreads the atomics)
 constexpr int CHUNK = 32;               // cut length of long segments (chunks hold < 2*CHUNK occurrences)
 constexpr int NUM_XCD = 8;               // MI355X: 8 accelerator dies, each with its own L2
@@ -121,6 +122,33 @@ __device__ __forceinline__ double block_sum_double(double v, double* smem) {
   }
   __syncthreads();
   return r;
+}
+
+// ------------------------------------------------------------------ loss totals
+// The loss kernels leave one fp64 value per workgroup in part[]; a kernel
+// that runs after them on the same stream (the merge's finalize pass) adds
+// part[0 .. n) in index order with one workgroup: eight independent loads
+// per thread and round, then the fixed block tree, so the total does not
+// depend on the launch or on timing.
+struct LossTotal {
+  const double* part;
+  int64_t n;
+  double* out;   // NULL: no total wanted
+};
+
+__device__ __forceinline__ void sum_loss_parts(const LossTotal& lt, double* smem) {
+  double s = 0.0;
+  int64_t i = threadIdx.x;
+  for (; i + 7 * BLOCK < lt.n; i += 8 * BLOCK) {
+    double x[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) x[k] = lt.part[i + k * BLOCK];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) s += x[k];
+  }
+  for (; i < lt.n; i += BLOCK) s += lt.part[i];
+  s = block_sum_double(s, smem);
+  if (threadIdx.x == 0) *lt.out = s;
 }
 
 // ------------------------------------------------------------------ AdaGrad

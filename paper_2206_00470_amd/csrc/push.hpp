@@ -409,11 +409,14 @@ __global__ __launch_bounds__(BLOCK) void k_seg_finalize(SegView sv, VT* __restri
                                                         int64_t ld, int64_t gld, int dim, float lr, float eps,
                                                         const double* __restrict__ partial,
                                                         const double* __restrict__ fold,
-                                                        const int32_t* __restrict__ split_list) {
+                                                        const int32_t* __restrict__ split_list, LossTotal lt) {
   constexpr int GPB = BLOCK / L;
   extern __shared__ double lds[];   // [GPB][dim]
   __shared__ double sm[WAVES_PER_BLOCK];
   __shared__ float den_sh;
+  // the step's loss, from the partials of its loss kernel (already complete:
+  // that kernel ran earlier on this stream)
+  if (lt.out && blockIdx.x == 0) sum_loss_parts(lt, sm);
   const int64_t nsplit = sv.hdr->num_split;
   for (int64_t e = blockIdx.x; e < nsplit; e += gridDim.x) {
     const int32_t u = split_list[e];

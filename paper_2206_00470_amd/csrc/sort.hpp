@@ -108,17 +108,22 @@ __global__ __launch_bounds__(BLOCK) void k_radix_scan(uint32_t* __restrict__ cou
   __shared__ uint32_t smem[WAVES_PER_BLOCK + 1];
   __shared__ double dsm[WAVES_PER_BLOCK];
   const int d = blockIdx.x;
-  // digit base: thread i sums digit i's count over the copies (independent
+  // digit base: thread i sums digits i + BLOCK q over the copies (independent
   // loads), then the block adds the digits below d (exact in double: the sum
   // is below 2^31)
-  static_assert(BLOCK == MAX_BINS, "one thread per digit");
-  uint32_t x[GH_COPIES];
+  static_assert(BLOCK * DIG_PER_THREAD == MAX_BINS, "every digit has a thread");
+  double part = 0.0;
 #pragma unroll
-  for (int c = 0; c < GH_COPIES; ++c) x[c] = ghist_pass[c * MAX_BINS + threadIdx.x];
-  uint32_t tot = 0;
+  for (int q = 0; q < DIG_PER_THREAD; ++q) {
+    const int dd = threadIdx.x + BLOCK * q;
+    uint32_t x[GH_COPIES];
 #pragma unroll
-  for (int c = 0; c < GH_COPIES; ++c) tot += x[c];
-  double part = (int)threadIdx.x < d ? (double)tot : 0.0;
+    for (int c = 0; c < GH_COPIES; ++c) x[c] = ghist_pass[c * MAX_BINS + dd];
+    uint32_t tot = 0;
+#pragma unroll
+    for (int c = 0; c < GH_COPIES; ++c) tot += x[c];
+    part += dd < d ? (double)tot : 0.0;
+  }
   double b = block_sum_double(part, dsm);
   __shared__ uint32_t sbase;
   if (threadIdx.x == 0) sbase = (uint32_t)b;
@@ -144,7 +149,7 @@ __global__ __launch_bounds__(BLOCK) void k_radix_scatter(const uint32_t* __restr
                                                          int bits, const uint32_t* __restrict__ offs, int tiles,
                                                          uint32_t* __restrict__ kout, uint32_t* __restrict__ vout,
                                                          uint32_t* __restrict__ rank) {
-  static_assert(BLOCK == MAX_BINS, "one thread per digit in the tile scan");
+  static_assert(BLOCK * DIG_PER_THREAD == MAX_BINS, "every digit has a thread in the tile scan");
   __shared__ uint32_t wc[WAVES_PER_BLOCK][MAX_BINS];
   __shared__ uint32_t toff[MAX_BINS];
   __shared__ uint32_t dstart[MAX_BINS];
@@ -193,19 +198,31 @@ __global__ __launch_bounds__(BLOCK) void k_radix_scatter(const uint32_t* __restr
   }
   __syncthreads();
   // per digit: offsets of the 4 waves inside the tile's run, and the run's
-  // start within the tile (exclusive scan over digits)
-  uint32_t tot = 0;
+  // start within the tile (exclusive scan over digits; thread i owns the
+  // DIG_PER_THREAD consecutive digits from i * DIG_PER_THREAD)
   {
-    const int d = threadIdx.x;   // BLOCK == MAX_BINS
-    if (d < bins) {
-      for (int ww = 0; ww < WAVES_PER_BLOCK; ++ww) {
-        const uint32_t t = wc[ww][d];
-        wc[ww][d] = tot;
-        tot += t;
+    uint32_t tot[DIG_PER_THREAD];
+    uint32_t mine = 0;
+#pragma unroll
+    for (int q = 0; q < DIG_PER_THREAD; ++q) {
+      const int d = threadIdx.x * DIG_PER_THREAD + q;
+      tot[q] = 0;
+      if (d < bins) {
+        for (int ww = 0; ww < WAVES_PER_BLOCK; ++ww) {
+          const uint32_t t = wc[ww][d];
+          wc[ww][d] = tot[q];
+          tot[q] += t;
+        }
       }
+      mine += tot[q];
     }
     uint32_t all;
-    dstart[d] = block_exclusive_scan(d < bins ? tot : 0u, scan_smem, &all);
+    uint32_t run = block_exclusive_scan(mine, scan_smem, &all);
+#pragma unroll
+    for (int q = 0; q < DIG_PER_THREAD; ++q) {
+      dstart[threadIdx.x * DIG_PER_THREAD + q] = run;
+      run += tot[q];
+    }
   }
   __syncthreads();
   // stage the tile in LDS in digit order ...

@@ -9,22 +9,9 @@
 namespace adapm {
 
 // Sum loss partials in index order (deterministic), then write the total.
-__global__ __launch_bounds__(BLOCK) void k_sum_loss(const double* __restrict__ part, int64_t n,
-                                                    double* __restrict__ out) {
+__global__ __launch_bounds__(BLOCK) void k_sum_loss(LossTotal lt) {
   __shared__ double sm[WAVES_PER_BLOCK];
-  double s = 0.0;
-  int64_t i = threadIdx.x;
-  // eight independent loads per round, added in index order
-  for (; i + 7 * BLOCK < n; i += 8 * BLOCK) {
-    double x[8];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) x[k] = part[i + k * BLOCK];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) s += x[k];
-  }
-  for (; i < n; i += BLOCK) s += part[i];
-  s = block_sum_double(s, sm);
-  if (threadIdx.x == 0) *out = s;
+  sum_loss_parts(lt, sm);
 }
 
 // ------------------------------------------------------------------ MF

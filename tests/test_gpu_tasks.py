@@ -119,7 +119,8 @@ def test_sgns_stream_start_has_absent_slots():
     run_steps("sgns", cfg, [0])
 
 
-@pytest.mark.parametrize("dim,F", [(64, 26), (16, 3), (100, 5), (7, 26), (256, 1)])
+@pytest.mark.parametrize("dim,F", [(64, 26), (16, 3), (100, 5), (7, 26), (256, 1), (64, 32), (64, 33), (8, 64),
+                                   (12, 65), (100, 16), (100, 17)])
 def test_ctr_other_shapes(dim, F):
     from dataclasses import replace
     cfg = replace(small_variant(CTR_33M), dim=dim, n_fields=F)
