@@ -81,9 +81,9 @@ def parse():
     return ap.parse_args()
 
 
-# device code of the sort, merge and task kernels: the counters taken on the
-# MF step stay valid while these files are unchanged
-COUNTER_SOURCES = ("common.hpp", "push.hpp", "sort.hpp", "tasks.hpp")
+# device code of the sort, merge and task kernels and their launches: the
+# committed counters stay valid while these files are unchanged
+COUNTER_SOURCES = ("common.hpp", "fp64math.hpp", "push.hpp", "sort.hpp", "tasks.hpp", "api.hip")
 
 
 def source_hash() -> str:
@@ -96,18 +96,22 @@ def source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def counter_traffic(workload: str, kernel: str):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if
-    it was taken on the current kernel sources (else None)."""
-    path = os.path.join(ROOT, "profiles", f"counters_{workload}.json")
+def counter_summary(name: str):
+    """A committed rocprofv3 counter summary (profiles/counters_<name>.json),
+    if it was taken on the current kernel sources (else None)."""
+    path = os.path.join(ROOT, "profiles", f"counters_{name}.json")
     try:
         with open(path) as f:
             data = json.load(f)
     except (OSError, ValueError):
         return None
-    if data.get("source_hash") != source_hash():
-        return None
-    k = data.get("kernels", {}).get(kernel)
+    return data if data.get("source_hash") == source_hash() else None
+
+
+def counter_traffic(workload: str, kernel: str):
+    """HBM bytes per launch of one kernel from the committed counters."""
+    data = counter_summary(workload)
+    k = (data or {}).get("kernels", {}).get(kernel)
     return None if k is None else k.get("hbm_bytes_per_launch")
 
 
@@ -572,7 +576,9 @@ def main():
     ops = {}
     if args.ops_only:
         ops = measure_ops(args, wb, store, dev, rowwise, unmerged)
-        print(json.dumps({"metric": "push / pull alone (" + cfg.name + ")", "ops": ops}), flush=True)
+        copy = calibrate_copy(dev) if args.calibrate_copy else None
+        print(json.dumps({"metric": "push / pull alone (" + cfg.name + ")", "ops": ops, "copy_calibration": copy}),
+              flush=True)
         store.close()
         return
 
@@ -717,22 +723,7 @@ def main():
     if not args.no_ops:
         ops = measure_ops(args, wb, store, dev, rowwise, unmerged)
 
-    copy = None
-    if args.calibrate_copy:
-        a = torch.empty(1 << 30, dtype=torch.float32, device=dev)
-        b = torch.empty_like(a)
-        a.fill_(1.0)
-        for _ in range(2):
-            b.copy_(a)
-        torch.cuda.synchronize()
-        t1 = time.perf_counter()
-        for _ in range(5):
-            b.copy_(a)
-        torch.cuda.synchronize()
-        tcp = (time.perf_counter() - t1) / 5
-        copy = {"bytes_read": a.numel() * 4, "bytes_written": b.numel() * 4, "ms": round(tcp * 1e3, 4),
-                "GBps": round(2 * a.numel() * 4 / tcp / 1e9, 1)}
-        del a, b
+    copy = calibrate_copy(dev) if args.calibrate_copy else None
 
     cpu = cpu_baseline(args, wb, rowwise)
 
@@ -772,6 +763,28 @@ def main():
     }
     print(json.dumps(line), flush=True)
     store.close()
+
+
+def calibrate_copy(dev):
+    """A 4 GiB device-to-device copy of known size: the reference for the HBM
+    counters, and the copy bandwidth of this part."""
+    import torch
+    a = torch.empty(1 << 30, dtype=torch.float32, device=dev)
+    b = torch.empty_like(a)
+    a.fill_(1.0)
+    for _ in range(2):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for _ in range(5):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    tcp = (time.perf_counter() - t1) / 5
+    out = {"bytes_read": a.numel() * 4, "bytes_written": b.numel() * 4, "ms": round(tcp * 1e3, 4),
+           "GBps": round(2 * a.numel() * 4 / tcp / 1e9, 1)}
+    del a, b
+    torch.cuda.empty_cache()
+    return out
 
 
 def launches_per_step(wb, store, i, loss):
@@ -882,12 +895,15 @@ def measure_ops(args, wb, store, dev, rowwise, unmerged):
     tab = 2.0 * RV + 8.0 if rowwise else 2.0 * RV + 2.0 * R
     push_alg = 8.0 * n + n * R + tab * U
     pull_alg = 8.0 * n + U * RV + n * R
+    oc = counter_summary(args.workload + "_ops") if not (rowwise or unmerged or wb.values == "bf16") else None
+    push_traffic = int(oc["push_hbm_bytes"]) if oc and "push_hbm_bytes" in oc else None
     ops = {
         "push": {"ms": round(tp * 1e3, 4), "rows_per_s": n / tp, "alg_GBps": round(push_alg / tp / 1e9, 1),
                  "frac_of_peak": round(push_alg / tp / 1e9 / HBM_PEAK_GBPS, 4), "occurrences": n, "unique_keys": U,
                  "roofline": {"bound": "hbm", "achieved": round(push_alg / tp / 1e9, 1), "peak": HBM_PEAK_GBPS,
                               "unit": "GB/s", "frac": round(push_alg / tp / 1e9 / HBM_PEAK_GBPS, 4),
-                              "alg_bytes": int(push_alg),
+                              "alg_bytes": int(push_alg), "traffic": push_traffic,
+                              "traffic_over_alg": round(push_traffic / push_alg, 3) if push_traffic else None,
                               "what": "8 n (keys) + n R (gradient rows) + per distinct key its value and "
                                       "accumulator rows read and written, over the whole ps_push (sort, "
                                       "segments, merge, finalize)"}},
