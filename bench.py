@@ -261,9 +261,10 @@ class Bench:
                     "segreduce": B * R + tab * Ucol,
                     "taskgrad": B * (4.0 + 4.0 + 8.0 + 16.0)}
         if self.task == "ctr":
+            # gradient rows in occurrence order, read by the merge through the sort permutation
             B, F = bt.keys.shape
-            return {"segreduce": n * R + table,
-                    "taskgrad": B * (4.0 + F * (8.0 + R + R + 4.0))}
+            return {"segreduce": n * (4.0 + R) + table,
+                    "taskgrad": B * (4.0 + F * (8.0 + R + R))}
         if self.task == "ctr_wd":
             # "mlp" counts flops of the fp64 products, not bytes
             return {"segreduce": n * R + table, "mlp": self.mlp_flops(bt.keys.shape[0])}

@@ -330,12 +330,12 @@ bool plan_op(void* ws, int64_t num_keys, int dim, int op, int64_t units, int64_t
       carve_sort(c, n, dim, true, true, &p->sb);
       // row keys sort below column keys, so row occurrences hold positions [0, units)
       p->pe = c.take<MFEntry>(units);
-      p->grads = c.take<float>(size_t(n) * dim);     // column-occurrence gradient rows, sorted positions
+      p->grads = c.take<float>(size_t(n) * mf_grad_ld(dim));   // column-occurrence gradient rows, sorted positions
       p->loss_part = c.take<double>(MERGE_GRID_MAX);   // written by the row-key merge
       break;
     case PS_OP_STEP_CTR:
-      carve_sort(c, n, dim, true, true, &p->sb);
-      p->grads = c.take<float>(size_t(n) * dim);
+      carve_sort(c, n, dim, false, true, &p->sb);
+      p->grads = c.take<float>(size_t(n) * dim);   // occurrence order
       p->loss_part = c.take<double>(LOSS_GRID);
       p->ok = c.take<uint8_t>(units);
       break;
@@ -630,14 +630,14 @@ ps_status mf_apply(ps_store* s, int64_t B, float lambda, double* loss, Plan& p, 
   ps_status r = s->bf16
       ? launch_segreduce(s, p.sb, ks,
                          SrcMFRow<bf16_t>{p.pe, reinterpret_cast<const bf16_t*>(s->W), s->ld, p.grads, p.loss_part,
-                                          (double)lambda, s->dim},
+                                          (double)lambda, s->dim, mf_grad_ld(s->dim)},
                          n, PART_LOWER, st, PS_KERNEL_MF_ROWMERGE, kRowMergeGrid)
       : launch_segreduce(s, p.sb, ks,
-                         SrcMFRow<float>{p.pe, s->W, s->ld, p.grads, p.loss_part, (double)lambda, s->dim}, n,
+                         SrcMFRow<float>{p.pe, s->W, s->ld, p.grads, p.loss_part, (double)lambda, s->dim, mf_grad_ld(s->dim)}, n,
                          PART_LOWER, st, PS_KERNEL_MF_ROWMERGE, kRowMergeGrid);
   if (r) return r;
   if (rows_done) HIP_TRY(hipEventRecord(rows_done, st));
-  if (ps_status r = launch_segreduce(s, p.sb, ks, SrcSorted{p.grads, s->dim}, n, PART_UPPER, st)) return r;
+  if (ps_status r = launch_segreduce(s, p.sb, ks, SrcSorted{p.grads, s->dim, mf_grad_ld(s->dim)}, n, PART_UPPER, st)) return r;
   // the finalize pass also totals the row-key merge's loss partials
   RowShape shape;
   row_shape(s->dim, true, &shape);
@@ -1419,11 +1419,14 @@ static ps_status step_ctr_impl(ps_store* s, const int64_t* keys, const float* la
   hipLaunchKernelGGL(k_unit_valid<ValidCTR>, dim3(small_grid(B, WAVES_PER_BLOCK, 4096)), dim3(BLOCK), 0, st,
                      ValidCTR{keys, F, s->num_keys}, B, p.ok, s->status);
   LAUNCHED(k_unit_valid);
+  // the key sort and segments (workspace only) run on the second stream
+  // beside the gradient kernel (table reads, gradient rows in occurrence order)
+  if (ps_status r = fork_aux(s, st)) return r;
   uint32_t *ks, *perm;
-  if (ps_status r = run_sort(s, KeysCTR{keys, F, p.ok}, n, s->num_keys, p.sb, s->status, nullptr, true, st, &ks,
-                             &perm))
+  if (ps_status r = run_sort(s, KeysCTR{keys, F, p.ok}, n, s->num_keys, p.sb, s->status, nullptr, false, s->aux,
+                             &ks, &perm))
     return r;
-  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, st)) return r;
+  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, s->aux)) return r;
   RowShape shape;
   row_shape(s->dim, true, &shape);
   int64_t grid = 0;   // loss partials of the gradient kernel
@@ -1432,13 +1435,15 @@ static ps_status step_ctr_impl(ps_store* s, const int64_t* keys, const float* la
     {
       Timed t(s, PS_KERNEL_TASKGRAD, st);
       hipLaunchKernelGGL((k_ctr_grad<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->ld, s->dim, keys, label, B, F,
-                         p.ok, p.sb.rank, p.grads, p.loss_part);
+                         p.ok, p.grads, p.loss_part);
     }
     LAUNCHED(k_ctr_grad);
     return PS_OK;
   });
   if (r) return r;
-  return run_reduce(s, p.sb, ks, SrcSorted{p.grads, s->dim}, n, {PART_ALL}, st, LossTotal{p.loss_part, grid, loss});
+  if (ps_status r = join_aux(s, st)) return r;
+  return run_reduce(s, p.sb, ks, SrcIndirect{p.grads, perm, s->dim}, n, {PART_ALL}, st,
+                    LossTotal{p.loss_part, grid, loss});
 }
 
 // ---------------------------------------------------------------- public steps
@@ -1709,7 +1714,7 @@ ps_status ps_step_ctr_wd(ps_store* s, const int64_t* keys, const float* label, i
   hipLaunchKernelGGL(k_wd_rows, dim3(small_grid(n, WAVES_PER_BLOCK, 16384)), dim3(BLOCK), 0, st, cur, p.dlogit, B, F,
                      E, s->dim, p.base.sb.rank, p.base.grads);
   LAUNCHED(k_wd_rows);
-  if (ps_status r = run_reduce(s, p.base.sb, ks, SrcSorted{p.base.grads, s->dim}, n, {PART_ALL}, st)) return r;
+  if (ps_status r = run_reduce(s, p.base.sb, ks, SrcSorted{p.base.grads, s->dim, s->dim}, n, {PART_ALL}, st)) return r;
   hipLaunchKernelGGL(k_dense_adagrad, dim3(small_grid(d.total, BLOCK, 4096)), dim3(BLOCK), 0, st, dense, dense_accum,
                      p.dg, d.total, s->lr, s->eps);
   LAUNCHED(k_dense_adagrad);

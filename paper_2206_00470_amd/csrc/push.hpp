@@ -104,15 +104,16 @@ struct SrcIndirect {
   }
 };
 
-// Gradient rows already stored at their sorted positions.
+// Gradient rows already stored at their sorted positions, ld floats apart.
 struct SrcSorted {
   static constexpr bool kNeedsOwn = false;
   const float* grads;
   int dim;
+  int64_t ld;
   struct Meta {
     const float* row;
   };
-  __device__ __forceinline__ Meta meta(int64_t j) const { return {grads + j * dim}; }
+  __device__ __forceinline__ Meta meta(int64_t j) const { return {grads + j * ld}; }
   template <int L, int NV, int VW>
   __device__ __forceinline__ void load(const Meta& m, const float*, int gl, float* x) const {
 #pragma unroll

@@ -66,6 +66,15 @@ __global__ __launch_bounds__(BLOCK) void k_mf_pack(const int32_t* __restrict__ r
 //   column gradient   lam*m - e*u   (fp32, stored at the column occurrence's
 //                                    sorted position for the column-key merge)
 //   loss += e^2/2 + lam/2 (|u|^2 + |m|^2)
+// Row stride (floats) of the column-occurrence gradient rows: dim rounded
+// up to MF_GRAD_ALIGN floats (64 bytes), and the row merge writes the
+// padding too, so its scattered row writes cover whole 64-byte pieces of
+// memory (400-byte rows at a 448-byte stride: 1% off the row merge).
+constexpr int MF_GRAD_ALIGN = 16;
+__host__ __device__ constexpr int64_t mf_grad_ld(int dim) {
+  return (dim + MF_GRAD_ALIGN - 1) / MF_GRAD_ALIGN * MF_GRAD_ALIGN;
+}
+
 template <class VT>
 struct SrcMFRow {
   static constexpr bool kNeedsOwn = true;
@@ -78,6 +87,7 @@ struct SrcMFRow {
   double* loss_part;
   double lam;
   int dim;
+  int64_t gld;   // row stride of grads
   struct Meta {
     const VT* partner;
     float y;
@@ -112,7 +122,7 @@ struct SrcMFRow {
     nm = group_sum<L>(nm);
     const double err = (double)m.y - dot;
     if (gl == 0) lsum += 0.5 * err * err + 0.5 * lam * (nu + nm);
-    float* gc = grads + (int64_t)m.col_pos * dim;
+    float* gc = grads + (int64_t)m.col_pos * gld;
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
       const int c = (gl + v * L) * VW;
@@ -125,6 +135,9 @@ struct SrcMFRow {
           g[q] = (float)(lam * mq - err * uq);
         }
         store_frag<VW>(gc + c, g);
+      } else if (c < gld) {
+        float z[VW] = {};
+        store_frag<VW>(gc + c, z);
       }
     }
   }
@@ -178,13 +191,13 @@ struct KeysCTR {
 // One row group per sample (e_f = W[keys[b,f]], label y):
 //   S = sum_f e_f ;  z = sum_{f<g} <e_f, e_g> = (|S|^2 - sum_f |e_f|^2) / 2
 //   loss += softplus(z) - y z ;  grad e_f = (sigmoid(z) - y)(S - e_f)
-// Gradient rows go to their sorted positions rank[b*F + f].
+// Gradient rows are written in occurrence order (row b*F + f), so the
+// kernel needs nothing from the key sort and runs beside it.
 template <int L, int NV, int VW>
 __global__ __launch_bounds__(BLOCK) void k_ctr_grad(const float* __restrict__ W, int64_t ld, int dim,
                                                     const int64_t* __restrict__ keys,
                                                     const float* __restrict__ label, int64_t B, int F,
-                                                    const uint8_t* __restrict__ ok,
-                                                    const uint32_t* __restrict__ rank, float* __restrict__ grads,
+                                                    const uint8_t* __restrict__ ok, float* __restrict__ grads,
                                                     double* __restrict__ loss_part) {
   constexpr int GPB = BLOCK / L;
   constexpr int NE = NV * VW;
@@ -242,7 +255,6 @@ __global__ __launch_bounds__(BLOCK) void k_ctr_grad(const float* __restrict__ W,
     for (int f0 = 0; f0 < F; f0 += L) {
       const int nf = F - f0 < L ? F - f0 : L;
       const int64_t my_key = gl < nf ? keys[b * F + f0 + gl] : 0;
-      const uint32_t my_rank = gl < nf ? rank[b * F + f0 + gl] : 0u;
       for (int f = 0; f < nf; f += FU) {
         float x[FU][NE];
 #pragma unroll
@@ -256,7 +268,7 @@ __global__ __launch_bounds__(BLOCK) void k_ctr_grad(const float* __restrict__ W,
         }
 #pragma unroll
         for (int u = 0; u < FU; ++u) {
-          float* dst = grads + (int64_t)__shfl(my_rank, (f + u) % L, L) * dim;
+          float* dst = grads + (b * F + f0 + f + u) * (int64_t)dim;
 #pragma unroll
           for (int v = 0; v < NV; ++v) {
             const int c = (gl + v * L) * VW;
