@@ -367,9 +367,14 @@ bool plan_op(void* ws, int64_t num_keys, int dim, int op, int64_t units, int64_t
 }
 
 // ------------------------------------------------------------------ pipeline pieces
+// The sort's header and whole-array histograms, cleared together before
+// each sort (by the sort itself, or by the unit-validity kernel before it).
+int64_t header_words(const SortBufs& b) {
+  return (reinterpret_cast<char*>(b.ghist + MAX_PASSES * GH_COPIES * MAX_BINS) - reinterpret_cast<char*>(b.hdr)) / 4;
+}
+
 void clear_header(const SortBufs& b, hipStream_t st) {
-  const int64_t words = (reinterpret_cast<char*>(b.ghist + MAX_PASSES * GH_COPIES * MAX_BINS) -
-                         reinterpret_cast<char*>(b.hdr)) / 4;
+  const int64_t words = header_words(b);
   hipLaunchKernelGGL(k_zero_words, dim3(ceil_div(words, 4 * BLOCK)), dim3(BLOCK), 0, st,
                      reinterpret_cast<uint32_t*>(b.hdr), words);
 }
@@ -380,11 +385,13 @@ void clear_header(const SortBufs& b, hipStream_t st) {
 template <class KS>
 ps_status run_sort(ps_store* s, KS ks, int64_t n, int64_t num_keys, SortBufs& b, int32_t* err,
                    uint32_t* perm_out, bool want_rank, hipStream_t st, uint32_t** keys_sorted,
-                   uint32_t** perm) {
+                   uint32_t** perm, bool header_cleared = false) {
   const RadixPlan plan = radix_plan(num_keys);
   const int tiles = (int)b.tiles;
-  clear_header(b, st);
-  LAUNCHED(k_zero_words);
+  if (!header_cleared) {
+    clear_header(b, st);
+    LAUNCHED(k_zero_words);
+  }
   return with_items(b.items, [&]<int IT>() -> ps_status {
     hipLaunchKernelGGL((k_keyprep<KS, IT>), dim3(tiles), dim3(BLOCK), 0, st, ks, n, (uint32_t)num_keys, plan, b.k[0],
                        b.counts, tiles, b.ghist, err);
@@ -1326,14 +1333,16 @@ static ps_status step_kge_impl(ps_store* s, const int32_t* head, const int32_t* 
   plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_KGE, B, per, &p);
   if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
   hipLaunchKernelGGL(k_unit_valid<ValidKGE>, dim3(small_grid(B, WAVES_PER_BLOCK, 4096)), dim3(BLOCK), 0, st,
-                     ValidKGE{head, rel, tail, neg, n_neg, rel_key_offset, s->num_keys}, B, p.ok, s->status);
+                     ValidKGE{head, rel, tail, neg, n_neg, rel_key_offset, s->num_keys}, B, p.ok, s->status,
+                     reinterpret_cast<uint32_t*>(p.sb.hdr), header_words(p.sb));
   LAUNCHED(k_unit_valid);
   // the key sort and segments (workspace only) run on the second stream
   // beside the gradient kernel (table reads, per-unit rows)
   if (ps_status r = fork_aux(s, st)) return r;
   uint32_t *ks, *perm;
   KeysKGE kk{head, rel, tail, neg, per, n_neg, rel_key_offset, p.ok};
-  if (ps_status r = run_sort(s, kk, n, s->num_keys, p.sb, s->status, nullptr, false, s->aux, &ks, &perm)) return r;
+  if (ps_status r = run_sort(s, kk, n, s->num_keys, p.sb, s->status, nullptr, false, s->aux, &ks, &perm, true))
+    return r;
   if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, s->aux)) return r;
   const int cdim = s->dim / 2;
   const int64_t grid = small_grid(B, WAVES_PER_BLOCK, LOSS_GRID);
@@ -1380,14 +1389,16 @@ static ps_status step_sgns_impl(ps_store* s, const int32_t* centre, const int32_
   plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_SGNS, B, per, &p);
   if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
   hipLaunchKernelGGL(k_unit_valid<ValidSGNS>, dim3(small_grid(B, WAVES_PER_BLOCK, 4096)), dim3(BLOCK), 0, st,
-                     ValidSGNS{centre, ctx, neg, slots, n_neg, out_key_offset, s->num_keys}, B, p.ok, s->status);
+                     ValidSGNS{centre, ctx, neg, slots, n_neg, out_key_offset, s->num_keys}, B, p.ok, s->status,
+                     reinterpret_cast<uint32_t*>(p.sb.hdr), header_words(p.sb));
   LAUNCHED(k_unit_valid);
   // the key sort and segments (workspace only) run on the second stream
   // beside the gradient kernel (table reads, per-unit rows)
   if (ps_status r = fork_aux(s, st)) return r;
   uint32_t *ks, *perm;
   KeysSGNS kk{centre, ctx, neg, (int)per, slots, n_neg, out_key_offset, p.ok};
-  if (ps_status r = run_sort(s, kk, n, s->num_keys, p.sb, s->status, nullptr, false, s->aux, &ks, &perm)) return r;
+  if (ps_status r = run_sort(s, kk, n, s->num_keys, p.sb, s->status, nullptr, false, s->aux, &ks, &perm, true))
+    return r;
   if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, s->aux,
                                  (uint32_t)out_key_offset))
     return r;
@@ -1429,14 +1440,15 @@ static ps_status step_ctr_impl(ps_store* s, const int64_t* keys, const float* la
   plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_CTR, B, F, &p);
   if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
   hipLaunchKernelGGL(k_unit_valid<ValidCTR>, dim3(small_grid(B, WAVES_PER_BLOCK, 4096)), dim3(BLOCK), 0, st,
-                     ValidCTR{keys, F, s->num_keys}, B, p.ok, s->status);
+                     ValidCTR{keys, F, s->num_keys}, B, p.ok, s->status, reinterpret_cast<uint32_t*>(p.sb.hdr),
+                     header_words(p.sb));
   LAUNCHED(k_unit_valid);
   // the key sort and segments (workspace only) run on the second stream
   // beside the gradient kernel (table reads, gradient rows in occurrence order)
   if (ps_status r = fork_aux(s, st)) return r;
   uint32_t *ks, *perm;
   if (ps_status r = run_sort(s, KeysCTR{keys, F, p.ok}, n, s->num_keys, p.sb, s->status, nullptr, false, s->aux,
-                             &ks, &perm))
+                             &ks, &perm, true))
     return r;
   if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, s->aux)) return r;
   RowShape shape;
@@ -1659,13 +1671,14 @@ ps_status ps_step_ctr_wd(ps_store* s, const int64_t* keys, const float* label, i
     keys = tk;
   }
   hipLaunchKernelGGL(k_unit_valid<ValidCTR>, dim3(small_grid(B, WAVES_PER_BLOCK, 4096)), dim3(BLOCK), 0, st,
-                     ValidCTR{keys, F, s->num_keys}, B, p.base.ok, s->status);
+                     ValidCTR{keys, F, s->num_keys}, B, p.base.ok, s->status,
+                     reinterpret_cast<uint32_t*>(p.base.sb.hdr), header_words(p.base.sb));
   LAUNCHED(k_unit_valid);
   // the key sort and segments run beside the MLP on the store's second stream
   if (ps_status r = fork_aux(s, st)) return r;
   uint32_t *ks, *perm;
   if (ps_status r = run_sort(s, KeysCTR{keys, F, p.base.ok}, n, s->num_keys, p.base.sb, s->status, nullptr, true,
-                             s->aux, &ks, &perm))
+                             s->aux, &ks, &perm, true))
     return r;
   if (ps_status r = run_segments(p.base.sb, ks, n, s->num_keys, p.base.sb.seg_off, nullptr, s->aux)) return r;
   // inputs

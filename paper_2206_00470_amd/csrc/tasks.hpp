@@ -150,9 +150,14 @@ struct SrcMFRow {
 // table is skipped entirely and raises the sticky error flag.
 template <class V>
 // One wavefront per unit: its lanes check the unit's ids (V::ids, V::id_ok)
-// side by side.
+// side by side.  The grid also zeroes clear[0, clear_words): the key sort's
+// header and histograms, which the sort that follows would otherwise clear
+// with a launch of its own.
 __global__ __launch_bounds__(BLOCK) void k_unit_valid(V v, int64_t B, uint8_t* __restrict__ ok,
-                                                      int32_t* __restrict__ err) {
+                                                      int32_t* __restrict__ err, uint32_t* __restrict__ clear,
+                                                      int64_t clear_words) {
+  for (int64_t i = (int64_t)blockIdx.x * BLOCK + threadIdx.x; i < clear_words; i += (int64_t)gridDim.x * BLOCK)
+    clear[i] = 0u;
   const int lane = lane_id();
   int bad = 0;
   for (int64_t b = (int64_t)blockIdx.x * WAVES_PER_BLOCK + threadIdx.x / WAVE; b < B;
