@@ -616,14 +616,13 @@ def main():
         assert store.error() == 0
         return secs, {name: store.read_timing(k) for name, k in KID.items()}
 
-    # warm-up steps, every big kernel timed: they pick the dominant kernel
-    # (the first step runs on cold caches and page tables, so with two or more
-    # warm-up steps the choice is made on the later ones)
-    skip = 1 if args.warmup >= 2 else 0
-    if skip:
-        run_steps(0, skip, 0)
-    _, kt_warm = run_steps(skip, args.warmup - skip, _lib.PS_TIMING_ALL)
-    dom = max(names, key=lambda k: kt_warm[k][0])
+    # warm-up steps, then the per-kernel breakdown: a few steps with every big
+    # kernel timed (instrumentation only, not part of the timed figure; run on
+    # batches after the timed ones), which also pick the dominant kernel
+    run_steps(0, args.warmup, 0)
+    nprof = max(1, min(args.steps, 5))
+    _, kt_all = run_steps(args.warmup + args.steps, nprof, _lib.PS_TIMING_ALL)
+    dom = max(names, key=lambda k: kt_all[k][0])
 
     # ------------------------------------------------------------ timed steps
     # Each HIP event costs the GPU a few microseconds, so only the dominant
@@ -656,10 +655,6 @@ def main():
         marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
         elapsed, kt = run_steps(args.warmup, args.steps, 1 << KID[dom], marks)
         step_ms = [marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)]
-    # per-kernel breakdown from a few more steps with every big kernel timed
-    # (instrumentation only, not part of the timed figure)
-    nprof = max(1, min(args.steps, 5))
-    _, kt_all = run_steps(args.warmup + args.steps, nprof, _lib.PS_TIMING_ALL)
     launches = launches_per_step(wb, store, args.warmup, loss)
 
     idx = [args.warmup + i for i in range(args.steps)]
@@ -690,7 +685,7 @@ def main():
     dk = kernels[dom] if args.graph else kernel_entry(dom, kt[dom], args.steps, idx)
     kernels["scatter"] = {"ms_per_step": kt_all["scatter"][0] / nprof, "launches": kt_all["scatter"][1]}
     symbol = {"segreduce": "k_segreduce<%s>" % {"mf": "SrcSorted", "kge": "SrcKGE", "sgns": "SrcSGNS",
-                                                 "ctr": "SrcSorted", "ctr_wd": "SrcSorted"}[wb.task],
+                                                 "ctr": "SrcIndirect", "ctr_wd": "SrcSorted"}[wb.task],
               "rowmerge": "k_segreduce<SrcMFRow>", "mlp": "k_gemm_f64", "async": "k_push_async",
               "taskgrad": {"mf": "k_mf_grad_rows" if unmerged else "k_mf_pack", "kge": "k_kge_grad", "sgns": "k_sgns_grad",
                            "ctr": "k_ctr_grad", "ctr_wd": "k_wd_head"}[wb.task]}[dom]
@@ -728,6 +723,8 @@ def main():
 
     if not args.no_ops:
         ops = measure_ops(args, wb, store, dev, rowwise, unmerged)
+        if wb.task == "sgns" and not bf16:
+            ops["gather_ceiling"] = gather_ceilings(wb, store, dev, kernels, idx[0], ops.get("merge_distinct_keys"))
 
     copy = calibrate_copy(dev) if args.calibrate_copy else None
 
@@ -758,7 +755,8 @@ def main():
         "roofline": roofline,
         "kernels": {k: {kk: (round(vv, 4) if isinstance(vv, float) else vv) for kk, vv in v.items()}
                     for k, v in kernels.items()},
-        "kernels_from": f"{nprof} extra steps with every big kernel timed (the timed steps time only {dom})"
+        "kernels_from": f"{nprof} steps before the timed ones with every big kernel timed (the timed steps "
+                        f"time only {dom})"
                         if not args.graph else f"{nprof} eager steps with every big kernel timed; the timed steps "
                                                f"are one HIP-graph replay",
         "median_from": "HIP events on the stream after each timed step" if not args.graph else
@@ -864,8 +862,8 @@ def pipelined_push(store, keys, grads, n, reps):
 def measure_ops(args, wb, store, dev, rowwise, unmerged):
     """ps_push and ps_pull alone on one batch's key occurrences (random
     gradient rows), each rep timed with HIP events; reported as medians.
-    MF also: the merge kernel alone on distinct random keys (the bare
-    read-modify-write pattern), and the unmerged push."""
+    Also the merge kernel alone on as many distinct random keys (the bare
+    read-modify-write pattern), and with unmerged updates the unmerged push."""
     import torch
 
     from paper_2206_00470_amd import _lib
@@ -930,7 +928,7 @@ def measure_ops(args, wb, store, dev, rowwise, unmerged):
         ta = timed(lambda: store.push_async(keys, grads))
         ops["push_async"] = {"ms": round(ta * 1e3, 4), "rows_per_s": n / ta,
                              "alg_GBps": round((n * R + tab * U) / ta / 1e9, 1)}
-    if wb.task == "mf" and not args.ops_only:
+    if not args.ops_only and not unmerged:
         # the bare read-modify-write pattern through the merge kernel: U distinct
         # random keys, one contiguous gradient row each (no duplicates to merge)
         ukeys = torch.from_numpy(np.sort(np.random.default_rng(11).choice(cfg.num_keys, U, replace=False))).to(dev)
@@ -952,6 +950,73 @@ def measure_ops(args, wb, store, dev, rowwise, unmerged):
     del keys, grads, out
     torch.cuda.empty_cache()
     return ops
+
+
+def gather_ceilings(wb, store, dev, kernels, i, ops_mdk=None):
+    """Skip-gram: how fast this part serves each of the step's two row-gather
+    streams — the gradient kernel's output rows in centre order, and the
+    output-key merge's centre rows in sorted output-key order — measured by
+    the gather probe on the same row sequences of batch i (median of 10),
+    beside the rate the step's kernels reach on them (their row bytes over
+    their time per step in the breakdown steps)."""
+    import torch
+
+    from paper_2206_00470_amd import _lib
+    c, bt = wb.cfg, wb.host_batches[i % len(wb.host_batches)]
+    ctx = bt.ctx.astype(np.int64)
+    present = ctx >= 0
+    rows = np.concatenate([ctx[:, :, None], bt.neg.astype(np.int64)], axis=2)   # [B, slots, 1 + n_neg]
+    out_keys = (c.vocab + rows[present]).ravel()            # per centre and present slot: context, negatives
+    centre_of = np.repeat(np.broadcast_to(bt.centre.astype(np.int64)[:, None], ctx.shape)[present], rows.shape[2])
+    order = np.argsort(out_keys, kind="stable")
+    R = wb.R
+    B = int(bt.centre.size)
+    n_out = int(out_keys.size)
+    streams = {"grad_stream": (out_keys, "taskgrad", "the gradient kernel: every output occurrence's row "
+                                                      "(1.2 GB output table), centre after centre"),
+               "merge_stream": (centre_of[order], "segreduce", "the output-key merge: each output "
+                                                                "occurrence's centre input row, in sorted "
+                                                                "output-key order")}
+    sink = torch.empty(_lib.PS_PROBE_GRID, dtype=torch.float64, device=dev)
+    out = {}
+    for name, (keys_np, kname, what) in streams.items():
+        keys = torch.from_numpy(keys_np.astype(np.int32)).to(dev)
+        for _ in range(2):
+            store.probe_gather(keys, sink)
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(11)]
+        ev[0].record()
+        for r in range(10):
+            store.probe_gather(keys, sink)
+            ev[r + 1].record()
+        torch.cuda.synchronize()
+        t = float(np.median([ev[r].elapsed_time(ev[r + 1]) for r in range(10)])) * 1e-3
+        probe = n_out * R / t / 1e9
+        # the gradient kernel also reads the B centre rows, the merge (its input-key
+        # launch) the B stored centre gradient rows
+        kms = kernels.get(kname, {}).get("ms_per_step")
+        kgb = (n_out + B) * R / (kms * 1e-3) / 1e9 if kms else None
+        out[name] = {"rows": n_out, "probe_ms": round(t * 1e3, 4), "probe_GBps": round(probe, 1),
+                     "kernel": kname, "kernel_ms": round(kms, 4) if kms else None,
+                     "kernel_GBps": round(kgb, 1) if kgb else None,
+                     "kernel_frac_of_probe": round(kgb / probe, 3) if kgb else None, "what": what}
+        del keys
+    # the merge also reads and writes each distinct output key's W and G rows,
+    # which the probe does not: add that read-modify-write at the rate of the
+    # merge kernel alone on distinct keys (ops.merge_distinct_keys)
+    mdk = ops_mdk or {}
+    if mdk.get("merge_ms") and out["merge_stream"]["kernel_ms"]:
+        u_out = int(np.unique(out_keys).size)
+        rmw_ms = mdk["merge_ms"] * u_out / mdk["keys"]
+        ceil_ms = out["merge_stream"]["probe_ms"] + rmw_ms
+        out["merge_stream"]["with_rmw"] = {
+            "distinct_output_keys": u_out, "rmw_ms": round(rmw_ms, 4), "ceiling_ms": round(ceil_ms, 4),
+            "kernel_frac_of_ceiling": round(ceil_ms / out["merge_stream"]["kernel_ms"], 3),
+            "what": "probe time of the gathers plus the distinct-key merge's time scaled to the step's "
+                    "distinct output keys, against the merge kernels' time per step"}
+    out["what"] = ("rows read per second by the gather probe (ps_probe_gather: the same reads without the "
+                   "kernels' arithmetic) against the kernels' row bytes per second")
+    return out
 
 
 if __name__ == "__main__":

@@ -321,6 +321,19 @@ const char* ps_last_error_message(void);
 ps_status ps_set_timing(ps_store* s, int32_t mask);
 ps_status ps_read_timing(ps_store* s, int32_t kernel_id, double* total_ms, int64_t* launches);
 
+/* Gather probe (instrumentation): reads the rows keys[0..n) of the store's
+ * value table the way a gather-bound kernel reads its rows, without that
+ * kernel's arithmetic, to measure how fast this part serves a given stream
+ * of row reads (the gather ceiling a task kernel is compared with).  keys:
+ * device int32[n], read in order by a grid of PS_PROBE_GRID workgroups
+ * (row group g of S takes positions g, g + S, ...); keys outside
+ * [0, num_keys) are skipped.  sink: device double[PS_PROBE_GRID] receives
+ * fp64 partial sums of what was read (their total is the sum of every value
+ * read, so the reads cannot be left out).  fp32 stores only (bf16:
+ * PS_ERR_UNSUPPORTED); enqueued on `stream`, nothing allocated. */
+#define PS_PROBE_GRID 2048
+ps_status ps_probe_gather(ps_store* s, const int32_t* keys, int64_t n, double* sink, void* stream);
+
 /* ======================================================================
  * Wide & Deep click-through-rate step (Appendix C, "Click-through-rate
  * prediction": the Wide & Deep model, AdaGrad).

@@ -30,6 +30,7 @@ PS_KERNEL_STAGE = 5
 PS_KERNEL_MLP = 6
 PS_KERNEL_ASYNC = 7
 PS_TIMING_ALL = -1
+PS_PROBE_GRID = 2048
 
 STAGE_STATS = ["clock", "rounds", "forced", "staged", "evicted", "resident", "pending", "stalled", "plan_us"]
 
@@ -60,6 +61,7 @@ SIGNATURES = {
     "ps_get_error": (_i32, [_p, _p]),
     "ps_status_string": (C.c_char_p, [_i32]),
     "ps_last_error_message": (C.c_char_p, []),
+    "ps_probe_gather": (_i32, [_p, _p, _i64, _p, _p]),
     "ps_set_timing": (_i32, [_p, _i32]),
     "ps_read_timing": (_i32, [_p, _i32, C.POINTER(C.c_double), C.POINTER(_i64)]),
     "ps_ctr_wd_workspace_bytes": (_sz, [_i64, _i32, _i64, _i32, _i32, _i32, _p]),

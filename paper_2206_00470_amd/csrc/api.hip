@@ -1981,6 +1981,22 @@ ps_status ps_get_error(ps_store* s, void* stream) {
   return PS_OK;
 }
 
+ps_status ps_probe_gather(ps_store* s, const int32_t* keys, int64_t n, double* sink, void* stream) {
+  if (ps_status st = check_store(s)) return st;
+  if (s->bf16) return fail(PS_ERR_UNSUPPORTED, "the gather probe reads fp32 values only");
+  if (n < 0) return fail(PS_ERR_INVALID, "negative size %lld", (long long)n);
+  if (!sink || (n > 0 && !keys)) return fail(PS_ERR_INVALID, "keys or sink is NULL");
+  RowShape shape;
+  if (!row_shape(s->dim, true, &shape)) return fail(PS_ERR_UNSUPPORTED, "dim %d not supported", s->dim);
+  hipStream_t st = as_stream(stream);
+  return with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
+    hipLaunchKernelGGL((k_gather_probe<L, NV, VW>), dim3(PS_PROBE_GRID), dim3(BLOCK), 0, st, s->W, s->ld, s->dim,
+                       s->num_keys, keys, n, sink);
+    LAUNCHED(k_gather_probe);
+    return PS_OK;
+  });
+}
+
 ps_status ps_set_timing(ps_store* s, int32_t mask) {
   if (ps_status st = check_store(s)) return st;
   s->timing = (uint32_t)mask;

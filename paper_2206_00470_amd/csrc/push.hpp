@@ -62,6 +62,62 @@ __global__ __launch_bounds__(BLOCK) void k_pull(const VT* __restrict__ W, int64_
   if (__syncthreads_or(miss) && threadIdx.x == 0) atomicOr(err + 1, 1);
 }
 
+// ------------------------------------------------------------------ gather probe
+// The row reads of a gather-bound kernel without its arithmetic (for
+// measurement): row group g reads the rows keys[i] of W for i = g, g + S,
+// g + 2S, ... (S row groups in the grid, UNROLL rows in flight per group)
+// and adds them into fp64 lane sums; each workgroup writes the sum of its
+// lanes' sums to sink[workgroup], so the loads cannot be left out.  Keys
+// outside [0, rows) are skipped.
+template <int L, int NV, int VW>
+__global__ __launch_bounds__(BLOCK) void k_gather_probe(const float* __restrict__ W, int64_t ld, int dim,
+                                                        int64_t rows, const int32_t* __restrict__ keys, int64_t n,
+                                                        double* __restrict__ sink) {
+  constexpr int GPB = BLOCK / L;
+  constexpr int NE = NV * VW;
+  constexpr int UNROLL = NE <= 4 ? 8 : 4;
+  __shared__ double sm[WAVES_PER_BLOCK];
+  const int gl = threadIdx.x % L;
+  const int64_t S = (int64_t)gridDim.x * GPB;
+  double acc[NE];
+#pragma unroll
+  for (int e = 0; e < NE; ++e) acc[e] = 0.0;
+  auto load_row = [&](int64_t i, float* x) {
+    const int32_t k = keys[i];
+    const bool ok = k >= 0 && k < rows;
+    const float* p = W + (ok ? (int64_t)k : 0) * ld;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+      const int c = (gl + v * L) * VW;
+      if (ok && c < dim) load_frag<VW>(p + c, x + v * VW);
+      else
+#pragma unroll
+        for (int e = 0; e < VW; ++e) x[v * VW + e] = 0.0f;
+    }
+  };
+  int64_t i = (int64_t)blockIdx.x * GPB + threadIdx.x / L;
+  for (; i + (UNROLL - 1) * S < n; i += UNROLL * S) {
+    float x[UNROLL][NE];
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) load_row(i + u * S, x[u]);
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u)
+#pragma unroll
+      for (int e = 0; e < NE; ++e) acc[e] += (double)x[u][e];
+  }
+  for (; i < n; i += S) {
+    float x[NE];
+    load_row(i, x);
+#pragma unroll
+    for (int e = 0; e < NE; ++e) acc[e] += (double)x[e];
+  }
+  double t = 0.0;
+#pragma unroll
+  for (int e = 0; e < NE; ++e) t += acc[e];
+  t = block_sum_double(t, sm);
+  if (threadIdx.x == 0) sink[blockIdx.x] = t;
+}
+
 // ------------------------------------------------------------------ gradient sources
 // A source describes the fp32 gradient row of the occurrence at sorted
 // position j in two steps:

@@ -328,6 +328,19 @@ class Store:
         check(lib().ps_read_timing(self._h, kernel_id, C.byref(ms), C.byref(n)))
         return ms.value, n.value
 
+    def probe_gather(self, keys: torch.Tensor, sink: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+        """Instrumentation: read the value rows keys (int32) in order, as a
+        gather-bound kernel would, without its arithmetic; returns the
+        per-workgroup fp64 sums of what was read (sink)."""
+        _dev(keys, torch.int32, "keys")
+        if sink is None:
+            sink = torch.empty(_lib.PS_PROBE_GRID, dtype=torch.float64, device=self.W.device)
+        _dev(sink, torch.float64, "sink")
+        if sink.numel() < _lib.PS_PROBE_GRID:
+            raise ValueError(f"sink needs {_lib.PS_PROBE_GRID} values")
+        check(lib().ps_probe_gather(self._h, _ptr(keys), keys.numel(), _ptr(sink), _stream(stream)))
+        return sink
+
 
 class StagedStore(Store):
     """A store whose full tables live in pinned host memory (the home store)
