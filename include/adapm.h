@@ -70,7 +70,15 @@ typedef int32_t ps_status;
 #define PS_OP_STEP_MF_ASYNC 7
 
 /* Limits: num_keys in [1, 2^31-1]; dim in [1, 512]; key occurrences per
- * call n < 2^31 - 2^20. */
+ * call n < 2^31 - 2^20.  Stores made by ps_create / ps_create_strided may
+ * also hold wider rows, dim in (512, 16384] and a multiple of 4 (the paper's
+ * widest models keep 1,000 floats per parameter row, Table 3): ps_pull,
+ * ps_push (and its two-phase and allocation-free forms) and ps_dedup serve
+ * them, one column slice of 512 floats at a time (per-element AdaGrad and
+ * per-element sums do not mix columns, so the result is the whole-row
+ * update); the task steps, ps_push_async and ps_step_mf_async return
+ * PS_ERR_UNSUPPORTED for them, and row-wise, bf16 and staged stores keep
+ * dim <= 512. */
 
 /* Create a store over caller-owned device tables W (values) and G
  * (AdaGrad accumulators), each num_keys*dim floats, with AdaGrad learning

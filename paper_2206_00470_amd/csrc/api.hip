@@ -48,6 +48,11 @@ ps_status fail(ps_status st, const char* fmt, ...) {
 #define LAUNCHED(name) HIP_TRY(hipGetLastError())
 
 constexpr int64_t MAX_OCC = (int64_t(1) << 31) - (int64_t(1) << 20);
+// Rows of up to ROW_MAX floats are one row group's; wider rows (up to
+// WIDE_MAX floats, a multiple of 4) are pulled and pushed in column slices
+// of ROW_MAX floats, each slice a row of the kernels that serve ROW_MAX.
+constexpr int ROW_MAX = 512;
+constexpr int WIDE_MAX = 16384;
 constexpr int NUM_TIMED = 8;
 constexpr size_t MAX_TIMED_LAUNCHES = 1 << 14;
 
@@ -295,8 +300,9 @@ void carve_sort(Carver& c, int64_t n, int dim, bool want_rank, bool want_segment
   b->chunk_start = c.take<int32_t>(n + 1);
   b->chunk_seg = c.take<int32_t>(n);
   b->split_list = c.take<int32_t>(n / CHUNK + 2);
-  b->partial = c.take<double>(size_t(2) * (n / CHUNK + 1) * dim);
-  b->fold = c.take<double>(size_t(n / (FOLD_SB * CHUNK) + 1) * dim);
+  const int rdim = dim < ROW_MAX ? dim : ROW_MAX;   // wide rows are merged one column slice at a time
+  b->partial = c.take<double>(size_t(2) * (n / CHUNK + 1) * rdim);
+  b->fold = c.take<double>(size_t(n / (FOLD_SB * CHUNK) + 1) * rdim);
 }
 
 struct Plan {
@@ -461,6 +467,13 @@ ps_status with_sgns_shape(int dim, int64_t ld, F&& f) {
   return with_shape(shape, f);
 }
 
+// Columns [col0, col0 + dim) of every row: a column slice of a wide row
+// (dim 0: the whole row of the store).
+struct ColSlice {
+  int64_t col0 = 0;
+  int dim = 0;
+};
+
 int64_t reduce_grid(int64_t n, int L, int64_t cap = MERGE_GRID_MAX) {
   const int64_t gpb = BLOCK / L;
   // one row group per chunk up to a cap (there are at most n + n/CHUNK + 1 chunks)
@@ -497,27 +510,31 @@ constexpr bool src_runs_on() {
 // there, 1% lost on 1,200-byte rows).
 template <class Src>
 ps_status launch_segreduce(ps_store* s, const SortBufs& b, const uint32_t* ks, Src src, int64_t n, int part,
-                           hipStream_t st, int timing_id = PS_KERNEL_SEGREDUCE, int64_t grid_cap = 0) {
+                           hipStream_t st, int timing_id = PS_KERNEL_SEGREDUCE, int64_t grid_cap = 0,
+                           ColSlice cs = ColSlice{}) {
+  const int dim = cs.dim ? cs.dim : s->dim;
   RowShape shape;
-  if (!row_shape(s->dim, true, &shape)) return fail(PS_ERR_UNSUPPORTED, "dim %d not supported", s->dim);
+  if (!row_shape(dim, true, &shape)) return fail(PS_ERR_UNSUPPORTED, "dim %d not supported", dim);
   SegView sv{ks, b.seg_off, b.chunk_start, b.chunk_seg, b.hdr};
+  float* W = s->W + (s->bf16 ? 0 : cs.col0);
+  bf16_t* Wb = reinterpret_cast<bf16_t*>(s->W) + (s->bf16 ? cs.col0 : 0);
+  float* G = s->G + (s->rowwise ? 0 : cs.col0);
   return with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
     const int64_t grid = reduce_grid(n, L, grid_cap ? grid_cap : (L <= 32 ? 1024 : MERGE_GRID_MAX));
     Timed t(s, timing_id, st);
     if (s->bf16) {
       if constexpr (src_runs_on<Src, bf16_t>())
         hipLaunchKernelGGL((k_segreduce<L, NV, VW, Src, false, bf16_t>), dim3(grid), dim3(BLOCK), 0, st, sv, src, n,
-                           reinterpret_cast<bf16_t*>(s->W), s->G, s->ld, s->gld, s->dim, s->lr, s->eps, b.partial,
-                           b.split_list, b.hdr, part);
+                           Wb, G, s->ld, s->gld, dim, s->lr, s->eps, b.partial, b.split_list, b.hdr, part);
       else
         return fail(PS_ERR_UNSUPPORTED, "this step does not run on bf16 values");
     } else if constexpr (src_runs_on<Src, float>()) {
       if (s->rowwise)
         hipLaunchKernelGGL((k_segreduce<L, NV, VW, Src, true, float>), dim3(grid), dim3(BLOCK), 0, st, sv, src, n,
-                           s->W, s->G, s->ld, s->gld, s->dim, s->lr, s->eps, b.partial, b.split_list, b.hdr, part);
+                           W, G, s->ld, s->gld, dim, s->lr, s->eps, b.partial, b.split_list, b.hdr, part);
       else
         hipLaunchKernelGGL((k_segreduce<L, NV, VW, Src, false, float>), dim3(grid), dim3(BLOCK), 0, st, sv, src, n,
-                           s->W, s->G, s->ld, s->gld, s->dim, s->lr, s->eps, b.partial, b.split_list, b.hdr, part);
+                           W, G, s->ld, s->gld, dim, s->lr, s->eps, b.partial, b.split_list, b.hdr, part);
     } else {
       return fail(PS_ERR_UNSUPPORTED, "this step does not run on fp32 values");
     }
@@ -527,31 +544,34 @@ ps_status launch_segreduce(ps_store* s, const SortBufs& b, const uint32_t* ks, S
 }
 
 ps_status launch_finalize(ps_store* s, const SortBufs& b, const uint32_t* ks, int64_t n, hipStream_t st,
-                          LossTotal lt = LossTotal{nullptr, 0, nullptr}) {
+                          LossTotal lt = LossTotal{nullptr, 0, nullptr}, ColSlice cs = ColSlice{}) {
+  const int dim = cs.dim ? cs.dim : s->dim;
   RowShape shape;
-  if (!row_shape(s->dim, true, &shape)) return fail(PS_ERR_UNSUPPORTED, "dim %d not supported", s->dim);
+  if (!row_shape(dim, true, &shape)) return fail(PS_ERR_UNSUPPORTED, "dim %d not supported", dim);
   SegView sv{ks, b.seg_off, b.chunk_start, b.chunk_seg, b.hdr};
+  float* W = s->W + (s->bf16 ? 0 : cs.col0);
+  bf16_t* Wb = reinterpret_cast<bf16_t*>(s->W) + (s->bf16 ? cs.col0 : 0);
+  float* G = s->G + (s->rowwise ? 0 : cs.col0);
   return with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
-    const size_t lds = size_t(BLOCK / L) * s->dim * sizeof(double);
+    const size_t lds = size_t(BLOCK / L) * dim * sizeof(double);
     const int64_t nsb = n / (FOLD_SB * CHUNK);   // super-blocks wholly inside [0, n)
     if (nsb > 0) {
       hipLaunchKernelGGL((k_seg_fold<L, NV, VW>), dim3(nsb < 1024 ? nsb : 1024), dim3(BLOCK), lds, st, sv, nsb,
-                         (uint32_t)s->num_keys, s->dim, b.partial, b.fold);
+                         (uint32_t)s->num_keys, dim, b.partial, b.fold);
       LAUNCHED(k_seg_fold);
     }
     // at most n / CHUNK + 1 split segments; blocks beyond their count exit at once
     int64_t fgrid = n / CHUNK + 1;
     if (fgrid > 16384) fgrid = 16384;
     if (s->bf16)
-      hipLaunchKernelGGL((k_seg_finalize<L, NV, VW, false, bf16_t>), dim3(fgrid), dim3(BLOCK), lds, st, sv,
-                         reinterpret_cast<bf16_t*>(s->W), s->G, s->ld, s->gld, s->dim, s->lr, s->eps, b.partial,
-                         b.fold, b.split_list, lt);
+      hipLaunchKernelGGL((k_seg_finalize<L, NV, VW, false, bf16_t>), dim3(fgrid), dim3(BLOCK), lds, st, sv, Wb, G,
+                         s->ld, s->gld, dim, s->lr, s->eps, b.partial, b.fold, b.split_list, lt);
     else if (s->rowwise)
-      hipLaunchKernelGGL((k_seg_finalize<L, NV, VW, true, float>), dim3(fgrid), dim3(BLOCK), lds, st, sv, s->W, s->G,
-                         s->ld, s->gld, s->dim, s->lr, s->eps, b.partial, b.fold, b.split_list, lt);
+      hipLaunchKernelGGL((k_seg_finalize<L, NV, VW, true, float>), dim3(fgrid), dim3(BLOCK), lds, st, sv, W, G,
+                         s->ld, s->gld, dim, s->lr, s->eps, b.partial, b.fold, b.split_list, lt);
     else
-      hipLaunchKernelGGL((k_seg_finalize<L, NV, VW, false, float>), dim3(fgrid), dim3(BLOCK), lds, st, sv, s->W, s->G,
-                         s->ld, s->gld, s->dim, s->lr, s->eps, b.partial, b.fold, b.split_list, lt);
+      hipLaunchKernelGGL((k_seg_finalize<L, NV, VW, false, float>), dim3(fgrid), dim3(BLOCK), lds, st, sv, W, G,
+                         s->ld, s->gld, dim, s->lr, s->eps, b.partial, b.fold, b.split_list, lt);
     LAUNCHED(k_seg_finalize);
     return PS_OK;
   });
@@ -581,6 +601,15 @@ ps_status check_ws(const Plan& p, void* ws, size_t ws_bytes) {
 
 ps_status check_store(const ps_store* s) {
   if (!s) return fail(PS_ERR_INVALID, "store is NULL");
+  return PS_OK;
+}
+
+// The task steps and unmerged updates work on whole rows of at most ROW_MAX
+// floats; wider rows have pull and push only.
+ps_status check_row_width(const ps_store* s) {
+  if (s->dim > ROW_MAX)
+    return fail(PS_ERR_UNSUPPORTED, "rows of %d floats: this call handles rows of at most %d (wider rows: pull and push)",
+                s->dim, ROW_MAX);
   return PS_OK;
 }
 
@@ -673,11 +702,14 @@ ps_status zero_loss(double* loss, hipStream_t st) {
 
 // Checks shared by the store constructors: key count, row shape, value
 // table, learning rate.
-ps_status check_values(int64_t num_keys, int32_t dim, int64_t row_stride, const float* values, float lr, float eps) {
+ps_status check_values(int64_t num_keys, int32_t dim, int64_t row_stride, const float* values, float lr, float eps,
+                       bool wide_ok = false) {
   if (num_keys < 1 || num_keys > INT32_MAX) return fail(PS_ERR_INVALID, "num_keys %lld outside [1, 2^31-1]", (long long)num_keys);
   RowShape shape;
-  if (dim < 1 || !row_shape(dim, true, &shape))
-    return fail(PS_ERR_UNSUPPORTED, "dim %d unsupported (at most 512)", dim);
+  const bool wide = wide_ok && dim > ROW_MAX && dim <= WIDE_MAX && dim % 4 == 0;
+  if (dim < 1 || (!wide && !row_shape(dim, true, &shape)))
+    return fail(PS_ERR_UNSUPPORTED, "dim %d unsupported (at most 512; per-element stores up to %d, a multiple of 4)",
+                dim, WIDE_MAX);
   if (row_stride < dim) return fail(PS_ERR_INVALID, "row_stride %lld < dim %d", (long long)row_stride, dim);
   if (!values) return fail(PS_ERR_INVALID, "table pointer is NULL");
   if (dim % 4 == 0 && (!aligned16(values) || row_stride % 4 != 0))
@@ -1057,7 +1089,7 @@ ps_status ps_create_strided(ps_store** out, int64_t num_keys, int32_t dim, int64
                             float* accum, float lr, float eps, void* stream) {
   if (!out) return fail(PS_ERR_INVALID, "out is NULL");
   *out = nullptr;
-  if (ps_status r = check_values(num_keys, dim, row_stride, values, lr, eps)) return r;
+  if (ps_status r = check_values(num_keys, dim, row_stride, values, lr, eps, true)) return r;
   if (!accum) return fail(PS_ERR_INVALID, "table pointer is NULL");
   {
     // rows of W and G must not overlap: either two separate tables, or rows
@@ -1159,24 +1191,30 @@ ps_status ps_pull(ps_store* s, const int64_t* keys, int64_t n, float* out, void*
   if (ps_status st = check_n(n, 1)) return st;
   if (n == 0) return PS_OK;
   if (!keys || !out) return fail(PS_ERR_INVALID, "keys or out is NULL");
-  RowShape shape;
-  row_shape(s->dim, aligned16(out), &shape);
   hipStream_t st = as_stream(stream);
-  return with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
-    int64_t grid = ceil_div(n, BLOCK / L);
-    if (grid > 65536) grid = 65536;
-    Timed t(s, PS_KERNEL_PULL, st);
-    if (s->bf16)
-      hipLaunchKernelGGL((k_pull<L, NV, VW, bf16_t>), dim3(grid), dim3(BLOCK), 0, st,
-                         reinterpret_cast<const bf16_t*>(s->W), s->ld, s->num_keys, s->dim, keys, n, out, s->status,
-                         (const int32_t*)nullptr, int64_t(0));
-    else
-      hipLaunchKernelGGL((k_pull<L, NV, VW, float>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->ld, s->num_keys, s->dim,
-                         keys, n, out, s->status, s->stg ? s->stg->map : nullptr,
-                         s->stg ? s->stg->num_keys : int64_t(0));
-    LAUNCHED(k_pull);
-    return PS_OK;
-  });
+  // rows of up to ROW_MAX floats in one pass; wider rows one column slice at a time
+  for (int64_t col0 = 0; col0 < s->dim; col0 += ROW_MAX) {
+    const int dim = (int)std::min<int64_t>(ROW_MAX, s->dim - col0);
+    RowShape shape;
+    row_shape(dim, aligned16(out) && s->dim % 4 == 0, &shape);
+    ps_status r = with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
+      int64_t grid = ceil_div(n, BLOCK / L);
+      if (grid > 65536) grid = 65536;
+      Timed t(s, PS_KERNEL_PULL, st);
+      if (s->bf16)
+        hipLaunchKernelGGL((k_pull<L, NV, VW, bf16_t>), dim3(grid), dim3(BLOCK), 0, st,
+                           reinterpret_cast<const bf16_t*>(s->W) + col0, s->ld, s->num_keys, dim, keys, n,
+                           out + col0, (int64_t)s->dim, s->status, (const int32_t*)nullptr, int64_t(0));
+      else
+        hipLaunchKernelGGL((k_pull<L, NV, VW, float>), dim3(grid), dim3(BLOCK), 0, st, s->W + col0, s->ld,
+                           s->num_keys, dim, keys, n, out + col0, (int64_t)s->dim, s->status,
+                           s->stg ? s->stg->map : nullptr, s->stg ? s->stg->num_keys : int64_t(0));
+      LAUNCHED(k_pull);
+      return PS_OK;
+    });
+    if (r) return r;
+  }
+  return PS_OK;
 }
 
 // The push in two phases: the key work (intake, sort, segments; workspace
@@ -1192,7 +1230,23 @@ static ps_status push_apply(ps_store* s, int64_t n, const float* grads, Plan& p,
   const int passes = radix_plan(s->num_keys).passes;   // where the sort left keys and permutation
   const uint32_t* ks = p.sb.k[passes % 2];
   const uint32_t* perm = p.sb.v[passes % 2];
-  return run_reduce(s, p.sb, ks, SrcIndirect{grads, perm, s->dim}, n, {PART_ALL}, st);
+  if (s->dim <= ROW_MAX) return run_reduce(s, p.sb, ks, SrcIndirect{grads, perm, s->dim, s->dim}, n, {PART_ALL}, st);
+  // a wide row: each column slice merged and updated on its own (per-element
+  // AdaGrad and per-element sums do not mix columns, so this is the same
+  // update); the segments are the sort's, the partials reused slice after
+  // slice, the list of cut segments rebuilt by each slice's merge
+  for (int64_t col0 = 0; col0 < s->dim; col0 += ROW_MAX) {
+    const ColSlice cs{col0, (int)std::min<int64_t>(ROW_MAX, s->dim - col0)};
+    if (col0 > 0) {
+      hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(BLOCK), 0, st, &p.sb.hdr->num_split, int64_t(1));
+      LAUNCHED(k_zero_words);
+    }
+    if (ps_status r = launch_segreduce(s, p.sb, ks, SrcIndirect{grads + col0, perm, cs.dim, s->dim}, n, PART_ALL, st,
+                                       PS_KERNEL_SEGREDUCE, 0, cs))
+      return r;
+    if (ps_status r = launch_finalize(s, p.sb, ks, n, st, LossTotal{nullptr, 0, nullptr}, cs)) return r;
+  }
+  return PS_OK;
 }
 
 static ps_status check_grads(const ps_store* s, const float* grads) {
@@ -1269,6 +1323,7 @@ ps_status ps_dedup(int64_t num_keys, const int64_t* keys, int64_t n, int64_t* un
 static ps_status step_mf_impl(ps_store* s, const int32_t* row, const int32_t* col, const float* val, int64_t B,
                               int64_t col_key_offset, float lambda, double* loss, void* ws, size_t ws_bytes, void* stream) {
   if (ps_status st = check_store(s)) return st;
+  if (ps_status st = check_row_width(s)) return st;
   if (ps_status st = check_n(B, 2)) return st;
   hipStream_t st = as_stream(stream);
   if (B == 0) return zero_loss(loss, st);
@@ -1284,6 +1339,7 @@ static ps_status step_mf_impl(ps_store* s, const int32_t* row, const int32_t* co
 ps_status ps_step_mf_prepare(ps_store* s, const int32_t* row, const int32_t* col, const float* val, int64_t B,
                              int64_t col_key_offset, void* ws, size_t ws_bytes, void* stream) {
   if (ps_status st = check_store(s)) return st;
+  if (ps_status st = check_row_width(s)) return st;
   if (s->stg) return fail(PS_ERR_UNSUPPORTED, "the two-phase MF step is not available on a staged store");
   if (ps_status st = check_n(B, 2)) return st;
   if (B == 0) return PS_OK;
@@ -1298,6 +1354,7 @@ ps_status ps_step_mf_prepare(ps_store* s, const int32_t* row, const int32_t* col
 ps_status ps_step_mf_apply(ps_store* s, int64_t B, float lambda, double* loss, void* ws, size_t ws_bytes,
                            void* stream, void* rows_done) {
   if (ps_status st = check_store(s)) return st;
+  if (ps_status st = check_row_width(s)) return st;
   if (s->stg) return fail(PS_ERR_UNSUPPORTED, "the two-phase MF step is not available on a staged store");
   if (ps_status st = check_n(B, 2)) return st;
   hipStream_t st = as_stream(stream);
@@ -1312,6 +1369,7 @@ static ps_status step_kge_impl(ps_store* s, const int32_t* head, const int32_t* 
                                int64_t B, int32_t n_neg, int32_t n_head_neg, int64_t rel_key_offset, double* loss, void* ws,
                                size_t ws_bytes, void* stream) {
   if (ps_status st = check_store(s)) return st;
+  if (ps_status st = check_row_width(s)) return st;
   if (s->bf16) return fail(PS_ERR_UNSUPPORTED, "this step runs on fp32 values only (bf16 stores: pull, push, MF)");
   if (n_neg < 0 || n_head_neg < 0 || n_head_neg > n_neg)
     return fail(PS_ERR_INVALID, "need 0 <= n_head_neg <= n_neg");
@@ -1367,6 +1425,7 @@ static ps_status step_sgns_impl(ps_store* s, const int32_t* centre, const int32_
                                 int32_t window, int32_t n_neg, int64_t out_key_offset, double* loss, void* ws,
                                 size_t ws_bytes, void* stream) {
   if (ps_status st = check_store(s)) return st;
+  if (ps_status st = check_row_width(s)) return st;
   if (s->bf16) return fail(PS_ERR_UNSUPPORTED, "this step runs on fp32 values only (bf16 stores: pull, push, MF)");
   if (window < 0 || n_neg < 0) return fail(PS_ERR_INVALID, "negative window or n_neg");
   const int slots = 2 * window;
@@ -1423,6 +1482,7 @@ static ps_status step_sgns_impl(ps_store* s, const int32_t* centre, const int32_
 static ps_status step_ctr_impl(ps_store* s, const int64_t* keys, const float* label, int64_t B, int32_t F, double* loss,
                                void* ws, size_t ws_bytes, void* stream) {
   if (ps_status st = check_store(s)) return st;
+  if (ps_status st = check_row_width(s)) return st;
   if (s->bf16) return fail(PS_ERR_UNSUPPORTED, "this step runs on fp32 values only (bf16 stores: pull, push, MF)");
   if (F < 1) return fail(PS_ERR_INVALID, "need F >= 1");
   if (ps_status st = check_n(B, F)) return st;
@@ -1466,7 +1526,7 @@ static ps_status step_ctr_impl(ps_store* s, const int64_t* keys, const float* la
   });
   if (r) return r;
   if (ps_status r = join_aux(s, st)) return r;
-  return run_reduce(s, p.sb, ks, SrcIndirect{p.grads, perm, s->dim}, n, {PART_ALL}, st,
+  return run_reduce(s, p.sb, ks, SrcIndirect{p.grads, perm, s->dim, s->dim}, n, {PART_ALL}, st,
                     LossTotal{p.loss_part, grid, loss});
 }
 
@@ -1503,6 +1563,7 @@ ps_status ps_push_noalloc(ps_store* s, const int64_t* keys, int64_t n, const flo
 // ------------------------------------------------------------------ unmerged (asynchronous) updates
 ps_status ps_push_async(ps_store* s, const int64_t* keys, int64_t n, const float* grads, void* stream) {
   if (ps_status st = check_store(s)) return st;
+  if (ps_status st = check_row_width(s)) return st;
   if (ps_status st = check_async(s)) return st;
   if (ps_status st = check_n(n, 1)) return st;
   if (n == 0) return PS_OK;
@@ -1514,6 +1575,7 @@ ps_status ps_step_mf_async(ps_store* s, const int32_t* row, const int32_t* col, 
                            int64_t col_key_offset, float lambda, double* loss, void* ws, size_t ws_bytes,
                            void* stream) {
   if (ps_status st = check_store(s)) return st;
+  if (ps_status st = check_row_width(s)) return st;
   if (ps_status st = check_async(s)) return st;
   if (ps_status st = check_n(B, 2)) return st;
   hipStream_t st = as_stream(stream);
@@ -1646,6 +1708,7 @@ ps_status ps_step_ctr_wd(ps_store* s, const int64_t* keys, const float* label, i
                          int32_t n_hidden, const int32_t* hidden, float* dense, float* dense_accum, double* loss,
                          void* ws, size_t ws_bytes, void* stream) {
   if (ps_status st = check_store(s)) return st;
+  if (ps_status st = check_row_width(s)) return st;
   if (s->bf16) return fail(PS_ERR_UNSUPPORTED, "this step runs on fp32 values only (bf16 stores: pull, push, MF)");
   if (F < 1) return fail(PS_ERR_INVALID, "need F >= 1");
   if (emb_dim < 1 || emb_dim >= s->dim) return fail(PS_ERR_INVALID, "need 1 <= emb_dim < dim (the row holds the wide weight)");
@@ -1767,6 +1830,7 @@ ps_status ps_create_staged(ps_store** out, int64_t num_keys, int32_t dim, float*
     total += range_slots[r];
   }
   if (total > INT32_MAX) return fail(PS_ERR_INVALID, "more than 2^31-1 slots");
+  if (dim > ROW_MAX) return fail(PS_ERR_UNSUPPORTED, "a staged store holds rows of at most %d floats", ROW_MAX);
   if (home_stride < dim) return fail(PS_ERR_INVALID, "home_stride %lld < dim %d", (long long)home_stride, dim);
   {
     const int64_t d = (int64_t)(home_accum - home_values);

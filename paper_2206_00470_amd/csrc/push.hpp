@@ -21,10 +21,12 @@ struct RowShape {
 // map_keys keys and rows are read from their slots; a key with no slot gives
 // a zero row and sets err[1].  VT: the table's value type (float or bf16_t);
 // the pulled rows are fp32 either way.
+// Pulled row i goes to out + i * out_ld (out_ld = dim, or the full row
+// width when a wide row is pulled in column slices).
 template <int L, int NV, int VW, class VT>
 __global__ __launch_bounds__(BLOCK) void k_pull(const VT* __restrict__ W, int64_t ld, int64_t num_keys, int dim,
                                                 const int64_t* __restrict__ keys, int64_t n,
-                                                float* __restrict__ out, int32_t* __restrict__ err,
+                                                float* __restrict__ out, int64_t out_ld, int32_t* __restrict__ err,
                                                 const int32_t* __restrict__ map, int64_t map_keys) {
   constexpr int GPB = BLOCK / L;
   const int gl = threadIdx.x % L;
@@ -44,7 +46,7 @@ __global__ __launch_bounds__(BLOCK) void k_pull(const VT* __restrict__ W, int64_
       bad |= !ok;
     }
     const VT* src = W + (ok ? key : 0) * ld;
-    float* dst = out + i * (int64_t)dim;
+    float* dst = out + i * out_ld;
 #pragma unroll
     for (int v = 0; v < NV; ++v) {
       const int c = (gl + v * L) * VW;
@@ -140,16 +142,18 @@ __device__ __forceinline__ T shfl_pod(const T& v, int src, int width) {
   return out.t;
 }
 
-// Gradient rows in occurrence order, read through the sort permutation.
+// Gradient rows in occurrence order, ld floats apart, read through the sort
+// permutation.
 struct SrcIndirect {
   static constexpr bool kNeedsOwn = false;
   const float* grads;
   const uint32_t* perm;
   int dim;
+  int64_t ld;
   struct Meta {
     const float* row;
   };
-  __device__ __forceinline__ Meta meta(int64_t j) const { return {grads + (int64_t)perm[j] * dim}; }
+  __device__ __forceinline__ Meta meta(int64_t j) const { return {grads + (int64_t)perm[j] * ld}; }
   template <int L, int NV, int VW>
   __device__ __forceinline__ void load(const Meta& m, const float*, int gl, float* x) const {
 #pragma unroll

@@ -51,10 +51,17 @@ def test_create_rejects_bad_arguments_on_host():
     assert L.ps_create(C.byref(h), 0, 4, fake, other, 0.1, 0.0, None) == _lib.PS_ERR_INVALID
     assert h.value is None
     assert L.ps_create(C.byref(h), 10, 0, fake, other, 0.1, 0.0, None) == _lib.PS_ERR_UNSUPPORTED
-    assert L.ps_create(C.byref(h), 10, 4096, fake, other, 0.1, 0.0, None) == _lib.PS_ERR_UNSUPPORTED
     assert L.ps_create(C.byref(h), 10, 513, fake, other, 0.1, 0.0, None) == _lib.PS_ERR_UNSUPPORTED
-    for wide in (516, 600, 1024, 2048):   # rows wider than 512 floats are not supported
-        assert L.ps_create(C.byref(h), 10, wide, fake, other, 0.1, 0.0, None) == _lib.PS_ERR_UNSUPPORTED
+    # rows wider than 512 floats: a multiple of 4 up to 16384 passes the width
+    # check (these fake tables then fail the overlap check), others do not
+    for bad in (514, 1001, 16388, 1 << 20):
+        assert L.ps_create(C.byref(h), 10, bad, fake, other, 0.1, 0.0, None) == _lib.PS_ERR_UNSUPPORTED
+    for wide in (516, 600, 1024, 4096, 16384):
+        assert L.ps_create(C.byref(h), 10, wide, fake, other, 0.1, 0.0, None) == _lib.PS_ERR_INVALID
+        assert b"overlap" in L.ps_last_error_message()
+        big = C.c_void_p(0x1000 + 16 * 10 * wide * 4)
+        assert L.ps_create_rowwise(C.byref(h), 10, wide, wide, fake, big, 1, 0.1, 0.0, None) == \
+            _lib.PS_ERR_UNSUPPORTED
     assert L.ps_create(C.byref(h), 10, 512, fake, None, 0.1, 0.0, None) == _lib.PS_ERR_INVALID
     assert L.ps_create(C.byref(h), 10, 4, None, other, 0.1, 0.0, None) == _lib.PS_ERR_INVALID
     assert L.ps_create(C.byref(h), 10, 4, fake, fake, 0.1, 0.0, None) == _lib.PS_ERR_INVALID
