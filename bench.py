@@ -52,6 +52,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="mf", choices=["mf", "mf_tiny", "mf_colorder", "kge", "kge2x100", "sgns",
                                                            "sgns_w2v", "ctr", "ctr_wd"])
+    ap.add_argument("--rank", type=int, default=0,
+                    help="MF workloads: factor rank in place of the configuration's (rows of more than 512 "
+                         "floats, such as the paper's rank 1,000, have pull and push only: use with --ops-only)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="bound on the CPU-oracle sample (0 = skip)")
     ap.add_argument("--no-ops", action="store_true", help="skip the pull-only / push-only measurements")
@@ -120,7 +123,7 @@ class Bench:
     """One workload: its table, resident step batches, the step call, the
     algorithmic bytes of its two big kernels and the oracle step."""
 
-    def __init__(self, name, dev, nbatches, rowwise=False, values="f32", unmerged=False):
+    def __init__(self, name, dev, nbatches, rowwise=False, values="f32", unmerged=False, rank=0):
         import torch
         from paper_2206_00470_amd import workloads as wls
 
@@ -133,6 +136,9 @@ class Bench:
                 "kge": wls.KGE_COMPLEX, "kge2x100": wls.KGE_COMPLEX_2x100, "sgns": wls.SGNS_1M,
                 "sgns_w2v": wls.SGNS_1M_W2V, "ctr": wls.CTR_33M, "ctr_wd": wls.CTR_33M_WD}
         self.cfg = cfg = cfgs[name]
+        if rank:
+            from dataclasses import replace
+            self.cfg = cfg = replace(cfg, rank=rank, name=f"{cfg.name.rsplit('_r', 1)[0]}_r{rank}")
         self.wl = wls.workload(cfg)
         self.dev = dev
         self.dim = cfg.dim
@@ -527,7 +533,11 @@ def main():
     if bf16 and (rowwise or args.staged or not args.workload.startswith("mf")):
         print("--values bf16 runs the MF workloads with per-element AdaGrad, in HBM", file=sys.stderr)
         sys.exit(2)
-    wb = Bench(args.workload, dev, nb, rowwise, args.values, unmerged)
+    if args.rank and (not args.workload.startswith("mf") or (args.rank > 512 and not args.ops_only)):
+        print("--rank applies to the MF workloads; ranks above 512 need --ops-only (pull and push only)",
+              file=sys.stderr)
+        sys.exit(2)
+    wb = Bench(args.workload, dev, nb, rowwise, args.values, unmerged, rank=args.rank)
     cfg = wb.cfg
     metric = ("param rows pulled+pushed/sec (MF 10m x 1m, rank 100)" if args.workload == "mf"
               else f"param rows pulled+pushed/sec ({cfg.name})")
