@@ -85,10 +85,11 @@ def test_dedup_bitexact(num_keys, n, zipf):
     assert_bitwise(offs.cpu().numpy(), ro, "offsets")
 
 
-def test_dedup_invalid_keys_sort_last_and_flag():
+@pytest.mark.parametrize("n", [3000, 9000])   # a few radix tiles, and more
+def test_dedup_invalid_keys_sort_last_and_flag(n):
     num_keys = 1000
     rng = np.random.default_rng(11)
-    keys = rng.integers(-50, num_keys + 50, 9000)
+    keys = rng.integers(-50, num_keys + 50, n)
     err = torch.zeros(1, dtype=torch.int32, device="cuda")
     uniq, perm, offs, U = dedup(num_keys, dev(keys), err=err)
     ru, rp, ro, bad = oracle.dedup(num_keys, keys)
@@ -148,6 +149,8 @@ def test_push_parity(K, d, n, zipf, gfill):
 # boundary, runs wholly inside a segment, ragged ends, and a segment that
 # fills the whole batch.
 FOLD_COUNTS = [
+    [4000, 90, 6],            # 4,096 occurrences, a fold run inside one segment
+    [2049, 2047],
     [8192, 16384, 3, 2],
     [100, 20000, 8192, 1],
     [2048, 4096, 6144, 12288],
