@@ -735,6 +735,8 @@ def main():
         ops = measure_ops(args, wb, store, dev, rowwise, unmerged)
         if wb.task == "sgns" and not bf16:
             ops["gather_ceiling"] = gather_ceilings(wb, store, dev, kernels, idx[0], ops.get("merge_distinct_keys"))
+        elif wb.task in ("kge", "ctr") and not bf16:
+            ops["gather_ceiling"] = task_gather_ceiling(wb, store, dev, kernels, idx[0])
 
     copy = calibrate_copy(dev) if args.calibrate_copy else None
 
@@ -962,6 +964,53 @@ def measure_ops(args, wb, store, dev, rowwise, unmerged):
     return ops
 
 
+def probe_ms(store, keys_np, sink, dev, reps=10):
+    """Median time (ms) of the gather probe over the row sequence keys_np."""
+    import torch
+    keys = torch.from_numpy(keys_np.astype(np.int32)).to(dev)
+    for _ in range(2):
+        store.probe_gather(keys, sink)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+    ev[0].record()
+    for r in range(reps):
+        store.probe_gather(keys, sink)
+        ev[r + 1].record()
+    torch.cuda.synchronize()
+    return float(np.median([ev[r].elapsed_time(ev[r + 1]) for r in range(reps)]))
+
+
+def task_gather_ceiling(wb, store, dev, kernels, i):
+    """ComplEx and CTR: the gradient kernel's row reads of batch i (ComplEx:
+    per triple the head, relation and tail rows, then every negative's row;
+    CTR: per sample its field rows, which the kernel reads twice, the second
+    time from the caches) through the gather probe (median of 10), beside
+    the rate the kernel reaches on them in the breakdown steps."""
+    import torch
+
+    from paper_2206_00470_amd import _lib
+    c, bt = wb.cfg, wb.host_batches[i % len(wb.host_batches)]
+    if wb.task == "kge":
+        keys = np.concatenate([bt.head.astype(np.int64)[:, None], (c.n_ent + bt.rel.astype(np.int64))[:, None],
+                               bt.tail.astype(np.int64)[:, None], bt.neg.astype(np.int64)], axis=1).ravel()
+        what = "the ComplEx gradient kernel: per triple its head, relation and tail rows, then its negatives' rows"
+    else:
+        keys = bt.keys.astype(np.int64).ravel()
+        what = "the CTR gradient kernel: per sample its field rows (read twice by the kernel, counted once)"
+    sink = torch.empty(_lib.PS_PROBE_GRID, dtype=torch.float64, device=dev)
+    t = probe_ms(store, keys, sink, dev) * 1e-3
+    rows = int(keys.size)
+    probe = rows * wb.R / t / 1e9
+    kms = kernels.get("taskgrad", {}).get("ms_per_step")
+    kgb = rows * wb.R / (kms * 1e-3) / 1e9 if kms else None
+    return {"grad_stream": {"rows": rows, "probe_ms": round(t * 1e3, 4), "probe_GBps": round(probe, 1),
+                            "kernel": "taskgrad", "kernel_ms": round(kms, 4) if kms else None,
+                            "kernel_GBps": round(kgb, 1) if kgb else None,
+                            "kernel_frac_of_probe": round(kgb / probe, 3) if kgb else None, "what": what},
+            "what": "rows read per second by the gather probe (ps_probe_gather: the same reads without the "
+                    "kernel's arithmetic) against the kernel's row bytes per second"}
+
+
 def gather_ceilings(wb, store, dev, kernels, i, ops_mdk=None):
     """Skip-gram: how fast this part serves each of the step's two row-gather
     streams — the gradient kernel's output rows in centre order, and the
@@ -990,17 +1039,7 @@ def gather_ceilings(wb, store, dev, kernels, i, ops_mdk=None):
     sink = torch.empty(_lib.PS_PROBE_GRID, dtype=torch.float64, device=dev)
     out = {}
     for name, (keys_np, kname, what) in streams.items():
-        keys = torch.from_numpy(keys_np.astype(np.int32)).to(dev)
-        for _ in range(2):
-            store.probe_gather(keys, sink)
-        torch.cuda.synchronize()
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(11)]
-        ev[0].record()
-        for r in range(10):
-            store.probe_gather(keys, sink)
-            ev[r + 1].record()
-        torch.cuda.synchronize()
-        t = float(np.median([ev[r].elapsed_time(ev[r + 1]) for r in range(10)])) * 1e-3
+        t = probe_ms(store, keys_np, sink, dev) * 1e-3
         probe = n_out * R / t / 1e9
         # the gradient kernel also reads the B centre rows, the merge (its input-key
         # launch) the B stored centre gradient rows
@@ -1010,7 +1049,6 @@ def gather_ceilings(wb, store, dev, kernels, i, ops_mdk=None):
                      "kernel": kname, "kernel_ms": round(kms, 4) if kms else None,
                      "kernel_GBps": round(kgb, 1) if kgb else None,
                      "kernel_frac_of_probe": round(kgb / probe, 3) if kgb else None, "what": what}
-        del keys
     # the merge also reads and writes each distinct output key's W and G rows,
     # which the probe does not: add that read-modify-write at the rate of the
     # merge kernel alone on distinct keys (ops.merge_distinct_keys)
