@@ -70,8 +70,8 @@ def parse():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a 4 GiB device-to-device copy (reference for HBM counters)")
     ap.add_argument("--no-overlap", action="store_true",
-                    help="MF: one ps_step_mf call per step instead of overlapping the next batch's key work "
-                         "(sort, segments, records) on a second stream with this batch's table update")
+                    help="MF and CTR: one step call per step instead of overlapping the next batch's key work "
+                         "(sort, segments; MF: records) on a second stream with this batch's table update")
     ap.add_argument("--values", default="f32", choices=["f32", "bf16"],
                     help="fp32 values, or bf16 values with fp32 accumulators (an update variant; MF workloads)")
     ap.add_argument("--staged", action="store_true",
@@ -205,6 +205,37 @@ class Bench:
             fl += 3 * 2.0 * B * fan * h
             fan = h
         return fl
+
+    def run_overlapped_ctr(self, store, first, count, loss, after_step=None):
+        """CTR steps first .. first+count-1 with the two-phase step: the key
+        work of batch i+1 (validity, sort, segments) runs on a second stream
+        while batch i forms its gradients and updates the table on the
+        current one; two workspaces, events for the order.  The results equal
+        those of ps_step_ctr step by step."""
+        import torch
+        main = torch.cuda.current_stream()
+        b = lambda i: self.batches[i % len(self.batches)]
+        B = b(0)["label"].numel()
+        F = b(0)["keys"].numel() // B
+        if not hasattr(self, "_ovl_ctr"):
+            self._ovl_ctr = (torch.cuda.Stream(), [store.ctr_workspace(B, F), store.ctr_workspace(B, F)],
+                             [torch.cuda.Event(), torch.cuda.Event()], [torch.cuda.Event(), torch.cuda.Event()])
+        side, ws, prepared, applied = self._ovl_ctr
+        side.wait_stream(main)
+        store.step_ctr_prepare(b(first)["keys"], F, ws[0], stream=side)
+        prepared[0].record(side)
+        for k in range(count):
+            bt = b(first + k)
+            main.wait_event(prepared[k % 2])
+            store.step_ctr_apply(bt["keys"], bt["label"], ws[k % 2], loss=loss, stream=main)
+            applied[k % 2].record(main)
+            if after_step is not None:
+                after_step(k)
+            if k + 1 < count:
+                if k >= 1:
+                    side.wait_event(applied[(k + 1) % 2])   # that workspace's apply is done
+                store.step_ctr_prepare(b(first + k + 1)["keys"], F, ws[(k + 1) % 2], stream=side)
+                prepared[(k + 1) % 2].record(side)
 
     def run_overlapped(self, store, first, count, loss, after_step=None):
         """MF steps first .. first+count-1 with the two-phase step: the key work
@@ -598,8 +629,11 @@ def main():
            "async": _lib.PS_KERNEL_ASYNC}
     names = list(wb.alg_bytes(0))                 # kernels with algorithmic bytes for this workload
 
-    # (MF tiny is launch-bound: the extra events of the overlap cost more than it hides)
-    overlap = args.workload in ("mf", "mf_colorder") and not args.no_overlap and not args.graph and not unmerged
+    # (MF tiny is launch-bound: the extra events of the overlap cost more than it hides; MF runs the
+    # overlap eagerly, CTR eagerly and captured in the graph)
+    overlap = not args.no_overlap and not unmerged and (
+        (args.workload in ("mf", "mf_colorder") and not args.graph) or args.workload == "ctr")
+    run_ovl = wb.run_overlapped_ctr if args.workload == "ctr" else wb.run_overlapped
 
     def run_steps(first, count, mask, marks=None):
         """count steps from batch `first` with the kernels in `mask` bracketed by HIP
@@ -613,7 +647,7 @@ def main():
             marks[0].record()
         t = time.perf_counter()
         if overlap:
-            wb.run_overlapped(store, first, count, loss,
+            run_ovl(store, first, count, loss,
                               after_step=(lambda k: marks[k + 1].record()) if marks is not None else None)
         else:
             for i in range(count):
@@ -643,8 +677,11 @@ def main():
         # the same steps, captured once (the workspace is already sized) and replayed
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
-            for i in range(args.steps):
-                wb.step(store, args.warmup + i, loss)
+            if overlap:
+                run_ovl(store, args.warmup, args.steps, loss)
+            else:
+                for i in range(args.steps):
+                    wb.step(store, args.warmup + i, loss)
         g.replay()                          # untimed first replay
         torch.cuda.synchronize()
         t = time.perf_counter()
@@ -760,7 +797,7 @@ def main():
         "config": {"workload": cfg.name, "num_keys": cfg.num_keys, "dim": cfg.dim, "layout": args.layout,
                    "update": args.update, "values": args.values,
                    "launch": "hip graph replay" if args.graph else "eager",
-                   "mf_key_work_overlapped": overlap,
+                   "next_key_work_overlapped": overlap,
                    "key_occurrences_per_step": occ, "avg_unique_keys_per_step": U_avg,
                    "batches_resident": nb, "distinct_batch_per_timed_step": nb >= args.warmup + args.steps,
                    "kernel_launches_per_step": launches},

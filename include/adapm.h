@@ -293,6 +293,27 @@ ps_status ps_step_sgns(ps_store* s, const int32_t* centre, const int32_t* ctx, c
 ps_status ps_step_ctr(ps_store* s, const int64_t* keys, const float* label, int64_t B, int32_t F,
                       double* loss, void* ws, size_t ws_bytes, void* stream);
 
+/* ps_step_ctr in two phases, for callers that overlap the key work of the
+ * next batch with the table update of this one (two workspaces, two
+ * streams), as ps_step_mf_prepare / ps_step_mf_apply do for the MF step.
+ * ps_step_ctr_prepare reads only the keys and writes the workspace (sample
+ * validity, sort, segments; a sample with a key outside [0, num_keys) is
+ * skipped and raises the store's sticky error here); it reads and writes no
+ * table row, so it may run while another workspace's apply updates W and G.
+ * ps_step_ctr_apply then forms the gradients from the pre-step table, merges
+ * them into W and G and writes the loss; it reads the keys again, so keys
+ * must be the array given to the prepare, unchanged, and ws the result of
+ * that prepare for this store and the same B and F, unmodified.  Ordering
+ * prepare before apply (and an apply before the next prepare into the same
+ * workspace) is the caller's, e.g. with events.  Prepare then apply gives
+ * exactly the results of ps_step_ctr.  Workspace size:
+ * ps_workspace_bytes(num_keys, dim, PS_OP_STEP_CTR, B, F).  Staged stores:
+ * PS_ERR_UNSUPPORTED. */
+ps_status ps_step_ctr_prepare(ps_store* s, const int64_t* keys, int64_t B, int32_t F, void* ws, size_t ws_bytes,
+                              void* stream);
+ps_status ps_step_ctr_apply(ps_store* s, const int64_t* keys, const float* label, int64_t B, int32_t F,
+                            double* loss, void* ws, size_t ws_bytes, void* stream);
+
 /* Synchronize `stream`, then return and clear the store's sticky device
  * error (PS_OK or PS_ERR_KEY_RANGE). */
 ps_status ps_get_error(ps_store* s, void* stream);

@@ -58,6 +58,8 @@ SIGNATURES = {
     "ps_step_kge": (_i32, [_p, _p, _p, _p, _p, _i64, _i32, _i32, _i64, _p, _p, _sz, _p]),
     "ps_step_sgns": (_i32, [_p, _p, _p, _p, _i64, _i32, _i32, _i64, _p, _p, _sz, _p]),
     "ps_step_ctr": (_i32, [_p, _p, _p, _i64, _i32, _p, _p, _sz, _p]),
+    "ps_step_ctr_prepare": (_i32, [_p, _p, _i64, _i32, _p, _sz, _p]),
+    "ps_step_ctr_apply": (_i32, [_p, _p, _p, _i64, _i32, _p, _p, _sz, _p]),
     "ps_get_error": (_i32, [_p, _p]),
     "ps_status_string": (C.c_char_p, [_i32]),
     "ps_last_error_message": (C.c_char_p, []),

@@ -1479,55 +1479,105 @@ static ps_status step_sgns_impl(ps_store* s, const int32_t* centre, const int32_
   return run_reduce(s, p.sb, ks, src, n, {PART_UPPER, PART_LOWER}, st, LossTotal{p.loss_part, grid, loss});
 }
 
-static ps_status step_ctr_impl(ps_store* s, const int64_t* keys, const float* label, int64_t B, int32_t F, double* loss,
-                               void* ws, size_t ws_bytes, void* stream) {
-  if (ps_status st = check_store(s)) return st;
-  if (ps_status st = check_row_width(s)) return st;
-  if (s->bf16) return fail(PS_ERR_UNSUPPORTED, "this step runs on fp32 values only (bf16 stores: pull, push, MF)");
-  if (F < 1) return fail(PS_ERR_INVALID, "need F >= 1");
-  if (ps_status st = check_n(B, F)) return st;
-  hipStream_t st = as_stream(stream);
-  if (B == 0) {
-    if (loss) {
-      hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(BLOCK), 0, st, reinterpret_cast<uint32_t*>(loss), int64_t(2));
-      LAUNCHED(k_zero_words);
-    }
-    return PS_OK;
-  }
-  if (!keys || !label) return fail(PS_ERR_INVALID, "keys or label is NULL");
-  const int64_t n = B * F;
-  Plan p;
-  plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_CTR, B, F, &p);
-  if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
+// The pieces of the CTR step: the key work (sort and segments; workspace
+// only), the gradient kernel (table reads, gradient rows in occurrence order)
+// and the merge of those rows.
+static ps_status ctr_keywork(ps_store* s, const int64_t* keys, int64_t B, int32_t F, Plan& p, hipStream_t st) {
+  uint32_t *ks, *perm;
+  if (ps_status r = run_sort(s, KeysCTR{keys, F, p.ok}, B * F, s->num_keys, p.sb, s->status, nullptr, false, st, &ks,
+                             &perm, true))
+    return r;
+  return run_segments(p.sb, ks, B * F, s->num_keys, p.sb.seg_off, nullptr, st);
+}
+
+static ps_status ctr_valid(ps_store* s, const int64_t* keys, int64_t B, int32_t F, Plan& p, hipStream_t st) {
   hipLaunchKernelGGL(k_unit_valid<ValidCTR>, dim3(small_grid(B, WAVES_PER_BLOCK, 4096)), dim3(BLOCK), 0, st,
                      ValidCTR{keys, F, s->num_keys}, B, p.ok, s->status, reinterpret_cast<uint32_t*>(p.sb.hdr),
                      header_words(p.sb));
   LAUNCHED(k_unit_valid);
-  // the key sort and segments (workspace only) run on the second stream
-  // beside the gradient kernel (table reads, gradient rows in occurrence order)
-  if (ps_status r = fork_aux(s, st)) return r;
-  uint32_t *ks, *perm;
-  if (ps_status r = run_sort(s, KeysCTR{keys, F, p.ok}, n, s->num_keys, p.sb, s->status, nullptr, false, s->aux,
-                             &ks, &perm, true))
-    return r;
-  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, s->aux)) return r;
+  return PS_OK;
+}
+
+// Launches the gradient kernel; *grid receives its number of loss partials.
+static ps_status ctr_grad(ps_store* s, const int64_t* keys, const float* label, int64_t B, int32_t F, Plan& p,
+                          hipStream_t st, int64_t* grid) {
   RowShape shape;
   row_shape(s->dim, true, &shape);
-  int64_t grid = 0;   // loss partials of the gradient kernel
-  ps_status r = with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
-    grid = small_grid(B, BLOCK / L, LOSS_GRID);
+  return with_shape(shape, [&]<int L, int NV, int VW>() -> ps_status {
+    *grid = small_grid(B, BLOCK / L, LOSS_GRID);
     {
       Timed t(s, PS_KERNEL_TASKGRAD, st);
-      hipLaunchKernelGGL((k_ctr_grad<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->ld, s->dim, keys, label, B, F,
-                         p.ok, p.grads, p.loss_part);
+      hipLaunchKernelGGL((k_ctr_grad<L, NV, VW>), dim3(*grid), dim3(BLOCK), 0, st, s->W, s->ld, s->dim, keys, label, B,
+                         F, p.ok, p.grads, p.loss_part);
     }
     LAUNCHED(k_ctr_grad);
     return PS_OK;
   });
-  if (r) return r;
-  if (ps_status r = join_aux(s, st)) return r;
-  return run_reduce(s, p.sb, ks, SrcIndirect{p.grads, perm, s->dim, s->dim}, n, {PART_ALL}, st,
+}
+
+static ps_status ctr_merge(ps_store* s, int64_t B, int32_t F, double* loss, Plan& p, hipStream_t st, int64_t grid) {
+  const int passes = radix_plan(s->num_keys).passes;   // where the sort left keys and permutation
+  const uint32_t* ks = p.sb.k[passes % 2];
+  const uint32_t* perm = p.sb.v[passes % 2];
+  return run_reduce(s, p.sb, ks, SrcIndirect{p.grads, perm, s->dim, s->dim}, B * F, {PART_ALL}, st,
                     LossTotal{p.loss_part, grid, loss});
+}
+
+static ps_status check_ctr(ps_store* s, int64_t B, int32_t F) {
+  if (ps_status st = check_store(s)) return st;
+  if (ps_status st = check_row_width(s)) return st;
+  if (s->bf16) return fail(PS_ERR_UNSUPPORTED, "this step runs on fp32 values only (bf16 stores: pull, push, MF)");
+  if (F < 1) return fail(PS_ERR_INVALID, "need F >= 1");
+  return check_n(B, F);
+}
+
+static ps_status step_ctr_impl(ps_store* s, const int64_t* keys, const float* label, int64_t B, int32_t F, double* loss,
+                               void* ws, size_t ws_bytes, void* stream) {
+  if (ps_status st = check_ctr(s, B, F)) return st;
+  hipStream_t st = as_stream(stream);
+  if (B == 0) return zero_loss(loss, st);
+  if (!keys || !label) return fail(PS_ERR_INVALID, "keys or label is NULL");
+  Plan p;
+  plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_CTR, B, F, &p);
+  if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
+  if (ps_status r = ctr_valid(s, keys, B, F, p, st)) return r;
+  // the key sort and segments (workspace only) run on the second stream
+  // beside the gradient kernel
+  if (ps_status r = fork_aux(s, st)) return r;
+  if (ps_status r = ctr_keywork(s, keys, B, F, p, s->aux)) return r;
+  int64_t grid = 0;
+  if (ps_status r = ctr_grad(s, keys, label, B, F, p, st, &grid)) return r;
+  if (ps_status r = join_aux(s, st)) return r;
+  return ctr_merge(s, B, F, loss, p, st, grid);
+}
+
+ps_status ps_step_ctr_prepare(ps_store* s, const int64_t* keys, int64_t B, int32_t F, void* ws, size_t ws_bytes,
+                              void* stream) {
+  if (ps_status st = check_ctr(s, B, F)) return st;
+  if (s->stg) return fail(PS_ERR_UNSUPPORTED, "the two-phase CTR step is not available on a staged store");
+  if (B == 0) return PS_OK;
+  if (!keys) return fail(PS_ERR_INVALID, "keys is NULL");
+  Plan p;
+  plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_CTR, B, F, &p);
+  if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
+  hipStream_t st = as_stream(stream);
+  if (ps_status r = ctr_valid(s, keys, B, F, p, st)) return r;
+  return ctr_keywork(s, keys, B, F, p, st);
+}
+
+ps_status ps_step_ctr_apply(ps_store* s, const int64_t* keys, const float* label, int64_t B, int32_t F, double* loss,
+                            void* ws, size_t ws_bytes, void* stream) {
+  if (ps_status st = check_ctr(s, B, F)) return st;
+  if (s->stg) return fail(PS_ERR_UNSUPPORTED, "the two-phase CTR step is not available on a staged store");
+  hipStream_t st = as_stream(stream);
+  if (B == 0) return zero_loss(loss, st);
+  if (!keys || !label) return fail(PS_ERR_INVALID, "keys or label is NULL");
+  Plan p;
+  plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_CTR, B, F, &p);
+  if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
+  int64_t grid = 0;
+  if (ps_status r = ctr_grad(s, keys, label, B, F, p, st, &grid)) return r;
+  return ctr_merge(s, B, F, loss, p, st, grid);
 }
 
 // ---------------------------------------------------------------- public steps

@@ -297,6 +297,27 @@ class Store:
         check(lib().ps_step_ctr(self._h, _ptr(keys), _ptr(label), B, F, _ptr(loss), ws, wsb, _stream(stream)))
         return loss
 
+    def ctr_workspace(self, B: int, F: int) -> torch.Tensor:
+        """A workspace of its own for the two-phase CTR step (one per batch in flight)."""
+        return torch.empty(self.workspace_bytes(_lib.PS_OP_STEP_CTR, B, max(F, 1)), dtype=torch.uint8,
+                           device=self.W.device)
+
+    def step_ctr_prepare(self, keys, F: int, ws: torch.Tensor, stream=None):
+        """Key work of a CTR step (validity, sort, segments) into ws; reads no table row."""
+        _dev(keys, torch.int64, "keys")
+        B = keys.numel() // F if F > 0 else 0
+        check(lib().ps_step_ctr_prepare(self._h, _ptr(keys), B, F, _ptr(ws), ws.numel(), _stream(stream)))
+
+    def step_ctr_apply(self, keys, label, ws: torch.Tensor, loss=None, stream=None):
+        """Gradients and merge of a prepared CTR step; keys as given to the prepare."""
+        _dev(keys, torch.int64, "keys"), _dev(label, torch.float32, "label")
+        B = label.numel()
+        F = keys.numel() // B if B else 1
+        loss = self._loss(loss)
+        check(lib().ps_step_ctr_apply(self._h, _ptr(keys), _ptr(label), B, F, _ptr(loss), _ptr(ws), ws.numel(),
+                                      _stream(stream)))
+        return loss
+
     def step_ctr_wd(self, keys, label, dense, dense_acc, emb_dim: int, hidden, loss=None, stream=None):
         """Wide & Deep CTR step: rows [embedding (emb_dim) | wide weight | ...],
         an MLP of the given hidden widths over the F embeddings; `dense` and
