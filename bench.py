@@ -70,8 +70,8 @@ def parse():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a 4 GiB device-to-device copy (reference for HBM counters)")
     ap.add_argument("--no-overlap", action="store_true",
-                    help="MF and CTR: one step call per step instead of overlapping the next batch's key work "
-                         "(sort, segments; MF: records) on a second stream with this batch's table update")
+                    help="one step call per step instead of overlapping the next batch's key work (sort, "
+                         "segments; MF: records) on a second stream with this batch's table update")
     ap.add_argument("--values", default="f32", choices=["f32", "bf16"],
                     help="fp32 values, or bf16 values with fp32 accumulators (an update variant; MF workloads)")
     ap.add_argument("--staged", action="store_true",
@@ -206,35 +206,56 @@ class Bench:
             fan = h
         return fl
 
-    def run_overlapped_ctr(self, store, first, count, loss, after_step=None):
-        """CTR steps first .. first+count-1 with the two-phase step: the key
-        work of batch i+1 (validity, sort, segments) runs on a second stream
-        while batch i forms its gradients and updates the table on the
-        current one; two workspaces, events for the order.  The results equal
-        those of ps_step_ctr step by step."""
+    def run_overlapped_task(self, store, first, count, loss, after_step=None):
+        """ComplEx, skip-gram or CTR steps first .. first+count-1 with the
+        two-phase step: the key work of batch i+1 (validity, sort, segments)
+        runs on a second stream while batch i forms its gradients and updates
+        the table on the current one; two workspaces, events for the order.
+        The results equal those of the one-call step, step by step."""
         import torch
+        c, t = self.cfg, self.task
         main = torch.cuda.current_stream()
         b = lambda i: self.batches[i % len(self.batches)]
-        B = b(0)["label"].numel()
-        F = b(0)["keys"].numel() // B
-        if not hasattr(self, "_ovl_ctr"):
-            self._ovl_ctr = (torch.cuda.Stream(), [store.ctr_workspace(B, F), store.ctr_workspace(B, F)],
-                             [torch.cuda.Event(), torch.cuda.Event()], [torch.cuda.Event(), torch.cuda.Event()])
-        side, ws, prepared, applied = self._ovl_ctr
+        if not hasattr(self, "_ovl_task"):
+            if t == "ctr":
+                B = max(x["label"].numel() for x in self.batches)
+                mk = lambda: store.ctr_workspace(B, b(0)["keys"].numel() // b(0)["label"].numel())
+            elif t == "kge":
+                B = max(x["head"].numel() for x in self.batches)
+                mk = lambda: store.kge_workspace(B, b(0)["neg"].numel() // b(0)["head"].numel())
+            else:
+                B = max(x["centre"].numel() for x in self.batches)
+                mk = lambda: store.sgns_workspace(B, c.window, c.n_neg)
+            self._ovl_task = (torch.cuda.Stream(), [mk(), mk()], [torch.cuda.Event(), torch.cuda.Event()],
+                              [torch.cuda.Event(), torch.cuda.Event()])
+        side, ws, prepared, applied = self._ovl_task
+        if t == "ctr":
+            F = b(0)["keys"].numel() // b(0)["label"].numel()
+            prep = lambda x, w, st: store.step_ctr_prepare(x["keys"], F, w, stream=st)
+            app = lambda x, w, st: store.step_ctr_apply(x["keys"], x["label"], w, loss=loss, stream=st)
+        elif t == "kge":
+            prep = lambda x, w, st: store.step_kge_prepare(x["head"], x["rel"], x["tail"], x["neg"], c.n_ent, w,
+                                                           stream=st)
+            app = lambda x, w, st: store.step_kge_apply(x["head"], x["rel"], x["tail"], x["neg"], c.n_head_neg,
+                                                        c.n_ent, w, loss=loss, stream=st)
+        else:
+            prep = lambda x, w, st: store.step_sgns_prepare(x["centre"], x["ctx"], x["neg"], c.window, c.vocab, w,
+                                                            stream=st)
+            app = lambda x, w, st: store.step_sgns_apply(x["centre"], x["ctx"], x["neg"], c.window, c.vocab, w,
+                                                         loss=loss, stream=st)
         side.wait_stream(main)
-        store.step_ctr_prepare(b(first)["keys"], F, ws[0], stream=side)
+        prep(b(first), ws[0], side)
         prepared[0].record(side)
         for k in range(count):
-            bt = b(first + k)
             main.wait_event(prepared[k % 2])
-            store.step_ctr_apply(bt["keys"], bt["label"], ws[k % 2], loss=loss, stream=main)
+            app(b(first + k), ws[k % 2], main)
             applied[k % 2].record(main)
             if after_step is not None:
                 after_step(k)
             if k + 1 < count:
                 if k >= 1:
                     side.wait_event(applied[(k + 1) % 2])   # that workspace's apply is done
-                store.step_ctr_prepare(b(first + k + 1)["keys"], F, ws[(k + 1) % 2], stream=side)
+                prep(b(first + k + 1), ws[(k + 1) % 2], side)
                 prepared[(k + 1) % 2].record(side)
 
     def run_overlapped(self, store, first, count, loss, after_step=None):
@@ -630,10 +651,11 @@ def main():
     names = list(wb.alg_bytes(0))                 # kernels with algorithmic bytes for this workload
 
     # (MF tiny is launch-bound: the extra events of the overlap cost more than it hides; MF runs the
-    # overlap eagerly, CTR eagerly and captured in the graph)
+    # overlap eagerly, ComplEx and CTR eagerly and captured in the graph; skip-gram's key work is small
+    # beside its two 5.6 ms kernels, and overlapping it with the merges gained nothing: 11.62 -> 11.73 ms)
     overlap = not args.no_overlap and not unmerged and (
-        (args.workload in ("mf", "mf_colorder") and not args.graph) or args.workload == "ctr")
-    run_ovl = wb.run_overlapped_ctr if args.workload == "ctr" else wb.run_overlapped
+        (args.workload in ("mf", "mf_colorder") and not args.graph) or wb.task in ("ctr", "kge"))
+    run_ovl = wb.run_overlapped_task if wb.task in ("ctr", "kge", "sgns") else wb.run_overlapped
 
     def run_steps(first, count, mask, marks=None):
         """count steps from batch `first` with the kernels in `mask` bracketed by HIP

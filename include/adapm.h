@@ -274,6 +274,22 @@ ps_status ps_step_kge(ps_store* s, const int32_t* head, const int32_t* rel, cons
                       int64_t rel_key_offset, double* loss, void* ws, size_t ws_bytes,
                       void* stream);
 
+/* ps_step_kge in two phases, as ps_step_ctr_prepare / ps_step_ctr_apply:
+ * the prepare reads only the ids (triple validity, key sort, segments into
+ * ws; no table row), the apply forms the gradients from the pre-step table,
+ * merges them into W and G and writes the loss, reading head, rel, tail and
+ * neg again: they must be the arrays given to the prepare, unchanged, with
+ * the same B, n_neg and rel_key_offset, and ws that prepare's result,
+ * unmodified.  Prepare then apply gives exactly the results of ps_step_kge.
+ * Workspace size: ps_workspace_bytes(num_keys, dim, PS_OP_STEP_KGE, B,
+ * 3 + n_neg).  Staged stores: PS_ERR_UNSUPPORTED. */
+ps_status ps_step_kge_prepare(ps_store* s, const int32_t* head, const int32_t* rel, const int32_t* tail,
+                              const int32_t* neg, int64_t B, int32_t n_neg, int64_t rel_key_offset, void* ws,
+                              size_t ws_bytes, void* stream);
+ps_status ps_step_kge_apply(ps_store* s, const int32_t* head, const int32_t* rel, const int32_t* tail,
+                            const int32_t* neg, int64_t B, int32_t n_neg, int32_t n_head_neg, int64_t rel_key_offset,
+                            double* loss, void* ws, size_t ws_bytes, void* stream);
+
 /* One skip-gram negative-sampling step (Appendix C, "Word vectors").
  * Centre b has input key centre[b]; slot q < 2*window holds a context word
  * ctx[b*2w + q] (-1 = no word, the slot is skipped) and n_neg negatives
@@ -284,6 +300,20 @@ ps_status ps_step_kge(ps_store* s, const int32_t* head, const int32_t* rel, cons
 ps_status ps_step_sgns(ps_store* s, const int32_t* centre, const int32_t* ctx, const int32_t* neg,
                        int64_t B, int32_t window, int32_t n_neg, int64_t out_key_offset,
                        double* loss, void* ws, size_t ws_bytes, void* stream);
+
+/* ps_step_sgns in two phases, as ps_step_kge_prepare / ps_step_kge_apply:
+ * the prepare reads only the ids (centre validity, key sort, segments), the
+ * apply reads centre, ctx and neg again (the arrays given to the prepare,
+ * unchanged, with the same B, window, n_neg and out_key_offset).  Prepare
+ * then apply gives exactly the results of ps_step_sgns.  Workspace size:
+ * ps_workspace_bytes(num_keys, dim, PS_OP_STEP_SGNS, B, 1 + 2 window
+ * (1 + n_neg)).  Staged stores: PS_ERR_UNSUPPORTED. */
+ps_status ps_step_sgns_prepare(ps_store* s, const int32_t* centre, const int32_t* ctx, const int32_t* neg, int64_t B,
+                               int32_t window, int32_t n_neg, int64_t out_key_offset, void* ws, size_t ws_bytes,
+                               void* stream);
+ps_status ps_step_sgns_apply(ps_store* s, const int32_t* centre, const int32_t* ctx, const int32_t* neg, int64_t B,
+                             int32_t window, int32_t n_neg, int64_t out_key_offset, double* loss, void* ws,
+                             size_t ws_bytes, void* stream);
 
 /* One CTR embedding step (Appendix C, "Click-through-rate prediction",
  * embedding part).  Sample b has F keys keys[b*F + f] and a label in {0,1}:

@@ -58,6 +58,10 @@ SIGNATURES = {
     "ps_step_kge": (_i32, [_p, _p, _p, _p, _p, _i64, _i32, _i32, _i64, _p, _p, _sz, _p]),
     "ps_step_sgns": (_i32, [_p, _p, _p, _p, _i64, _i32, _i32, _i64, _p, _p, _sz, _p]),
     "ps_step_ctr": (_i32, [_p, _p, _p, _i64, _i32, _p, _p, _sz, _p]),
+    "ps_step_kge_prepare": (_i32, [_p, _p, _p, _p, _p, _i64, _i32, _i64, _p, _sz, _p]),
+    "ps_step_kge_apply": (_i32, [_p, _p, _p, _p, _p, _i64, _i32, _i32, _i64, _p, _p, _sz, _p]),
+    "ps_step_sgns_prepare": (_i32, [_p, _p, _p, _p, _i64, _i32, _i32, _i64, _p, _sz, _p]),
+    "ps_step_sgns_apply": (_i32, [_p, _p, _p, _p, _i64, _i32, _i32, _i64, _p, _p, _sz, _p]),
     "ps_step_ctr_prepare": (_i32, [_p, _p, _i64, _i32, _p, _sz, _p]),
     "ps_step_ctr_apply": (_i32, [_p, _p, _p, _i64, _i32, _p, _p, _sz, _p]),
     "ps_get_error": (_i32, [_p, _p]),

@@ -1365,9 +1365,18 @@ ps_status ps_step_mf_apply(ps_store* s, int64_t B, float lambda, double* loss, v
   return mf_apply(s, B, lambda, loss, p, st, static_cast<hipEvent_t>(rows_done));
 }
 
-static ps_status step_kge_impl(ps_store* s, const int32_t* head, const int32_t* rel, const int32_t* tail, const int32_t* neg,
-                               int64_t B, int32_t n_neg, int32_t n_head_neg, int64_t rel_key_offset, double* loss, void* ws,
-                               size_t ws_bytes, void* stream) {
+// Where the key sort of a workspace left the sorted keys and the
+// permutation (no caller-owned permutation, so the sort's own buffers).
+static void sorted_view(const ps_store* s, const Plan& p, const uint32_t** ks, const uint32_t** perm) {
+  const int passes = radix_plan(s->num_keys).passes;
+  *ks = p.sb.k[passes % 2];
+  *perm = p.sb.v[passes % 2];
+}
+
+// The pieces of the ComplEx step: validity of the triples, the key work
+// (sort and segments; workspace only), the gradient kernel (table reads,
+// per-triple rows and per-negative coefficients) and the merge.
+static ps_status check_kge(ps_store* s, int64_t B, int32_t n_neg, int32_t n_head_neg) {
   if (ps_status st = check_store(s)) return st;
   if (ps_status st = check_row_width(s)) return st;
   if (s->bf16) return fail(PS_ERR_UNSUPPORTED, "this step runs on fp32 values only (bf16 stores: pull, push, MF)");
@@ -1375,108 +1384,237 @@ static ps_status step_kge_impl(ps_store* s, const int32_t* head, const int32_t* 
     return fail(PS_ERR_INVALID, "need 0 <= n_head_neg <= n_neg");
   if (ps_status st = check_n(B, 3 + (int64_t)n_neg)) return st;
   if (s->dim % 2 != 0) return fail(PS_ERR_UNSUPPORTED, "ComplEx rows need an even dim");
-  hipStream_t st = as_stream(stream);
-  if (B == 0) {
-    if (loss) {
-      hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(BLOCK), 0, st, reinterpret_cast<uint32_t*>(loss), int64_t(2));
-      LAUNCHED(k_zero_words);
-    }
-    return PS_OK;
-  }
+  return PS_OK;
+}
+
+static ps_status check_kge_ids(const int32_t* head, const int32_t* rel, const int32_t* tail, const int32_t* neg,
+                               int32_t n_neg, int64_t rel_key_offset) {
   if (!head || !rel || !tail || (n_neg > 0 && !neg)) return fail(PS_ERR_INVALID, "head, rel, tail or neg is NULL");
   if (rel_key_offset < 0) return fail(PS_ERR_INVALID, "negative rel_key_offset");
+  return PS_OK;
+}
+
+static ps_status kge_keywork(ps_store* s, const int32_t* head, const int32_t* rel, const int32_t* tail,
+                             const int32_t* neg, int64_t B, int32_t n_neg, int64_t rel_key_offset, Plan& p,
+                             hipStream_t st) {
   const int per = 3 + n_neg;
-  const int64_t n = B * per;
-  Plan p;
-  plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_KGE, B, per, &p);
-  if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
+  uint32_t *ks, *perm;
+  KeysKGE kk{head, rel, tail, neg, per, n_neg, rel_key_offset, p.ok};
+  if (ps_status r = run_sort(s, kk, B * per, s->num_keys, p.sb, s->status, nullptr, false, st, &ks, &perm, true))
+    return r;
+  return run_segments(p.sb, ks, B * per, s->num_keys, p.sb.seg_off, nullptr, st);
+}
+
+static ps_status kge_valid(ps_store* s, const int32_t* head, const int32_t* rel, const int32_t* tail,
+                           const int32_t* neg, int64_t B, int32_t n_neg, int64_t rel_key_offset, Plan& p,
+                           hipStream_t st) {
   hipLaunchKernelGGL(k_unit_valid<ValidKGE>, dim3(small_grid(B, WAVES_PER_BLOCK, 4096)), dim3(BLOCK), 0, st,
                      ValidKGE{head, rel, tail, neg, n_neg, rel_key_offset, s->num_keys}, B, p.ok, s->status,
                      reinterpret_cast<uint32_t*>(p.sb.hdr), header_words(p.sb));
   LAUNCHED(k_unit_valid);
-  // the key sort and segments (workspace only) run on the second stream
-  // beside the gradient kernel (table reads, per-unit rows)
-  if (ps_status r = fork_aux(s, st)) return r;
-  uint32_t *ks, *perm;
-  KeysKGE kk{head, rel, tail, neg, per, n_neg, rel_key_offset, p.ok};
-  if (ps_status r = run_sort(s, kk, n, s->num_keys, p.sb, s->status, nullptr, false, s->aux, &ks, &perm, true))
-    return r;
-  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, s->aux)) return r;
+  return PS_OK;
+}
+
+// Launches the gradient kernel; *grid receives its number of loss partials.
+static ps_status kge_grad(ps_store* s, const int32_t* head, const int32_t* rel, const int32_t* tail,
+                          const int32_t* neg, int64_t B, int32_t n_neg, int32_t n_head_neg, int64_t rel_key_offset,
+                          Plan& p, hipStream_t st, int64_t* grid) {
   const int cdim = s->dim / 2;
-  const int64_t grid = small_grid(B, WAVES_PER_BLOCK, LOSS_GRID);
+  *grid = small_grid(B, WAVES_PER_BLOCK, LOSS_GRID);
   auto launch = [&](auto kernel) -> ps_status {
     Timed t(s, PS_KERNEL_TASKGRAD, st);
-    hipLaunchKernelGGL(kernel, dim3(grid), dim3(BLOCK), 0, st, s->W, s->ld, s->dim, head, rel, tail, neg, B, n_neg,
+    hipLaunchKernelGGL(kernel, dim3(*grid), dim3(BLOCK), 0, st, s->W, s->ld, s->dim, head, rel, tail, neg, B, n_neg,
                        n_head_neg, rel_key_offset, p.ok, p.mat, p.base, p.coef, p.loss_part);
     LAUNCHED(k_kge_grad);
     return PS_OK;
   };
-  ps_status r;
-  if (cdim <= 64) r = launch(k_kge_grad<1>);
-  else if (cdim <= 128) r = launch(k_kge_grad<2>);
-  else r = launch(k_kge_grad<4>);   // cdim <= 256: the store holds rows of at most 512 floats
-  if (r) return r;
+  if (cdim <= 64) return launch(k_kge_grad<1>);
+  if (cdim <= 128) return launch(k_kge_grad<2>);
+  return launch(k_kge_grad<4>);   // cdim <= 256: the store holds rows of at most 512 floats
+}
+
+static ps_status kge_merge(ps_store* s, int64_t B, int32_t n_neg, int32_t n_head_neg, double* loss, Plan& p,
+                           hipStream_t st, int64_t grid) {
+  const uint32_t *ks, *perm;
+  sorted_view(s, p, &ks, &perm);
+  const int per = 3 + n_neg;
+  return run_reduce(s, p.sb, ks, SrcKGE{perm, p.mat, p.base, p.coef, per, n_head_neg, s->dim}, B * per, {PART_ALL},
+                    st, LossTotal{p.loss_part, grid, loss});
+}
+
+static ps_status step_kge_impl(ps_store* s, const int32_t* head, const int32_t* rel, const int32_t* tail, const int32_t* neg,
+                               int64_t B, int32_t n_neg, int32_t n_head_neg, int64_t rel_key_offset, double* loss, void* ws,
+                               size_t ws_bytes, void* stream) {
+  if (ps_status st = check_kge(s, B, n_neg, n_head_neg)) return st;
+  hipStream_t st = as_stream(stream);
+  if (B == 0) return zero_loss(loss, st);
+  if (ps_status r = check_kge_ids(head, rel, tail, neg, n_neg, rel_key_offset)) return r;
+  Plan p;
+  plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_KGE, B, 3 + n_neg, &p);
+  if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
+  if (ps_status r = kge_valid(s, head, rel, tail, neg, B, n_neg, rel_key_offset, p, st)) return r;
+  // the key sort and segments (workspace only) run on the second stream
+  // beside the gradient kernel (table reads, per-unit rows)
+  if (ps_status r = fork_aux(s, st)) return r;
+  if (ps_status r = kge_keywork(s, head, rel, tail, neg, B, n_neg, rel_key_offset, p, s->aux)) return r;
+  int64_t grid = 0;
+  if (ps_status r = kge_grad(s, head, rel, tail, neg, B, n_neg, n_head_neg, rel_key_offset, p, st, &grid)) return r;
   if (ps_status r = join_aux(s, st)) return r;
-  return run_reduce(s, p.sb, ks, SrcKGE{perm, p.mat, p.base, p.coef, per, n_head_neg, s->dim}, n, {PART_ALL}, st,
-                    LossTotal{p.loss_part, grid, loss});
+  return kge_merge(s, B, n_neg, n_head_neg, loss, p, st, grid);
+}
+
+ps_status ps_step_kge_prepare(ps_store* s, const int32_t* head, const int32_t* rel, const int32_t* tail,
+                              const int32_t* neg, int64_t B, int32_t n_neg, int64_t rel_key_offset, void* ws,
+                              size_t ws_bytes, void* stream) {
+  if (ps_status st = check_store(s)) return st;
+  if (s->stg) return fail(PS_ERR_UNSUPPORTED, "the two-phase ComplEx step is not available on a staged store");
+  if (ps_status st = check_kge(s, B, n_neg, 0)) return st;
+  if (B == 0) return PS_OK;
+  if (ps_status r = check_kge_ids(head, rel, tail, neg, n_neg, rel_key_offset)) return r;
+  Plan p;
+  plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_KGE, B, 3 + n_neg, &p);
+  if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
+  hipStream_t st = as_stream(stream);
+  if (ps_status r = kge_valid(s, head, rel, tail, neg, B, n_neg, rel_key_offset, p, st)) return r;
+  return kge_keywork(s, head, rel, tail, neg, B, n_neg, rel_key_offset, p, st);
+}
+
+ps_status ps_step_kge_apply(ps_store* s, const int32_t* head, const int32_t* rel, const int32_t* tail,
+                            const int32_t* neg, int64_t B, int32_t n_neg, int32_t n_head_neg, int64_t rel_key_offset,
+                            double* loss, void* ws, size_t ws_bytes, void* stream) {
+  if (ps_status st = check_store(s)) return st;
+  if (s->stg) return fail(PS_ERR_UNSUPPORTED, "the two-phase ComplEx step is not available on a staged store");
+  if (ps_status st = check_kge(s, B, n_neg, n_head_neg)) return st;
+  hipStream_t st = as_stream(stream);
+  if (B == 0) return zero_loss(loss, st);
+  if (ps_status r = check_kge_ids(head, rel, tail, neg, n_neg, rel_key_offset)) return r;
+  Plan p;
+  plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_KGE, B, 3 + n_neg, &p);
+  if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
+  int64_t grid = 0;
+  if (ps_status r = kge_grad(s, head, rel, tail, neg, B, n_neg, n_head_neg, rel_key_offset, p, st, &grid)) return r;
+  return kge_merge(s, B, n_neg, n_head_neg, loss, p, st, grid);
+}
+
+// The pieces of the skip-gram step, as for ComplEx.
+static ps_status check_sgns(ps_store* s, int64_t B, int32_t window, int32_t n_neg, int64_t out_key_offset) {
+  if (ps_status st = check_store(s)) return st;
+  if (ps_status st = check_row_width(s)) return st;
+  if (s->bf16) return fail(PS_ERR_UNSUPPORTED, "this step runs on fp32 values only (bf16 stores: pull, push, MF)");
+  if (window < 0 || n_neg < 0) return fail(PS_ERR_INVALID, "negative window or n_neg");
+  if (ps_status st = check_n(B, 1 + 2 * (int64_t)window * (1 + (int64_t)n_neg))) return st;
+  if (out_key_offset < 1 || out_key_offset >= s->num_keys)
+    return fail(PS_ERR_INVALID, "out_key_offset must split the table into input and output rows");
+  return PS_OK;
+}
+
+static ps_status check_sgns_ids(const int32_t* centre, const int32_t* ctx, const int32_t* neg, int32_t window,
+                                int32_t n_neg) {
+  if (!centre || (window > 0 && !ctx) || (window > 0 && n_neg > 0 && !neg))
+    return fail(PS_ERR_INVALID, "centre, ctx or neg is NULL");
+  return PS_OK;
+}
+
+static ps_status sgns_valid(ps_store* s, const int32_t* centre, const int32_t* ctx, const int32_t* neg, int64_t B,
+                            int32_t window, int32_t n_neg, int64_t out_key_offset, Plan& p, hipStream_t st) {
+  hipLaunchKernelGGL(k_unit_valid<ValidSGNS>, dim3(small_grid(B, WAVES_PER_BLOCK, 4096)), dim3(BLOCK), 0, st,
+                     ValidSGNS{centre, ctx, neg, 2 * window, n_neg, out_key_offset, s->num_keys}, B, p.ok, s->status,
+                     reinterpret_cast<uint32_t*>(p.sb.hdr), header_words(p.sb));
+  LAUNCHED(k_unit_valid);
+  return PS_OK;
+}
+
+static ps_status sgns_keywork(ps_store* s, const int32_t* centre, const int32_t* ctx, const int32_t* neg, int64_t B,
+                              int32_t window, int32_t n_neg, int64_t out_key_offset, Plan& p, hipStream_t st) {
+  const int slots = 2 * window;
+  const int64_t per = 1 + (int64_t)slots * (1 + n_neg);
+  uint32_t *ks, *perm;
+  KeysSGNS kk{centre, ctx, neg, (int)per, slots, n_neg, out_key_offset, p.ok};
+  if (ps_status r = run_sort(s, kk, B * per, s->num_keys, p.sb, s->status, nullptr, false, st, &ks, &perm, true))
+    return r;
+  return run_segments(p.sb, ks, B * per, s->num_keys, p.sb.seg_off, nullptr, st, (uint32_t)out_key_offset);
+}
+
+// Launches the gradient kernel; *grid receives its number of loss partials.
+static ps_status sgns_grad(ps_store* s, const int32_t* centre, const int32_t* ctx, const int32_t* neg, int64_t B,
+                           int32_t window, int32_t n_neg, int64_t out_key_offset, Plan& p, hipStream_t st,
+                           int64_t* grid) {
+  const int slots = 2 * window;
+  return with_sgns_shape(s->dim, s->ld, [&]<int L, int NV, int VW>() -> ps_status {
+    *grid = small_grid(B, BLOCK / L, LOSS_GRID);
+    {
+      Timed t(s, PS_KERNEL_TASKGRAD, st);
+      hipLaunchKernelGGL((k_sgns_grad<L, NV, VW>), dim3(*grid), dim3(BLOCK), 0, st, s->W, s->ld, s->dim, centre, ctx,
+                         neg, B, slots, n_neg, out_key_offset, p.ok, p.mat, p.coef, p.loss_part);
+    }
+    LAUNCHED(k_sgns_grad);
+    return PS_OK;
+  });
+}
+
+static ps_status sgns_merge(ps_store* s, const int32_t* centre, int64_t B, int32_t window, int32_t n_neg,
+                            double* loss, Plan& p, hipStream_t st, int64_t grid) {
+  const uint32_t *ks, *perm;
+  sorted_view(s, p, &ks, &perm);
+  const int64_t per = 1 + 2 * (int64_t)window * (1 + n_neg);
+  // output rows first: their gradients read the input rows, which are updated second
+  SrcSGNS src{perm, p.mat, p.coef, centre, s->W, s->ld, (int)per, s->dim};
+  return run_reduce(s, p.sb, ks, src, B * per, {PART_UPPER, PART_LOWER}, st, LossTotal{p.loss_part, grid, loss});
 }
 
 static ps_status step_sgns_impl(ps_store* s, const int32_t* centre, const int32_t* ctx, const int32_t* neg, int64_t B,
                                 int32_t window, int32_t n_neg, int64_t out_key_offset, double* loss, void* ws,
                                 size_t ws_bytes, void* stream) {
-  if (ps_status st = check_store(s)) return st;
-  if (ps_status st = check_row_width(s)) return st;
-  if (s->bf16) return fail(PS_ERR_UNSUPPORTED, "this step runs on fp32 values only (bf16 stores: pull, push, MF)");
-  if (window < 0 || n_neg < 0) return fail(PS_ERR_INVALID, "negative window or n_neg");
-  const int slots = 2 * window;
-  const int64_t per = 1 + (int64_t)slots * (1 + n_neg);
-  if (ps_status st = check_n(B, per)) return st;
-  if (out_key_offset < 1 || out_key_offset >= s->num_keys)
-    return fail(PS_ERR_INVALID, "out_key_offset must split the table into input and output rows");
+  if (ps_status st = check_sgns(s, B, window, n_neg, out_key_offset)) return st;
   hipStream_t st = as_stream(stream);
-  if (B == 0) {
-    if (loss) {
-      hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(BLOCK), 0, st, reinterpret_cast<uint32_t*>(loss), int64_t(2));
-      LAUNCHED(k_zero_words);
-    }
-    return PS_OK;
-  }
-  if (!centre || (slots > 0 && !ctx) || (slots > 0 && n_neg > 0 && !neg))
-    return fail(PS_ERR_INVALID, "centre, ctx or neg is NULL");
-  const int64_t n = B * per;
+  if (B == 0) return zero_loss(loss, st);
+  if (ps_status r = check_sgns_ids(centre, ctx, neg, window, n_neg)) return r;
+  const int64_t per = 1 + 2 * (int64_t)window * (1 + n_neg);
   Plan p;
   plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_SGNS, B, per, &p);
   if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
-  hipLaunchKernelGGL(k_unit_valid<ValidSGNS>, dim3(small_grid(B, WAVES_PER_BLOCK, 4096)), dim3(BLOCK), 0, st,
-                     ValidSGNS{centre, ctx, neg, slots, n_neg, out_key_offset, s->num_keys}, B, p.ok, s->status,
-                     reinterpret_cast<uint32_t*>(p.sb.hdr), header_words(p.sb));
-  LAUNCHED(k_unit_valid);
+  if (ps_status r = sgns_valid(s, centre, ctx, neg, B, window, n_neg, out_key_offset, p, st)) return r;
   // the key sort and segments (workspace only) run on the second stream
   // beside the gradient kernel (table reads, per-unit rows)
   if (ps_status r = fork_aux(s, st)) return r;
-  uint32_t *ks, *perm;
-  KeysSGNS kk{centre, ctx, neg, (int)per, slots, n_neg, out_key_offset, p.ok};
-  if (ps_status r = run_sort(s, kk, n, s->num_keys, p.sb, s->status, nullptr, false, s->aux, &ks, &perm, true))
-    return r;
-  if (ps_status r = run_segments(p.sb, ks, n, s->num_keys, p.sb.seg_off, nullptr, s->aux,
-                                 (uint32_t)out_key_offset))
-    return r;
-  int64_t grid = 0;   // loss partials of the gradient kernel
-  ps_status r = with_sgns_shape(s->dim, s->ld, [&]<int L, int NV, int VW>() -> ps_status {
-    grid = small_grid(B, BLOCK / L, LOSS_GRID);
-    {
-      Timed t(s, PS_KERNEL_TASKGRAD, st);
-      hipLaunchKernelGGL((k_sgns_grad<L, NV, VW>), dim3(grid), dim3(BLOCK), 0, st, s->W, s->ld, s->dim, centre, ctx, neg,
-                         B, slots, n_neg, out_key_offset, p.ok, p.mat, p.coef, p.loss_part);
-    }
-    LAUNCHED(k_sgns_grad);
-    return PS_OK;
-  });
-  if (r) return r;
+  if (ps_status r = sgns_keywork(s, centre, ctx, neg, B, window, n_neg, out_key_offset, p, s->aux)) return r;
+  int64_t grid = 0;
+  if (ps_status r = sgns_grad(s, centre, ctx, neg, B, window, n_neg, out_key_offset, p, st, &grid)) return r;
   if (ps_status r = join_aux(s, st)) return r;
-  // output rows first: their gradients read the input rows, which are updated second
-  SrcSGNS src{perm, p.mat, p.coef, centre, s->W, s->ld, (int)per, s->dim};
-  return run_reduce(s, p.sb, ks, src, n, {PART_UPPER, PART_LOWER}, st, LossTotal{p.loss_part, grid, loss});
+  return sgns_merge(s, centre, B, window, n_neg, loss, p, st, grid);
+}
+
+ps_status ps_step_sgns_prepare(ps_store* s, const int32_t* centre, const int32_t* ctx, const int32_t* neg, int64_t B,
+                               int32_t window, int32_t n_neg, int64_t out_key_offset, void* ws, size_t ws_bytes,
+                               void* stream) {
+  if (ps_status st = check_store(s)) return st;
+  if (s->stg) return fail(PS_ERR_UNSUPPORTED, "the two-phase skip-gram step is not available on a staged store");
+  if (ps_status st = check_sgns(s, B, window, n_neg, out_key_offset)) return st;
+  if (B == 0) return PS_OK;
+  if (ps_status r = check_sgns_ids(centre, ctx, neg, window, n_neg)) return r;
+  Plan p;
+  plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_SGNS, B, 1 + 2 * (int64_t)window * (1 + n_neg), &p);
+  if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
+  hipStream_t st = as_stream(stream);
+  if (ps_status r = sgns_valid(s, centre, ctx, neg, B, window, n_neg, out_key_offset, p, st)) return r;
+  return sgns_keywork(s, centre, ctx, neg, B, window, n_neg, out_key_offset, p, st);
+}
+
+ps_status ps_step_sgns_apply(ps_store* s, const int32_t* centre, const int32_t* ctx, const int32_t* neg, int64_t B,
+                             int32_t window, int32_t n_neg, int64_t out_key_offset, double* loss, void* ws,
+                             size_t ws_bytes, void* stream) {
+  if (ps_status st = check_store(s)) return st;
+  if (s->stg) return fail(PS_ERR_UNSUPPORTED, "the two-phase skip-gram step is not available on a staged store");
+  if (ps_status st = check_sgns(s, B, window, n_neg, out_key_offset)) return st;
+  hipStream_t st = as_stream(stream);
+  if (B == 0) return zero_loss(loss, st);
+  if (ps_status r = check_sgns_ids(centre, ctx, neg, window, n_neg)) return r;
+  Plan p;
+  plan_op(ws, s->num_keys, s->dim, PS_OP_STEP_SGNS, B, 1 + 2 * (int64_t)window * (1 + n_neg), &p);
+  if (ps_status r = check_ws(p, ws, ws_bytes)) return r;
+  int64_t grid = 0;
+  if (ps_status r = sgns_grad(s, centre, ctx, neg, B, window, n_neg, out_key_offset, p, st, &grid)) return r;
+  return sgns_merge(s, centre, B, window, n_neg, loss, p, st, grid);
 }
 
 // The pieces of the CTR step: the key work (sort and segments; workspace
@@ -1516,9 +1654,8 @@ static ps_status ctr_grad(ps_store* s, const int64_t* keys, const float* label, 
 }
 
 static ps_status ctr_merge(ps_store* s, int64_t B, int32_t F, double* loss, Plan& p, hipStream_t st, int64_t grid) {
-  const int passes = radix_plan(s->num_keys).passes;   // where the sort left keys and permutation
-  const uint32_t* ks = p.sb.k[passes % 2];
-  const uint32_t* perm = p.sb.v[passes % 2];
+  const uint32_t *ks, *perm;
+  sorted_view(s, p, &ks, &perm);
   return run_reduce(s, p.sb, ks, SrcIndirect{p.grads, perm, s->dim, s->dim}, B * F, {PART_ALL}, st,
                     LossTotal{p.loss_part, grid, loss});
 }
@@ -1553,8 +1690,9 @@ static ps_status step_ctr_impl(ps_store* s, const int64_t* keys, const float* la
 
 ps_status ps_step_ctr_prepare(ps_store* s, const int64_t* keys, int64_t B, int32_t F, void* ws, size_t ws_bytes,
                               void* stream) {
-  if (ps_status st = check_ctr(s, B, F)) return st;
+  if (ps_status st = check_store(s)) return st;
   if (s->stg) return fail(PS_ERR_UNSUPPORTED, "the two-phase CTR step is not available on a staged store");
+  if (ps_status st = check_ctr(s, B, F)) return st;
   if (B == 0) return PS_OK;
   if (!keys) return fail(PS_ERR_INVALID, "keys is NULL");
   Plan p;
@@ -1567,8 +1705,9 @@ ps_status ps_step_ctr_prepare(ps_store* s, const int64_t* keys, int64_t B, int32
 
 ps_status ps_step_ctr_apply(ps_store* s, const int64_t* keys, const float* label, int64_t B, int32_t F, double* loss,
                             void* ws, size_t ws_bytes, void* stream) {
-  if (ps_status st = check_ctr(s, B, F)) return st;
+  if (ps_status st = check_store(s)) return st;
   if (s->stg) return fail(PS_ERR_UNSUPPORTED, "the two-phase CTR step is not available on a staged store");
+  if (ps_status st = check_ctr(s, B, F)) return st;
   hipStream_t st = as_stream(stream);
   if (B == 0) return zero_loss(loss, st);
   if (!keys || !label) return fail(PS_ERR_INVALID, "keys or label is NULL");

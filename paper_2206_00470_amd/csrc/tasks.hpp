@@ -331,7 +331,10 @@ struct KeysKGE {
 // and a tail-corrupted one phi(s,r,x) = <x, h>, so the gradient row of each
 // negative occurrence is (its coefficient) x (f or h): the kernel stores the
 // fp64 rows f, h per triple and one fp64 coefficient per negative, and
-// writes the full fp32 gradient rows of s, r and o.
+// writes the full fp32 gradient rows of s, r and o.  The negatives' terms in
+// those three rows are linear in x, so the kernel sums c_j x_j over the
+// head-corrupted and over the tail-corrupted negatives (fp64) and multiplies
+// the two sums by (r, o) and (s, r) once per triple.
 template <int KPL>
 __global__ __launch_bounds__(BLOCK) void k_kge_grad(const float* __restrict__ W, int64_t ld, int dim,
                                                     const int32_t* __restrict__ head,
@@ -343,9 +346,10 @@ __global__ __launch_bounds__(BLOCK) void k_kge_grad(const float* __restrict__ W,
                                                     double* __restrict__ coef, double* __restrict__ loss_part) {
   constexpr int JB = 4;   // negatives in flight, scored together (8 costs occupancy)
   __shared__ double sm[WAVES_PER_BLOCK];
-  // per-thread fp64 gradient accumulators of s, r, o (Re, Im), and the
-  // current batch of negative rows, kept in LDS: the coefficient's fp64
-  // transcendentals would otherwise run with all of them in registers
+  // per-thread fp64 gradient rows of s, r, o (Re, Im) of the true triple's
+  // term, and the current batch of negative rows, kept in LDS: the
+  // coefficient's fp64 transcendentals would otherwise run with all of them
+  // in registers
   __shared__ double gacc[6 * KPL][BLOCK];
   __shared__ float xstash[2 * JB * KPL][BLOCK];
   const int cdim = dim / 2;
@@ -432,6 +436,10 @@ __global__ __launch_bounds__(BLOCK) void k_kge_grad(const float* __restrict__ W,
         }
       }
     };
+    // sums over the negatives of c_j x_j (head-corrupted: Xh, tail-corrupted: Xt)
+    double XhR[KPL], XhI[KPL], XtR[KPL], XtI[KPL];
+#pragma unroll
+    for (int i = 0; i < KPL; ++i) XhR[i] = XhI[i] = XtR[i] = XtI[i] = 0.0;
     if (n_neg > 0) load_batch(0);
     for (int j0 = 0; j0 < n_neg; j0 += JB) {
       // convert s, r, o per batch instead of holding fp64 copies across the loop
@@ -482,28 +490,30 @@ __global__ __launch_bounds__(BLOCK) void k_kge_grad(const float* __restrict__ W,
         const int j = j0 + jj;
         const double cj = __shfl(c_my, jj * (WAVE / JB), WAVE);
         if (j >= n_neg) break;
-        if (j < n_head) {   // (x, r, o): d/dr and d/do
+        const bool hd = j < n_head;
 #pragma unroll
-          for (int i = 0; i < KPL; ++i) {
-            const double x_r = xstash[(jj * KPL + i) * 2][threadIdx.x];
-            const double x_i = xstash[(jj * KPL + i) * 2 + 1][threadIdx.x];
-            grR[i * BLOCK] += cj * (x_r * (double)oRf[i] + x_i * (double)oIf[i]);
-            grI[i * BLOCK] += cj * (x_r * (double)oIf[i] - x_i * (double)oRf[i]);
-            goR[i * BLOCK] += cj * (x_r * (double)rRf[i] - x_i * (double)rIf[i]);
-            goI[i * BLOCK] += cj * (x_i * (double)rRf[i] + x_r * (double)rIf[i]);
-          }
-        } else {            // (s, r, x): d/ds and d/dr
-#pragma unroll
-          for (int i = 0; i < KPL; ++i) {
-            const double x_r = xstash[(jj * KPL + i) * 2][threadIdx.x];
-            const double x_i = xstash[(jj * KPL + i) * 2 + 1][threadIdx.x];
-            gsR[i * BLOCK] += cj * ((double)rRf[i] * x_r + (double)rIf[i] * x_i);
-            gsI[i * BLOCK] += cj * ((double)rRf[i] * x_i - (double)rIf[i] * x_r);
-            grR[i * BLOCK] += cj * ((double)sRf[i] * x_r + (double)sIf[i] * x_i);
-            grI[i * BLOCK] += cj * ((double)sRf[i] * x_i - (double)sIf[i] * x_r);
+        for (int i = 0; i < KPL; ++i) {
+          const double x_r = xstash[(jj * KPL + i) * 2][threadIdx.x];
+          const double x_i = xstash[(jj * KPL + i) * 2 + 1][threadIdx.x];
+          if (hd) {
+            XhR[i] = __builtin_fma(cj, x_r, XhR[i]);
+            XhI[i] = __builtin_fma(cj, x_i, XhI[i]);
+          } else {
+            XtR[i] = __builtin_fma(cj, x_r, XtR[i]);
+            XtI[i] = __builtin_fma(cj, x_i, XtI[i]);
           }
         }
       }
+    }
+#pragma unroll
+    for (int i = 0; i < KPL; ++i) {
+      const double sR = sRf[i], sI = sIf[i], rR = rRf[i], rI = rIf[i], oR = oRf[i], oI = oIf[i];
+      grR[i * BLOCK] += (XhR[i] * oR + XhI[i] * oI) + (sR * XtR[i] + sI * XtI[i]);
+      grI[i * BLOCK] += (XhR[i] * oI - XhI[i] * oR) + (sR * XtI[i] - sI * XtR[i]);
+      goR[i * BLOCK] += XhR[i] * rR - XhI[i] * rI;
+      goI[i * BLOCK] += XhI[i] * rR + XhR[i] * rI;
+      gsR[i * BLOCK] += rR * XtR[i] + rI * XtI[i];
+      gsI[i * BLOCK] += rR * XtI[i] - rI * XtR[i];
     }
     float* ms = mat + (3 * t) * dim;
 #pragma unroll

@@ -277,6 +277,58 @@ class Store:
                                 rel_key_offset, _ptr(loss), ws, wsb, _stream(stream)))
         return loss
 
+    def kge_workspace(self, B: int, n_neg: int) -> torch.Tensor:
+        """A workspace of its own for the two-phase ComplEx step (one per batch in flight)."""
+        return torch.empty(self.workspace_bytes(_lib.PS_OP_STEP_KGE, B, 3 + n_neg), dtype=torch.uint8,
+                           device=self.W.device)
+
+    def step_kge_prepare(self, head, rel, tail, neg, rel_key_offset: int, ws: torch.Tensor, stream=None):
+        """Key work of a ComplEx step (validity, sort, segments) into ws; reads no table row."""
+        for t, nm in ((head, "head"), (rel, "rel"), (tail, "tail"), (neg, "neg")):
+            _dev(t, torch.int32, nm)
+        B = head.numel()
+        n_neg = neg.numel() // B if B else 0
+        check(lib().ps_step_kge_prepare(self._h, _ptr(head), _ptr(rel), _ptr(tail), _ptr(neg), B, n_neg,
+                                        rel_key_offset, _ptr(ws), ws.numel(), _stream(stream)))
+
+    def step_kge_apply(self, head, rel, tail, neg, n_head_neg: int, rel_key_offset: int, ws: torch.Tensor,
+                       loss=None, stream=None):
+        """Gradients and merge of a prepared ComplEx step; ids as given to the prepare."""
+        for t, nm in ((head, "head"), (rel, "rel"), (tail, "tail"), (neg, "neg")):
+            _dev(t, torch.int32, nm)
+        B = head.numel()
+        n_neg = neg.numel() // B if B else 0
+        loss = self._loss(loss)
+        check(lib().ps_step_kge_apply(self._h, _ptr(head), _ptr(rel), _ptr(tail), _ptr(neg), B, n_neg, n_head_neg,
+                                      rel_key_offset, _ptr(loss), _ptr(ws), ws.numel(), _stream(stream)))
+        return loss
+
+    def sgns_workspace(self, B: int, window: int, n_neg: int) -> torch.Tensor:
+        """A workspace of its own for the two-phase skip-gram step (one per batch in flight)."""
+        return torch.empty(self.workspace_bytes(_lib.PS_OP_STEP_SGNS, B, 1 + 2 * window * (1 + n_neg)),
+                           dtype=torch.uint8, device=self.W.device)
+
+    def step_sgns_prepare(self, centre, ctx, neg, window: int, out_key_offset: int, ws: torch.Tensor, stream=None):
+        """Key work of a skip-gram step (validity, sort, segments) into ws; reads no table row."""
+        for t, nm in ((centre, "centre"), (ctx, "ctx"), (neg, "neg")):
+            _dev(t, torch.int32, nm)
+        B = centre.numel()
+        n_neg = neg.numel() // (B * 2 * window) if B and window else 0
+        check(lib().ps_step_sgns_prepare(self._h, _ptr(centre), _ptr(ctx), _ptr(neg), B, window, n_neg,
+                                         out_key_offset, _ptr(ws), ws.numel(), _stream(stream)))
+
+    def step_sgns_apply(self, centre, ctx, neg, window: int, out_key_offset: int, ws: torch.Tensor, loss=None,
+                        stream=None):
+        """Gradients and merges of a prepared skip-gram step; ids as given to the prepare."""
+        for t, nm in ((centre, "centre"), (ctx, "ctx"), (neg, "neg")):
+            _dev(t, torch.int32, nm)
+        B = centre.numel()
+        n_neg = neg.numel() // (B * 2 * window) if B and window else 0
+        loss = self._loss(loss)
+        check(lib().ps_step_sgns_apply(self._h, _ptr(centre), _ptr(ctx), _ptr(neg), B, window, n_neg,
+                                       out_key_offset, _ptr(loss), _ptr(ws), ws.numel(), _stream(stream)))
+        return loss
+
     def step_sgns(self, centre, ctx, neg, window: int, out_key_offset: int, loss=None, stream=None):
         for t, nm in ((centre, "centre"), (ctx, "ctx"), (neg, "neg")):
             _dev(t, torch.int32, nm)
