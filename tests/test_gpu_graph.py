@@ -199,3 +199,64 @@ def test_mf_async_graph_replays_within_bounds():
         assert float(loss.item()) == pytest.approx(rloss, rel=1e-9)
         check_bounds(s.W.cpu().numpy(), Wb, Gb, keys, grads, lr=cfg.opt.lr, eps=cfg.opt.eps)
         check_accumulators(s.G.cpu().numpy(), Gb, keys, grads)
+
+
+@pytest.mark.parametrize("cfg", [MF_TINY, small_variant(MF_10Mx1M)], ids=["mf_tiny", "mf_small"])
+def test_mf_two_phase_pipeline_graph_replays_match_eager(cfg):
+    """The MF two-phase loop over three resident batches (prepare of batch
+    i+1 on a side stream after the row-key merge of batch i, ordered by the
+    library's rows_done event and per-workspace events) captured once; each
+    replay follows three eager ps_step_mf calls on the twin store and must
+    leave both stores equal bit for bit."""
+    wl = MFWorkload(cfg)
+    W0 = wl.init_table()
+    WA, GA = dev(W0), torch.zeros(W0.shape, dtype=torch.float32, device="cuda")
+    WB, GB = dev(W0), torch.zeros(W0.shape, dtype=torch.float32, device="cuda")
+    A, B = Store(WA, GA, cfg.opt.lr, cfg.opt.eps), Store(WB, GB, cfg.opt.lr, cfg.opt.eps)
+    batches = []
+    for i in range(3):
+        bt = wl.batch(i)
+        batches.append((dev(bt.row), dev(bt.col), dev(bt.val)))
+    nB = batches[0][0].numel()
+    assert all(b[0].numel() == nB for b in batches)
+    side = torch.cuda.Stream()
+    ws = [B.mf_workspace(nB), B.mf_workspace(nB)]
+    prepared = [torch.cuda.Event(), torch.cuda.Event()]
+    applied = [torch.cuda.Event(), torch.cuda.Event()]
+    rows_done = torch.cuda.Event()
+    rows_done.record()
+    losses = [torch.zeros(1, dtype=torch.float64, device="cuda") for _ in batches]
+
+    def pipeline():
+        main = torch.cuda.current_stream()      # the capture stream inside torch.cuda.graph
+        side.wait_stream(main)
+        B.step_mf_prepare(*batches[0], cfg.n_rows, ws[0], stream=side)
+        prepared[0].record(side)
+        for i in range(len(batches)):
+            main.wait_event(prepared[i % 2])
+            B.step_mf_apply(nB, cfg.lam, ws[i % 2], loss=losses[i], stream=main, rows_done=rows_done)
+            applied[i % 2].record(main)
+            if i + 1 < len(batches):
+                if i >= 1:
+                    side.wait_event(applied[(i + 1) % 2])
+                side.wait_event(rows_done)
+                B.step_mf_prepare(*batches[i + 1], cfg.n_rows, ws[(i + 1) % 2], stream=side)
+                prepared[(i + 1) % 2].record(side)
+
+    for r, c, v in batches:
+        A.step_mf(r, c, v, cfg.n_rows, cfg.lam)
+    pipeline()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        pipeline()
+    for rep in range(3):
+        lossA = [A.step_mf(r, c, v, cfg.n_rows, cfg.lam).clone() for r, c, v in batches]
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert A.error() == 0 and B.error() == 0
+        assert_bitwise(WB.cpu().numpy(), WA.cpu().numpy(), f"W after replay {rep}")
+        assert_bitwise(GB.cpu().numpy(), GA.cpu().numpy(), f"G after replay {rep}")
+        assert [l.item() for l in losses] == [l.item() for l in lossA]
+        say(f"{cfg.name}: replay {rep} equal")
