@@ -265,3 +265,53 @@ def test_two_phase_argument_checks():
             assert e.value.status == _lib.PS_ERR_UNSUPPORTED
     finally:
         staged.close()
+
+
+def test_every_unit_invalid_leaves_tables_and_zero_loss():
+    """A batch in which every unit holds an id out of range: no key reaches
+    a segment, so the one-call and the two-phase steps both leave W and G
+    bit-identical, report a zero loss and raise the sticky error (ComplEx,
+    skip-gram and CTR; the oracle skips every unit too)."""
+    from paper_2206_00470_amd.workloads import CTR_33M, CTRWorkload
+    cases = []
+    cfg = small_variant(KGE_COMPLEX)
+    bt = KGEWorkload(cfg).batch(0)
+    bt.rel[:] = -1
+    cases.append((KGE, cfg, bt))
+    cfg = small_variant(SGNS_1M)
+    bt = SGNSWorkload(cfg).batch(0)
+    bt.centre[:] = cfg.vocab                       # an output-table id as centre: invalid
+    cases.append((SGNS, cfg, bt))
+    for T, cfg, bt in cases:
+        W0 = T.WL(cfg).init_table()
+        (WA, GA, A), (WB, GB, B) = stores(cfg, W0, False)
+        x = T.to_dev(bt)
+        la = T.one_call(A, cfg, x)
+        ws = T.workspace(B, cfg, x)
+        T.prepare(B, cfg, x, ws)
+        lb = T.apply(B, cfg, x, ws)
+        assert A.error() == _lib.PS_ERR_KEY_RANGE and B.error() == _lib.PS_ERR_KEY_RANGE
+        assert la.item() == 0.0 and lb.item() == 0.0
+        for t in (WA, WB):
+            assert_bitwise(t.cpu().numpy(), W0, "W")
+        assert not GA.cpu().numpy().any() and not GB.cpu().numpy().any()
+        rloss, bad = T.oracle(W0.copy(), np.zeros_like(W0), cfg, bt)
+        assert bad == bt.centre.size if T is SGNS else bad == bt.head.size
+        assert rloss == 0.0
+    cfg = small_variant(CTR_33M)
+    bt = CTRWorkload(cfg).batch(0)
+    bt.keys[:, 0] = -1
+    W0 = CTRWorkload(cfg).init_table()
+    (WA, GA, A), (WB, GB, B) = stores(cfg, W0, False)
+    k, y = dev(bt.keys), dev(bt.label)
+    la = A.step_ctr(k, y)
+    ws = B.ctr_workspace(cfg.batch, cfg.n_fields)
+    B.step_ctr_prepare(k, cfg.n_fields, ws)
+    lb = B.step_ctr_apply(k, y, ws)
+    assert A.error() == _lib.PS_ERR_KEY_RANGE and B.error() == _lib.PS_ERR_KEY_RANGE
+    assert la.item() == 0.0 and lb.item() == 0.0
+    for t in (WA, WB):
+        assert_bitwise(t.cpu().numpy(), W0, "W")
+    assert not GA.cpu().numpy().any() and not GB.cpu().numpy().any()
+    rloss, bad = oracle.step_ctr(W0.copy(), np.zeros_like(W0), bt.keys, bt.label, cfg.opt.lr, cfg.opt.eps)
+    assert bad == cfg.batch and rloss == 0.0
