@@ -95,6 +95,28 @@ def test_mf_invalid_entries_are_skipped_and_flagged():
     assert float(loss.item()) == pytest.approx(rloss, rel=1e-9)
 
 
+def test_mf_two_phase_invalid_entries_match_one_call():
+    """Invalid entries in the two-phase step: flagged by the prepare, skipped
+    by the apply, tables and loss equal to ps_step_mf's bit for bit."""
+    cfg = small_variant(MF_10Mx1M)
+    wl = MFWorkload(cfg)
+    W = wl.init_table()
+    bt = wl.batch(0)
+    bt.row[[3, 100]] = [-1, cfg.n_rows + cfg.n_cols]
+    bt.col[7] = cfg.n_cols
+    WA, GA, WB, GB = dev(W), dev(np.zeros_like(W)), dev(W), dev(np.zeros_like(W))
+    A, B = Store(WA, GA, cfg.opt.lr, cfg.opt.eps), Store(WB, GB, cfg.opt.lr, cfg.opt.eps)
+    la = gpu_step(A, cfg, bt)
+    r, c, v = dev(bt.row), dev(bt.col), dev(bt.val)
+    ws = B.mf_workspace(r.numel())
+    B.step_mf_prepare(r, c, v, cfg.n_rows, ws)
+    lb = B.step_mf_apply(r.numel(), cfg.lam, ws)
+    assert A.error() == -2 and B.error() == -2
+    assert_bitwise(WB.cpu().numpy(), WA.cpu().numpy(), "W")
+    assert_bitwise(GB.cpu().numpy(), GA.cpu().numpy(), "G")
+    assert lb.item() == la.item()
+
+
 def test_mf_step_equals_pull_host_gradient_push():
     """The fused step and the composition pull -> oracle gradient -> push agree."""
     cfg = small_variant(MF_10Mx1M)
