@@ -651,8 +651,8 @@ def main():
     names = list(wb.alg_bytes(0))                 # kernels with algorithmic bytes for this workload
 
     # (MF tiny is launch-bound: the overlap's second stream costs more than it hides, eagerly and in a
-    # graph replay, 0.063 -> 0.078 ms; skip-gram's key work is small beside its two 5.6 ms kernels, and
-    # overlapping it with the merges gained nothing: 11.62 -> 11.73 ms)
+    # graph replay, 0.063 -> 0.078 ms; skip-gram's key sort already ends beside its 5.7 ms gradient
+    # kernel, and overlapping it with the merges instead gained nothing: 11.62 -> 11.73 ms)
     overlap = not args.no_overlap and not unmerged and (
         (args.workload in ("mf", "mf_colorder") and not args.graph) or wb.task in ("ctr", "kge"))
     run_ovl = wb.run_overlapped_task if wb.task in ("ctr", "kge", "sgns") else wb.run_overlapped
