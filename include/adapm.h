@@ -37,6 +37,12 @@
  *     the caller, sized by ps_workspace_bytes(); the library allocates no
  *     device memory except a small status block in ps_create() (and, once
  *     per device, the static scratch array of ps_push_noalloc).
+ *   - Two-phase calls (the *_prepare / *_apply pairs): the apply trusts the
+ *     workspace its prepare filled (sorted keys, permutation, segments,
+ *     validity) and does not check it again; an apply on a workspace that
+ *     no matching prepare filled, or with other ids than the prepare's, is
+ *     undefined behaviour (its kernels index the tables with whatever the
+ *     workspace holds).
  */
 #ifndef ADAPM_H
 #define ADAPM_H
